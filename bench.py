@@ -1,0 +1,196 @@
+#!/usr/bin/env python3
+"""Benchmark: hyperbatch data preparation on one MI355X.
+
+A step is one call of agnes_hyperbatch_prepare: L hops of block-bucketed
+sampling for H minibatches plus the block-bucketed feature gather, on a fresh
+hyperbatch of targets (step s uses targets s and mb_base = s * H).  All inputs
+(graph, features, every step's targets) are resident in HBM before timing.
+
+Default workload: R-MAT 2^23 nodes, average degree 30, fp32 features of 256
+dims, fanouts [25, 10], 64 minibatches of 1024 targets, 64 KiB blocks.
+
+Printed (one JSON line): value = algorithmic bytes of sampling + gather per
+second (GB/s), with sampled edges/s, gathered feature GB/s and the fraction of
+the 8 TB/s HBM peak; the roofline of the row-copy kernel (HIP events on the
+prepare stream); the CPU oracle timed on a bounded sample of the same work.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0
+
+
+def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int) -> tuple:
+    """Bytes the method must move (exact counts from the batch statistics).
+
+    sampling, per hop: per request the node id, two offsets and the row-pointer
+    write; per sampled edge the index read and the column write; per new node
+    its id write.  gather: per output row the node-id write and the row write;
+    per distinct row one read."""
+    bs = 0
+    for R, S, U in zip(st["requests"], st["sampled"], st["new_nodes"]):
+        bs += R * (4 + 2 * offset_bytes + 4) + 8 * S + 4 * U
+    bg = st["rows"] * (4 + row_bytes) + st["distinct_rows"] * row_bytes
+    copy = st["rows"] * row_bytes + st["distinct_rows"] * row_bytes
+    return bs, bg, copy
+
+
+def cpu_baseline(w, cfg, steps_targets, budget_s=20.0):
+    """The plain oracle on the host: whole minibatches (sampling + gather) of the
+    benchmark's hyperbatches, in order, until about budget_s seconds of work."""
+    import oracle
+    o = oracle.Oracle(w["offsets64"], w["indices"])
+    fb = np.ascontiguousarray(w["features"]).view(np.uint8).reshape(w["num_nodes"], -1)
+    ob = 8 if w["offsets"].dtype == np.int64 else 4
+    rb = cfg.row_bytes
+    done = 0
+    total_bytes = 0
+    edges = 0
+    seen_rows = set()
+    t0 = time.perf_counter()
+    H = w["H"]
+    for s, tg in enumerate(steps_targets):
+        for j in range(H):
+            mb = o.minibatch(tg[j], cfg.fanouts, cfg.seed, s * H + j)
+            feats = oracle.gather(fb, mb.nodes)
+            del feats
+            L = len(cfg.fanouts)
+            for l in range(L):
+                R = int(mb.layer_sizes[l])
+                S = len(mb.col[l])
+                U = int(mb.layer_sizes[l + 1] - mb.layer_sizes[l])
+                total_bytes += R * (4 + 2 * ob + 4) + 8 * S + 4 * U
+                edges += S
+            total_bytes += len(mb.nodes) * (4 + rb)
+            new_distinct = [int(v) for v in mb.nodes if int(v) not in seen_rows]
+            seen_rows.update(new_distinct)
+            total_bytes += len(new_distinct) * rb
+            done += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return dict(value=total_bytes / dt / 1e9, unit="GB/s", cores=1, kind="oracle",
+                sample=f"{done} minibatches of {H} per hyperbatch (sampling + gather, single thread), "
+                       f"{dt:.1f} s", sampled_edges_per_s=edges / dt)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c3")
+    ap.add_argument("--H", type=int, default=None, help="minibatches per hyperbatch (default: the config's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              f"(the path shards by minibatch with no communication; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    root = os.path.dirname(os.path.abspath(__file__))
+    sys.path.insert(0, root)
+    import torch
+    import synth
+    import paper_2601_01473_amd as ag
+
+    cfg = synth.CONFIGS[args.config]
+    t0 = time.time()
+    w = synth.workload(cfg, H=args.H)
+    H, B = w["H"], w["B"]
+    print(f"# inputs ready in {time.time() - t0:.1f}s (E={len(w['indices'])})", file=sys.stderr, flush=True)
+    nsteps = args.steps + args.warmup
+    # distinct targets per step: consecutive slices of one permutation of the nodes
+    perm = synth.targets(cfg.num_nodes, min(cfg.num_nodes, nsteps * H * B), cfg.data_seed + 7)
+    step_targets = []
+    for s in range(nsteps):
+        a = (s * H * B) % (len(perm) - H * B + 1)
+        step_targets.append(perm[a:a + H * B].reshape(H, B))
+    dev_targets = [torch.from_numpy(np.ascontiguousarray(t)).cuda() for t in step_targets]
+
+    store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
+    store.set_profiling(True)
+    stream = torch.cuda.current_stream()
+    ob = 8 if w["offsets"].dtype == np.int64 else 4
+    rb = cfg.row_bytes
+
+    batch = None
+    for s in range(args.warmup):
+        batch = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=batch,
+                              stream=stream)
+    torch.cuda.synchronize()
+    print("# warm-up done", file=sys.stderr, flush=True)
+
+    tot_bytes = tot_sample = tot_gather = tot_copy_bytes = 0
+    edges = rows = 0
+    sample_ms = gather_ms = copy_ms = 0.0
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        s = args.warmup + k
+        batch = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=batch,
+                              stream=stream)
+        st = batch.stats()
+        bs, bg, bc = algorithmic_bytes(st, ob, rb)
+        tot_sample += bs
+        tot_gather += bg
+        tot_copy_bytes += bc
+        tot_bytes += bs + bg
+        edges += sum(st["sampled"])
+        rows += st["rows"]
+        sample_ms += st["sample_ms"]
+        gather_ms += st["gather_ms"]
+        copy_ms += st["copy_ms"]
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    K = args.steps
+    value = tot_bytes / elapsed / 1e9
+    copy_avg_ms = copy_ms / K
+    achieved = (tot_copy_bytes / K) / (copy_avg_ms * 1e-3) / 1e9
+    result = {
+        "metric": "sampled edges/s + gathered feature GB/s per hyperbatch (% of HBM peak)",
+        "value": round(value, 2),
+        "unit": "GB/s (algorithmic bytes of sampling + gather)",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / K * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic (seeded R-MAT graph, N(0,1) features, uniform distinct targets)",
+        "config": {"workload": cfg.describe(), "nodes": cfg.num_nodes, "edges": int(len(w["indices"])),
+                   "hyperbatch": H, "minibatch": B, "fanouts": list(cfg.fanouts),
+                   "block_bytes": cfg.block_bytes, "feature_dtype": cfg.feat_dtype, "dim": cfg.dim,
+                   "parallelism": "single GPU"},
+        "hbm_frac": round(value / HBM_PEAK_GBPS, 4),
+        "sampled_edges_per_s": round(edges / elapsed, 1),
+        "gathered_feature_GBps": round(rows * rb / elapsed / 1e9, 2),
+        "gather_phase_GBps": round(rows * rb / (gather_ms * 1e-3) / 1e9, 2) if gather_ms > 0 else None,
+        "phase_ms": {"sample": round(sample_ms / K, 4), "gather": round(gather_ms / K, 4),
+                     "copy_kernel": round(copy_avg_ms, 4)},
+        "per_step": {"algorithmic_bytes": tot_bytes // K, "sample_bytes": tot_sample // K,
+                     "gather_bytes": tot_gather // K, "rows": rows // K, "sampled_edges": edges // K},
+        "roofline": {"kernel": "k_gather (row copy)", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, cfg, step_targets[args.warmup:], args.cpu_budget)
+    print(json.dumps(result), flush=True)
+    batch.close()
+    store.close()
+
+
+if __name__ == "__main__":
+    main()

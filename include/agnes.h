@@ -1,0 +1,204 @@
+/*
+ * agnes.h -- C ABI of the MI355X (gfx950) hyperbatch GNN data-preparation library.
+ *
+ * Implements the data-preparation path of AGNES (arXiv 2601.01473): multi-hop
+ * neighbour sampling and feature-row gathering for H minibatches at once, with
+ * the requests of every minibatch bucketed by fixed-size storage block so that
+ * each block serves all the requests that fall in it (Sec. 3.3, Sec. 3.4(3),
+ * Alg. 1).  Blocks are pages resident in HBM.
+ *
+ * Conventions shared by every entry point:
+ *   - Return value: AGNES_OK or an error code; on error every out-handle is set
+ *     to NULL and agnes_last_error() describes the failure.  No exception, abort
+ *     or exit crosses this boundary.
+ *   - "host" pointers are ordinary CPU memory; "device" pointers are HIP device
+ *     memory of the current device.
+ *   - hip_stream is a hipStream_t passed as void* (NULL = the null stream).
+ *   - All node ids are int32 in [0, num_nodes); num_nodes < 2^31.
+ */
+#ifndef AGNES_H
+#define AGNES_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    AGNES_OK = 0,
+    AGNES_ERR_INVALID = 1,   /* bad argument or input content */
+    AGNES_ERR_NOMEM = 2,     /* device or host allocation failed */
+    AGNES_ERR_DEVICE = 3,    /* a HIP call failed; the HIP error string is in last-error */
+    AGNES_ERR_RANGE = 4,     /* a per-minibatch count or a total exceeds 2^31 - 1 */
+    AGNES_ERR_INTERNAL = 5
+} agnes_status;
+
+typedef enum {
+    AGNES_INT32 = 0,
+    AGNES_INT64 = 1,
+    AGNES_FLOAT32 = 2,
+    AGNES_FLOAT16 = 3,
+    AGNES_BFLOAT16 = 4
+} agnes_dtype;
+
+typedef struct agnes_store agnes_store;   /* opaque: HBM-resident topology/feature blocks */
+typedef struct agnes_batch agnes_batch;   /* opaque: device outputs of one hyperbatch */
+
+/* Graph topology in CSR form with source rows (host memory, read only).
+ * offsets: num_nodes+1 entries of offsets_dtype (AGNES_INT32 or AGNES_INT64),
+ *          offsets[0] = 0, nondecreasing, offsets[num_nodes] = num_edges.
+ * indices: num_edges int32 neighbour ids, each in [0, num_nodes).  A row's order
+ *          is the order in which its neighbours are numbered (positions). */
+typedef struct {
+    int64_t num_nodes;
+    int64_t num_edges;
+    agnes_dtype offsets_dtype;
+    const void* offsets;
+    const int32_t* indices;
+} agnes_csr;
+
+/* Node features (host memory, read only): num_nodes rows of dim elements,
+ * row-major.  The rows are moved as opaque bytes: row_bytes = dim * size(dtype),
+ * which must be a multiple of 4. */
+typedef struct {
+    const void* data;
+    int64_t dim;
+    agnes_dtype dtype;   /* AGNES_FLOAT32, AGNES_FLOAT16 or AGNES_BFLOAT16 */
+} agnes_features;
+
+/*
+ * Build the block store (Sec. 3.2(1) storage layer; Sec. 3.2(2) object index
+ * table).  The CSR index array is cut into topology blocks of block_bytes/4
+ * edges; a node's object is its adjacency list and its home block is the block
+ * holding its first edge, so objects sit in ascending node order and a long list
+ * continues into the following blocks.  The feature matrix is cut into feature
+ * blocks of floor(block_bytes / row_bytes) rows.  The object index table keeps,
+ * per topology block, the first and last node whose home it is.
+ *
+ * csr, feat: host inputs, copied into library-owned HBM; the caller may free
+ *            them once the call returns.
+ * block_bytes: power of two in [16, 2^24] and >= row_bytes.
+ * hip_stream: stream used for the uploads; the call returns after they finish.
+ * out: receives the store; release it with agnes_free().
+ * Errors: INVALID (null pointer, non-monotone offsets, offsets[N] != E, index
+ * out of range, num_nodes >= 2^31, bad dtype, row_bytes % 4 != 0, bad
+ * block_bytes), NOMEM, DEVICE.
+ */
+agnes_status agnes_build_blocks(const agnes_csr* csr, const agnes_features* feat,
+                                uint64_t block_bytes, void* hip_stream, agnes_store** out);
+
+/*
+ * Prepare one hyperbatch (Alg. 1): for each of the H minibatches (row j of
+ * targets, global minibatch index m = mb_base + j) run L hops of neighbour
+ * sampling, then gather the feature rows of every sampled node.
+ *
+ * Hop l (fanout f_l = fanouts[l], l = 0 nearest the targets): every node already
+ * in minibatch j is a request; it receives min(deg, f_l) distinct neighbours,
+ * drawn uniformly without replacement by Floyd's algorithm from Philox4x64-10
+ * words at key (seed, 0), counter (i >> 2, v, m, l), word i taking lane i & 3,
+ * integer draws floor(w * n / 2^64), listed in ascending edge position.  The
+ * minibatch's node list grows by the sampled neighbours not yet in it, in
+ * ascending global id (targets first, in the given order).  Hop l is emitted as
+ * a CSR block: one row per node present before the hop, columns in local ids.
+ * Requests are served block by block: the frontier of all minibatches is
+ * bucketed by topology block (the bucket matrix Bck of Sec. 3.4(3)) and each
+ * block's requests are sampled together; the gather is bucketed by feature
+ * block the same way (Alg. 1, gathering loop).  Results depend only on
+ * (store, targets, fanouts, seed, mb_base), not on the bucketing, the launch
+ * geometry or how minibatches are grouped into hyperbatches.
+ *
+ * targets: DEVICE int32 [H][B]; distinct within each row, each in [0, N).
+ * H in [1, 4096], B >= 1, L in [1, AGNES_MAX_LAYERS], fanouts: host int32 [L],
+ * each in [0, 1024].  seed: any 64-bit value.  mb_base >= 0.
+ * out: if *out is NULL a new batch is created; if it holds a batch previously
+ *      returned for the same store, that batch's device buffers are reused (and
+ *      grown when needed) and its previous contents are overwritten.
+ * The call enqueues on hip_stream and returns when the outputs are complete.
+ * One call at a time per store: the store owns the scratch workspace.
+ * Errors: INVALID (bad sizes, target out of range or duplicated within a
+ * minibatch), RANGE (a minibatch with >= 2^31 nodes or edges), NOMEM, DEVICE.
+ * On error *out is NULL and a batch passed in is released.
+ */
+agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets, int32_t H,
+                                      int32_t B, const int32_t* fanouts, int32_t L,
+                                      uint64_t seed, int64_t mb_base, void* hip_stream,
+                                      agnes_batch** out);
+
+#define AGNES_MAX_LAYERS 8
+
+/* Read-only view of a batch.  Host arrays stay valid until the batch is freed
+ * or reused; device arrays likewise.
+ *   node_off[H+1]: minibatch j owns nodes[node_off[j] .. node_off[j+1]) and the
+ *                  same rows of features.
+ *   layer_sizes[H*(L+1)]: |D_0| = B, then the node count after each hop.
+ *   nodes (device int32): global ids in local-id order, minibatch-major.
+ *   rp_off[l][H+1], row_ptr[l] (device int32): hop l's row pointers of minibatch
+ *                  j are row_ptr[l][rp_off[l][j] .. +layer_sizes[j][l]+1), from 0.
+ *   col_off[l][H+1], col[l] (device int32): hop l's columns of minibatch j are
+ *                  col[l][col_off[l][j] .. col_off[l][j+1]), local ids.
+ *   features (device): [node_off[H]][row_bytes] gathered rows. */
+typedef struct {
+    int32_t H, L;
+    int64_t row_bytes;
+    const int64_t* node_off;
+    const int32_t* layer_sizes;
+    const int32_t* nodes;
+    const int64_t* rp_off[AGNES_MAX_LAYERS];
+    const int32_t* row_ptr[AGNES_MAX_LAYERS];
+    const int64_t* col_off[AGNES_MAX_LAYERS];
+    const int32_t* col[AGNES_MAX_LAYERS];
+    const void* features;
+} agnes_batch_view;
+
+agnes_status agnes_batch_view_get(const agnes_batch* batch, agnes_batch_view* out);
+
+/* Exact integer statistics of a prepared hyperbatch (per hop l: requests R_l,
+ * sampled edges S_l, new nodes U_l, non-empty topology-block rows of Bck T_l;
+ * gathered rows sum |N_j|, distinct rows, non-empty feature-block rows) and the
+ * device time of each phase when profiling is on (else -1). */
+typedef struct {
+    int32_t L;
+    int64_t requests[AGNES_MAX_LAYERS];
+    int64_t sampled[AGNES_MAX_LAYERS];
+    int64_t new_nodes[AGNES_MAX_LAYERS];
+    int64_t topo_blocks[AGNES_MAX_LAYERS];
+    int64_t rows;
+    int64_t distinct_rows;
+    int64_t feat_blocks;
+    float sample_ms;     /* all hops: bucketing, sampling, dedupe, relabel */
+    float gather_ms;     /* gather bucketing and row copy */
+    float copy_ms;       /* the row-copy kernel alone */
+} agnes_stats;
+
+agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);
+
+/* Store options.  AGNES_OPT_PROFILE: 1 = record HIP events around the phases of
+ * every prepare (reported by agnes_batch_stats), 0 = off (default). */
+typedef enum { AGNES_OPT_PROFILE = 1 } agnes_option;
+agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value);
+
+/* Store facts: out[0] num_nodes, out[1] num_edges, out[2] topology blocks,
+ * out[3] edges per topology block, out[4] feature blocks, out[5] rows per
+ * feature block, out[6] row_bytes, out[7] device bytes held by the store. */
+agnes_status agnes_store_info(const agnes_store* store, int64_t out[8]);
+
+/* Object index table (Sec. 3.2(2)): copies to host first_node[b] and
+ * last_node[b] (int32, -1 for a block that no object starts in) for every
+ * topology block b; each array needs agnes_store_info()[2] entries. */
+agnes_status agnes_store_object_table(const agnes_store* store, int32_t* first_node,
+                                      int32_t* last_node);
+
+/* Release a store or a batch (NULL is a no-op).  A store must outlive the
+ * prepares running on it. */
+void agnes_free(void* handle);
+
+/* Message of the last failure on the calling thread ("" if none); valid until
+ * the next call on that thread. */
+const char* agnes_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AGNES_H */

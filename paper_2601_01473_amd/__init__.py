@@ -1,0 +1,177 @@
+"""MI355X (gfx950) hyperbatch GNN data preparation (AGNES, arXiv 2601.01473).
+
+The work runs in libagnes.so (HIP kernels behind the C ABI of include/agnes.h).
+This package marshals arguments: numpy arrays in, torch CUDA tensors (device
+memory, streams) for the targets, and copies of the outputs back to numpy.
+
+    store = Store(offsets, indices, features, block_bytes=65536)
+    batch = store.prepare(targets_cuda_int32_HxB, fanouts=[25, 10], seed=0)
+    out = batch.to_host()          # per-minibatch nodes, per-hop CSR, features
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+
+from . import _binding as B
+from ._binding import AgnesError, agnes_batch_stats, agnes_batch_view_get, agnes_build_blocks  # noqa: F401
+from ._binding import agnes_free, agnes_hyperbatch_prepare, agnes_last_error  # noqa: F401
+from ._binding import agnes_store_info, agnes_store_object_table, agnes_store_set_option  # noqa: F401
+
+_FEAT_DTYPES = {np.dtype(np.float32): B.AGNES_FLOAT32, np.dtype(np.float16): B.AGNES_FLOAT16}
+
+_hip = None
+
+
+def _hiprt():
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so.7")
+        _hip.hipMemcpy.restype = ctypes.c_int
+        _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+    return _hip
+
+
+def device_to_host(ptr: int, count: int, dtype) -> np.ndarray:
+    """Copy `count` elements of `dtype` from device memory to a new numpy array."""
+    out = np.empty(count, dtype=dtype)
+    if count:
+        rc = _hiprt().hipMemcpy(out.ctypes.data, ctypes.c_void_p(ptr), out.nbytes, 2)
+        if rc != 0:
+            raise RuntimeError("hipMemcpy device->host failed with %d" % rc)
+    return out
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else 0
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+class Store:
+    """HBM-resident topology and feature blocks (agnes_build_blocks)."""
+
+    def __init__(self, offsets, indices, features, block_bytes: int, feat_dtype: str | None = None,
+                 stream=None):
+        off = np.ascontiguousarray(offsets)
+        if off.dtype not in (np.int32, np.int64):
+            raise TypeError("offsets must be int32 or int64")
+        idx = np.ascontiguousarray(indices, dtype=np.int32)
+        feat = np.ascontiguousarray(features)
+        if feat.ndim != 2:
+            raise ValueError("features must be 2-D [num_nodes, dim]")
+        if feat_dtype == "bfloat16" or (feat_dtype is None and feat.dtype == np.uint16):
+            fdt = B.AGNES_BFLOAT16
+        elif feat.dtype in _FEAT_DTYPES:
+            fdt = _FEAT_DTYPES[feat.dtype]
+        else:
+            raise TypeError("features must be float32, float16 or bfloat16 (as uint16)")
+        csr = B.agnes_csr(len(off) - 1, len(idx), B.AGNES_INT64 if off.dtype == np.int64 else B.AGNES_INT32,
+                          off.ctypes.data, idx.ctypes.data if len(idx) else None)
+        fs = B.agnes_features(feat.ctypes.data, feat.shape[1], fdt)
+        self.handle = agnes_build_blocks(csr, fs, block_bytes, _stream_handle(stream))
+        self.num_nodes = len(off) - 1
+        self.row_bytes = feat.shape[1] * feat.itemsize
+        self.block_bytes = block_bytes
+
+    def info(self) -> dict:
+        v = agnes_store_info(self.handle)
+        keys = ["num_nodes", "num_edges", "topo_blocks", "edges_per_block", "feat_blocks",
+                "rows_per_block", "row_bytes", "device_bytes"]
+        return dict(zip(keys, v))
+
+    def object_table(self):
+        nblk = self.info()["topo_blocks"]
+        first = np.empty(nblk, np.int32)
+        last = np.empty(nblk, np.int32)
+        agnes_store_object_table(self.handle, first.ctypes.data, last.ctypes.data)
+        return first, last
+
+    def set_profiling(self, on: bool) -> None:
+        agnes_store_set_option(self.handle, B.AGNES_OPT_PROFILE, 1 if on else 0)
+
+    def prepare(self, targets: torch.Tensor, fanouts, seed: int = 0, mb_base: int = 0,
+                batch: "Batch | None" = None, stream=None) -> "Batch":
+        """One hyperbatch: targets is a CUDA int32 tensor [H, B]."""
+        if not (isinstance(targets, torch.Tensor) and targets.is_cuda and targets.dtype == torch.int32):
+            raise TypeError("targets must be a CUDA int32 tensor [H, B]")
+        if targets.dim() != 2:
+            raise ValueError("targets must be [H, B]")
+        t = targets.contiguous()
+        H, Bsz = t.shape
+        fan = (ctypes.c_int32 * len(fanouts))(*[int(f) for f in fanouts])
+        prev = batch.handle if batch is not None else None
+        if batch is not None:
+            batch.handle = None          # ownership passes to the call (released on error)
+        h = agnes_hyperbatch_prepare(self.handle, t.data_ptr(), H, Bsz, fan, len(fanouts), seed,
+                                     mb_base, _stream_handle(stream), prev)
+        if batch is None:
+            batch = Batch(self)
+        batch.handle = h
+        return batch
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            agnes_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        self.close()
+
+
+class Batch:
+    """Device outputs of one hyperbatch (agnes_batch)."""
+
+    def __init__(self, store: Store):
+        self.store = store
+        self.handle = None
+
+    def stats(self) -> dict:
+        s = agnes_batch_stats(self.handle)
+        L = s.L
+        return dict(requests=list(s.requests[:L]), sampled=list(s.sampled[:L]),
+                    new_nodes=list(s.new_nodes[:L]), topo_blocks=list(s.topo_blocks[:L]),
+                    rows=s.rows, distinct_rows=s.distinct_rows, feat_blocks=s.feat_blocks,
+                    sample_ms=s.sample_ms, gather_ms=s.gather_ms, copy_ms=s.copy_ms)
+
+    def view(self) -> B.agnes_batch_view:
+        return agnes_batch_view_get(self.handle)
+
+    def to_host(self, minibatches=None, features: bool = True) -> list:
+        """Per-minibatch host copies: dict(nodes, layer_sizes, row_ptr[l], col[l], features)."""
+        v = self.view()
+        H, L = v.H, v.L
+        node_off = np.ctypeslib.as_array(v.node_off, shape=(H + 1,)).copy()
+        lsz = np.ctypeslib.as_array(v.layer_sizes, shape=(H * (L + 1),)).reshape(H, L + 1).copy()
+        rows = int(node_off[H])
+        nodes = device_to_host(v.nodes, rows, np.int32)
+        rp, col, rpo, colo = [], [], [], []
+        for l in range(L):
+            ro = np.ctypeslib.as_array(v.rp_off[l], shape=(H + 1,)).copy()
+            co = np.ctypeslib.as_array(v.col_off[l], shape=(H + 1,)).copy()
+            rpo.append(ro)
+            colo.append(co)
+            rp.append(device_to_host(v.row_ptr[l], int(ro[H]), np.int32))
+            col.append(device_to_host(v.col[l], int(co[H]), np.int32))
+        rb = v.row_bytes
+        out = []
+        mbs = range(H) if minibatches is None else minibatches
+        for j in mbs:
+            a, b = int(node_off[j]), int(node_off[j + 1])
+            d = dict(nodes=nodes[a:b], layer_sizes=lsz[j],
+                     row_ptr=[rp[l][rpo[l][j]:rpo[l][j + 1]] for l in range(L)],
+                     col=[col[l][colo[l][j]:colo[l][j + 1]] for l in range(L)])
+            if features:
+                d["features"] = device_to_host(v.features + a * rb, (b - a) * rb, np.uint8).reshape(b - a, rb)
+            out.append(d)
+        return out
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            agnes_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        self.close()

@@ -1,0 +1,189 @@
+// The C ABI (include/agnes.h): argument checks, error mapping and handle
+// management around the store (store.hip) and the pipeline (pipeline.hip).
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "runtime.hpp"
+
+namespace agnes {
+
+static thread_local std::string g_last_error;
+
+void set_last_error(const std::string& msg) { g_last_error = msg; }
+void clear_last_error() { g_last_error.clear(); }
+
+template <typename F>
+static agnes_status guarded(F&& f) {
+    try {
+        clear_last_error();
+        f();
+        return AGNES_OK;
+    } catch (const Error& e) {
+        set_last_error(e.msg);
+        return e.code;
+    } catch (const std::bad_alloc&) {
+        set_last_error("host allocation failed");
+        return AGNES_ERR_NOMEM;
+    } catch (const std::exception& e) {
+        set_last_error(e.what());
+        return AGNES_ERR_INTERNAL;
+    } catch (...) {
+        set_last_error("unknown internal error");
+        return AGNES_ERR_INTERNAL;
+    }
+}
+
+static Store* as_store(void* p) {
+    Store* s = static_cast<Store*>(p);
+    AGNES_REQUIRE(s && s->magic == kStoreMagic, AGNES_ERR_INVALID, "not a store handle");
+    return s;
+}
+
+}  // namespace agnes
+
+using namespace agnes;
+
+extern "C" {
+
+agnes_status agnes_build_blocks(const agnes_csr* csr, const agnes_features* feat,
+                                uint64_t block_bytes, void* hip_stream, agnes_store** out) {
+    if (out) *out = nullptr;
+    return guarded([&] {
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        Store* s = build_store(csr, feat, block_bytes, (hipStream_t)hip_stream);
+        *out = reinterpret_cast<agnes_store*>(s);
+    });
+}
+
+agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets, int32_t H,
+                                      int32_t B, const int32_t* fanouts, int32_t L,
+                                      uint64_t seed, int64_t mb_base, void* hip_stream,
+                                      agnes_batch** out) {
+    Batch* reuse = nullptr;
+    if (out && *out) reuse = reinterpret_cast<Batch*>(*out);
+    if (out) *out = nullptr;
+    Store* s = nullptr;
+    agnes_status rc = guarded([&] {
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        s = as_store(store);
+        AGNES_REQUIRE(!reuse || (reuse->magic == kBatchMagic && reuse->store == s), AGNES_ERR_INVALID,
+                      "the batch passed in was not produced by this store");
+        AGNES_REQUIRE(targets, AGNES_ERR_INVALID, "targets must not be NULL");
+        AGNES_REQUIRE(H >= 1 && H <= 4096, AGNES_ERR_INVALID, "H must be in [1, 4096]");
+        AGNES_REQUIRE(B >= 1, AGNES_ERR_INVALID, "B must be >= 1");
+        AGNES_REQUIRE((int64_t)H * B < 0x7FFFFFFFll, AGNES_ERR_RANGE, "H * B must be < 2^31");
+        AGNES_REQUIRE(L >= 1 && L <= AGNES_MAX_LAYERS, AGNES_ERR_INVALID, "L must be in [1, 8]");
+        AGNES_REQUIRE(fanouts, AGNES_ERR_INVALID, "fanouts must not be NULL");
+        for (int l = 0; l < L; l++)
+            AGNES_REQUIRE(fanouts[l] >= 0 && fanouts[l] <= 1024, AGNES_ERR_INVALID, "fanouts must be in [0, 1024]");
+        AGNES_REQUIRE(mb_base >= 0, AGNES_ERR_INVALID, "mb_base must be >= 0");
+        AGNES_REQUIRE(!s->busy, AGNES_ERR_INVALID, "another prepare is running on this store");
+        int dev = 0;
+        AGNES_CHECK_HIP(hipGetDevice(&dev));
+        AGNES_REQUIRE(dev == s->device, AGNES_ERR_INVALID, "the current device is not the store's device");
+        Batch* b = reuse ? reuse : new Batch();
+        reuse = b;
+        s->busy = true;
+        try {
+            prepare_hyperbatch(*s, *b, targets, H, B, fanouts, L, seed, mb_base, (hipStream_t)hip_stream);
+        } catch (...) {
+            s->busy = false;
+            throw;
+        }
+        s->busy = false;
+        *out = reinterpret_cast<agnes_batch*>(b);
+    });
+    if (rc != AGNES_OK && reuse) {
+        if (reuse->magic == kBatchMagic) {
+            reuse->magic = 0;
+            delete reuse;
+        }
+    }
+    return rc;
+}
+
+agnes_status agnes_batch_view_get(const agnes_batch* batch, agnes_batch_view* out) {
+    return guarded([&] {
+        const Batch* b = reinterpret_cast<const Batch*>(batch);
+        AGNES_REQUIRE(b && b->magic == kBatchMagic, AGNES_ERR_INVALID, "not a batch handle");
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        memset(out, 0, sizeof(*out));
+        out->H = b->H;
+        out->L = b->L;
+        out->row_bytes = b->store->row_bytes;
+        out->node_off = b->node_off.data();
+        out->layer_sizes = b->layer_sizes.data();
+        out->nodes = b->nodes.as<int32_t>();
+        for (int l = 0; l < b->L; l++) {
+            out->rp_off[l] = b->rp_off[l].data();
+            out->row_ptr[l] = b->row_ptr[l].as<int32_t>();
+            out->col_off[l] = b->col_off[l].data();
+            out->col[l] = b->col[l].as<int32_t>();
+        }
+        out->features = b->features.ptr;
+    });
+}
+
+agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out) {
+    return guarded([&] {
+        const Batch* b = reinterpret_cast<const Batch*>(batch);
+        AGNES_REQUIRE(b && b->magic == kBatchMagic, AGNES_ERR_INVALID, "not a batch handle");
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        *out = b->stats;
+    });
+}
+
+agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value) {
+    return guarded([&] {
+        Store* s = as_store(store);
+        AGNES_REQUIRE(opt == AGNES_OPT_PROFILE, AGNES_ERR_INVALID, "unknown option");
+        s->profile = value ? 1 : 0;
+    });
+}
+
+agnes_status agnes_store_info(const agnes_store* store, int64_t out[8]) {
+    return guarded([&] {
+        Store* s = as_store((void*)store);
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        out[0] = s->num_nodes;
+        out[1] = s->num_edges;
+        out[2] = s->nblk;
+        out[3] = s->e_blk;
+        out[4] = s->nfblk;
+        out[5] = s->rpb;
+        out[6] = s->row_bytes;
+        out[7] = (int64_t)(s->offsets.bytes + s->indices.bytes + s->features.bytes +
+                           s->first_node.bytes + s->last_node.bytes);
+    });
+}
+
+agnes_status agnes_store_object_table(const agnes_store* store, int32_t* first_node,
+                                      int32_t* last_node) {
+    return guarded([&] {
+        Store* s = as_store((void*)store);
+        AGNES_REQUIRE(first_node && last_node, AGNES_ERR_INVALID, "outputs must not be NULL");
+        AGNES_CHECK_HIP(hipMemcpy(first_node, s->first_node.ptr, (size_t)s->nblk * 4, hipMemcpyDeviceToHost));
+        AGNES_CHECK_HIP(hipMemcpy(last_node, s->last_node.ptr, (size_t)s->nblk * 4, hipMemcpyDeviceToHost));
+    });
+}
+
+void agnes_free(void* handle) {
+    if (!handle) return;
+    uint32_t magic = *static_cast<uint32_t*>(handle);
+    if (magic == kStoreMagic) {
+        Store* s = static_cast<Store*>(handle);
+        for (auto& e : s->ws.ev)
+            if (e) (void)hipEventDestroy(e);
+        s->magic = 0;
+        delete s;
+    } else if (magic == kBatchMagic) {
+        Batch* b = static_cast<Batch*>(handle);
+        b->magic = 0;
+        delete b;
+    }
+}
+
+const char* agnes_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,172 @@
+// Host runtime types of the library: error state, device buffers, the block
+// store, the per-store scratch workspace and the batch (outputs of a prepare).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/agnes.h"
+
+namespace agnes {
+
+// ----------------------------------------------------------------- errors
+
+struct Error {
+    agnes_status code;
+    std::string msg;
+};
+
+void set_last_error(const std::string& msg);
+void clear_last_error();
+
+#define AGNES_CHECK_HIP(expr)                                                               \
+    do {                                                                                    \
+        hipError_t e_ = (expr);                                                             \
+        if (e_ != hipSuccess)                                                               \
+            throw ::agnes::Error{e_ == hipErrorOutOfMemory ? AGNES_ERR_NOMEM : AGNES_ERR_DEVICE, \
+                                 std::string(#expr) + ": " + hipGetErrorString(e_)};        \
+    } while (0)
+
+#define AGNES_REQUIRE(cond, code, msg)                                                      \
+    do {                                                                                    \
+        if (!(cond)) throw ::agnes::Error{(code), (msg)};                                   \
+    } while (0)
+
+// ----------------------------------------------------------------- device buffer
+
+// An owned device allocation that only grows (contents are not preserved).
+struct DevBuf {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+    ~DevBuf() { release(); }
+    void release() {
+        if (ptr) (void)hipFree(ptr);
+        ptr = nullptr;
+        bytes = 0;
+    }
+    // Make room for `need` bytes; returns true when a new allocation was made.
+    bool reserve(size_t need) {
+        if (need <= bytes && ptr) return false;
+        release();
+        size_t b = need ? need : 256;
+        AGNES_CHECK_HIP(hipMalloc(&ptr, b));
+        bytes = b;
+        return true;
+    }
+    template <typename T> T* as() const { return static_cast<T*>(ptr); }
+};
+
+constexpr uint32_t kStoreMagic = 0x53454E47u;   // "GNES"
+constexpr uint32_t kBatchMagic = 0x42454E47u;
+
+// Counters and statistics kept in device memory during a prepare.
+struct Ctl {
+    int64_t R;          // requests of the current hop
+    int64_t S;          // sampled edges of the current hop
+    int64_t n_new;      // new nodes of the current hop (all minibatches)
+    int64_t rows;       // gathered rows (sum of |N_j|)
+    int64_t err;        // bit 0: target out of range, bit 1: duplicate target, bit 2: capacity
+    int64_t distinct;   // distinct gathered rows
+    int64_t fblocks;    // non-empty feature-block rows
+    int64_t nblk;       // topology blocks (element count of the Bck row scan)
+    int64_t nfblk;      // feature blocks
+    int64_t requests[AGNES_MAX_LAYERS];
+    int64_t sampled[AGNES_MAX_LAYERS];
+    int64_t new_nodes[AGNES_MAX_LAYERS];
+    int64_t topo_blocks[AGNES_MAX_LAYERS];
+};
+
+// Scratch memory of a prepare, owned by the store and grown on demand.
+struct Workspace {
+    DevBuf ht_words, ht_vals;         // (minibatch, node) -> local id
+    int ht_log2 = 0;
+    uint64_t gen = 0;                 // generation tag of the live hash entries
+    DevBuf nodes;                     // [H][capN] node lists in local-id order
+    DevBuf size, newcnt, lsz, ecount; // per minibatch
+    DevBuf req_off, mb_off;           // [H+1] int64
+    DevBuf ctl;                       // Ctl
+    DevBuf cnt, bkey, bck, e_off;     // per request
+    DevBuf bcnt, bcur;                // per topology block (+1)
+    DevBuf cg, eslot;                 // per sampled edge
+    DevBuf nkeys, nvals, nkeys2, nvals2;   // new nodes and their sort buffers
+    DevBuf rs_hist, rs_dtot;          // radix-sort histograms
+    DevBuf scan_part;                 // scan partial sums
+    DevBuf gkey, gent;                // per gathered row
+    DevBuf fbcnt, fbcur;              // per feature block (+1)
+    DevBuf dbits;                     // one bit per node
+    hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+};
+
+struct Store {
+    uint32_t magic = kStoreMagic;
+    int device = 0;
+    int64_t num_nodes = 0, num_edges = 0;
+    int offsets64 = 0;                // 1: int64 offsets, 0: int32
+    int64_t e_blk = 0;                // edges per topology block
+    int e_blk_log2 = 0;
+    int64_t nblk = 0;                 // topology blocks
+    int64_t row_bytes = 0;
+    int64_t rpb = 0;                  // feature rows per block
+    int64_t nfblk = 0;                // feature blocks
+    int64_t block_bytes = 0;
+    int64_t max_degree = 0;
+    int node_bits = 0;                // bits of a node id (ceil log2 num_nodes)
+    DevBuf offsets, indices, features, first_node, last_node;
+    Workspace ws;
+    int profile = 0;
+    bool busy = false;
+};
+
+struct Batch {
+    uint32_t magic = kBatchMagic;
+    const Store* store = nullptr;
+    int32_t H = 0, B = 0, L = 0;
+    std::vector<int64_t> node_off;
+    std::vector<int32_t> layer_sizes;
+    std::vector<int64_t> rp_off[AGNES_MAX_LAYERS];
+    std::vector<int64_t> col_off[AGNES_MAX_LAYERS];
+    DevBuf nodes, features;
+    DevBuf row_ptr[AGNES_MAX_LAYERS], col[AGNES_MAX_LAYERS];
+    agnes_stats stats{};
+};
+
+// Pipeline entry points (pipeline.hip).
+void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
+                        const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
+                        hipStream_t stream);
+// Store construction (store.hip).
+Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t block_bytes,
+                   hipStream_t stream);
+
+// ----------------------------------------------------------------- primitives (prims.hip)
+
+// Exclusive scan of n int32 counts (n read from *n_dev, at most n_max) into
+// out[0..n] int64; out[n] = total, also stored to *total_dev when not null.
+void scan_counts(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
+                 int64_t* total_dev, int64_t* partials, hipStream_t st);
+// Same for int64 counts.
+void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
+                   int64_t* total_dev, int64_t* partials, hipStream_t st);
+int64_t scan_partials_needed();
+
+// Stable LSD radix sort of (key, value) pairs on key bits [0, bits); n read from
+// *n_dev (at most n_max).  The result is left in keys/vals.
+void radix_sort_pairs(uint64_t* keys, uint32_t* vals, uint64_t* keys_tmp, uint32_t* vals_tmp,
+                      const int64_t* n_dev, int64_t n_max, int bits, int64_t* hist,
+                      int64_t* dtot, hipStream_t st);
+int64_t radix_hist_entries();
+
+// Fill n 32-bit words with a value (a kernel, so that it can be captured in a graph).
+void fill_u32(void* p, uint32_t value, int64_t n, hipStream_t st);
+
+inline int grid_for(int64_t n, int max_blocks = 4096) {
+    int64_t g = (n + 255) / 256;
+    if (g < 1) g = 1;
+    if (g > max_blocks) g = max_blocks;
+    return (int)g;
+}
+
+}  // namespace agnes

@@ -1,0 +1,198 @@
+"""GPU parity on small inputs: the HIP library against the CPU oracle, element by
+element (node ids, per-hop CSR, feature bytes) and the exact statistics.
+
+Sizes span many blocks, several minibatches and ragged tails; cases cover int32
+and int64 offsets, fp32/fp16/bf16 and 4-byte-multiple rows, fanout 0, fanouts
+above every degree (take-all rows), fanouts above 32 (the sampler's memory
+path), isolated targets, multigraph rows and batch reuse with growing shapes.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.graphs import distinct_targets, features, hand_graph, random_graph
+from tests.parity import compare_minibatch, feature_bytes, log
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def agnes():
+    import paper_2601_01473_amd as ag
+    return ag
+
+
+def run_case(ag, off, idx, feat, tg, fan, seed, mb_base, block_bytes, batch=None, check_stats=True,
+             tag=""):
+    store = ag.Store(off, idx, feat, block_bytes)
+    t = torch.from_numpy(np.ascontiguousarray(tg, dtype=np.int32)).cuda()
+    b = store.prepare(t, fan, seed=seed, mb_base=mb_base, batch=batch)
+    got = b.to_host()
+    o = oracle.Oracle(off, idx)
+    ref = o.hyperbatch(tg, fan, seed, mb_base)
+    fb = feature_bytes(feat)
+    for j in range(tg.shape[0]):
+        compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=(tag, j))
+    if check_stats:
+        st = b.stats()
+        want = oracle.hyperbatch_stats(off, block_bytes, fb.shape[1], ref, len(fan))
+        for k, v in want.items():
+            assert st[k] == v, (tag, k, st[k], v)
+    return store, b
+
+
+def test_hand_example_on_gpu(agnes):
+    off, idx = hand_graph()
+    feat = features(6, 4, 0)
+    store, b = run_case(agnes, off, idx, feat, np.array([[2, 5]]), [3, 3], 0, 0, 16, tag="hand")
+    g = b.to_host()[0]
+    assert g["nodes"].tolist() == [2, 5, 0, 1, 4, 3]
+    assert g["col"][1].tolist() == [2, 4, 1, 3, 3, 0, 5, 1]
+    first, last = store.object_table()
+    # 4 edges per block: homes 0,0,0,1,1,1 -> block 0 holds nodes 0..2, block 1 nodes 3..5
+    assert first.tolist() == [0, 3] and last.tolist() == [2, 5]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_graphs_int64(agnes, seed):
+    off, idx = random_graph(3000, 14, seed, hubs=4, hub_deg=900)
+    H, B = 5, 37
+    tg = distinct_targets(3000, H, B, seed + 10)
+    feat = features(3000, 20, seed)                     # 80-byte rows: 16-byte lanes
+    log("random int64", seed)
+    run_case(agnes, off, idx, feat, tg, [7, 3, 2], seed=seed, mb_base=3 * seed, block_bytes=256,
+             tag=("rand64", seed))
+
+
+def test_random_graph_int32_offsets_fp16(agnes):
+    off, idx = random_graph(2000, 9, 7, hubs=3, hub_deg=700)
+    tg = distinct_targets(2000, 3, 64, 1)
+    feat = features(2000, 24, 2, np.float16)            # 48-byte rows
+    run_case(agnes, off.astype(np.int32), idx, feat, tg, [10, 4], 5, 0, 64, tag="int32-fp16")
+
+
+def test_rows_not_multiple_of_16_bytes(agnes):
+    off, idx = random_graph(1500, 6, 3)
+    tg = distinct_targets(1500, 2, 50, 2)
+    feat = features(1500, 3, 1)                         # 12-byte rows: 4-byte lanes
+    run_case(agnes, off, idx, feat, tg, [5, 5], 1, 0, 32, tag="rows12")
+
+
+def test_bfloat16_rows(agnes):
+    off, idx = random_graph(1000, 8, 4)
+    tg = distinct_targets(1000, 4, 30, 3)
+    rng = np.random.default_rng(0)
+    feat = rng.integers(0, 65536, size=(1000, 64), dtype=np.uint16)   # arbitrary bf16 bit patterns
+    store = agnes.Store(off, idx, feat, 4096, feat_dtype="bfloat16")
+    t = torch.from_numpy(tg).cuda()
+    got = store.prepare(t, [6, 2], seed=9).to_host()
+    ref = oracle.Oracle(off, idx).hyperbatch(tg, [6, 2], 9, 0)
+    for j in range(4):
+        compare_minibatch(got[j], ref[j], oracle.gather(feature_bytes(feat), ref[j].nodes), tag=("bf16", j))
+
+
+def test_zero_fanout_and_take_all(agnes):
+    off, idx = random_graph(800, 5, 5, hubs=1, hub_deg=30)
+    tg = distinct_targets(800, 3, 20, 4)
+    feat = features(800, 8, 3)
+    run_case(agnes, off, idx, feat, tg, [0, 40, 0], 2, 0, 128, tag="fan0-all")
+
+
+def test_large_fanout_memory_path(agnes):
+    off, idx = random_graph(1200, 60, 6, hubs=5, hub_deg=1000)
+    tg = distinct_targets(1200, 2, 40, 5)
+    feat = features(1200, 4, 4)
+    run_case(agnes, off, idx, feat, tg, [100, 33], 3, 1, 1024, tag="fanout>32")
+
+
+@pytest.mark.parametrize("fan", [[1], [4, 4, 4, 4], [3, 8, 16, 32]])
+def test_fanout_register_paths(agnes, fan):
+    off, idx = random_graph(2500, 30, 8, hubs=3, hub_deg=2000)
+    tg = distinct_targets(2500, 3, 25, 6)
+    feat = features(2500, 4, 5)
+    run_case(agnes, off, idx, feat, tg, fan, 4, 7, 512, tag=("regs", tuple(fan)))
+
+
+def test_multigraph_rows(agnes):
+    off, idx = random_graph(600, 12, 2, multi=True)
+    tg = distinct_targets(600, 3, 15, 7)
+    feat = features(600, 4, 6)
+    run_case(agnes, off, idx, feat, tg, [5, 3], 8, 0, 64, tag="multi")
+
+
+def test_isolated_and_single_node_graph(agnes):
+    off = np.zeros(11, np.int64)
+    idx = np.zeros(0, np.int32)
+    feat = features(10, 4, 0)
+    run_case(agnes, off, idx, feat, np.array([[3, 1], [0, 9]]), [5, 5], 0, 0, 16, tag="no-edges")
+
+
+def test_determinism_reuse_and_grouping(agnes):
+    off, idx = random_graph(2000, 12, 11, hubs=3, hub_deg=600)
+    feat = features(2000, 16, 7)
+    tg = distinct_targets(2000, 6, 40, 8)
+    store = agnes.Store(off, idx, feat, 256)
+    t = torch.from_numpy(tg).cuda()
+    b = store.prepare(t, [6, 4], seed=3, mb_base=20)
+    first = b.to_host()
+    b = store.prepare(t, [6, 4], seed=3, mb_base=20, batch=b)        # reuse the batch
+    second = b.to_host()
+    for x, y in zip(first, second):
+        for k in ("nodes", "features"):
+            assert np.array_equal(x[k], y[k])
+        for l in range(2):
+            assert np.array_equal(x["col"][l], y["col"][l])
+    # minibatch j alone, with mb_base + j, equals its place in the hyperbatch
+    for j in range(6):
+        alone = store.prepare(t[j:j + 1], [6, 4], seed=3, mb_base=20 + j).to_host()[0]
+        for k in ("nodes", "features"):
+            assert np.array_equal(alone[k], first[j][k])
+        for l in range(2):
+            assert np.array_equal(alone["row_ptr"][l], first[j]["row_ptr"][l])
+            assert np.array_equal(alone["col"][l], first[j]["col"][l])
+    # a bigger hyperbatch reusing the smaller batch's buffers
+    tg2 = distinct_targets(2000, 9, 100, 9)
+    b = store.prepare(torch.from_numpy(tg2).cuda(), [8, 5, 2], seed=4, batch=b)
+    ref = oracle.Oracle(off, idx).hyperbatch(tg2, [8, 5, 2], 4, 0)
+    got = b.to_host()
+    for j in range(9):
+        compare_minibatch(got[j], ref[j], oracle.gather(feature_bytes(feat), ref[j].nodes), tag=("grow", j))
+
+
+def test_invalid_targets_are_rejected_and_store_stays_usable(agnes):
+    off, idx = random_graph(500, 6, 1)
+    feat = features(500, 4, 1)
+    store = agnes.Store(off, idx, feat, 64)
+    bad_dup = torch.tensor([[1, 2, 1]], dtype=torch.int32).cuda()
+    with pytest.raises(agnes.AgnesError) as e:
+        store.prepare(bad_dup, [3])
+    assert e.value.status == 1
+    bad_range = torch.tensor([[1, 500]], dtype=torch.int32).cuda()
+    with pytest.raises(agnes.AgnesError) as e:
+        store.prepare(bad_range, [3])
+    assert e.value.status == 1
+    with pytest.raises(agnes.AgnesError):
+        store.prepare(torch.tensor([[1, -3]], dtype=torch.int32).cuda(), [3])
+    with pytest.raises(agnes.AgnesError):
+        store.prepare(torch.tensor([[1, 2]], dtype=torch.int32).cuda(), [2000])
+    tg = distinct_targets(500, 2, 10, 0)
+    got = store.prepare(torch.from_numpy(tg).cuda(), [3, 3], seed=1).to_host()
+    ref = oracle.Oracle(off, idx).hyperbatch(tg, [3, 3], 1, 0)
+    for j in range(2):
+        compare_minibatch(got[j], ref[j], oracle.gather(feature_bytes(feat), ref[j].nodes))
+
+
+def test_object_table_matches_offsets(agnes):
+    off, idx = random_graph(4000, 10, 12, hubs=2, hub_deg=3000)
+    store = agnes.Store(off, idx, features(4000, 4, 0), 1024)
+    first, last = store.object_table()
+    e_blk = 1024 // 4
+    nblk = max(1, -(-int(off[-1]) // e_blk))
+    home = np.minimum(off[:-1] // e_blk, nblk - 1)
+    for blk in range(nblk):
+        vs = np.nonzero(home == blk)[0]
+        if len(vs):
+            assert first[blk] == vs[0] and last[blk] == vs[-1]
+        else:
+            assert first[blk] == -1 and last[blk] == -1
