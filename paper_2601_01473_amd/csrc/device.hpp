@@ -71,7 +71,8 @@ __device__ __forceinline__ int upper_segment(const T* off, int n, T x) {
 // Wave-aggregated atomicAdd of 1 per active lane on counters[key]: lanes sharing
 // a key are combined into one atomic.  Returns, per lane, the counter value its
 // own increment corresponds to (base + rank among same-key lanes, in lane order)
-// and sets `first` when this lane's group found the counter at zero.
+// and sets `first` on the one lane (the group's lowest) whose group found the
+// counter at zero.
 __device__ __forceinline__ int64_t wave_aggregated_increment(int64_t* counters, int64_t key,
                                                              bool active, bool& first) {
     uint64_t todo = __ballot(active);
@@ -87,7 +88,7 @@ __device__ __forceinline__ int64_t wave_aggregated_increment(int64_t* counters, 
         base = (int64_t)shfl64((uint64_t)base, leader);
         if (peers & (1ull << lane_id())) {
             result = base + __popcll(peers & lanemask_lt());
-            first = (base == 0);
+            first = (base == 0) && (lane_id() == leader);
         }
         todo &= ~peers;
     }
