@@ -95,6 +95,49 @@ __device__ __forceinline__ int64_t wave_aggregated_increment(int64_t* counters, 
     return result;
 }
 
+// Lanes whose key equals the key of the active lane just below them form a run.
+// Each run's first lane adds the run length to counters[key] with one atomic;
+// all runs of the wave issue their atomics together (one round trip).  Returns,
+// per active lane, the counter value of its own increment (run base + offset in
+// the run).  All lanes of the wave must call this.
+__device__ __forceinline__ int64_t run_increment(int64_t* counters, int64_t key, bool active) {
+    const int lane = lane_id();
+    uint64_t prev = shfl64((uint64_t)key, lane > 0 ? lane - 1 : 0);
+    uint64_t act = __ballot(active);
+    bool prev_active = lane > 0 && ((act >> (lane - 1)) & 1);
+    bool head = active && (!prev_active || (int64_t)prev != key);
+    uint64_t heads = __ballot(head);
+    uint64_t below_eq = (lane == 63) ? ~0ull : ((2ull << lane) - 1);
+    int my_head = 63 - __clzll((long long)(heads & below_eq));   // valid for active lanes
+    int64_t base = 0;
+    if (head) {
+        uint64_t above = heads & ~below_eq;                       // heads strictly above me
+        int next = above ? (__ffsll((unsigned long long)above) - 1) : 64;
+        uint64_t span = (next == 64 ? ~0ull : ((1ull << next) - 1)) & ~((1ull << lane) - 1);
+        base = atomicAdd((unsigned long long*)&counters[key], (unsigned long long)__popcll(act & span));
+    }
+    base = (int64_t)shfl64((uint64_t)base, active ? my_head : lane);
+    return active ? base + (lane - my_head) : -1;
+}
+
+// Same run grouping for a histogram: no value comes back, so the atomics do not
+// stall the wave.
+__device__ __forceinline__ void run_count(int64_t* counters, int64_t key, bool active) {
+    const int lane = lane_id();
+    uint64_t prev = shfl64((uint64_t)key, lane > 0 ? lane - 1 : 0);
+    uint64_t act = __ballot(active);
+    bool prev_active = lane > 0 && ((act >> (lane - 1)) & 1);
+    bool head = active && (!prev_active || (int64_t)prev != key);
+    uint64_t heads = __ballot(head);
+    if (head) {
+        uint64_t below_eq = (lane == 63) ? ~0ull : ((2ull << lane) - 1);
+        uint64_t above = heads & ~below_eq;
+        int next = above ? (__ffsll((unsigned long long)above) - 1) : 64;
+        uint64_t span = (next == 64 ? ~0ull : ((1ull << next) - 1)) & ~((1ull << lane) - 1);
+        atomicAdd((unsigned long long*)&counters[key], (unsigned long long)__popcll(act & span));
+    }
+}
+
 // Wave-aggregated atomicAdd of 1 per active lane on a single counter.
 __device__ __forceinline__ int64_t wave_append(int64_t* counter, bool active) {
     uint64_t m = __ballot(active);
@@ -196,36 +239,35 @@ __device__ __forceinline__ void floyd_sample_mem(uint64_t deg, int k, uint64_t s
 
 // ----------------------------------------------------------------- hash table
 
-// Open addressing with linear probing over 64-bit words.  A word holds
-// (generation << kKeyBits) | key; words of another generation count as empty, so
-// the table is reused across hyperbatches without being cleared.  Keys are
+// Open addressing with linear probing over 64-bit words, cleared before each
+// hyperbatch; a word holds key + 1 (0 = empty).  Keys are
 // (minibatch << node_bits) | node.
-constexpr int kKeyBits = 44;
-constexpr uint64_t kKeyMask = (1ull << kKeyBits) - 1;
-
 __device__ __forceinline__ uint64_t ht_hash(uint64_t key, int log2cap) {
     return (key * 0x9E3779B97F4A7C15ull) >> (64 - log2cap);
 }
 
 // Insert (or find) `key`; returns the slot and whether this call inserted it.
-// Terminates because the table is sized to at least twice the keys of a
-// hyperbatch and a word, once it holds a current-generation key, never changes.
-__device__ __forceinline__ uint32_t ht_insert(unsigned long long* words, int log2cap, uint64_t gen,
-                                              uint64_t key, bool& inserted) {
+// After kMaxProbes probes without success the table counts as overfull:
+// `overflow` is set and slot 0 is returned (the host then repeats the hyperbatch
+// with a larger table), so the loop always ends.  At the load factors used
+// (at most one half) probe sequences stay far below that bound.
+constexpr uint64_t kMaxProbes = 4096;
+__device__ __forceinline__ uint32_t ht_insert(unsigned long long* words, int log2cap, uint64_t key,
+                                              bool& inserted, bool& overflow) {
     const uint64_t mask = (1ull << log2cap) - 1;
-    const unsigned long long tagged = (gen << kKeyBits) | key;
+    const unsigned long long want = key + 1;
     uint64_t slot = ht_hash(key, log2cap);
-    for (;;) {
-        unsigned long long cur = __hip_atomic_load(&words[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        for (;;) {
-            if (cur == tagged) { inserted = false; return (uint32_t)slot; }
-            if ((cur >> kKeyBits) == gen) break;                 // another live key
-            unsigned long long prev = atomicCAS(&words[slot], cur, tagged);
-            if (prev == cur) { inserted = true; return (uint32_t)slot; }
-            cur = prev;
-        }
+    inserted = false;
+    overflow = false;
+    const uint64_t limit = mask < kMaxProbes ? mask + 1 : kMaxProbes;
+    for (uint64_t probe = 0; probe < limit; probe++) {
+        unsigned long long prev = atomicCAS(&words[slot], 0ull, want);
+        if (prev == 0ull) { inserted = true; return (uint32_t)slot; }
+        if (prev == want) return (uint32_t)slot;
         slot = (slot + 1) & mask;
     }
+    overflow = true;
+    return 0;
 }
 
 }  // namespace agnes

@@ -12,17 +12,20 @@
 //                hop's row pointers (Alg. 1, sampling loop)
 //   k_insert     (minibatch, neighbour) into the hash table; first inserters are
 //                the hop's new nodes (the union of Alg. 1)
+//   scan         positions of the new nodes; k_compact gathers them
 //   radix sort   new nodes by (minibatch, node id)
 //   k_assign     local ids of the new nodes: |S_{l-1}| + rank
 //   k_relabel    hop columns in local ids
 // Gather (Alg. 1, gathering loop):
-//   k_gkey       feature block of every output row, Bck row sizes, distinct rows
-//   scan         Bck row offsets
+//   k_gkey       feature block of every output row, Bck row sizes, row bitmap
+//   scan         Bck row offsets (and the number of non-empty rows)
 //   k_gscatter   output rows into their Bck rows
 //   k_gather     row copies in block order, 16-byte lanes, non-temporal stores
 //
 // All sizes produced on the device stay there until one synchronisation before
-// the gather, where the host learns the output sizes.
+// the gather, where the host learns the output sizes.  Counters are combined
+// per run of equal keys inside a wave (one atomic per run, all runs at once),
+// and the new nodes are compacted with a scan rather than a shared counter.
 #include <algorithm>
 #include <cstring>
 
@@ -138,8 +141,8 @@ __global__ void k_ctl_init(Ctl* ctl, int64_t nblk, int64_t nfblk) {
 __global__ __launch_bounds__(kBlock) void k_init(const int32_t* targets, int H, int B,
                                                  int64_t num_nodes, int node_bits, int64_t capN,
                                                  unsigned long long* ht_words, int32_t* ht_vals,
-                                                 int ht_log2, uint64_t gen, int32_t* nodes,
-                                                 int32_t* size, int64_t* newcnt, Ctl* ctl) {
+                                                 int ht_log2, int32_t* nodes, int32_t* size,
+                                                 int64_t* newcnt, Ctl* ctl) {
     int64_t n = (int64_t)H * B;
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) {
         int64_t j = i / B, r = i - j * B;
@@ -148,9 +151,11 @@ __global__ __launch_bounds__(kBlock) void k_init(const int32_t* targets, int H, 
             atomicOr((unsigned long long*)&ctl->err, 1ull);
             v = 0;
         } else {
-            bool inserted;
-            uint32_t slot = ht_insert(ht_words, ht_log2, gen, ((uint64_t)j << node_bits) | (uint64_t)v, inserted);
-            if (inserted) ht_vals[slot] = (int32_t)r;
+            bool inserted, overflow;
+            uint32_t slot = ht_insert(ht_words, ht_log2, ((uint64_t)j << node_bits) | (uint64_t)v, inserted,
+                                      overflow);
+            if (overflow) atomicOr((unsigned long long*)&ctl->err, 8ull);
+            else if (inserted) ht_vals[slot] = (int32_t)r;
             else atomicOr((unsigned long long*)&ctl->err, 2ull);
         }
         nodes[j * capN + r] = v;
@@ -162,11 +167,11 @@ __global__ __launch_bounds__(kBlock) void k_init(const int32_t* targets, int H, 
 }
 
 template <typename OffT>
-__global__ __launch_bounds__(kBlock) void k_frontier(int l, int H, int64_t capN, int32_t f,
+__global__ __launch_bounds__(kBlock) void k_frontier(int H, int64_t capN, int32_t f,
                                                      const OffT* off, int e_blk_log2, int64_t nblk,
                                                      const int32_t* nodes, const int64_t* req_off_g,
                                                      int32_t* cnt, int32_t* bkey, int64_t* bcnt,
-                                                     Ctl* ctl) {
+                                                     const Ctl* ctl) {
     extern __shared__ int64_t req_off[];
     load_offsets(req_off, req_off_g, H);
     const int64_t R = ctl->R;
@@ -185,9 +190,7 @@ __global__ __launch_bounds__(kBlock) void k_frontier(int l, int H, int64_t capN,
             if (b >= nblk) b = nblk - 1;
             bkey[q] = (int32_t)b;
         }
-        bool first;
-        wave_aggregated_increment(bcnt, b, active, first);
-        if (first) atomicAdd((unsigned long long*)&ctl->topo_blocks[l], 1ull);
+        run_count(bcnt, b, active);
     }
 }
 
@@ -199,8 +202,7 @@ __global__ __launch_bounds__(kBlock) void k_bscatter(const int32_t* bkey, int64_
         int64_t q = base + threadIdx.x;
         bool active = q < R;
         int64_t key = active ? bkey[q] : 0;
-        bool first;
-        int64_t pos = wave_aggregated_increment(bcur, key, active, first);
+        int64_t pos = run_increment(bcur, key, active);
         if (active) bck[pos] = q;
     }
 }
@@ -243,52 +245,55 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int64_t capN, i
     }
 }
 
-// Union of Alg. 1: insert every sampled (minibatch, neighbour); the thread whose
-// insert creates the key records a new node of the hop.
+// Union of Alg. 1: insert every sampled (minibatch, neighbour); the insert that
+// creates a key marks a new node of the hop (flag[e] = 1).
 __global__ __launch_bounds__(kBlock) void k_insert(int H, int node_bits, const int64_t* req_off_g,
                                                    const int64_t* e_off, const int32_t* cg,
                                                    unsigned long long* ht_words, int ht_log2,
-                                                   uint64_t gen, uint32_t* eslot, uint64_t* nkeys,
-                                                   uint32_t* nvals, int64_t* newcnt, Ctl* ctl) {
+                                                   uint32_t* eslot, int32_t* flag, Ctl* ctl) {
     extern __shared__ int64_t mb_e[];
     for (int i = threadIdx.x; i <= H; i += kBlock) mb_e[i] = e_off[req_off_g[i]];
     __syncthreads();
     const int64_t S = ctl->S;
-    for (int64_t base = (int64_t)blockIdx.x * kBlock; base < S; base += (int64_t)gridDim.x * kBlock) {
-        int64_t e = base + threadIdx.x;
-        bool active = e < S;
-        bool inserted = false;
-        int j = 0;
-        uint64_t key = 0;
-        uint32_t slot = 0;
-        if (active) {
-            j = upper_segment(mb_e, H, e);
-            key = ((uint64_t)j << node_bits) | (uint64_t)(uint32_t)cg[e];
-            slot = ht_insert(ht_words, ht_log2, gen, key, inserted);
-            eslot[e] = slot;
-        }
-        int64_t pos = wave_append(&ctl->n_new, inserted);
-        if (inserted) {
-            nkeys[pos] = key;
-            nvals[pos] = slot;
-        }
-        bool first;
-        wave_aggregated_increment(newcnt, j, inserted, first);
+    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < S; e += (int64_t)gridDim.x * kBlock) {
+        int j = upper_segment(mb_e, H, e);
+        uint64_t key = ((uint64_t)j << node_bits) | (uint64_t)(uint32_t)cg[e];
+        bool inserted, overflow;
+        uint32_t slot = ht_insert(ht_words, ht_log2, key, inserted, overflow);
+        if (overflow) atomicOr((unsigned long long*)&ctl->err, 8ull);
+        eslot[e] = slot;
+        flag[e] = inserted ? 1 : 0;
     }
 }
 
+// New node number fpre[e] of the hop: its sort key and hash slot.
+__global__ __launch_bounds__(kBlock) void k_compact(int H, int node_bits, const int64_t* req_off_g,
+                                                    const int64_t* e_off, const int32_t* cg,
+                                                    const int32_t* flag, const int64_t* fpre,
+                                                    const uint32_t* eslot, uint64_t* nkeys,
+                                                    uint32_t* nvals, const Ctl* ctl) {
+    extern __shared__ int64_t mb_e[];
+    for (int i = threadIdx.x; i <= H; i += kBlock) mb_e[i] = e_off[req_off_g[i]];
+    __syncthreads();
+    const int64_t S = ctl->S;
+    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < S; e += (int64_t)gridDim.x * kBlock) {
+        if (!flag[e]) continue;
+        int j = upper_segment(mb_e, H, e);
+        int64_t pos = fpre[e];
+        nkeys[pos] = ((uint64_t)j << node_bits) | (uint64_t)(uint32_t)cg[e];
+        nvals[pos] = eslot[e];
+    }
+}
+
+// Per minibatch j: new nodes of the hop (newcnt) and
 // base[j] = |S_{j,l-1}| - (start of minibatch j in the sorted new-node list).
-__global__ __launch_bounds__(kBlock) void k_newbase(int H, const int32_t* size, const int64_t* newcnt,
-                                                    int64_t* base) {
-    __shared__ int64_t lds[kWavesPerBlock];
-    int64_t carry = 0;
-    for (int b0 = 0; b0 < H; b0 += kBlock) {
-        int j = b0 + threadIdx.x;
-        int64_t v = (j < H) ? newcnt[j] : 0;
-        int64_t total;
-        int64_t ex = block_exclusive_scan(v, lds, total);
-        if (j < H) base[j] = (int64_t)size[j] - (carry + ex);
-        carry += total;
+__global__ __launch_bounds__(kBlock) void k_newbase(int H, const int32_t* size, const int64_t* req_off,
+                                                    const int64_t* e_off, const int64_t* fpre,
+                                                    int64_t* newcnt, int64_t* base) {
+    for (int j = threadIdx.x; j < H; j += kBlock) {
+        int64_t a = fpre[e_off[req_off[j]]], b = fpre[e_off[req_off[j + 1]]];
+        newcnt[j] = b - a;
+        base[j] = (int64_t)size[j] - a;
     }
 }
 
@@ -325,11 +330,11 @@ __global__ __launch_bounds__(kBlock) void k_relabel(const uint32_t* eslot, const
 // ----------------------------------------------------------------- gather kernels
 
 // Output row i of minibatch j is node nodes[j][i - node_off[j]]; its feature
-// block is the Bck row it falls in.
+// block is the Bck row it falls in.  dbits marks every gathered node.
 __global__ __launch_bounds__(kBlock) void k_gkey(int H, int64_t capN, const int64_t* node_off_g,
                                                  const int32_t* nodes, int32_t* nodes_out,
                                                  int32_t rpb, int32_t* gkey, int64_t* fbcnt,
-                                                 uint32_t* dbits, Ctl* ctl) {
+                                                 uint32_t* dbits, const Ctl* ctl) {
     extern __shared__ int64_t node_off[];
     load_offsets(node_off, node_off_g, H);
     const int64_t rows = ctl->rows;
@@ -337,20 +342,31 @@ __global__ __launch_bounds__(kBlock) void k_gkey(int H, int64_t capN, const int6
         int64_t i = base + threadIdx.x;
         bool active = i < rows;
         int64_t fb = 0;
-        bool fresh = false;
         if (active) {
             int j = upper_segment(node_off, H, i);
             int32_t v = nodes[(int64_t)j * capN + (i - node_off[j])];
             nodes_out[i] = v;
             fb = (uint32_t)v / (uint32_t)rpb;
             gkey[i] = (int32_t)fb;
-            uint32_t bit = 1u << (v & 31);
-            fresh = (atomicOr(&dbits[v >> 5], bit) & bit) == 0;
+            atomicOr(&dbits[v >> 5], 1u << (v & 31));
         }
-        bool first;
-        wave_aggregated_increment(fbcnt, fb, active, first);
-        if (first) atomicAdd((unsigned long long*)&ctl->fblocks, 1ull);
-        wave_append(&ctl->distinct, fresh);
+        run_count(fbcnt, fb, active);
+    }
+}
+
+// Number of set bits of a bitmap, added to *out.
+__global__ __launch_bounds__(kBlock) void k_popcount(const uint32_t* bits, int64_t nwords, int64_t* out) {
+    __shared__ int64_t lds[kWavesPerBlock];
+    int64_t c = 0;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < nwords; i += (int64_t)gridDim.x * kBlock)
+        c += __popc(bits[i]);
+    c = wave_inclusive_scan(c);
+    if (lane_id() == kWave - 1) lds[wave_id()] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t t = 0;
+        for (int w = 0; w < kWavesPerBlock; w++) t += lds[w];
+        if (t) atomicAdd((unsigned long long*)out, (unsigned long long)t);
     }
 }
 
@@ -361,8 +377,7 @@ __global__ __launch_bounds__(kBlock) void k_gscatter(const int32_t* gkey, const 
         int64_t i = base + threadIdx.x;
         bool active = i < rows;
         int64_t key = active ? gkey[i] : 0;
-        bool first;
-        int64_t pos = wave_aggregated_increment(fbcur, key, active, first);
+        int64_t pos = run_increment(fbcur, key, active);
         if (active) gent[pos] = ((uint64_t)i << 32) | (uint32_t)nodes_out[i];
     }
 }
@@ -426,28 +441,43 @@ static void launch_gather(const void* feat, void* out, const uint64_t* gent, int
 
 // ----------------------------------------------------------------- host orchestration
 
+// Layout of the block that the host reads at the synchronisation point:
+// [Ctl][layer sizes H x (L+1) int32][edge counts H x L int64].
+struct SyncLayout {
+    size_t lsz, ecount, bytes;
+};
+
+static SyncLayout sync_layout(int H, int L) {
+    SyncLayout y;
+    y.lsz = (sizeof(Ctl) + 255) / 256 * 256;
+    y.ecount = (y.lsz + (size_t)H * (L + 1) * 4 + 255) / 256 * 256;
+    y.bytes = y.ecount + (size_t)H * L * 8;
+    return y;
+}
+
 template <typename OffT>
 static void launch_layer(Store& s, const Geometry& g, int l, int32_t f, uint64_t seed, int64_t mb_base,
-                         Batch& b, hipStream_t st) {
+                         Batch& b, const SyncLayout& y, hipStream_t st) {
     Workspace& w = s.ws;
-    Ctl* ctl = w.ctl.as<Ctl>();
+    Ctl* ctl = w.sync.as<Ctl>();
+    int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
+    int64_t* ecount = (int64_t*)((char*)w.sync.ptr + y.ecount);
     const OffT* off = s.offsets.as<OffT>();
     const size_t lds_req = (size_t)(g.H + 1) * sizeof(int64_t);
     const int gR = grid_for(g.Rmax, 2048);
     const int gS = grid_for(g.Smax, 4096);
+    int64_t* part = w.scan_part.as<int64_t>();
 
     hipLaunchKernelGGL(k_begin, dim3(1 + grid_for(s.nblk + 1, 256)), dim3(kBlock), 0, st, l, g.L, g.H, ctl,
-                       w.size.as<int32_t>(), w.newcnt.as<int64_t>(), w.lsz.as<int32_t>(),
-                       w.ecount.as<int64_t>(), w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
-                       (int64_t*)nullptr, w.bcnt.as<int64_t>(), s.nblk);
-    hipLaunchKernelGGL(k_frontier<OffT>, dim3(gR), dim3(kBlock), lds_req, st, l, g.H, g.capN, f, off,
+                       w.size.as<int32_t>(), w.newcnt.as<int64_t>(), lsz, ecount, w.req_off.as<int64_t>(),
+                       w.e_off.as<int64_t>(), (int64_t*)nullptr, w.bcnt.as<int64_t>(), s.nblk);
+    hipLaunchKernelGGL(k_frontier<OffT>, dim3(gR), dim3(kBlock), lds_req, st, g.H, g.capN, f, off,
                        s.e_blk_log2, s.nblk, w.nodes.as<int32_t>(), w.req_off.as<int64_t>(),
                        w.cnt.as<int32_t>(), w.bkey.as<int32_t>(), w.bcnt.as<int64_t>(), ctl);
-    scan_counts(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, g.Rmax, &ctl->S,
-                w.scan_part.as<int64_t>(), st);
-    // Bck row offsets over the topology blocks (count read from the Ctl copy of nblk)
-    scan_counts64(w.bcnt.as<int64_t>(), w.bcur.as<int64_t>(), &ctl->nblk, s.nblk, nullptr,
-                  w.scan_part.as<int64_t>(), st);
+    scan_counts(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, g.Rmax, &ctl->S, part, st);
+    // Bck row offsets over the topology blocks; the non-empty rows are T_l
+    scan_counts64(w.bcnt.as<int64_t>(), w.bcur.as<int64_t>(), &ctl->nblk, s.nblk, nullptr, part, st,
+                  &ctl->topo_blocks[l]);
     hipLaunchKernelGGL(k_bscatter, dim3(gR), dim3(kBlock), 0, st, w.bkey.as<int32_t>(),
                        w.bcur.as<int64_t>(), w.bck.as<int64_t>(), ctl);
     int32_t* rp = b.row_ptr[l].as<int32_t>();
@@ -465,42 +495,54 @@ static void launch_layer(Store& s, const Geometry& g, int l, int32_t f, uint64_t
 #undef AGNES_SAMPLE
     hipLaunchKernelGGL(k_insert, dim3(gS), dim3(kBlock), lds_req, st, g.H, s.node_bits,
                        w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), w.cg.as<int32_t>(),
-                       w.ht_words.as<unsigned long long>(), w.ht_log2, w.gen, w.eslot.as<uint32_t>(),
-                       w.nkeys.as<uint64_t>(), w.nvals.as<uint32_t>(), w.newcnt.as<int64_t>(), ctl);
-    radix_sort_pairs(w.nkeys.as<uint64_t>(), w.nvals.as<uint32_t>(), w.nkeys2.as<uint64_t>(),
-                     w.nvals2.as<uint32_t>(), &ctl->n_new, g.Smax, s.node_bits + g.jbits,
-                     w.rs_hist.as<int64_t>(), w.rs_dtot.as<int64_t>(), st);
+                       w.ht_words.as<unsigned long long>(), w.ht_log2, w.eslot.as<uint32_t>(),
+                       w.flag.as<int32_t>(), ctl);
+    scan_counts(w.flag.as<int32_t>(), w.fpre.as<int64_t>(), &ctl->S, g.Smax, &ctl->n_new, part, st);
+    hipLaunchKernelGGL(k_compact, dim3(gS), dim3(kBlock), lds_req, st, g.H, s.node_bits,
+                       w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), w.cg.as<int32_t>(),
+                       w.flag.as<int32_t>(), w.fpre.as<int64_t>(), w.eslot.as<uint32_t>(),
+                       w.nkeys.as<uint64_t>(), w.nvals.as<uint32_t>(), ctl);
+    int in_tmp = radix_sort_pairs(w.nkeys.as<uint64_t>(), w.nvals.as<uint32_t>(), w.nkeys2.as<uint64_t>(),
+                                  w.nvals2.as<uint32_t>(), &ctl->n_new, g.Smax, s.node_bits + g.jbits,
+                                  w.rs_hist.as<int64_t>(), w.rs_dtot.as<int64_t>(), st);
+    const uint64_t* skeys = in_tmp ? w.nkeys2.as<uint64_t>() : w.nkeys.as<uint64_t>();
+    const uint32_t* svals = in_tmp ? w.nvals2.as<uint32_t>() : w.nvals.as<uint32_t>();
     hipLaunchKernelGGL(k_newbase, dim3(1), dim3(kBlock), 0, st, g.H, w.size.as<int32_t>(),
+                       w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), w.fpre.as<int64_t>(),
                        w.newcnt.as<int64_t>(), w.mb_off.as<int64_t>());
     hipLaunchKernelGGL(k_assign, dim3(gS), dim3(kBlock), (size_t)g.H * sizeof(int64_t), st, g.H,
-                       s.node_bits, g.capN, w.nkeys.as<uint64_t>(), w.nvals.as<uint32_t>(),
-                       w.mb_off.as<int64_t>(), w.ht_vals.as<int32_t>(), w.nodes.as<int32_t>(), ctl);
+                       s.node_bits, g.capN, skeys, svals, w.mb_off.as<int64_t>(), w.ht_vals.as<int32_t>(),
+                       w.nodes.as<int32_t>(), ctl);
     hipLaunchKernelGGL(k_relabel, dim3(gS), dim3(kBlock), 0, st, w.eslot.as<uint32_t>(),
                        w.ht_vals.as<int32_t>(), b.col[l].as<int32_t>(), ctl);
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
-static void reserve_workspace(Store& s, const Geometry& g, hipStream_t st) {
+static int ceil_log2(int64_t x) {
+    int lg = 0;
+    while (((int64_t)1 << lg) < x) lg++;
+    return lg;
+}
+
+static void reserve_workspace(Store& s, const Geometry& g, const SyncLayout& y) {
     Workspace& w = s.ws;
     const int64_t H = g.H;
-    // hash table: at least twice the worst-case number of (minibatch, node) keys
-    int lg = 10;
-    while (((int64_t)1 << lg) < 2 * g.rows_max) lg++;
+    // hash table: one key per (minibatch, node); at most half full in the worst
+    // case, about a third full when sized from the rows seen so far
+    int lg_max = std::max(10, ceil_log2(2 * g.rows_max));
+    int lg = s.ht_hint > 0 ? std::max(10, ceil_log2(3 * s.ht_hint)) : lg_max;
+    lg = std::min(std::max(lg, s.ht_min_log2), lg_max);
     AGNES_REQUIRE(lg <= 31, AGNES_ERR_RANGE, "hyperbatch too large for the 2^31-slot hash table");
-    if (w.ht_words.reserve(((size_t)1 << lg) * 8) || lg != w.ht_log2) {
-        AGNES_CHECK_HIP(hipMemsetAsync(w.ht_words.ptr, 0, ((size_t)1 << lg) * 8, st));
-        w.gen = 0;
-    }
     w.ht_log2 = lg;
+    w.ht_words.reserve(((size_t)1 << lg) * 8);
     w.ht_vals.reserve(((size_t)1 << lg) * 4);
     w.nodes.reserve((size_t)g.rows_max * 4);
     w.size.reserve((size_t)H * 4);
     w.newcnt.reserve((size_t)H * 8);
-    w.lsz.reserve((size_t)H * (g.L + 1) * 4);
-    w.ecount.reserve((size_t)H * g.L * 8);
     w.req_off.reserve((size_t)(H + 1) * 8);
     w.mb_off.reserve((size_t)(H + 1) * 8);
-    w.ctl.reserve(sizeof(Ctl));
+    w.sync.reserve(y.bytes);
+    w.sync_host.reserve(y.bytes);
     w.cnt.reserve((size_t)g.Rmax * 4);
     w.bkey.reserve((size_t)g.Rmax * 4);
     w.bck.reserve((size_t)g.Rmax * 8);
@@ -509,12 +551,14 @@ static void reserve_workspace(Store& s, const Geometry& g, hipStream_t st) {
     w.bcur.reserve((size_t)(s.nblk + 2) * 8);
     w.cg.reserve((size_t)g.Smax * 4);
     w.eslot.reserve((size_t)g.Smax * 4);
+    w.flag.reserve((size_t)g.Smax * 4);
+    w.fpre.reserve((size_t)(g.Smax + 1) * 8);
     w.nkeys.reserve((size_t)g.Smax * 8);
     w.nkeys2.reserve((size_t)g.Smax * 8);
     w.nvals.reserve((size_t)g.Smax * 4);
     w.nvals2.reserve((size_t)g.Smax * 4);
     w.rs_hist.reserve((size_t)radix_hist_entries() * 8);
-    w.rs_dtot.reserve(256 * 8);
+    w.rs_dtot.reserve((size_t)radix_dtot_entries() * 8);
     w.scan_part.reserve((size_t)scan_partials_needed() * 8);
     w.gkey.reserve((size_t)g.rows_max * 4);
     w.gent.reserve((size_t)g.rows_max * 8);
@@ -525,20 +569,54 @@ static void reserve_workspace(Store& s, const Geometry& g, hipStream_t st) {
         for (auto& e : w.ev) AGNES_CHECK_HIP(hipEventCreate(&e));
 }
 
+// Sampling of all hops; returns false when the hash table overflowed (the host
+// then grows it and runs again).
+static bool run_sampling(Store& s, Batch& b, const Geometry& g, const SyncLayout& y,
+                         const int32_t* targets, const int32_t* fanouts, uint64_t seed,
+                         int64_t mb_base, hipStream_t st, Ctl& hc, std::vector<int64_t>& ecount) {
+    Workspace& w = s.ws;
+    reserve_workspace(s, g, y);
+    Ctl* ctl = w.sync.as<Ctl>();
+    int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
+    int64_t* ec = (int64_t*)((char*)w.sync.ptr + y.ecount);
+    const int H = g.H, B = g.B, L = g.L;
+
+    if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[0], st));
+    hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(kBlock), 0, st, ctl, s.nblk, s.nfblk);
+    fill_u32(w.ht_words.ptr, 0, ((int64_t)1 << w.ht_log2) * 2, st);
+    hipLaunchKernelGGL(k_init, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st, targets, H, B,
+                       s.num_nodes, s.node_bits, g.capN, w.ht_words.as<unsigned long long>(),
+                       w.ht_vals.as<int32_t>(), w.ht_log2, w.nodes.as<int32_t>(), w.size.as<int32_t>(),
+                       w.newcnt.as<int64_t>(), ctl);
+    AGNES_CHECK_HIP(hipGetLastError());
+    for (int l = 0; l < L; l++) {
+        if (s.offsets64) launch_layer<int64_t>(s, g, l, fanouts[l], seed, mb_base, b, y, st);
+        else launch_layer<int32_t>(s, g, l, fanouts[l], seed, mb_base, b, y, st);
+    }
+    // close the last hop: edge counts, final node counts, output row offsets
+    hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
+                       w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
+                       w.mb_off.as<int64_t>(), w.bcnt.as<int64_t>(), s.nblk);
+    AGNES_CHECK_HIP(hipGetLastError());
+    if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
+
+    // the one host synchronisation: sizes of the outputs
+    AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, w.sync.ptr, y.bytes, hipMemcpyDeviceToHost, st));
+    AGNES_CHECK_HIP(hipStreamSynchronize(st));
+    memcpy(&hc, w.sync_host.ptr, sizeof(Ctl));
+    b.layer_sizes.assign((size_t)H * (L + 1), 0);
+    memcpy(b.layer_sizes.data(), (char*)w.sync_host.ptr + y.lsz, b.layer_sizes.size() * 4);
+    ecount.assign((size_t)H * L, 0);
+    memcpy(ecount.data(), (char*)w.sync_host.ptr + y.ecount, ecount.size() * 8);
+    return !(hc.err & 8);
+}
+
 void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
                         const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
                         hipStream_t st) {
     Geometry g = plan(s, H, B, fanouts, L);
-    reserve_workspace(s, g, st);
+    SyncLayout y = sync_layout(H, L);
     Workspace& w = s.ws;
-    Ctl* ctl = w.ctl.as<Ctl>();
-
-    // generation tag of this hyperbatch's hash entries (cleared on wrap-around)
-    w.gen++;
-    if (w.gen >= (1ull << (64 - kKeyBits))) {
-        AGNES_CHECK_HIP(hipMemsetAsync(w.ht_words.ptr, 0, ((size_t)1 << w.ht_log2) * 8, st));
-        w.gen = 1;
-    }
 
     // outputs with worst-case capacity for the per-hop CSR
     b.store = &s;
@@ -548,35 +626,15 @@ void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, i
         b.col[l].reserve((size_t)std::max<int64_t>(1, H * g.cap[l] * fanouts[l]) * 4);
     }
 
-    if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[0], st));
-    hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(kBlock), 0, st, ctl, s.nblk, s.nfblk);
-    hipLaunchKernelGGL(k_init, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st, targets, H, B,
-                       s.num_nodes, s.node_bits, g.capN, w.ht_words.as<unsigned long long>(),
-                       w.ht_vals.as<int32_t>(), w.ht_log2, w.gen, w.nodes.as<int32_t>(),
-                       w.size.as<int32_t>(), w.newcnt.as<int64_t>(), ctl);
-    AGNES_CHECK_HIP(hipGetLastError());
-    for (int l = 0; l < L; l++) {
-        if (s.offsets64) launch_layer<int64_t>(s, g, l, fanouts[l], seed, mb_base, b, st);
-        else launch_layer<int32_t>(s, g, l, fanouts[l], seed, mb_base, b, st);
-    }
-    // close the last hop: edge counts, final node counts, output row offsets
-    hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
-                       w.newcnt.as<int64_t>(), w.lsz.as<int32_t>(), w.ecount.as<int64_t>(),
-                       w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), w.mb_off.as<int64_t>(),
-                       w.bcnt.as<int64_t>(), s.nblk);
-    AGNES_CHECK_HIP(hipGetLastError());
-    if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
-
-    // the one host synchronisation: sizes of the outputs
     Ctl hc{};
-    b.layer_sizes.assign((size_t)H * (L + 1), 0);
-    std::vector<int64_t> ecount((size_t)H * L);
-    AGNES_CHECK_HIP(hipMemcpyAsync(&hc, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st));
-    AGNES_CHECK_HIP(hipMemcpyAsync(b.layer_sizes.data(), w.lsz.ptr, b.layer_sizes.size() * 4,
-                                   hipMemcpyDeviceToHost, st));
-    AGNES_CHECK_HIP(hipMemcpyAsync(ecount.data(), w.ecount.ptr, ecount.size() * 8,
-                                   hipMemcpyDeviceToHost, st));
-    AGNES_CHECK_HIP(hipStreamSynchronize(st));
+    std::vector<int64_t> ecount;
+    while (!run_sampling(s, b, g, y, targets, fanouts, seed, mb_base, st, hc, ecount)) {
+        // the table was sized from earlier hyperbatches and this one did not fit
+        AGNES_REQUIRE(w.ht_log2 < std::max(10, ceil_log2(2 * g.rows_max)), AGNES_ERR_INTERNAL,
+                      "hash table overflow at its worst-case size");
+        s.ht_min_log2 = w.ht_log2 + 1;
+    }
+    Ctl* ctl = w.sync.as<Ctl>();
     AGNES_REQUIRE(!(hc.err & 1), AGNES_ERR_INVALID, "a target is outside [0, num_nodes)");
     AGNES_REQUIRE(!(hc.err & 2), AGNES_ERR_INVALID, "a target appears twice in one minibatch");
     AGNES_REQUIRE(!(hc.err & 4), AGNES_ERR_INTERNAL, "node capacity exceeded");
@@ -600,20 +658,24 @@ void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, i
     }
     const int64_t rows = b.node_off[H];
     AGNES_REQUIRE(rows < 0x7FFFFFFFll, AGNES_ERR_RANGE, "more than 2^31-1 gathered rows");
-    b.nodes.reserve((size_t)std::max<int64_t>(rows, 1) * 4);
-    b.features.reserve((size_t)std::max<int64_t>(rows, 1) * (size_t)s.row_bytes);
+    s.ht_hint = std::max<int64_t>(s.ht_hint, rows);
+    b.nodes.reserve_slack((size_t)std::max<int64_t>(rows, 1) * 4);
+    b.features.reserve_slack((size_t)std::max<int64_t>(rows, 1) * (size_t)s.row_bytes);
 
     // gather
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
     fill_u32(w.fbcnt.ptr, 0, (s.nfblk + 1) * 2, st);
-    fill_u32(w.dbits.ptr, 0, (s.num_nodes + 31) / 32, st);
+    const int64_t nwords = (s.num_nodes + 31) / 32;
+    fill_u32(w.dbits.ptr, 0, nwords, st);
     const size_t lds_node = (size_t)(H + 1) * sizeof(int64_t);
     const int gG = grid_for(rows, 4096);
     hipLaunchKernelGGL(k_gkey, dim3(gG), dim3(kBlock), lds_node, st, H, g.capN, w.mb_off.as<int64_t>(),
                        w.nodes.as<int32_t>(), b.nodes.as<int32_t>(), (int32_t)s.rpb, w.gkey.as<int32_t>(),
                        w.fbcnt.as<int64_t>(), w.dbits.as<uint32_t>(), ctl);
+    hipLaunchKernelGGL(k_popcount, dim3(grid_for(nwords, 1024)), dim3(kBlock), 0, st, w.dbits.as<uint32_t>(),
+                       nwords, &ctl->distinct);
     scan_counts64(w.fbcnt.as<int64_t>(), w.fbcur.as<int64_t>(), &ctl->nfblk, s.nfblk, nullptr,
-                  w.scan_part.as<int64_t>(), st);
+                  w.scan_part.as<int64_t>(), st, &ctl->fblocks);
     hipLaunchKernelGGL(k_gscatter, dim3(gG), dim3(kBlock), 0, st, w.gkey.as<int32_t>(), b.nodes.as<int32_t>(),
                        w.fbcur.as<int64_t>(), w.gent.as<uint64_t>(), ctl);
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
@@ -625,8 +687,9 @@ void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, i
     }
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));
-    AGNES_CHECK_HIP(hipMemcpyAsync(&hc, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st));
+    AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st));
     AGNES_CHECK_HIP(hipStreamSynchronize(st));
+    memcpy(&hc, w.sync_host.ptr, sizeof(Ctl));
 
     // statistics
     agnes_stats& so = b.stats;

@@ -38,20 +38,33 @@ __device__ __forceinline__ void scan_range(int64_t n, int G, int g, int64_t& lo,
 }
 
 template <typename T>
-__global__ void k_scan_reduce(const T* in, const int64_t* n_dev, int G, int64_t* partials) {
+__global__ void k_scan_reduce(const T* in, const int64_t* n_dev, int G, int64_t* partials,
+                              int64_t* nonzero) {
     __shared__ int64_t lds[kWavesPerBlock];
+    __shared__ int64_t ldz[kWavesPerBlock];
     int64_t lo, hi;
     scan_range(*n_dev, G, blockIdx.x, lo, hi);
-    int64_t s = 0;
-    for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock) s += (int64_t)in[i];
-    // block reduction
+    int64_t s = 0, z = 0;
+    for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock) {
+        T x = in[i];
+        s += (int64_t)x;
+        z += (x != 0) ? 1 : 0;
+    }
     s = wave_inclusive_scan(s);
-    if (lane_id() == kWave - 1) lds[wave_id()] = s;
+    z = wave_inclusive_scan(z);
+    if (lane_id() == kWave - 1) {
+        lds[wave_id()] = s;
+        ldz[wave_id()] = z;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
-        int64_t t = 0;
-        for (int w = 0; w < kWavesPerBlock; w++) t += lds[w];
+        int64_t t = 0, tz = 0;
+        for (int w = 0; w < kWavesPerBlock; w++) {
+            t += lds[w];
+            tz += ldz[w];
+        }
         partials[blockIdx.x] = t;
+        if (nonzero && tz) atomicAdd((unsigned long long*)nonzero, (unsigned long long)tz);
     }
 }
 
@@ -110,29 +123,32 @@ __global__ void k_scan_final(const T* in, int64_t* out, const int64_t* n_dev, in
 
 template <typename T>
 static void scan_impl(const T* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
-                      int64_t* total_dev, int64_t* partials, hipStream_t st) {
+                      int64_t* total_dev, int64_t* partials, int64_t* nonzero, hipStream_t st) {
     int64_t g = (n_max + kScanTile - 1) / kScanTile;
     int G = (int)(g < 1 ? 1 : (g > kScanGroups ? kScanGroups : g));
-    hipLaunchKernelGGL(k_scan_reduce<T>, dim3(G), dim3(kBlock), 0, st, in, n_dev, G, partials);
+    hipLaunchKernelGGL(k_scan_reduce<T>, dim3(G), dim3(kBlock), 0, st, in, n_dev, G, partials, nonzero);
     hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, st, partials, G, n_dev, out, total_dev);
     hipLaunchKernelGGL(k_scan_final<T>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials);
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
 void scan_counts(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
-                 int64_t* total_dev, int64_t* partials, hipStream_t st) {
-    scan_impl<int32_t>(in, out, n_dev, n_max, total_dev, partials, st);
+                 int64_t* total_dev, int64_t* partials, hipStream_t st, int64_t* nonzero) {
+    scan_impl<int32_t>(in, out, n_dev, n_max, total_dev, partials, nonzero, st);
 }
 
 void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
-                   int64_t* total_dev, int64_t* partials, hipStream_t st) {
-    scan_impl<int64_t>(in, out, n_dev, n_max, total_dev, partials, st);
+                   int64_t* total_dev, int64_t* partials, hipStream_t st, int64_t* nonzero) {
+    scan_impl<int64_t>(in, out, n_dev, n_max, total_dev, partials, nonzero, st);
 }
 
 // ----------------------------------------------------------------- radix sort
 
 constexpr int kSortGroups = 512;     // workgroups per pass; each owns a contiguous range
-int64_t radix_hist_entries() { return 256 * (int64_t)kSortGroups; }
+constexpr int kMaxDigitBits = 11;
+constexpr int kMaxBins = 1 << kMaxDigitBits;
+int64_t radix_hist_entries() { return (int64_t)kMaxBins * kSortGroups; }
+int64_t radix_dtot_entries() { return kMaxBins; }
 
 __device__ __forceinline__ void sort_range(int64_t n, int g, int64_t& lo, int64_t& hi) {
     int64_t chunk = (n + kSortGroups - 1) / kSortGroups;
@@ -143,22 +159,22 @@ __device__ __forceinline__ void sort_range(int64_t n, int g, int64_t& lo, int64_
 }
 
 // Digit histogram of each workgroup's range: hist[d * kSortGroups + g].
-__global__ void k_rs_hist(const uint64_t* keys, const int64_t* n_dev, int shift, int dbits,
-                          int64_t* hist) {
-    __shared__ uint32_t h[256];
+__global__ __launch_bounds__(kBlock) void k_rs_hist(const uint64_t* keys, const int64_t* n_dev,
+                                                    int shift, int dbits, int64_t* hist) {
+    __shared__ uint32_t h[kMaxBins];
     const int nb = 1 << dbits;
-    h[threadIdx.x] = 0;
+    for (int d = threadIdx.x; d < nb; d += kBlock) h[d] = 0;
     __syncthreads();
     int64_t lo, hi;
     sort_range(*n_dev, blockIdx.x, lo, hi);
     for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock)
         atomicAdd(&h[(keys[i] >> shift) & (uint64_t)(nb - 1)], 1u);
     __syncthreads();
-    if (threadIdx.x < nb) hist[(int64_t)threadIdx.x * kSortGroups + blockIdx.x] = h[threadIdx.x];
+    for (int d = threadIdx.x; d < nb; d += kBlock) hist[(int64_t)d * kSortGroups + blockIdx.x] = h[d];
 }
 
 // Per digit d (one workgroup each): exclusive scan over the workgroups, digit total.
-__global__ void k_rs_scan(int64_t* hist, int64_t* dtot) {
+__global__ __launch_bounds__(kBlock) void k_rs_scan(int64_t* hist, int64_t* dtot) {
     __shared__ int64_t lds[kWavesPerBlock];
     int64_t* row = hist + (int64_t)blockIdx.x * kSortGroups;
     constexpr int per = kSortGroups / kBlock;
@@ -179,23 +195,29 @@ __global__ void k_rs_scan(int64_t* hist, int64_t* dtot) {
     if (threadIdx.x == 0) dtot[blockIdx.x] = total;
 }
 
-// Stable scatter: rounds of 256 consecutive keys; inside a round the rank of a key
-// among equal digits comes from wave ballots (lane order) and per-wave counts
-// (wave order), so the output keeps the input order of equal digits.
-__global__ void k_rs_scatter(const uint64_t* kin, const uint32_t* vin, uint64_t* kout,
-                             uint32_t* vout, const int64_t* n_dev, int shift, int dbits,
-                             const int64_t* hist, const int64_t* dtot) {
-    __shared__ int64_t cursor[256];
-    __shared__ int32_t wcnt[kWavesPerBlock][256];
-    __shared__ int64_t wpre[kWavesPerBlock][256];
+// Stable scatter in rounds of 256 consecutive keys.  Inside a wave, keys with the
+// same digit are matched with ballots (rank = lane order); the waves then take
+// their digit ranges from the running cursors one after the other (wave order),
+// so equal digits keep their input order.
+__global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint64_t* kin, const uint32_t* vin,
+                                                       uint64_t* kout, uint32_t* vout,
+                                                       const int64_t* n_dev, int shift, int dbits,
+                                                       const int64_t* hist, const int64_t* dtot) {
+    __shared__ int64_t cursor[kMaxBins];
     __shared__ int64_t lds[kWavesPerBlock];
     const int nb = 1 << dbits;
     const int t = threadIdx.x;
     const int g = blockIdx.x;
-    int64_t tot = (t < nb) ? dtot[t] : 0;
-    int64_t total;
-    int64_t ex = block_exclusive_scan(tot, lds, total);
-    if (t < nb) cursor[t] = ex + hist[(int64_t)t * kSortGroups + g];
+    // digit bases: exclusive scan of the digit totals, plus this group's offset
+    int64_t carry = 0;
+    for (int d0 = 0; d0 < nb; d0 += kBlock) {
+        int d = d0 + t;
+        int64_t v = (d < nb) ? dtot[d] : 0;
+        int64_t total;
+        int64_t ex = block_exclusive_scan(v, lds, total);
+        if (d < nb) cursor[d] = carry + ex + hist[(int64_t)d * kSortGroups + g];
+        carry += total;
+    }
     int64_t lo, hi;
     sort_range(*n_dev, g, lo, hi);
     __syncthreads();
@@ -211,36 +233,32 @@ __global__ void k_rs_scatter(const uint64_t* kin, const uint32_t* vin, uint64_t*
             peers &= ((d >> b) & 1) ? m : ~m;
         }
         int rank = __popcll(peers & lanemask_lt());
-        for (int x = t; x < kWavesPerBlock * 256; x += kBlock) (&wcnt[0][0])[x] = 0;
-        __syncthreads();
-        if (valid && rank == 0) wcnt[wave_id()][d] = __popcll(peers);
-        __syncthreads();
-        if (t < nb) {
-            int64_t c = cursor[t];
-#pragma unroll
-            for (int w = 0; w < kWavesPerBlock; w++) {
-                wpre[w][t] = c;
-                c += wcnt[w][t];
+        int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane_id();
+        int64_t dbase = 0;
+        for (int w = 0; w < kWavesPerBlock; w++) {
+            if (wave_id() == w) {
+                if (valid && rank == 0) {
+                    dbase = cursor[d];
+                    cursor[d] = dbase + __popcll(peers);
+                }
+                dbase = (int64_t)shfl64((uint64_t)dbase, leader);
             }
-            cursor[t] = c;
+            __syncthreads();
         }
-        __syncthreads();
         if (valid) {
-            int64_t dst = wpre[wave_id()][d] + rank;
+            int64_t dst = dbase + rank;
             kout[dst] = key;
             vout[dst] = val;
         }
-        __syncthreads();
     }
 }
 
-void radix_sort_pairs(uint64_t* keys, uint32_t* vals, uint64_t* keys_tmp, uint32_t* vals_tmp,
-                      const int64_t* n_dev, int64_t n_max, int bits, int64_t* hist,
-                      int64_t* dtot, hipStream_t st) {
+int radix_sort_pairs(uint64_t* keys, uint32_t* vals, uint64_t* keys_tmp, uint32_t* vals_tmp,
+                     const int64_t* n_dev, int64_t n_max, int bits, int64_t* hist,
+                     int64_t* dtot, hipStream_t st) {
     (void)n_max;
     if (bits < 1) bits = 1;
-    int passes = (bits + 7) / 8;
-    if (passes & 1) passes++;                         // even: the result lands in keys/vals
+    int passes = (bits + kMaxDigitBits - 1) / kMaxDigitBits;
     int dbits = (bits + passes - 1) / passes;
     uint64_t *ka = keys, *kb = keys_tmp;
     uint32_t *va = vals, *vb = vals_tmp;
@@ -254,6 +272,7 @@ void radix_sort_pairs(uint64_t* keys, uint32_t* vals, uint64_t* keys_tmp, uint32
         uint32_t* tv = va; va = vb; vb = tv;
     }
     AGNES_CHECK_HIP(hipGetLastError());
+    return passes & 1;   // 1: the sorted pairs are in keys_tmp / vals_tmp
 }
 
 }  // namespace agnes

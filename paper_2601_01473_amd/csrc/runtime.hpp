@@ -56,7 +56,29 @@ struct DevBuf {
         bytes = b;
         return true;
     }
+    // Same, with 25% headroom when growing, for sizes that vary call to call.
+    bool reserve_slack(size_t need) {
+        if (need <= bytes && ptr) return false;
+        return reserve(need + need / 4);
+    }
     template <typename T> T* as() const { return static_cast<T*>(ptr); }
+};
+
+// Pinned host memory that only grows.
+struct PinnedBuf {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+    ~PinnedBuf() {
+        if (ptr) (void)hipHostFree(ptr);
+    }
+    void reserve(size_t need) {
+        if (need <= bytes && ptr) return;
+        if (ptr) (void)hipHostFree(ptr);
+        ptr = nullptr;
+        bytes = 0;
+        AGNES_CHECK_HIP(hipHostMalloc(&ptr, need ? need : 256, hipHostMallocDefault));
+        bytes = need ? need : 256;
+    }
 };
 
 constexpr uint32_t kStoreMagic = 0x53454E47u;   // "GNES"
@@ -83,14 +105,14 @@ struct Ctl {
 struct Workspace {
     DevBuf ht_words, ht_vals;         // (minibatch, node) -> local id
     int ht_log2 = 0;
-    uint64_t gen = 0;                 // generation tag of the live hash entries
     DevBuf nodes;                     // [H][capN] node lists in local-id order
-    DevBuf size, newcnt, lsz, ecount; // per minibatch
+    DevBuf size, newcnt;              // per minibatch
     DevBuf req_off, mb_off;           // [H+1] int64
-    DevBuf ctl;                       // Ctl
+    DevBuf sync;                      // Ctl, layer sizes, edge counts (read by the host)
+    PinnedBuf sync_host;
     DevBuf cnt, bkey, bck, e_off;     // per request
     DevBuf bcnt, bcur;                // per topology block (+1)
-    DevBuf cg, eslot;                 // per sampled edge
+    DevBuf cg, eslot, flag, fpre;     // per sampled edge
     DevBuf nkeys, nvals, nkeys2, nvals2;   // new nodes and their sort buffers
     DevBuf rs_hist, rs_dtot;          // radix-sort histograms
     DevBuf scan_part;                 // scan partial sums
@@ -116,6 +138,8 @@ struct Store {
     int node_bits = 0;                // bits of a node id (ceil log2 num_nodes)
     DevBuf offsets, indices, features, first_node, last_node;
     Workspace ws;
+    int64_t ht_hint = 0;              // most rows seen in one hyperbatch (hash sizing)
+    int ht_min_log2 = 0;              // raised after an overflow
     int profile = 0;
     bool busy = false;
 };
@@ -144,20 +168,23 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
 // ----------------------------------------------------------------- primitives (prims.hip)
 
 // Exclusive scan of n int32 counts (n read from *n_dev, at most n_max) into
-// out[0..n] int64; out[n] = total, also stored to *total_dev when not null.
+// out[0..n] int64; out[n] = total, also stored to *total_dev when not null.  When
+// `nonzero` is not null, the number of nonzero inputs is added to *nonzero.
 void scan_counts(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
-                 int64_t* total_dev, int64_t* partials, hipStream_t st);
+                 int64_t* total_dev, int64_t* partials, hipStream_t st, int64_t* nonzero = nullptr);
 // Same for int64 counts.
 void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
-                   int64_t* total_dev, int64_t* partials, hipStream_t st);
+                   int64_t* total_dev, int64_t* partials, hipStream_t st, int64_t* nonzero = nullptr);
 int64_t scan_partials_needed();
 
-// Stable LSD radix sort of (key, value) pairs on key bits [0, bits); n read from
-// *n_dev (at most n_max).  The result is left in keys/vals.
-void radix_sort_pairs(uint64_t* keys, uint32_t* vals, uint64_t* keys_tmp, uint32_t* vals_tmp,
-                      const int64_t* n_dev, int64_t n_max, int bits, int64_t* hist,
-                      int64_t* dtot, hipStream_t st);
+// Stable LSD radix sort of (key, value) pairs on key bits [0, bits), digits of
+// at most 11 bits; n read from *n_dev (at most n_max).  Returns 0 when the result
+// is in keys/vals and 1 when it is in keys_tmp/vals_tmp.
+int radix_sort_pairs(uint64_t* keys, uint32_t* vals, uint64_t* keys_tmp, uint32_t* vals_tmp,
+                     const int64_t* n_dev, int64_t n_max, int bits, int64_t* hist,
+                     int64_t* dtot, hipStream_t st);
 int64_t radix_hist_entries();
+int64_t radix_dtot_entries();
 
 // Fill n 32-bit words with a value (a kernel, so that it can be captured in a graph).
 void fill_u32(void* p, uint32_t value, int64_t n, hipStream_t st);
