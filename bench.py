@@ -81,6 +81,23 @@ def cpu_baseline(w, cfg, steps_targets, budget_s=20.0):
                        f"{dt:.1f} s", sampled_edges_per_s=edges / dt)
 
 
+def copy_calibration(torch, nbytes=4 << 30, reps=5):
+    """A plain copy of known size: reads nbytes and writes nbytes per launch."""
+    x = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda").fill_(1)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        y.copy_(x)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "ms": round(ms, 4),
+                      "GBps_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -90,6 +107,8 @@ def main():
     ap.add_argument("--H", type=int, default=None, help="minibatches per hyperbatch (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -100,6 +119,9 @@ def main():
     root = os.path.dirname(os.path.abspath(__file__))
     sys.path.insert(0, root)
     import torch
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
     import synth
     import paper_2601_01473_amd as ag
 

@@ -1,6 +1,5 @@
 // Device-side building blocks shared by the gfx950 kernels: wave64 primitives,
-// workgroup scans, the counter-based RNG, Floyd's subset sampler and the
-// (minibatch, node) hash table.  Everything here is written for 64-lane
+// workgroup scans, the counter-based RNG and Floyd's subset sampler.  Everything here is written for 64-lane
 // wavefronts and 256-thread workgroups.
 #pragma once
 
@@ -66,87 +65,6 @@ __device__ __forceinline__ int upper_segment(const T* off, int n, T x) {
         if (off[mid] <= x) lo = mid; else hi = mid;
     }
     return lo;
-}
-
-// Wave-aggregated atomicAdd of 1 per active lane on counters[key]: lanes sharing
-// a key are combined into one atomic.  Returns, per lane, the counter value its
-// own increment corresponds to (base + rank among same-key lanes, in lane order)
-// and sets `first` on the one lane (the group's lowest) whose group found the
-// counter at zero.
-__device__ __forceinline__ int64_t wave_aggregated_increment(int64_t* counters, int64_t key,
-                                                             bool active, bool& first) {
-    uint64_t todo = __ballot(active);
-    int64_t result = 0;
-    first = false;
-    while (todo) {
-        int leader = __ffsll((unsigned long long)todo) - 1;
-        int64_t k = (int64_t)shfl64((uint64_t)key, leader);
-        uint64_t peers = __ballot(active && key == k) & todo;
-        int64_t base = 0;
-        if (lane_id() == leader)
-            base = atomicAdd((unsigned long long*)&counters[k], (unsigned long long)__popcll(peers));
-        base = (int64_t)shfl64((uint64_t)base, leader);
-        if (peers & (1ull << lane_id())) {
-            result = base + __popcll(peers & lanemask_lt());
-            first = (base == 0) && (lane_id() == leader);
-        }
-        todo &= ~peers;
-    }
-    return result;
-}
-
-// Lanes whose key equals the key of the active lane just below them form a run.
-// Each run's first lane adds the run length to counters[key] with one atomic;
-// all runs of the wave issue their atomics together (one round trip).  Returns,
-// per active lane, the counter value of its own increment (run base + offset in
-// the run).  All lanes of the wave must call this.
-__device__ __forceinline__ int64_t run_increment(int64_t* counters, int64_t key, bool active) {
-    const int lane = lane_id();
-    uint64_t prev = shfl64((uint64_t)key, lane > 0 ? lane - 1 : 0);
-    uint64_t act = __ballot(active);
-    bool prev_active = lane > 0 && ((act >> (lane - 1)) & 1);
-    bool head = active && (!prev_active || (int64_t)prev != key);
-    uint64_t heads = __ballot(head);
-    uint64_t below_eq = (lane == 63) ? ~0ull : ((2ull << lane) - 1);
-    int my_head = 63 - __clzll((long long)(heads & below_eq));   // valid for active lanes
-    int64_t base = 0;
-    if (head) {
-        uint64_t above = heads & ~below_eq;                       // heads strictly above me
-        int next = above ? (__ffsll((unsigned long long)above) - 1) : 64;
-        uint64_t span = (next == 64 ? ~0ull : ((1ull << next) - 1)) & ~((1ull << lane) - 1);
-        base = atomicAdd((unsigned long long*)&counters[key], (unsigned long long)__popcll(act & span));
-    }
-    base = (int64_t)shfl64((uint64_t)base, active ? my_head : lane);
-    return active ? base + (lane - my_head) : -1;
-}
-
-// Same run grouping for a histogram: no value comes back, so the atomics do not
-// stall the wave.
-__device__ __forceinline__ void run_count(int64_t* counters, int64_t key, bool active) {
-    const int lane = lane_id();
-    uint64_t prev = shfl64((uint64_t)key, lane > 0 ? lane - 1 : 0);
-    uint64_t act = __ballot(active);
-    bool prev_active = lane > 0 && ((act >> (lane - 1)) & 1);
-    bool head = active && (!prev_active || (int64_t)prev != key);
-    uint64_t heads = __ballot(head);
-    if (head) {
-        uint64_t below_eq = (lane == 63) ? ~0ull : ((2ull << lane) - 1);
-        uint64_t above = heads & ~below_eq;
-        int next = above ? (__ffsll((unsigned long long)above) - 1) : 64;
-        uint64_t span = (next == 64 ? ~0ull : ((1ull << next) - 1)) & ~((1ull << lane) - 1);
-        atomicAdd((unsigned long long*)&counters[key], (unsigned long long)__popcll(act & span));
-    }
-}
-
-// Wave-aggregated atomicAdd of 1 per active lane on a single counter.
-__device__ __forceinline__ int64_t wave_append(int64_t* counter, bool active) {
-    uint64_t m = __ballot(active);
-    if (m == 0) return -1;
-    int leader = __ffsll((unsigned long long)m) - 1;
-    int64_t base = 0;
-    if (lane_id() == leader) base = atomicAdd((unsigned long long*)counter, (unsigned long long)__popcll(m));
-    base = (int64_t)shfl64((uint64_t)base, leader);
-    return active ? base + __popcll(m & lanemask_lt()) : -1;
 }
 
 // ----------------------------------------------------------------- RNG
@@ -235,39 +153,6 @@ __device__ __forceinline__ void floyd_sample_mem(uint64_t deg, int k, uint64_t s
         out[s + 1] = x;
     }
     for (int i = 0; i < k; i++) out[i] = adj[out[i]];
-}
-
-// ----------------------------------------------------------------- hash table
-
-// Open addressing with linear probing over 64-bit words, cleared before each
-// hyperbatch; a word holds key + 1 (0 = empty).  Keys are
-// (minibatch << node_bits) | node.
-__device__ __forceinline__ uint64_t ht_hash(uint64_t key, int log2cap) {
-    return (key * 0x9E3779B97F4A7C15ull) >> (64 - log2cap);
-}
-
-// Insert (or find) `key`; returns the slot and whether this call inserted it.
-// After kMaxProbes probes without success the table counts as overfull:
-// `overflow` is set and slot 0 is returned (the host then repeats the hyperbatch
-// with a larger table), so the loop always ends.  At the load factors used
-// (at most one half) probe sequences stay far below that bound.
-constexpr uint64_t kMaxProbes = 4096;
-__device__ __forceinline__ uint32_t ht_insert(unsigned long long* words, int log2cap, uint64_t key,
-                                              bool& inserted, bool& overflow) {
-    const uint64_t mask = (1ull << log2cap) - 1;
-    const unsigned long long want = key + 1;
-    uint64_t slot = ht_hash(key, log2cap);
-    inserted = false;
-    overflow = false;
-    const uint64_t limit = mask < kMaxProbes ? mask + 1 : kMaxProbes;
-    for (uint64_t probe = 0; probe < limit; probe++) {
-        unsigned long long prev = atomicCAS(&words[slot], 0ull, want);
-        if (prev == 0ull) { inserted = true; return (uint32_t)slot; }
-        if (prev == want) return (uint32_t)slot;
-        slot = (slot + 1) & mask;
-    }
-    overflow = true;
-    return 0;
 }
 
 }  // namespace agnes

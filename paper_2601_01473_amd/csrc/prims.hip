@@ -144,131 +144,157 @@ void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_
 
 // ----------------------------------------------------------------- radix sort
 
-constexpr int kSortGroups = 512;     // workgroups per pass; each owns a contiguous range
-constexpr int kMaxDigitBits = 11;
-constexpr int kMaxBins = 1 << kMaxDigitBits;
-int64_t radix_hist_entries() { return (int64_t)kMaxBins * kSortGroups; }
-int64_t radix_dtot_entries() { return kMaxBins; }
+// LSD radix sort of 32-bit keys with 32-bit values, 8-bit digits, tiles of
+// 2048 keys.  Per pass: (1) digit histogram of every tile, (2) per digit, an
+// exclusive scan over the tiles, (3) each tile ranks its keys stably, reorders
+// them by digit in LDS and writes every digit's run contiguously.
+constexpr int kSortItems = 8;
+constexpr int kSortTile = kBlock * kSortItems;     // 2048 keys
+constexpr int kRadixBits = 8;
+constexpr int kRadixBins = 1 << kRadixBits;
 
-__device__ __forceinline__ void sort_range(int64_t n, int g, int64_t& lo, int64_t& hi) {
-    int64_t chunk = (n + kSortGroups - 1) / kSortGroups;
-    lo = (int64_t)g * chunk;
-    if (lo > n) lo = n;
-    hi = lo + chunk;
-    if (hi > n) hi = n;
-}
+int64_t radix_tiles(int64_t n_max) { return (n_max + kSortTile - 1) / kSortTile + 1; }
+int64_t radix_hist_entries(int64_t n_max) { return (int64_t)kRadixBins * radix_tiles(n_max); }
+int64_t radix_dtot_entries() { return kRadixBins; }
 
-// Digit histogram of each workgroup's range: hist[d * kSortGroups + g].
-__global__ __launch_bounds__(kBlock) void k_rs_hist(const uint64_t* keys, const int64_t* n_dev,
-                                                    int shift, int dbits, int64_t* hist) {
-    __shared__ uint32_t h[kMaxBins];
-    const int nb = 1 << dbits;
-    for (int d = threadIdx.x; d < nb; d += kBlock) h[d] = 0;
+__global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const int64_t* n_dev, int shift,
+                                                    int tiles, uint32_t* hist) {
+    __shared__ uint32_t h[kRadixBins];
+    h[threadIdx.x] = 0;
     __syncthreads();
-    int64_t lo, hi;
-    sort_range(*n_dev, blockIdx.x, lo, hi);
-    for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock)
-        atomicAdd(&h[(keys[i] >> shift) & (uint64_t)(nb - 1)], 1u);
+    const int64_t n = *n_dev;
+    const int64_t t0 = (int64_t)blockIdx.x * kSortTile;
+    for (int k = 0; k < kSortItems; k++) {
+        int64_t i = t0 + k * kBlock + threadIdx.x;
+        if (i < n) atomicAdd(&h[(keys[i] >> shift) & (kRadixBins - 1)], 1u);
+    }
     __syncthreads();
-    for (int d = threadIdx.x; d < nb; d += kBlock) hist[(int64_t)d * kSortGroups + blockIdx.x] = h[d];
+    hist[(int64_t)threadIdx.x * tiles + blockIdx.x] = h[threadIdx.x];
 }
 
-// Per digit d (one workgroup each): exclusive scan over the workgroups, digit total.
-__global__ __launch_bounds__(kBlock) void k_rs_scan(int64_t* hist, int64_t* dtot) {
-    __shared__ int64_t lds[kWavesPerBlock];
-    int64_t* row = hist + (int64_t)blockIdx.x * kSortGroups;
-    constexpr int per = kSortGroups / kBlock;
-    int64_t v[per];
-    int64_t local = 0;
-#pragma unroll
-    for (int k = 0; k < per; k++) {
-        v[k] = row[threadIdx.x * per + k];
-        local += v[k];
-    }
-    int64_t total;
-    int64_t ex = block_exclusive_scan(local, lds, total);
-#pragma unroll
-    for (int k = 0; k < per; k++) {
-        row[threadIdx.x * per + k] = ex;
-        ex += v[k];
-    }
-    if (threadIdx.x == 0) dtot[blockIdx.x] = total;
-}
-
-// Stable scatter in rounds of 256 consecutive keys.  Inside a wave, keys with the
-// same digit are matched with ballots (rank = lane order); the waves then take
-// their digit ranges from the running cursors one after the other (wave order),
-// so equal digits keep their input order.
-__global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint64_t* kin, const uint32_t* vin,
-                                                       uint64_t* kout, uint32_t* vout,
-                                                       const int64_t* n_dev, int shift, int dbits,
-                                                       const int64_t* hist, const int64_t* dtot) {
-    __shared__ int64_t cursor[kMaxBins];
-    __shared__ int64_t lds[kWavesPerBlock];
-    const int nb = 1 << dbits;
-    const int t = threadIdx.x;
-    const int g = blockIdx.x;
-    // digit bases: exclusive scan of the digit totals, plus this group's offset
-    int64_t carry = 0;
-    for (int d0 = 0; d0 < nb; d0 += kBlock) {
-        int d = d0 + t;
-        int64_t v = (d < nb) ? dtot[d] : 0;
-        int64_t total;
-        int64_t ex = block_exclusive_scan(v, lds, total);
-        if (d < nb) cursor[d] = carry + ex + hist[(int64_t)d * kSortGroups + g];
+// One workgroup per digit: exclusive scan over the tiles (in place), digit total.
+__global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, int tiles, uint32_t* dtot) {
+    __shared__ uint32_t lds[kWavesPerBlock];
+    uint32_t* row = hist + (int64_t)blockIdx.x * tiles;
+    uint32_t carry = 0;
+    for (int b0 = 0; b0 < tiles; b0 += kBlock * 4) {
+        uint32_t v[4];
+        uint32_t local = 0;
+        for (int k = 0; k < 4; k++) {
+            int i = b0 + threadIdx.x * 4 + k;
+            v[k] = i < tiles ? row[i] : 0u;
+            local += v[k];
+        }
+        uint32_t total;
+        uint32_t ex = block_exclusive_scan(local, lds, total) + carry;
+        for (int k = 0; k < 4; k++) {
+            int i = b0 + threadIdx.x * 4 + k;
+            if (i < tiles) row[i] = ex;
+            ex += v[k];
+        }
         carry += total;
     }
-    int64_t lo, hi;
-    sort_range(*n_dev, g, lo, hi);
+    if (threadIdx.x == 0) dtot[blockIdx.x] = carry;
+}
+
+// Wave w ranks the keys [w*512, (w+1)*512) of the tile in 8 rounds of 64; ranks
+// inside a round follow lane order (ballot match), rounds follow each other, and
+// waves follow each other, so equal digits keep their input order.
+__global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, const uint32_t* vin,
+                                                       uint32_t* kout, uint32_t* vout, const int64_t* n_dev,
+                                                       int shift, int tiles, const uint32_t* hist,
+                                                       const uint32_t* dtot) {
+    __shared__ uint32_t wcnt[kWavesPerBlock][kRadixBins];
+    __shared__ uint32_t lbase[kRadixBins];
+    __shared__ uint32_t gbase[kRadixBins];
+    __shared__ uint32_t lds[kWavesPerBlock];
+    __shared__ uint32_t sk[kSortTile];
+    __shared__ uint32_t sv[kSortTile];
+    const int64_t n = *n_dev;
+    const int64_t t0 = (int64_t)blockIdx.x * kSortTile;
+    if (t0 >= n) return;
+    const int t = threadIdx.x, w = wave_id(), lane = lane_id();
+    for (int x = t; x < kWavesPerBlock * kRadixBins; x += kBlock) (&wcnt[0][0])[x] = 0;
+    {
+        uint32_t tot;
+        uint32_t ex = block_exclusive_scan(dtot[t], lds, tot);
+        gbase[t] = ex + hist[(int64_t)t * tiles + blockIdx.x];
+    }
     __syncthreads();
-    for (int64_t base = lo; base < hi; base += kBlock) {
-        int64_t i = base + t;
-        bool valid = i < hi;
-        uint64_t key = valid ? kin[i] : 0;
-        uint32_t val = valid ? vin[i] : 0;
-        int d = (int)((key >> shift) & (uint64_t)(nb - 1));
+    uint32_t key[kSortItems], val[kSortItems], rnk[kSortItems];
+    int dig[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; r++) {
+        int64_t i = t0 + w * (kSortItems * kWave) + r * kWave + lane;
+        bool valid = i < n;
+        key[r] = valid ? kin[i] : 0u;
+        val[r] = valid ? (vin ? vin[i] : (uint32_t)i) : 0u;
+        int d = valid ? (int)((key[r] >> shift) & (kRadixBins - 1)) : -1;
+        dig[r] = d;
         uint64_t peers = __ballot(valid);
-        for (int b = 0; b < dbits; b++) {
+#pragma unroll
+        for (int b = 0; b < kRadixBits; b++) {
             uint64_t m = __ballot((d >> b) & 1);
             peers &= ((d >> b) & 1) ? m : ~m;
         }
         int rank = __popcll(peers & lanemask_lt());
-        int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane_id();
-        int64_t dbase = 0;
-        for (int w = 0; w < kWavesPerBlock; w++) {
-            if (wave_id() == w) {
-                if (valid && rank == 0) {
-                    dbase = cursor[d];
-                    cursor[d] = dbase + __popcll(peers);
-                }
-                dbase = (int64_t)shfl64((uint64_t)dbase, leader);
-            }
-            __syncthreads();
+        int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
+        uint32_t old = 0;
+        if (valid && rank == 0) {
+            old = wcnt[w][d];
+            wcnt[w][d] = old + (uint32_t)__popcll(peers);
         }
-        if (valid) {
-            int64_t dst = dbase + rank;
-            kout[dst] = key;
-            vout[dst] = val;
+        old = (uint32_t)__shfl((int)old, leader, kWave);
+        rnk[r] = old + rank;
+    }
+    __syncthreads();
+    // per digit (thread t = digit t): wave prefixes and the tile's digit offsets
+    {
+        uint32_t c0 = wcnt[0][t], c1 = wcnt[1][t], c2 = wcnt[2][t], c3 = wcnt[3][t];
+        uint32_t tot;
+        uint32_t ex = block_exclusive_scan(c0 + c1 + c2 + c3, lds, tot);
+        lbase[t] = ex;
+        wcnt[0][t] = ex;
+        wcnt[1][t] = ex + c0;
+        wcnt[2][t] = ex + c0 + c1;
+        wcnt[3][t] = ex + c0 + c1 + c2;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSortItems; r++) {
+        if (dig[r] >= 0) {
+            uint32_t pos = wcnt[w][dig[r]] + rnk[r];
+            sk[pos] = key[r];
+            sv[pos] = val[r];
         }
+    }
+    __syncthreads();
+    const int cnt = (int)((n - t0) < kSortTile ? (n - t0) : kSortTile);
+    for (int i = t; i < cnt; i += kBlock) {
+        uint32_t k = sk[i];
+        int d = (int)((k >> shift) & (kRadixBins - 1));
+        uint32_t dst = gbase[d] + (uint32_t)i - lbase[d];
+        kout[dst] = k;
+        vout[dst] = sv[i];
     }
 }
 
-int radix_sort_pairs(uint64_t* keys, uint32_t* vals, uint64_t* keys_tmp, uint32_t* vals_tmp,
-                     const int64_t* n_dev, int64_t n_max, int bits, int64_t* hist,
-                     int64_t* dtot, hipStream_t st) {
-    (void)n_max;
+int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
+                       const int64_t* n_dev, int64_t n_max, int bits, uint32_t* hist,
+                       uint32_t* dtot, hipStream_t st, bool vals_iota) {
     if (bits < 1) bits = 1;
-    int passes = (bits + kMaxDigitBits - 1) / kMaxDigitBits;
-    int dbits = (bits + passes - 1) / passes;
-    uint64_t *ka = keys, *kb = keys_tmp;
+    const int passes = (bits + kRadixBits - 1) / kRadixBits;
+    const int tiles = (int)radix_tiles(n_max);
+    uint32_t *ka = keys, *kb = keys_tmp;
     uint32_t *va = vals, *vb = vals_tmp;
     for (int p = 0; p < passes; p++) {
-        int shift = p * dbits;
-        hipLaunchKernelGGL(k_rs_hist, dim3(kSortGroups), dim3(kBlock), 0, st, ka, n_dev, shift, dbits, hist);
-        hipLaunchKernelGGL(k_rs_scan, dim3(1 << dbits), dim3(kBlock), 0, st, hist, dtot);
-        hipLaunchKernelGGL(k_rs_scatter, dim3(kSortGroups), dim3(kBlock), 0, st, ka, va, kb, vb,
-                           n_dev, shift, dbits, hist, dtot);
-        uint64_t* tk = ka; ka = kb; kb = tk;
+        int shift = p * kRadixBits;
+        const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
+        hipLaunchKernelGGL(k_rs_hist, dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, tiles, hist);
+        hipLaunchKernelGGL(k_rs_scan, dim3(kRadixBins), dim3(kBlock), 0, st, hist, tiles, dtot);
+        hipLaunchKernelGGL(k_rs_scatter, dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev, shift,
+                           tiles, hist, dtot);
+        uint32_t* tk = ka; ka = kb; kb = tk;
         uint32_t* tv = va; va = vb; vb = tv;
     }
     AGNES_CHECK_HIP(hipGetLastError());

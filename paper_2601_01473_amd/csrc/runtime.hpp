@@ -93,8 +93,8 @@ struct Ctl {
     int64_t err;        // bit 0: target out of range, bit 1: duplicate target, bit 2: capacity
     int64_t distinct;   // distinct gathered rows
     int64_t fblocks;    // non-empty feature-block rows
-    int64_t nblk;       // topology blocks (element count of the Bck row scan)
-    int64_t nfblk;      // feature blocks
+    int64_t targets;    // H * B
+    int64_t pktot;      // (runs << 32) | new nodes of the current hop
     int64_t requests[AGNES_MAX_LAYERS];
     int64_t sampled[AGNES_MAX_LAYERS];
     int64_t new_nodes[AGNES_MAX_LAYERS];
@@ -103,22 +103,20 @@ struct Ctl {
 
 // Scratch memory of a prepare, owned by the store and grown on demand.
 struct Workspace {
-    DevBuf ht_words, ht_vals;         // (minibatch, node) -> local id
-    int ht_log2 = 0;
     DevBuf nodes;                     // [H][capN] node lists in local-id order
     DevBuf size, newcnt;              // per minibatch
     DevBuf req_off, mb_off;           // [H+1] int64
     DevBuf sync;                      // Ctl, layer sizes, edge counts (read by the host)
     PinnedBuf sync_host;
-    DevBuf cnt, bkey, bck, e_off;     // per request
-    DevBuf bcnt, bcur;                // per topology block (+1)
-    DevBuf cg, eslot, flag, fpre;     // per sampled edge
-    DevBuf nkeys, nvals, nkeys2, nvals2;   // new nodes and their sort buffers
+    DevBuf cnt, e_off;                // per request
+    DevBuf rl_key[2], rl_val[2];      // (node, minibatch) list and local ids, two buffers
+    DevBuf skey, sval, skey2, sval2;  // sort buffers (sampled neighbours, targets)
+    DevBuf pk, pkx, hl;               // per sorted edge: run/new flags, their scan, old local id
+    DevBuf nl_key, nl_run, nl_val;    // new (node, minibatch) pairs of a hop
+    DevBuf run_local;                 // local id of every run
+    DevBuf ghist;                     // per-minibatch counts of the new-node ranking
     DevBuf rs_hist, rs_dtot;          // radix-sort histograms
     DevBuf scan_part;                 // scan partial sums
-    DevBuf gkey, gent;                // per gathered row
-    DevBuf fbcnt, fbcur;              // per feature block (+1)
-    DevBuf dbits;                     // one bit per node
     hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
 };
 
@@ -138,8 +136,6 @@ struct Store {
     int node_bits = 0;                // bits of a node id (ceil log2 num_nodes)
     DevBuf offsets, indices, features, first_node, last_node;
     Workspace ws;
-    int64_t ht_hint = 0;              // most rows seen in one hyperbatch (hash sizing)
-    int ht_min_log2 = 0;              // raised after an overflow
     int profile = 0;
     bool busy = false;
 };
@@ -177,13 +173,16 @@ void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_
                    int64_t* total_dev, int64_t* partials, hipStream_t st, int64_t* nonzero = nullptr);
 int64_t scan_partials_needed();
 
-// Stable LSD radix sort of (key, value) pairs on key bits [0, bits), digits of
-// at most 11 bits; n read from *n_dev (at most n_max).  Returns 0 when the result
-// is in keys/vals and 1 when it is in keys_tmp/vals_tmp.
-int radix_sort_pairs(uint64_t* keys, uint32_t* vals, uint64_t* keys_tmp, uint32_t* vals_tmp,
-                     const int64_t* n_dev, int64_t n_max, int bits, int64_t* hist,
-                     int64_t* dtot, hipStream_t st);
-int64_t radix_hist_entries();
+// Stable LSD radix sort of 32-bit keys with 32-bit values on key bits
+// [0, bits), 8 bits per pass; n read from *n_dev (at most n_max).  With
+// vals_iota the input values are 0, 1, 2, ... (vals is then only an output
+// buffer).  hist needs radix_hist_entries(n_max) entries, dtot
+// radix_dtot_entries().  Returns 0 when the result is in keys/vals and 1 when it
+// is in keys_tmp/vals_tmp.
+int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
+                       const int64_t* n_dev, int64_t n_max, int bits, uint32_t* hist,
+                       uint32_t* dtot, hipStream_t st, bool vals_iota = false);
+int64_t radix_hist_entries(int64_t n_max);
 int64_t radix_dtot_entries();
 
 // Fill n 32-bit words with a value (a kernel, so that it can be captured in a graph).
