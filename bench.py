@@ -107,6 +107,8 @@ def main():
     ap.add_argument("--H", type=int, default=None, help="minibatches per hyperbatch (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--gather-groups", type=int, default=None, help="row-copy kernel workgroups")
+    ap.add_argument("--gather-unroll", type=int, default=None, help="rows in flight per lane group")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
     args = ap.parse_args()
@@ -130,6 +132,7 @@ def main():
     w = synth.workload(cfg, H=args.H)
     H, B = w["H"], w["B"]
     print(f"# inputs ready in {time.time() - t0:.1f}s (E={len(w['indices'])})", file=sys.stderr, flush=True)
+    args.warmup = max(2, args.warmup)            # both batches are allocated before timing
     nsteps = args.steps + args.warmup
     # distinct targets per step: consecutive slices of one permutation of the nodes
     perm = synth.targets(cfg.num_nodes, min(cfg.num_nodes, nsteps * H * B), cfg.data_seed + 7)
@@ -141,40 +144,73 @@ def main():
 
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
     store.set_profiling(True)
+    store.set_gather_shape(args.gather_groups, args.gather_unroll)
     stream = torch.cuda.current_stream()
     ob = 8 if w["offsets"].dtype == np.int64 else 4
     rb = cfg.row_bytes
 
-    batch = None
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]   # default priority
+    acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, sample_ms=0.0, gather_ms=0.0,
+               copy_ms=0.0, steps=0)
+
+    def account(batch):
+        st = batch.stats()                      # waits for the batch
+        bs, bg, bc = algorithmic_bytes(st, ob, rb)
+        acc["sample"] += bs
+        acc["gather"] += bg
+        acc["copy_bytes"] += bc
+        acc["bytes"] += bs + bg
+        acc["edges"] += sum(st["sampled"])
+        acc["rows"] += st["rows"]
+        acc["sample_ms"] += st["sample_ms"]
+        acc["gather_ms"] += st["gather_ms"]
+        acc["copy_ms"] += st["copy_ms"]
+        acc["steps"] += 1
+
+    # warm-up: both batches, both streams (allocations happen here)
+    slots = [None, None]
     for s in range(args.warmup):
-        batch = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=batch,
-                              stream=stream)
+        k = s % 2
+        slots[k] = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[k],
+                                 stream=streams[k])
     torch.cuda.synchronize()
     print("# warm-up done", file=sys.stderr, flush=True)
 
-    tot_bytes = tot_sample = tot_gather = tot_copy_bytes = 0
-    edges = rows = 0
-    sample_ms = gather_ms = copy_ms = 0.0
+    # timed: step k's gather (stream k % 2) overlaps step k+1's sampling (other stream)
+    K = args.steps
+    s0 = args.warmup
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    for k in range(args.steps):
-        s = args.warmup + k
-        batch = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=batch,
-                              stream=stream)
-        st = batch.stats()
-        bs, bg, bc = algorithmic_bytes(st, ob, rb)
-        tot_sample += bs
-        tot_gather += bg
-        tot_copy_bytes += bc
-        tot_bytes += bs + bg
-        edges += sum(st["sampled"])
-        rows += st["rows"]
-        sample_ms += st["sample_ms"]
-        gather_ms += st["gather_ms"]
-        copy_ms += st["copy_ms"]
+    slots[0] = store.begin(dev_targets[s0], cfg.fanouts, seed=cfg.seed, mb_base=s0 * H, batch=slots[0],
+                           stream=streams[0])
+    for k in range(K):
+        if k + 1 < K:
+            n = (k + 1) % 2
+            if k >= 1:
+                account(slots[n])               # step k-1, before its batch is reused
+            slots[n] = store.begin(dev_targets[s0 + k + 1], cfg.fanouts, seed=cfg.seed,
+                                   mb_base=(s0 + k + 1) * H, batch=slots[n], stream=streams[n])
+        slots[k % 2].finish(stream=streams[k % 2])
+    for k in range(max(0, K - 2), K):
+        account(slots[k % 2])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
-    K = args.steps
+    assert acc["steps"] == K
+
+    # reference: the same work one hyperbatch at a time (synchronous prepare)
+    nser = min(K, 5)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for k in range(nser):
+        s = s0 + k
+        slots[0] = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[0],
+                                 stream=streams[0])
+    torch.cuda.synchronize()
+    serial_ms = (time.perf_counter() - t1) / nser * 1e3
+
+    tot_bytes, tot_sample, tot_gather = acc["bytes"], acc["sample"], acc["gather"]
+    tot_copy_bytes, edges, rows = acc["copy_bytes"], acc["edges"], acc["rows"]
+    sample_ms, gather_ms, copy_ms = acc["sample_ms"], acc["gather_ms"], acc["copy_ms"]
     value = tot_bytes / elapsed / 1e9
     copy_avg_ms = copy_ms / K
     achieved = (tot_copy_bytes / K) / (copy_avg_ms * 1e-3) / 1e9
@@ -201,6 +237,8 @@ def main():
         "gather_phase_GBps": round(rows * rb / (gather_ms * 1e-3) / 1e9, 2) if gather_ms > 0 else None,
         "phase_ms": {"sample": round(sample_ms / K, 4), "gather": round(gather_ms / K, 4),
                      "copy_kernel": round(copy_avg_ms, 4)},
+        "mode": "pipelined: two batches on two streams, hyperbatch t+1 sampled while t gathers",
+        "serial_ms_per_step": round(serial_ms, 4),
         "per_step": {"algorithmic_bytes": tot_bytes // K, "sample_bytes": tot_sample // K,
                      "gather_bytes": tot_gather // K, "rows": rows // K, "sampled_edges": edges // K},
         "roofline": {"kernel": "k_gather (row copy)", "bound": "hbm", "achieved": round(achieved, 1),
@@ -210,7 +248,8 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, cfg, step_targets[args.warmup:], args.cpu_budget)
     print(json.dumps(result), flush=True)
-    batch.close()
+    for b in slots:
+        b.close()
     store.close()
 
 

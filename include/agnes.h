@@ -115,7 +115,8 @@ agnes_status agnes_build_blocks(const agnes_csr* csr, const agnes_features* feat
  *      returned for the same store, that batch's device buffers are reused (and
  *      grown when needed) and its previous contents are overwritten.
  * The call enqueues on hip_stream and returns when the outputs are complete.
- * One call at a time per store: the store owns the scratch workspace.
+ * Each batch owns the scratch memory of its hyperbatch, so several batches can
+ * be in flight on one store.
  * Errors: INVALID (bad sizes, target out of range or duplicated within a
  * minibatch), RANGE (a minibatch with >= 2^31 nodes or edges), NOMEM, DEVICE.
  * On error *out is NULL and a batch passed in is released.
@@ -124,6 +125,30 @@ agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets
                                       int32_t B, const int32_t* fanouts, int32_t L,
                                       uint64_t seed, int64_t mb_base, void* hip_stream,
                                       agnes_batch** out);
+
+/*
+ * The same hyperbatch in two steps, so that the sampling of one hyperbatch can
+ * run while the gather of another streams rows (Sec. 3.4(4): work continues
+ * while data moves).  agnes_hyperbatch_prepare = begin + finish + wait.
+ *
+ * agnes_hyperbatch_begin: same arguments and checks as prepare; enqueues the L
+ *   sampling hops on hip_stream and returns without waiting.  `targets` must
+ *   stay valid until the hyperbatch is finished.  A batch that is still
+ *   gathering from an earlier hyperbatch may be passed in: the call first waits
+ *   for that gather; the batch's previous views become invalid.
+ * agnes_batch_finish: waits on the host for the output sizes of the begun
+ *   hyperbatch, sizes the outputs, and enqueues the gather on hip_stream (which
+ *   may differ from the begin stream; it is ordered after the sampling).  Returns
+ *   without waiting for the gather.  Views are valid after this call; device
+ *   contents after agnes_batch_wait (or once hip_stream has been synchronised).
+ *   Errors (INVALID targets, RANGE) leave the batch empty and reusable.
+ * agnes_batch_wait: blocks until the batch's outputs and statistics are complete.
+ */
+agnes_status agnes_hyperbatch_begin(agnes_store* store, const int32_t* targets, int32_t H,
+                                    int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed,
+                                    int64_t mb_base, void* hip_stream, agnes_batch** out);
+agnes_status agnes_batch_finish(agnes_batch* batch, void* hip_stream);
+agnes_status agnes_batch_wait(agnes_batch* batch);
 
 #define AGNES_MAX_LAYERS 8
 
@@ -171,11 +196,21 @@ typedef struct {
     float copy_ms;       /* the row-copy kernel alone */
 } agnes_stats;
 
-agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);
+agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);   /* waits for the batch */
 
-/* Store options.  AGNES_OPT_PROFILE: 1 = record HIP events around the phases of
- * every prepare (reported by agnes_batch_stats), 0 = off (default). */
-typedef enum { AGNES_OPT_PROFILE = 1 } agnes_option;
+/* Store options.
+ *   AGNES_OPT_PROFILE: 1 = record HIP events around the phases of every
+ *     hyperbatch (reported by agnes_batch_stats), 0 = off (default).
+ *   AGNES_OPT_GATHER_GROUPS: most workgroups of the row-copy kernel, in
+ *     [8, 65536] (default 2048).  Fewer leave room for another stream's work.
+ *   AGNES_OPT_GATHER_UNROLL: rows each lane group keeps in flight, 2, 4 or 8
+ *     (default 4).
+ * Options change launch shapes only, never results. */
+typedef enum {
+    AGNES_OPT_PROFILE = 1,
+    AGNES_OPT_GATHER_GROUPS = 2,
+    AGNES_OPT_GATHER_UNROLL = 3
+} agnes_option;
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value);
 
 /* Store facts: out[0] num_nodes, out[1] num_edges, out[2] topology blocks,
@@ -189,8 +224,8 @@ agnes_status agnes_store_info(const agnes_store* store, int64_t out[8]);
 agnes_status agnes_store_object_table(const agnes_store* store, int32_t* first_node,
                                       int32_t* last_node);
 
-/* Release a store or a batch (NULL is a no-op).  A store must outlive the
- * prepares running on it. */
+/* Release a store or a batch (NULL is a no-op; a batch's enqueued work is
+ * waited for).  A store must outlive the work of its batches. */
 void agnes_free(void* handle);
 
 /* Message of the last failure on the calling thread ("" if none); valid until

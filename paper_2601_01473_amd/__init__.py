@@ -17,6 +17,7 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 
 from . import _binding as B
 from ._binding import AgnesError, agnes_batch_stats, agnes_batch_view_get, agnes_build_blocks  # noqa: F401
+from ._binding import agnes_batch_finish, agnes_batch_wait, agnes_hyperbatch_begin  # noqa: F401
 from ._binding import agnes_free, agnes_hyperbatch_prepare, agnes_last_error  # noqa: F401
 from ._binding import agnes_store_info, agnes_store_object_table, agnes_store_set_option  # noqa: F401
 
@@ -92,9 +93,24 @@ class Store:
     def set_profiling(self, on: bool) -> None:
         agnes_store_set_option(self.handle, B.AGNES_OPT_PROFILE, 1 if on else 0)
 
+    def set_gather_shape(self, groups: int | None = None, unroll: int | None = None) -> None:
+        """Launch shape of the row-copy kernel (never changes results)."""
+        if groups is not None:
+            agnes_store_set_option(self.handle, B.AGNES_OPT_GATHER_GROUPS, int(groups))
+        if unroll is not None:
+            agnes_store_set_option(self.handle, B.AGNES_OPT_GATHER_UNROLL, int(unroll))
+
     def prepare(self, targets: torch.Tensor, fanouts, seed: int = 0, mb_base: int = 0,
                 batch: "Batch | None" = None, stream=None) -> "Batch":
-        """One hyperbatch: targets is a CUDA int32 tensor [H, B]."""
+        """One hyperbatch, synchronously: targets is a CUDA int32 tensor [H, B]."""
+        return self._start(agnes_hyperbatch_prepare, targets, fanouts, seed, mb_base, batch, stream)
+
+    def begin(self, targets: torch.Tensor, fanouts, seed: int = 0, mb_base: int = 0,
+              batch: "Batch | None" = None, stream=None) -> "Batch":
+        """Enqueue the sampling hops of one hyperbatch and return (see Batch.finish)."""
+        return self._start(agnes_hyperbatch_begin, targets, fanouts, seed, mb_base, batch, stream)
+
+    def _start(self, fn, targets, fanouts, seed, mb_base, batch, stream):
         if not (isinstance(targets, torch.Tensor) and targets.is_cuda and targets.dtype == torch.int32):
             raise TypeError("targets must be a CUDA int32 tensor [H, B]")
         if targets.dim() != 2:
@@ -105,11 +121,11 @@ class Store:
         prev = batch.handle if batch is not None else None
         if batch is not None:
             batch.handle = None          # ownership passes to the call (released on error)
-        h = agnes_hyperbatch_prepare(self.handle, t.data_ptr(), H, Bsz, fan, len(fanouts), seed,
-                                     mb_base, _stream_handle(stream), prev)
+        h = fn(self.handle, t.data_ptr(), H, Bsz, fan, len(fanouts), seed, mb_base, _stream_handle(stream), prev)
         if batch is None:
             batch = Batch(self)
         batch.handle = h
+        batch._targets = t               # kept alive until the hyperbatch is finished
         return batch
 
     def close(self) -> None:
@@ -118,7 +134,10 @@ class Store:
             self.handle = None
 
     def __del__(self):
-        self.close()
+        try:
+            self.close()
+        except Exception:       # interpreter shutdown: the process releases everything
+            pass
 
 
 class Batch:
@@ -127,6 +146,15 @@ class Batch:
     def __init__(self, store: Store):
         self.store = store
         self.handle = None
+
+    def finish(self, stream=None) -> "Batch":
+        """Wait for the output sizes and enqueue the gather (returns without waiting)."""
+        agnes_batch_finish(self.handle, _stream_handle(stream))
+        return self
+
+    def wait(self) -> "Batch":
+        agnes_batch_wait(self.handle)
+        return self
 
     def stats(self) -> dict:
         s = agnes_batch_stats(self.handle)
@@ -141,6 +169,7 @@ class Batch:
 
     def to_host(self, minibatches=None, features: bool = True) -> list:
         """Per-minibatch host copies: dict(nodes, layer_sizes, row_ptr[l], col[l], features)."""
+        self.wait()
         v = self.view()
         H, L = v.H, v.L
         node_off = np.ctypeslib.as_array(v.node_off, shape=(H + 1,)).copy()
@@ -174,4 +203,7 @@ class Batch:
             self.handle = None
 
     def __del__(self):
-        self.close()
+        try:
+            self.close()
+        except Exception:       # interpreter shutdown: the process releases everything
+            pass

@@ -17,8 +17,11 @@ STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "NOMEM", 3: "DEVICE", 4: "RANGE", 5: "
 AGNES_INT32, AGNES_INT64, AGNES_FLOAT32, AGNES_FLOAT16, AGNES_BFLOAT16 = range(5)
 AGNES_MAX_LAYERS = 8
 AGNES_OPT_PROFILE = 1
+AGNES_OPT_GATHER_GROUPS = 2
+AGNES_OPT_GATHER_UNROLL = 3
 
-EXPORTED = ["agnes_build_blocks", "agnes_hyperbatch_prepare", "agnes_batch_view_get",
+EXPORTED = ["agnes_build_blocks", "agnes_hyperbatch_prepare", "agnes_hyperbatch_begin",
+            "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
             "agnes_batch_stats", "agnes_store_set_option", "agnes_store_info",
             "agnes_store_object_table", "agnes_free", "agnes_last_error"]
 
@@ -82,6 +85,12 @@ def lib():
                                      ctypes.POINTER(vp)]
     L.agnes_hyperbatch_prepare.restype = st
     L.agnes_hyperbatch_prepare.argtypes = [vp, vp, i32, i32, vp, i32, u64, i64, vp, ctypes.POINTER(vp)]
+    L.agnes_hyperbatch_begin.restype = st
+    L.agnes_hyperbatch_begin.argtypes = [vp, vp, i32, i32, vp, i32, u64, i64, vp, ctypes.POINTER(vp)]
+    L.agnes_batch_finish.restype = st
+    L.agnes_batch_finish.argtypes = [vp, vp]
+    L.agnes_batch_wait.restype = st
+    L.agnes_batch_wait.argtypes = [vp]
     L.agnes_batch_view_get.restype = st
     L.agnes_batch_view_get.argtypes = [vp, ctypes.POINTER(agnes_batch_view)]
     L.agnes_batch_stats.restype = st
@@ -121,6 +130,23 @@ def agnes_hyperbatch_prepare(store: int, targets_ptr: int, H: int, B: int, fanou
                                          fanouts_arr, L, seed, mb_base, ctypes.c_void_p(stream),
                                          ctypes.byref(out)))
     return out.value
+
+
+def agnes_hyperbatch_begin(store: int, targets_ptr: int, H: int, B: int, fanouts_arr, L: int,
+                           seed: int, mb_base: int, stream: int = 0, batch: int | None = None) -> int:
+    out = ctypes.c_void_p(batch)
+    check(lib().agnes_hyperbatch_begin(ctypes.c_void_p(store), ctypes.c_void_p(targets_ptr), H, B,
+                                       fanouts_arr, L, seed, mb_base, ctypes.c_void_p(stream),
+                                       ctypes.byref(out)))
+    return out.value
+
+
+def agnes_batch_finish(batch: int, stream: int = 0) -> None:
+    check(lib().agnes_batch_finish(ctypes.c_void_p(batch), ctypes.c_void_p(stream)))
+
+
+def agnes_batch_wait(batch: int) -> None:
+    check(lib().agnes_batch_wait(ctypes.c_void_p(batch)))
 
 
 def agnes_batch_view_get(batch: int) -> agnes_batch_view:

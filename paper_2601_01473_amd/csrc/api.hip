@@ -56,58 +56,111 @@ agnes_status agnes_build_blocks(const agnes_csr* csr, const agnes_features* feat
     });
 }
 
+}  // extern "C"
+
+namespace agnes {
+
+// Argument checks shared by prepare and begin; returns the batch to fill (the
+// one passed in, or a new one).
+static Batch* check_begin(agnes_store* store, const int32_t* targets, int32_t H, int32_t B,
+                          const int32_t* fanouts, int32_t L, int64_t mb_base, Batch* reuse, Store*& s) {
+    s = as_store(store);
+    AGNES_REQUIRE(!reuse || (reuse->magic == kBatchMagic && reuse->store == s), AGNES_ERR_INVALID,
+                  "the batch passed in was not produced by this store");
+    AGNES_REQUIRE(targets, AGNES_ERR_INVALID, "targets must not be NULL");
+    AGNES_REQUIRE(H >= 1 && H <= 4096, AGNES_ERR_INVALID, "H must be in [1, 4096]");
+    AGNES_REQUIRE(B >= 1, AGNES_ERR_INVALID, "B must be >= 1");
+    AGNES_REQUIRE((int64_t)H * B < 0x7FFFFFFFll, AGNES_ERR_RANGE, "H * B must be < 2^31");
+    AGNES_REQUIRE(L >= 1 && L <= AGNES_MAX_LAYERS, AGNES_ERR_INVALID, "L must be in [1, 8]");
+    AGNES_REQUIRE(fanouts, AGNES_ERR_INVALID, "fanouts must not be NULL");
+    for (int l = 0; l < L; l++)
+        AGNES_REQUIRE(fanouts[l] >= 0 && fanouts[l] <= 1024, AGNES_ERR_INVALID, "fanouts must be in [0, 1024]");
+    AGNES_REQUIRE(mb_base >= 0, AGNES_ERR_INVALID, "mb_base must be >= 0");
+    int dev = 0;
+    AGNES_CHECK_HIP(hipGetDevice(&dev));
+    AGNES_REQUIRE(dev == s->device, AGNES_ERR_INVALID, "the current device is not the store's device");
+    return reuse ? reuse : new Batch();
+}
+
+static void release_batch(Batch* b) {
+    if (b && b->magic == kBatchMagic) {
+        if (b->state == kSampled || b->state == kGathering) {
+            // let enqueued work finish before the memory goes away
+            if (b->state == kSampled && b->sampled) (void)hipEventSynchronize(b->sampled);
+            if (b->state == kGathering && b->gathered) (void)hipEventSynchronize(b->gathered);
+        }
+        b->magic = 0;
+        delete b;
+    }
+}
+
+static Batch* as_batch(void* p) {
+    Batch* b = static_cast<Batch*>(p);
+    AGNES_REQUIRE(b && b->magic == kBatchMagic, AGNES_ERR_INVALID, "not a batch handle");
+    return b;
+}
+
+}  // namespace agnes
+
+extern "C" {
+
 agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets, int32_t H,
                                       int32_t B, const int32_t* fanouts, int32_t L,
                                       uint64_t seed, int64_t mb_base, void* hip_stream,
                                       agnes_batch** out) {
-    Batch* reuse = nullptr;
-    if (out && *out) reuse = reinterpret_cast<Batch*>(*out);
+    Batch* reuse = (out && *out) ? reinterpret_cast<Batch*>(*out) : nullptr;
     if (out) *out = nullptr;
-    Store* s = nullptr;
+    Batch* b = nullptr;
     agnes_status rc = guarded([&] {
         AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
-        s = as_store(store);
-        AGNES_REQUIRE(!reuse || (reuse->magic == kBatchMagic && reuse->store == s), AGNES_ERR_INVALID,
-                      "the batch passed in was not produced by this store");
-        AGNES_REQUIRE(targets, AGNES_ERR_INVALID, "targets must not be NULL");
-        AGNES_REQUIRE(H >= 1 && H <= 4096, AGNES_ERR_INVALID, "H must be in [1, 4096]");
-        AGNES_REQUIRE(B >= 1, AGNES_ERR_INVALID, "B must be >= 1");
-        AGNES_REQUIRE((int64_t)H * B < 0x7FFFFFFFll, AGNES_ERR_RANGE, "H * B must be < 2^31");
-        AGNES_REQUIRE(L >= 1 && L <= AGNES_MAX_LAYERS, AGNES_ERR_INVALID, "L must be in [1, 8]");
-        AGNES_REQUIRE(fanouts, AGNES_ERR_INVALID, "fanouts must not be NULL");
-        for (int l = 0; l < L; l++)
-            AGNES_REQUIRE(fanouts[l] >= 0 && fanouts[l] <= 1024, AGNES_ERR_INVALID, "fanouts must be in [0, 1024]");
-        AGNES_REQUIRE(mb_base >= 0, AGNES_ERR_INVALID, "mb_base must be >= 0");
-        AGNES_REQUIRE(!s->busy, AGNES_ERR_INVALID, "another prepare is running on this store");
-        int dev = 0;
-        AGNES_CHECK_HIP(hipGetDevice(&dev));
-        AGNES_REQUIRE(dev == s->device, AGNES_ERR_INVALID, "the current device is not the store's device");
-        Batch* b = reuse ? reuse : new Batch();
-        reuse = b;
-        s->busy = true;
-        try {
-            prepare_hyperbatch(*s, *b, targets, H, B, fanouts, L, seed, mb_base, (hipStream_t)hip_stream);
-        } catch (...) {
-            s->busy = false;
-            throw;
-        }
-        s->busy = false;
+        Store* s = nullptr;
+        b = check_begin(store, targets, H, B, fanouts, L, mb_base, reuse, s);
+        hipStream_t st = (hipStream_t)hip_stream;
+        begin_hyperbatch(*s, *b, targets, H, B, fanouts, L, seed, mb_base, st);
+        finish_hyperbatch(*b, st);
+        wait_batch(*b);
         *out = reinterpret_cast<agnes_batch*>(b);
     });
-    if (rc != AGNES_OK && reuse) {
-        if (reuse->magic == kBatchMagic) {
-            reuse->magic = 0;
-            delete reuse;
-        }
-    }
+    if (rc != AGNES_OK) release_batch(b ? b : reuse);
     return rc;
+}
+
+agnes_status agnes_hyperbatch_begin(agnes_store* store, const int32_t* targets, int32_t H,
+                                    int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed,
+                                    int64_t mb_base, void* hip_stream, agnes_batch** out) {
+    Batch* reuse = (out && *out) ? reinterpret_cast<Batch*>(*out) : nullptr;
+    if (out) *out = nullptr;
+    Batch* b = nullptr;
+    agnes_status rc = guarded([&] {
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        Store* s = nullptr;
+        b = check_begin(store, targets, H, B, fanouts, L, mb_base, reuse, s);
+        begin_hyperbatch(*s, *b, targets, H, B, fanouts, L, seed, mb_base, (hipStream_t)hip_stream);
+        *out = reinterpret_cast<agnes_batch*>(b);
+    });
+    if (rc != AGNES_OK) release_batch(b ? b : reuse);
+    return rc;
+}
+
+agnes_status agnes_batch_finish(agnes_batch* batch, void* hip_stream) {
+    Batch* b = nullptr;
+    agnes_status rc = guarded([&] {
+        b = as_batch(batch);
+        finish_hyperbatch(*b, (hipStream_t)hip_stream);
+    });
+    return rc;
+}
+
+agnes_status agnes_batch_wait(agnes_batch* batch) {
+    return guarded([&] { wait_batch(*as_batch(batch)); });
 }
 
 agnes_status agnes_batch_view_get(const agnes_batch* batch, agnes_batch_view* out) {
     return guarded([&] {
-        const Batch* b = reinterpret_cast<const Batch*>(batch);
-        AGNES_REQUIRE(b && b->magic == kBatchMagic, AGNES_ERR_INVALID, "not a batch handle");
+        const Batch* b = as_batch((void*)batch);
         AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        AGNES_REQUIRE(b->state == kGathering || b->state == kDone, AGNES_ERR_INVALID,
+                      "the batch holds no finished hyperbatch");
         memset(out, 0, sizeof(*out));
         out->H = b->H;
         out->L = b->L;
@@ -127,9 +180,9 @@ agnes_status agnes_batch_view_get(const agnes_batch* batch, agnes_batch_view* ou
 
 agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out) {
     return guarded([&] {
-        const Batch* b = reinterpret_cast<const Batch*>(batch);
-        AGNES_REQUIRE(b && b->magic == kBatchMagic, AGNES_ERR_INVALID, "not a batch handle");
+        Batch* b = as_batch((void*)batch);
         AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        wait_batch(*b);
         *out = b->stats;
     });
 }
@@ -137,8 +190,17 @@ agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out) {
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value) {
     return guarded([&] {
         Store* s = as_store(store);
-        AGNES_REQUIRE(opt == AGNES_OPT_PROFILE, AGNES_ERR_INVALID, "unknown option");
-        s->profile = value ? 1 : 0;
+        if (opt == AGNES_OPT_PROFILE) {
+            s->profile = value ? 1 : 0;
+        } else if (opt == AGNES_OPT_GATHER_GROUPS) {
+            AGNES_REQUIRE(value >= 8 && value <= 65536, AGNES_ERR_INVALID, "gather groups must be in [8, 65536]");
+            s->gather_groups = (int)value;
+        } else if (opt == AGNES_OPT_GATHER_UNROLL) {
+            AGNES_REQUIRE(value == 2 || value == 4 || value == 8, AGNES_ERR_INVALID, "gather unroll must be 2, 4 or 8");
+            s->gather_unroll = (int)value;
+        } else {
+            throw Error{AGNES_ERR_INVALID, "unknown option"};
+        }
     });
 }
 
@@ -173,14 +235,10 @@ void agnes_free(void* handle) {
     uint32_t magic = *static_cast<uint32_t*>(handle);
     if (magic == kStoreMagic) {
         Store* s = static_cast<Store*>(handle);
-        for (auto& e : s->ws.ev)
-            if (e) (void)hipEventDestroy(e);
         s->magic = 0;
         delete s;
     } else if (magic == kBatchMagic) {
-        Batch* b = static_cast<Batch*>(handle);
-        b->magic = 0;
-        delete b;
+        release_batch(static_cast<Batch*>(handle));
     }
 }
 

@@ -67,6 +67,28 @@ __device__ __forceinline__ int upper_segment(const T* off, int n, T x) {
     return lo;
 }
 
+// Workgroup-wide search over a sorted array: the first index i in [lo, hi) with
+// !before(i) (or hi), for a predicate `before` that holds on a prefix.  Each
+// round, 256 threads test 256 evenly spaced indices, which narrows the range by
+// a factor of ~256; all threads must call it and all get the answer.
+template <typename Pred>
+__device__ __forceinline__ int64_t block_partition_point(int64_t lo, int64_t hi, Pred before) {
+    while (lo < hi) {
+        const int64_t n = hi - lo;
+        const int64_t step = (n + kBlock - 1) / kBlock;
+        const int64_t p = lo + (int64_t)threadIdx.x * step;
+        const bool probe = p < hi;
+        const int c = __syncthreads_count(probe && before(p));
+        const int probes = (int)((n + step - 1) / step);
+        const int64_t nlo = c == 0 ? lo : lo + (int64_t)(c - 1) * step + 1;
+        const int64_t nhi = c < probes ? lo + (int64_t)c * step : hi;
+        if (c == 0) return lo;
+        lo = nlo;
+        hi = nhi;
+    }
+    return lo;
+}
+
 // ----------------------------------------------------------------- RNG
 
 // Philox4x64 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC 2011): two 64x64->128

@@ -62,6 +62,7 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
 }
 
 constexpr int kGroupWGs = 512;          // workgroups of the by-minibatch counting pass
+constexpr int kSortTileR = 2048;        // entries per tile of the by-minibatch ranking
 
 // ----------------------------------------------------------------- small kernels
 
@@ -191,11 +192,17 @@ template <typename OffT, int MAXK>
 __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, uint64_t seed, int64_t mb_base,
                                                    const OffT* off, const int32_t* adj, int e_blk_log2,
                                                    int64_t nblk, const uint64_t* rl_key, const int32_t* rl_val,
-                                                   const int64_t* req_off_g, const int32_t* cnt,
-                                                   const int64_t* e_off, int32_t* cg, int32_t* row_ptr,
+                                                   const int64_t* req_off_g, const int64_t* e_off,
+                                                   int32_t* cg, int32_t* row_ptr,
                                                    Ctl* ctl) {
-    extern __shared__ int64_t req_off[];
-    load_offsets(req_off, req_off_g, H);
+    extern __shared__ int64_t req_off[];      // [H+1] request offsets, then [H+1] edge offsets
+    int64_t* mb_e = req_off + (H + 1);
+    for (int i = threadIdx.x; i <= H; i += kBlock) {
+        int64_t ro = req_off_g[i];
+        req_off[i] = ro;
+        mb_e[i] = e_off[ro];
+    }
+    __syncthreads();
     const int64_t R = ctl->R;
     for (int64_t base = (int64_t)blockIdx.x * kBlock; base < R; base += (int64_t)gridDim.x * kBlock) {
         int64_t p = base + threadIdx.x;
@@ -211,9 +218,9 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, uint
             int64_t deg = (int64_t)off[v + 1] - o0;
             blk = o0 >> e_blk_log2;
             if (blk >= nblk) blk = nblk - 1;
-            int k = cnt[q];
+            int k = (int)(deg < f ? deg : f);
             int64_t eo = e_off[q];
-            int64_t mb_e0 = e_off[req_off[j]];
+            int64_t mb_e0 = mb_e[j];
             int32_t* out = cg + eo;
             const int32_t* a = adj + o0;
             if (k == deg) {
@@ -271,16 +278,12 @@ __global__ __launch_bounds__(kBlock) void k_heads(int H, const int64_t* req_off,
             prevk = t0 > 0 ? (((uint64_t)su[t0 - 1] << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)se[t0 - 1]))
                            : ~0ull;
         __syncthreads();
-        if (t < 2) {
-            // lower_bound of the first key / upper_bound of the last key in the list
-            const uint64_t k = t == 0 ? tk[0] : tk[cnt - 1];
-            int64_t lo = 0, hi = R;
-            while (lo < hi) {
-                int64_t mid = (lo + hi) >> 1;
-                uint64_t x = rl_key[mid];
-                if (t == 0 ? (x < k) : (x <= k)) lo = mid + 1; else hi = mid;
-            }
-            range[t] = lo;
+        {
+            // the list range holding the tile's keys: [lower_bound(first), upper_bound(last))
+            const uint64_t kf = tk[0], kl = tk[cnt - 1];
+            const int64_t a = block_partition_point(0, R, [&](int64_t i) { return rl_key[i] < kf; });
+            const int64_t b = block_partition_point(a, R, [&](int64_t i) { return rl_key[i] <= kl; });
+            if (t == 0) { range[0] = a; range[1] = b; }
         }
         __syncthreads();
         const int64_t lo = range[0], hi = range[1];
@@ -391,52 +394,72 @@ __global__ __launch_bounds__(kBlock) void k_grp_scan(int64_t* ghist, int64_t* ne
 }
 
 // Stable rank of each new node among the new nodes of its minibatch (the list
-// is in id order within a minibatch): local id = |S_{j,l-1}| + rank.  Ranks in a
-// round of 256 entries come from ballots (lane order) and per-wave turns on
-// the minibatch cursors (wave order).
+// is in id order within a minibatch): local id = |S_{j,l-1}| + rank.  A
+// workgroup walks its range in tiles of 2048: wave w counts its 512 entries per
+// minibatch with ballots (lane order, then round order), the waves' counts are
+// stacked per minibatch (wave order), then every entry gets its local id.
+// Dynamic LDS: H int64 cursors + 4 x H int32 counts.
 __global__ __launch_bounds__(kBlock) void k_grp_rank(const uint64_t* nl_key, const int32_t* nl_run, int H,
                                                      int jbits, const int64_t* ghist, const int32_t* size,
                                                      int64_t capN, int32_t* nodes, int32_t* run_local,
                                                      int32_t* nl_val, Ctl* ctl) {
     extern __shared__ int64_t cursor[];
-    const int t = threadIdx.x;
+    int32_t* wc = (int32_t*)(cursor + H);           // [kWavesPerBlock][H]
+    const int t = threadIdx.x, w = wave_id(), lane = lane_id();
     for (int j = t; j < H; j += kBlock) cursor[j] = ghist[(int64_t)j * kGroupWGs + blockIdx.x] + size[j];
     int64_t lo, hi;
     group_range(ctl->n_new, blockIdx.x, lo, hi);
-    __syncthreads();
-    for (int64_t base = lo; base < hi; base += kBlock) {
-        int64_t i = base + t;
-        bool valid = i < hi;
-        uint64_t key = valid ? nl_key[i] : 0;
-        int j = (int)(uint32_t)key;
-        uint64_t peers = __ballot(valid);
-        for (int b = 0; b < jbits; b++) {
-            uint64_t m = __ballot((j >> b) & 1);
-            peers &= ((j >> b) & 1) ? m : ~m;
-        }
-        int rank = __popcll(peers & lanemask_lt());
-        int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane_id();
-        int64_t jbase = 0;
-        for (int w = 0; w < kWavesPerBlock; w++) {
-            if (wave_id() == w) {
-                if (valid && rank == 0) {
-                    jbase = cursor[j];
-                    cursor[j] = jbase + __popcll(peers);
-                }
-                jbase = (int64_t)shfl64((uint64_t)jbase, leader);
+    for (int64_t t0 = lo; t0 < hi; t0 += kSortTileR) {
+        for (int x = t; x < kWavesPerBlock * H; x += kBlock) wc[x] = 0;
+        __syncthreads();
+        int jr[8], rk[8];
+#pragma unroll
+        for (int r = 0; r < 8; r++) {
+            const int64_t i = t0 + w * 512 + r * kWave + lane;
+            const bool valid = i < hi;
+            const int j = valid ? (int)(uint32_t)nl_key[i] : 0;
+            uint64_t peers = __ballot(valid);
+            for (int b = 0; b < jbits; b++) {
+                uint64_t m = __ballot((j >> b) & 1);
+                peers &= ((j >> b) & 1) ? m : ~m;
             }
-            __syncthreads();
+            const int rank = __popcll(peers & lanemask_lt());
+            const int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
+            int old = 0;
+            if (valid && rank == 0) {
+                old = wc[w * H + j];
+                wc[w * H + j] = old + __popcll(peers);
+            }
+            old = __shfl(old, leader, kWave);
+            jr[r] = valid ? j : -1;
+            rk[r] = old + rank;
         }
-        if (valid) {
-            int64_t local = jbase + rank;
+        __syncthreads();
+        for (int j = t; j < H; j += kBlock) {
+            int64_t c = cursor[j];
+            for (int ww = 0; ww < kWavesPerBlock; ww++) {
+                int n = wc[ww * H + j];
+                wc[ww * H + j] = (int32_t)c;
+                c += n;
+            }
+            cursor[j] = c;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < 8; r++) {
+            if (jr[r] < 0) continue;
+            const int64_t i = t0 + w * 512 + r * kWave + lane;
+            const int j = jr[r];
+            const int64_t local = (int64_t)wc[w * H + j] + rk[r];
             if (local >= capN) {
                 atomicOr((unsigned long long*)&ctl->err, 4ull);
             } else {
-                nodes[(int64_t)j * capN + local] = (int32_t)(key >> 32);
+                nodes[(int64_t)j * capN + local] = (int32_t)(nl_key[i] >> 32);
                 run_local[nl_run[i]] = (int32_t)local;
                 nl_val[i] = (int32_t)local;
             }
         }
+        __syncthreads();
     }
 }
 
@@ -467,6 +490,7 @@ __global__ __launch_bounds__(kBlock) void k_merge(const uint64_t* ak, const int3
     for (int64_t d0 = (int64_t)blockIdx.x * kMergeTile; d0 < n; d0 += (int64_t)gridDim.x * kMergeTile) {
         const int64_t d1 = (n - d0) < kMergeTile ? n : d0 + kMergeTile;
         if (t < 2) {
+            // merge path: number of A elements among the first d outputs
             const int64_t d = t == 0 ? d0 : d1;
             int64_t lo = d > nb ? d - nb : 0, hi = d < na ? d : na;
             while (lo < hi) {
@@ -508,20 +532,22 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Row copy over the final list, which is the feature bucket of Alg. 1's
 // gathering loop in block order: the requests of a feature block are contiguous
-// and those of one node are neighbours, so each row is loaded once and written
-// to every minibatch that needs it (dest = node_off[j] + local id).  LPR lanes
-// share a row (16-byte or 4-byte units); each group handles two rows per step.
-// Workgroup b takes a contiguous range; ranges are dealt so that neighbouring
-// ranges (the same blocks) run on the same XCD.  Counts distinct rows and
-// non-empty feature-block rows.
-template <typename Unit, int LPR>
+// and those of one node are neighbours, so each row is loaded from HBM once and
+// written to every minibatch that needs it (dest = node_off[j] + local id).
+// LPR lanes share a row (16-byte or 4-byte units).  Each lane group loads the
+// keys of U rows, then U row pieces, then stores them, so U rows are in flight
+// per group.  Workgroup b takes a contiguous range; ranges are dealt so that
+// neighbouring ranges (the same blocks) run on the same XCD.  Also counts the
+// distinct rows and the non-empty feature-block rows.
+template <typename Unit, int LPR, int U>
 __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat, Unit* __restrict__ out,
                                                    int32_t* __restrict__ nodes_out,
                                                    const uint64_t* __restrict__ rl_key,
                                                    const int32_t* __restrict__ rl_val, const int64_t* node_off_g,
                                                    int H, int64_t rows, int64_t row_units, uint32_t rpb,
                                                    Ctl* ctl) {
-    constexpr int RPW = kWave / LPR;             // rows per wave access
+    constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
+    constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
     extern __shared__ int64_t node_off[];
     __shared__ unsigned long long cnt[2];
     if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
@@ -532,39 +558,40 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
     const int64_t chunk = (rows + G - 1) / G;
     const int64_t lo = std::min<int64_t>(rows, (int64_t)lb * chunk);
     const int64_t hi = std::min<int64_t>(rows, lo + chunk);
-    const int grp = lane_id() / LPR, li = lane_id() % LPR;
-    const int64_t step = (int64_t)kWavesPerBlock * RPW;
+    const int li = lane_id() % LPR;
+    const int gid = wave_id() * RPW + lane_id() / LPR;
     unsigned long long nd = 0, nf = 0;
-    for (int64_t e = lo + (int64_t)wave_id() * RPW + grp; e < hi; e += 2 * step) {
-        int64_t e2 = e + step;
-        bool two = e2 < hi;
-        uint64_t ka = rl_key[e];
-        uint64_t kb = two ? rl_key[e2] : 0;
-        uint32_t ua = (uint32_t)(ka >> 32), ub = (uint32_t)(kb >> 32);
-        int64_t da = node_off[(uint32_t)ka] + rl_val[e];
-        int64_t db = two ? node_off[(uint32_t)kb] + rl_val[e2] : 0;
-        if (li == 0) {
-            nodes_out[da] = (int32_t)ua;
-            uint32_t pa = e > 0 ? (uint32_t)(rl_key[e - 1] >> 32) : 0xFFFFFFFFu;
-            nd += (pa != ua);
-            nf += (e == 0 || pa / rpb != ua / rpb);
-            if (two) {
-                nodes_out[db] = (int32_t)ub;
-                uint32_t pb = (uint32_t)(rl_key[e2 - 1] >> 32);
-                nd += (pb != ub);
-                nf += (pb / rpb != ub / rpb);
+    for (int64_t e0 = lo + gid; e0 < hi; e0 += (int64_t)GPB * U) {
+        int64_t src[U], dst[U];
+        bool ok[U];
+#pragma unroll
+        for (int k = 0; k < U; k++) {
+            const int64_t e = e0 + (int64_t)k * GPB;
+            ok[k] = e < hi;
+            src[k] = 0;
+            dst[k] = 0;
+            if (ok[k]) {
+                const uint64_t key = rl_key[e];
+                const uint32_t u = (uint32_t)(key >> 32);
+                src[k] = (int64_t)u * row_units;
+                const int64_t d = node_off[(uint32_t)key] + rl_val[e];
+                dst[k] = d * row_units;
+                if (li == 0) {
+                    nodes_out[d] = (int32_t)u;
+                    const uint32_t pu = e > 0 ? (uint32_t)(rl_key[e - 1] >> 32) : 0xFFFFFFFFu;
+                    nd += (pu != u);
+                    nf += (e == 0 || pu / rpb != u / rpb);
+                }
             }
         }
-        const Unit* sa = feat + (int64_t)ua * row_units;
-        const Unit* sb = feat + (int64_t)ub * row_units;
-        Unit* xa_out = out + da * row_units;
-        Unit* xb_out = out + db * row_units;
-        for (int64_t u = li; u < row_units; u += LPR) {
-            Unit xa = sa[u];
-            Unit xb;
-            if (two) xb = sb[u];
-            __builtin_nontemporal_store(xa, xa_out + u);
-            if (two) __builtin_nontemporal_store(xb, xb_out + u);
+        for (int64_t c = li; c < row_units; c += LPR) {
+            Unit x[U];
+#pragma unroll
+            for (int k = 0; k < U; k++)
+                if (ok[k]) x[k] = feat[src[k] + c];
+#pragma unroll
+            for (int k = 0; k < U; k++)
+                if (ok[k]) __builtin_nontemporal_store(x[k], out + dst[k] + c);
         }
     }
     if (nd) atomicAdd(&cnt[0], nd);
@@ -576,24 +603,42 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
     }
 }
 
+template <typename Unit, int LPR>
+static void launch_gather_u(int unroll, dim3 grid, size_t lds, hipStream_t st, const Unit* f, Unit* o,
+                            int32_t* nodes_out, const uint64_t* rl_key, const int32_t* rl_val,
+                            const int64_t* node_off, int H, int64_t rows, int64_t row_units, uint32_t rpb,
+                            Ctl* ctl) {
+    if (unroll >= 8)
+        hipLaunchKernelGGL((k_gather<Unit, LPR, 8>), grid, dim3(kBlock), lds, st, f, o, nodes_out, rl_key, rl_val,
+                           node_off, H, rows, row_units, rpb, ctl);
+    else if (unroll >= 4)
+        hipLaunchKernelGGL((k_gather<Unit, LPR, 4>), grid, dim3(kBlock), lds, st, f, o, nodes_out, rl_key, rl_val,
+                           node_off, H, rows, row_units, rpb, ctl);
+    else
+        hipLaunchKernelGGL((k_gather<Unit, LPR, 2>), grid, dim3(kBlock), lds, st, f, o, nodes_out, rl_key, rl_val,
+                           node_off, H, rows, row_units, rpb, ctl);
+}
+
 template <typename Unit>
 static void launch_gather(const void* feat, void* out, int32_t* nodes_out, const uint64_t* rl_key,
                           const int32_t* rl_val, const int64_t* node_off, int H, int64_t rows,
-                          int64_t row_units, uint32_t rpb, Ctl* ctl, hipStream_t st) {
-    int G = grid_for(rows * row_units / 64 + 1, 8192);
+                          int64_t row_units, uint32_t rpb, Ctl* ctl, int groups, int unroll, hipStream_t st) {
+    int G = grid_for(rows * row_units / 64 + 1, groups);
     G = std::max(8, (G + 7) / 8 * 8);
     const Unit* f = (const Unit*)feat;
     Unit* o = (Unit*)out;
     const size_t lds = (size_t)(H + 1) * sizeof(int64_t);
-#define AGNES_GATHER(LPR)                                                                          \
-    hipLaunchKernelGGL((k_gather<Unit, LPR>), dim3(G), dim3(kBlock), lds, st, f, o, nodes_out, rl_key, \
-                       rl_val, node_off, H, rows, row_units, rpb, ctl)
-    if (row_units >= 64) AGNES_GATHER(64);
-    else if (row_units > 16) AGNES_GATHER(32);
-    else if (row_units > 8) AGNES_GATHER(16);
-    else if (row_units > 4) AGNES_GATHER(8);
-    else AGNES_GATHER(4);
-#undef AGNES_GATHER
+    const dim3 grid(G);
+    if (row_units >= 64)
+        launch_gather_u<Unit, 64>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
+    else if (row_units > 16)
+        launch_gather_u<Unit, 32>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
+    else if (row_units > 8)
+        launch_gather_u<Unit, 16>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
+    else if (row_units > 4)
+        launch_gather_u<Unit, 8>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
+    else
+        launch_gather_u<Unit, 4>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
 }
 
 // ----------------------------------------------------------------- host orchestration
@@ -612,8 +657,7 @@ static SyncLayout sync_layout(int H, int L) {
     return y;
 }
 
-static void reserve_workspace(Store& s, const Geometry& g, const SyncLayout& y) {
-    Workspace& w = s.ws;
+static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout& y) {
     const int64_t H = g.H;
     w.nodes.reserve((size_t)g.rows_max * 4);
     w.size.reserve((size_t)H * 4);
@@ -648,9 +692,8 @@ static void reserve_workspace(Store& s, const Geometry& g, const SyncLayout& y) 
 }
 
 template <typename OffT>
-static void launch_layer(Store& s, const Geometry& g, int l, int32_t f, uint64_t seed, int64_t mb_base,
-                         Batch& b, const SyncLayout& y, int cur, hipStream_t st) {
-    Workspace& w = s.ws;
+static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l, int32_t f, uint64_t seed,
+                         int64_t mb_base, Batch& b, const SyncLayout& y, int cur, hipStream_t st) {
     Ctl* ctl = w.sync.as<Ctl>();
     int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
     int64_t* ecount = (int64_t*)((char*)w.sync.ptr + y.ecount);
@@ -672,9 +715,9 @@ static void launch_layer(Store& s, const Geometry& g, int l, int32_t f, uint64_t
     const int32_t* adj = s.indices.as<int32_t>();
     int32_t* cg = w.skey.as<int32_t>();
 #define AGNES_SAMPLE(MK)                                                                               \
-    hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, seed, mb_base, \
-                       off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),              \
-                       w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), cg, rp, ctl)
+    hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), 2 * lds_h, st, l, g.H, f, seed,     \
+                       mb_base, off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),      \
+                       w.e_off.as<int64_t>(), cg, rp, ctl)
     if (f <= 4) AGNES_SAMPLE(4);
     else if (f <= 8) AGNES_SAMPLE(8);
     else if (f <= 16) AGNES_SAMPLE(16);
@@ -698,7 +741,8 @@ static void launch_layer(Store& s, const Geometry& g, int l, int32_t f, uint64_t
     hipLaunchKernelGGL(k_grp_hist, dim3(kGroupWGs), dim3(kBlock), (size_t)g.H * 4, st, w.nl_key.as<uint64_t>(),
                        g.H, w.ghist.as<int64_t>(), ctl);
     hipLaunchKernelGGL(k_grp_scan, dim3(g.H), dim3(kBlock), 0, st, w.ghist.as<int64_t>(), w.newcnt.as<int64_t>());
-    hipLaunchKernelGGL(k_grp_rank, dim3(kGroupWGs), dim3(kBlock), (size_t)g.H * 8, st, w.nl_key.as<uint64_t>(),
+    hipLaunchKernelGGL(k_grp_rank, dim3(kGroupWGs), dim3(kBlock), (size_t)g.H * 8 + (size_t)kWavesPerBlock * g.H * 4,
+                       st, w.nl_key.as<uint64_t>(),
                        w.nl_run.as<int32_t>(), g.H, g.jbits, w.ghist.as<int64_t>(), w.size.as<int32_t>(), g.capN,
                        w.nodes.as<int32_t>(), w.run_local.as<int32_t>(), w.nl_val.as<int32_t>(), ctl);
     hipLaunchKernelGGL(k_relabel, dim3(gS), dim3(kBlock), 0, st, w.pk.as<int64_t>(), w.pkx.as<int64_t>(), se,
@@ -710,15 +754,23 @@ static void launch_layer(Store& s, const Geometry& g, int l, int32_t f, uint64_t
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
-void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
-                        const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
-                        hipStream_t st) {
+void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
+                      const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
+                      hipStream_t st) {
+    AGNES_REQUIRE(b.state != kSampled, AGNES_ERR_INVALID, "the batch has a hyperbatch begun but not finished");
+    // a batch still gathering: its buffers are in use until the gather ends
+    if (b.state == kGathering) wait_batch(b);
+    b.state = kIdle;
     Geometry g = plan(s, H, B, fanouts, L);
     SyncLayout y = sync_layout(H, L);
-    Workspace& w = s.ws;
-    reserve_workspace(s, g, y);
+    Workspace& w = b.ws;
+    reserve_workspace(w, g, y);
+    if (!b.sampled) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.sampled, hipEventDisableTiming));
+    if (!b.gathered) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.gathered, hipEventDisableTiming));
     b.store = &s;
     b.H = H; b.B = B; b.L = L;
+    b.capN = g.capN;
+    b.stream = st;
     for (int l = 0; l < L; l++) {
         b.row_ptr[l].reserve((size_t)(H * g.cap[l] + H) * 4);
         b.col[l].reserve((size_t)std::max<int64_t>(1, H * g.cap[l] * fanouts[l]) * 4);
@@ -742,29 +794,48 @@ void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, i
     AGNES_CHECK_HIP(hipGetLastError());
     int cur = 0;
     for (int l = 0; l < L; l++) {
-        if (s.offsets64) launch_layer<int64_t>(s, g, l, fanouts[l], seed, mb_base, b, y, cur, st);
-        else launch_layer<int32_t>(s, g, l, fanouts[l], seed, mb_base, b, y, cur, st);
+        if (s.offsets64) launch_layer<int64_t>(s, w, g, l, fanouts[l], seed, mb_base, b, y, cur, st);
+        else launch_layer<int32_t>(s, w, g, l, fanouts[l], seed, mb_base, b, y, cur, st);
         cur ^= 1;
     }
+    b.cur = cur;
     // close the last hop: edge counts, final node counts, output row offsets
     hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
                        w.mb_off.as<int64_t>());
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
-
-    // the one host synchronisation: sizes of the outputs
+    // sizes of the outputs travel to pinned host memory; finish reads them
     AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, w.sync.ptr, y.bytes, hipMemcpyDeviceToHost, st));
-    AGNES_CHECK_HIP(hipStreamSynchronize(st));
+    AGNES_CHECK_HIP(hipEventRecord(b.sampled, st));
+    b.state = kSampled;
+}
+
+void finish_hyperbatch(Batch& b, hipStream_t st) {
+    AGNES_REQUIRE(b.state == kSampled, AGNES_ERR_INVALID, "finish needs a begun hyperbatch");
+    const Store& s = *b.store;
+    Workspace& w = b.ws;
+    const int H = b.H, L = b.L;
+    SyncLayout y = sync_layout(H, L);
+    AGNES_CHECK_HIP(hipEventSynchronize(b.sampled));
+    b.state = kIdle;   // until the gather is enqueued
     Ctl hc;
     memcpy(&hc, w.sync_host.ptr, sizeof(Ctl));
+    AGNES_REQUIRE(!(hc.err & 1), AGNES_ERR_INVALID, "a target is outside [0, num_nodes)");
+    AGNES_REQUIRE(!(hc.err & 2), AGNES_ERR_INVALID, "a target appears twice in one minibatch");
+    AGNES_REQUIRE(!(hc.err & 4), AGNES_ERR_INTERNAL, "node capacity exceeded");
     b.layer_sizes.assign((size_t)H * (L + 1), 0);
     memcpy(b.layer_sizes.data(), (char*)w.sync_host.ptr + y.lsz, b.layer_sizes.size() * 4);
     std::vector<int64_t> ecount((size_t)H * L);
     memcpy(ecount.data(), (char*)w.sync_host.ptr + y.ecount, ecount.size() * 8);
-    AGNES_REQUIRE(!(hc.err & 1), AGNES_ERR_INVALID, "a target is outside [0, num_nodes)");
-    AGNES_REQUIRE(!(hc.err & 2), AGNES_ERR_INVALID, "a target appears twice in one minibatch");
-    AGNES_REQUIRE(!(hc.err & 4), AGNES_ERR_INTERNAL, "node capacity exceeded");
+    memset(&b.stats, 0, sizeof(b.stats));
+    b.stats.L = L;
+    for (int l = 0; l < L; l++) {
+        b.stats.requests[l] = hc.requests[l];
+        b.stats.sampled[l] = hc.sampled[l];
+        b.stats.new_nodes[l] = hc.new_nodes[l];
+        b.stats.topo_blocks[l] = hc.topo_blocks[l];
+    }
 
     // host view offsets
     b.node_off.assign((size_t)H + 1, 0);
@@ -782,49 +853,53 @@ void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, i
     }
     const int64_t rows = b.node_off[H];
     AGNES_REQUIRE(rows < 0x7FFFFFFFll, AGNES_ERR_RANGE, "more than 2^31-1 gathered rows");
+    b.stats.rows = rows;
     b.nodes.reserve_slack((size_t)std::max<int64_t>(rows, 1) * 4);
     b.features.reserve_slack((size_t)std::max<int64_t>(rows, 1) * (size_t)s.row_bytes);
 
-    // gather over the final list
+    // gather over the final list, ordered after the sampling phase
+    if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.sampled, 0));
+    Ctl* ctl = w.sync.as<Ctl>();
     if (s.profile) {
         AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
         AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
     }
-    const uint64_t* rlk = w.rl_key[cur].as<uint64_t>();
-    const int32_t* rlv = w.rl_val[cur].as<int32_t>();
+    const uint64_t* rlk = w.rl_key[b.cur].as<uint64_t>();
+    const int32_t* rlv = w.rl_val[b.cur].as<int32_t>();
     if (rows > 0) {
         if (s.row_bytes % 16 == 0)
             launch_gather<u32x4>(s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv,
-                                 w.mb_off.as<int64_t>(), H, rows, s.row_bytes / 16, (uint32_t)s.rpb, ctl, st);
+                                 w.mb_off.as<int64_t>(), H, rows, s.row_bytes / 16, (uint32_t)s.rpb, ctl,
+                                 s.gather_groups, s.gather_unroll, st);
         else
             launch_gather<uint32_t>(s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv,
-                                    w.mb_off.as<int64_t>(), H, rows, s.row_bytes / 4, (uint32_t)s.rpb, ctl, st);
+                                    w.mb_off.as<int64_t>(), H, rows, s.row_bytes / 4, (uint32_t)s.rpb, ctl,
+                                    s.gather_groups, s.gather_unroll, st);
     }
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));
     AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st));
-    AGNES_CHECK_HIP(hipStreamSynchronize(st));
-    memcpy(&hc, w.sync_host.ptr, sizeof(Ctl));
+    AGNES_CHECK_HIP(hipEventRecord(b.gathered, st));
+    b.stream = st;
+    b.state = kGathering;
+}
 
-    // statistics
-    agnes_stats& so = b.stats;
-    memset(&so, 0, sizeof(so));
-    so.L = L;
-    for (int l = 0; l < L; l++) {
-        so.requests[l] = hc.requests[l];
-        so.sampled[l] = hc.sampled[l];
-        so.new_nodes[l] = hc.new_nodes[l];
-        so.topo_blocks[l] = hc.topo_blocks[l];
+void wait_batch(Batch& b) {
+    if (b.state == kDone) return;
+    AGNES_REQUIRE(b.state == kGathering, AGNES_ERR_INVALID, "the batch holds no finished hyperbatch");
+    AGNES_CHECK_HIP(hipEventSynchronize(b.gathered));
+    Ctl hc;
+    memcpy(&hc, b.ws.sync_host.ptr, sizeof(Ctl));
+    b.stats.distinct_rows = hc.distinct;
+    b.stats.feat_blocks = hc.fblocks;
+    b.stats.sample_ms = b.stats.gather_ms = b.stats.copy_ms = -1.0f;
+    if (b.store->profile) {
+        Workspace& w = b.ws;
+        AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.sample_ms, w.ev[0], w.ev[1]));
+        AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.gather_ms, w.ev[2], w.ev[4]));
+        AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.copy_ms, w.ev[3], w.ev[4]));
     }
-    so.rows = rows;
-    so.distinct_rows = hc.distinct;
-    so.feat_blocks = hc.fblocks;
-    so.sample_ms = so.gather_ms = so.copy_ms = -1.0f;
-    if (s.profile) {
-        AGNES_CHECK_HIP(hipEventElapsedTime(&so.sample_ms, w.ev[0], w.ev[1]));
-        AGNES_CHECK_HIP(hipEventElapsedTime(&so.gather_ms, w.ev[2], w.ev[4]));
-        AGNES_CHECK_HIP(hipEventElapsedTime(&so.copy_ms, w.ev[3], w.ev[4]));
-    }
+    b.state = kDone;
 }
 
 }  // namespace agnes

@@ -160,10 +160,11 @@ int64_t radix_dtot_entries() { return kRadixBins; }
 __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const int64_t* n_dev, int shift,
                                                     int tiles, uint32_t* hist) {
     __shared__ uint32_t h[kRadixBins];
-    h[threadIdx.x] = 0;
-    __syncthreads();
     const int64_t n = *n_dev;
     const int64_t t0 = (int64_t)blockIdx.x * kSortTile;
+    if (t0 >= n) return;                        // tiles past the end are not scanned
+    h[threadIdx.x] = 0;
+    __syncthreads();
     for (int k = 0; k < kSortItems; k++) {
         int64_t i = t0 + k * kBlock + threadIdx.x;
         if (i < n) atomicAdd(&h[(keys[i] >> shift) & (kRadixBins - 1)], 1u);
@@ -172,10 +173,13 @@ __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const 
     hist[(int64_t)threadIdx.x * tiles + blockIdx.x] = h[threadIdx.x];
 }
 
-// One workgroup per digit: exclusive scan over the tiles (in place), digit total.
-__global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, int tiles, uint32_t* dtot) {
+// One workgroup per digit: exclusive scan over the tiles that hold keys (in
+// place), digit total.
+__global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, int tiles_max, const int64_t* n_dev,
+                                                    uint32_t* dtot) {
     __shared__ uint32_t lds[kWavesPerBlock];
-    uint32_t* row = hist + (int64_t)blockIdx.x * tiles;
+    uint32_t* row = hist + (int64_t)blockIdx.x * tiles_max;
+    const int tiles = (int)((*n_dev + kSortTile - 1) / kSortTile);
     uint32_t carry = 0;
     for (int b0 = 0; b0 < tiles; b0 += kBlock * 4) {
         uint32_t v[4];
@@ -291,7 +295,7 @@ int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint3
         int shift = p * kRadixBits;
         const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
         hipLaunchKernelGGL(k_rs_hist, dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, tiles, hist);
-        hipLaunchKernelGGL(k_rs_scan, dim3(kRadixBins), dim3(kBlock), 0, st, hist, tiles, dtot);
+        hipLaunchKernelGGL(k_rs_scan, dim3(kRadixBins), dim3(kBlock), 0, st, hist, tiles, n_dev, dtot);
         hipLaunchKernelGGL(k_rs_scatter, dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev, shift,
                            tiles, hist, dtot);
         uint32_t* tk = ka; ka = kb; kb = tk;

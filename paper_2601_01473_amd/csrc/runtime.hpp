@@ -135,28 +135,50 @@ struct Store {
     int64_t max_degree = 0;
     int node_bits = 0;                // bits of a node id (ceil log2 num_nodes)
     DevBuf offsets, indices, features, first_node, last_node;
-    Workspace ws;
     int profile = 0;
-    bool busy = false;
+    int gather_groups = 2048;         // workgroups of the row-copy kernel (upper bound)
+    int gather_unroll = 4;            // rows in flight per lane group (2, 4 or 8)
 };
+
+// A batch: the outputs of one hyperbatch and the scratch memory that produces
+// them.  State: kIdle -> (begin) kSampled -> (finish) kGathering -> (wait) kDone.
+enum BatchState { kIdle = 0, kSampled = 1, kGathering = 2, kDone = 3 };
 
 struct Batch {
     uint32_t magic = kBatchMagic;
     const Store* store = nullptr;
     int32_t H = 0, B = 0, L = 0;
+    int state = kIdle;
+    hipStream_t stream = nullptr;     // stream of the sampling phase
+    hipEvent_t sampled = nullptr;     // sizes of the outputs are in ws.sync_host
+    hipEvent_t gathered = nullptr;    // outputs and statistics are complete
+    int64_t capN = 0;
+    int cur = 0;                      // which list buffer holds the final list
     std::vector<int64_t> node_off;
     std::vector<int32_t> layer_sizes;
     std::vector<int64_t> rp_off[AGNES_MAX_LAYERS];
     std::vector<int64_t> col_off[AGNES_MAX_LAYERS];
     DevBuf nodes, features;
     DevBuf row_ptr[AGNES_MAX_LAYERS], col[AGNES_MAX_LAYERS];
+    Workspace ws;
     agnes_stats stats{};
+    ~Batch() {
+        if (sampled) (void)hipEventDestroy(sampled);
+        if (gathered) (void)hipEventDestroy(gathered);
+        for (auto& e : ws.ev)
+            if (e) (void)hipEventDestroy(e);
+    }
 };
 
-// Pipeline entry points (pipeline.hip).
-void prepare_hyperbatch(Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
-                        const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
-                        hipStream_t stream);
+// Pipeline entry points (pipeline.hip).  begin enqueues the sampling hops on
+// `stream` and returns; finish waits for the output sizes, makes room for the
+// outputs and enqueues the gather on `stream`; wait blocks until the batch is
+// complete and fills its statistics.
+void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
+                      const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
+                      hipStream_t stream);
+void finish_hyperbatch(Batch& b, hipStream_t stream);
+void wait_batch(Batch& b);
 // Store construction (store.hip).
 Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t block_bytes,
                    hipStream_t stream);

@@ -196,3 +196,89 @@ def test_object_table_matches_offsets(agnes):
             assert first[blk] == vs[0] and last[blk] == vs[-1]
         else:
             assert first[blk] == -1 and last[blk] == -1
+
+
+def test_two_batches_in_flight_on_two_streams(agnes):
+    """begin/finish interleaved over two batches and two streams, as a loader
+    overlapping the sampling of one hyperbatch with the gather of another."""
+    off, idx = random_graph(3000, 12, 21, hubs=3, hub_deg=900)
+    feat = features(3000, 32, 9)
+    store = agnes.Store(off, idx, feat, 512)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    fan = [6, 3]
+    tgs = [distinct_targets(3000, 5, 40, 100 + k) for k in range(6)]
+    dev = [torch.from_numpy(t).cuda() for t in tgs]
+    o = oracle.Oracle(off, idx)
+    fb = feature_bytes(feat)
+    slots = [None, None]
+    done = []
+    slots[0] = store.begin(dev[0], fan, seed=5, mb_base=0, batch=None, stream=streams[0])
+    for k in range(6):
+        if k + 1 < 6:
+            n = (k + 1) % 2
+            if k >= 1:
+                done.append((k - 1, slots[n].to_host()))
+            slots[n] = store.begin(dev[k + 1], fan, seed=5, mb_base=(k + 1) * 5, batch=slots[n],
+                                   stream=streams[n])
+        slots[k % 2].finish(stream=streams[k % 2])
+    for k in range(4, 6):
+        done.append((k, slots[k % 2].to_host()))
+    assert sorted(k for k, _ in done) == list(range(6))
+    for k, got in done:
+        ref = o.hyperbatch(tgs[k], fan, 5, k * 5)
+        for j in range(5):
+            compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=("async", k, j))
+
+
+def test_finish_on_other_stream_and_errors(agnes):
+    off, idx = random_graph(800, 8, 3)
+    feat = features(800, 8, 1)
+    store = agnes.Store(off, idx, feat, 256)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    tg = distinct_targets(800, 3, 20, 1)
+    b = store.begin(torch.from_numpy(tg).cuda(), [4, 4], seed=2, stream=s1)
+    b.finish(stream=s2)
+    got = b.to_host()
+    ref = oracle.Oracle(off, idx).hyperbatch(tg, [4, 4], 2, 0)
+    for j in range(3):
+        compare_minibatch(got[j], ref[j], oracle.gather(feature_bytes(feat), ref[j].nodes))
+    with pytest.raises(agnes.AgnesError):
+        b.finish()                          # nothing begun
+    bad = torch.tensor([[1, 1]], dtype=torch.int32).cuda()
+    b2 = store.begin(bad, [2], seed=0)
+    with pytest.raises(agnes.AgnesError):
+        b2.finish()                         # duplicate target is reported at finish
+    b2 = store.begin(torch.from_numpy(tg).cuda(), [4, 4], seed=2, batch=b2)   # the batch stays usable
+    got = b2.finish().to_host()
+    for j in range(3):
+        compare_minibatch(got[j], ref[j], oracle.gather(feature_bytes(feat), ref[j].nodes))
+
+
+@pytest.mark.parametrize("rows_dim", [20, 3, 64])
+def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim):
+    """Every row-copy launch shape (workgroups, rows in flight) gives the same
+    bytes; small workgroup counts force many rows per lane group and ragged ends."""
+    off, idx = random_graph(2500, 8, 21, hubs=2, hub_deg=600)
+    tg = distinct_targets(2500, 4, 45, 3)
+    feat = features(2500, rows_dim, 4)
+    fan = [6, 3]
+    store = agnes.Store(off, idx, feat, 256)
+    t = torch.from_numpy(np.ascontiguousarray(tg, dtype=np.int32)).cuda()
+    ref = oracle.Oracle(off, idx).hyperbatch(tg, fan, 9, 0)
+    fb = feature_bytes(feat)
+    want = oracle.hyperbatch_stats(off, 256, fb.shape[1], ref, len(fan))
+    for groups, unroll in [(8, 2), (8, 8), (24, 4), (2048, 4), (65536, 8), (1000, 2)]:
+        log("gather shape", rows_dim, groups, unroll)
+        store.set_gather_shape(groups, unroll)
+        b = store.prepare(t, fan, seed=9, mb_base=0)
+        got = b.to_host()
+        for j in range(tg.shape[0]):
+            compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=(groups, unroll, j))
+        st = b.stats()
+        for k, v in want.items():
+            assert st[k] == v, (groups, unroll, k, st[k], v)
+        b.close()
+    for bad in [(7, None), (65537, None), (None, 3), (None, 16)]:
+        with pytest.raises(agnes.AgnesError):
+            store.set_gather_shape(*bad)
+    store.close()
