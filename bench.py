@@ -107,8 +107,12 @@ def main():
     ap.add_argument("--H", type=int, default=None, help="minibatches per hyperbatch (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--depth", type=int, default=1, help="hyperbatches sampled ahead of the one gathering")
+    ap.add_argument("--gather-first", action="store_true",
+                    help="queue each gather before waiting for the previous one")
     ap.add_argument("--gather-groups", type=int, default=None, help="row-copy kernel workgroups")
     ap.add_argument("--gather-unroll", type=int, default=None, help="rows in flight per lane group")
+    ap.add_argument("--gather-nt", type=int, default=None, help="1 = non-temporal row stores, 0 = ordinary")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
     args = ap.parse_args()
@@ -132,7 +136,7 @@ def main():
     w = synth.workload(cfg, H=args.H)
     H, B = w["H"], w["B"]
     print(f"# inputs ready in {time.time() - t0:.1f}s (E={len(w['indices'])})", file=sys.stderr, flush=True)
-    args.warmup = max(2, args.warmup)            # both batches are allocated before timing
+    args.warmup = max(args.depth + 1, args.warmup)   # every batch slot is allocated before timing
     nsteps = args.steps + args.warmup
     # distinct targets per step: consecutive slices of one permutation of the nodes
     perm = synth.targets(cfg.num_nodes, min(cfg.num_nodes, nsteps * H * B), cfg.data_seed + 7)
@@ -144,12 +148,14 @@ def main():
 
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
     store.set_profiling(True)
-    store.set_gather_shape(args.gather_groups, args.gather_unroll)
+    store.set_gather_shape(args.gather_groups, args.gather_unroll,
+                           None if args.gather_nt is None else bool(args.gather_nt))
     stream = torch.cuda.current_stream()
     ob = 8 if w["offsets"].dtype == np.int64 else 4
     rb = cfg.row_bytes
 
-    streams = [torch.cuda.Stream(), torch.cuda.Stream()]   # default priority
+    # sampling runs on one stream, gathers on another (both default priority)
+    s_stream, g_stream = torch.cuda.Stream(), torch.cuda.Stream()
     acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, sample_ms=0.0, gather_ms=0.0,
                copy_ms=0.0, steps=0)
 
@@ -167,32 +173,47 @@ def main():
         acc["copy_ms"] += st["copy_ms"]
         acc["steps"] += 1
 
-    # warm-up: both batches, both streams (allocations happen here)
-    slots = [None, None]
-    for s in range(args.warmup):
-        k = s % 2
-        slots[k] = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[k],
-                                 stream=streams[k])
+    D = max(1, args.depth)                      # hyperbatches sampled ahead of the one gathering
+    NSLOT = D + 1
+    slots = [None] * NSLOT
+
+    def begin(s):
+        k = s % NSLOT
+        slots[k] = store.begin(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[k],
+                               stream=s_stream)
+
+    def pipeline(first, n, record):
+        """Steps first .. first+n-1 with the sampling of steps s+1 .. s+D in flight
+        while step s gathers.  Default order: the sampling of step s+D is enqueued
+        before the gather of step s, so it starts on an idle GPU; with
+        --gather-first the gather of step s is queued before step s-1 is waited
+        for, so the gather stream never drains."""
+        for s in range(first, first + min(D, n)):
+            begin(s)
+        for i in range(n):
+            s = first + i
+            if args.gather_first:
+                slots[s % NSLOT].finish(stream=g_stream)   # waits for step s's sizes only
+            if i >= 1:
+                b = slots[(s - 1) % NSLOT]
+                account(b) if record else b.wait()          # step s-1 done: its slot is free
+            if i + D < n:
+                begin(s + D)
+            if not args.gather_first:
+                slots[s % NSLOT].finish(stream=g_stream)
+        last = slots[(first + n - 1) % NSLOT]
+        account(last) if record else last.wait()
+
+    # warm-up: every slot allocated at the largest shape seen so far
+    pipeline(0, args.warmup, record=False)
     torch.cuda.synchronize()
     print("# warm-up done", file=sys.stderr, flush=True)
 
-    # timed: step k's gather (stream k % 2) overlaps step k+1's sampling (other stream)
     K = args.steps
     s0 = args.warmup
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    slots[0] = store.begin(dev_targets[s0], cfg.fanouts, seed=cfg.seed, mb_base=s0 * H, batch=slots[0],
-                           stream=streams[0])
-    for k in range(K):
-        if k + 1 < K:
-            n = (k + 1) % 2
-            if k >= 1:
-                account(slots[n])               # step k-1, before its batch is reused
-            slots[n] = store.begin(dev_targets[s0 + k + 1], cfg.fanouts, seed=cfg.seed,
-                                   mb_base=(s0 + k + 1) * H, batch=slots[n], stream=streams[n])
-        slots[k % 2].finish(stream=streams[k % 2])
-    for k in range(max(0, K - 2), K):
-        account(slots[k % 2])
+    pipeline(s0, K, record=True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     assert acc["steps"] == K
@@ -204,7 +225,7 @@ def main():
     for k in range(nser):
         s = s0 + k
         slots[0] = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[0],
-                                 stream=streams[0])
+                                 stream=s_stream)
     torch.cuda.synchronize()
     serial_ms = (time.perf_counter() - t1) / nser * 1e3
 
@@ -237,7 +258,9 @@ def main():
         "gather_phase_GBps": round(rows * rb / (gather_ms * 1e-3) / 1e9, 2) if gather_ms > 0 else None,
         "phase_ms": {"sample": round(sample_ms / K, 4), "gather": round(gather_ms / K, 4),
                      "copy_kernel": round(copy_avg_ms, 4)},
-        "mode": "pipelined: two batches on two streams, hyperbatch t+1 sampled while t gathers",
+        "mode": f"pipelined: {NSLOT} batch slots, a sampling stream and a gather stream; "
+                f"hyperbatches t+1..t+{D} sample while t gathers"
+                + ("; gathers queued back to back" if args.gather_first else "; sampling enqueued first"),
         "serial_ms_per_step": round(serial_ms, 4),
         "per_step": {"algorithmic_bytes": tot_bytes // K, "sample_bytes": tot_sample // K,
                      "gather_bytes": tot_gather // K, "rows": rows // K, "sampled_edges": edges // K},

@@ -203,13 +203,16 @@ agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);   /*
  *     hyperbatch (reported by agnes_batch_stats), 0 = off (default).
  *   AGNES_OPT_GATHER_GROUPS: most workgroups of the row-copy kernel, in
  *     [8, 65536] (default 2048).  Fewer leave room for another stream's work.
- *   AGNES_OPT_GATHER_UNROLL: rows each lane group keeps in flight, 2, 4 or 8
- *     (default 4).
- * Options change launch shapes only, never results. */
+ *   AGNES_OPT_GATHER_UNROLL: rows each lane group keeps in flight, 4, 8 or
+ *     16 (default 4).
+ *   AGNES_OPT_GATHER_NONTEMPORAL: 1 = write gathered rows with non-temporal
+ *     stores (default), 0 = ordinary stores.
+ * Options change launch shapes and store kinds only, never results. */
 typedef enum {
     AGNES_OPT_PROFILE = 1,
     AGNES_OPT_GATHER_GROUPS = 2,
-    AGNES_OPT_GATHER_UNROLL = 3
+    AGNES_OPT_GATHER_UNROLL = 3,
+    AGNES_OPT_GATHER_NONTEMPORAL = 4
 } agnes_option;
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value);
 

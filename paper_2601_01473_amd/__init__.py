@@ -93,12 +93,15 @@ class Store:
     def set_profiling(self, on: bool) -> None:
         agnes_store_set_option(self.handle, B.AGNES_OPT_PROFILE, 1 if on else 0)
 
-    def set_gather_shape(self, groups: int | None = None, unroll: int | None = None) -> None:
-        """Launch shape of the row-copy kernel (never changes results)."""
+    def set_gather_shape(self, groups: int | None = None, unroll: int | None = None,
+                         nontemporal: bool | None = None) -> None:
+        """Launch shape and store kind of the row-copy kernel (never change results)."""
         if groups is not None:
             agnes_store_set_option(self.handle, B.AGNES_OPT_GATHER_GROUPS, int(groups))
         if unroll is not None:
             agnes_store_set_option(self.handle, B.AGNES_OPT_GATHER_UNROLL, int(unroll))
+        if nontemporal is not None:
+            agnes_store_set_option(self.handle, B.AGNES_OPT_GATHER_NONTEMPORAL, 1 if nontemporal else 0)
 
     def prepare(self, targets: torch.Tensor, fanouts, seed: int = 0, mb_base: int = 0,
                 batch: "Batch | None" = None, stream=None) -> "Batch":

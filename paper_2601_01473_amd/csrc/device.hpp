@@ -67,22 +67,24 @@ __device__ __forceinline__ int upper_segment(const T* off, int n, T x) {
     return lo;
 }
 
-// Workgroup-wide search over a sorted array: the first index i in [lo, hi) with
-// !before(i) (or hi), for a predicate `before` that holds on a prefix.  Each
-// round, 256 threads test 256 evenly spaced indices, which narrows the range by
-// a factor of ~256; all threads must call it and all get the answer.
+// First index in [lo, hi) where before() is false, for a predicate that is true
+// on a prefix of the range, searched by one wave: every round the 64 lanes test
+// 64 evenly spaced indices, which narrows the range by a factor of ~64, so a
+// search over n entries costs about log64(n) memory round trips.  All lanes of
+// the wave must call it and all get the answer.
 template <typename Pred>
-__device__ __forceinline__ int64_t block_partition_point(int64_t lo, int64_t hi, Pred before) {
+__device__ __forceinline__ int64_t wave_partition_point(int64_t lo, int64_t hi, Pred before) {
+    const int lane = lane_id();
     while (lo < hi) {
         const int64_t n = hi - lo;
-        const int64_t step = (n + kBlock - 1) / kBlock;
-        const int64_t p = lo + (int64_t)threadIdx.x * step;
+        const int64_t step = (n + kWave - 1) / kWave;
+        const int64_t p = lo + (int64_t)lane * step;
         const bool probe = p < hi;
-        const int c = __syncthreads_count(probe && before(p));
-        const int probes = (int)((n + step - 1) / step);
-        const int64_t nlo = c == 0 ? lo : lo + (int64_t)(c - 1) * step + 1;
-        const int64_t nhi = c < probes ? lo + (int64_t)c * step : hi;
+        const int c = __popcll(__ballot(probe && before(p)));
         if (c == 0) return lo;
+        const int probes = (int)((n + step - 1) / step);
+        const int64_t nlo = lo + (int64_t)(c - 1) * step + 1;
+        const int64_t nhi = c < probes ? lo + (int64_t)c * step : hi;
         lo = nlo;
         hi = nhi;
     }
@@ -118,16 +120,13 @@ __device__ __forceinline__ uint64_t draw_below(uint64_t w, uint64_t n) { return 
 
 // ----------------------------------------------------------------- Floyd
 
-// Sample k of deg positions of node v (k < deg) and write the neighbours at those
-// positions, in ascending position order, to out[0..k).  Floyd's algorithm: draw
-// i (i = 0..k-1) picks d in [0, t], t = deg - k + i, and keeps t when d was
-// already chosen.  Word i comes from Philox(counter (i>>2, v, m, l), key (seed, 0)),
-// lane i & 3.  Positions live in registers; MAXK >= k.
+// Floyd's algorithm for k of deg positions of node v (k < deg): draw i
+// (i = 0..k-1) picks d in [0, t], t = deg - k + i, and keeps t when d was
+// already chosen.  Word i comes from Philox(counter (i>>2, v, m, l), key
+// (seed, 0)), lane i & 3.  pos[0..k) receives the positions in draw order; MAXK >= k.
 template <int MAXK>
-__device__ __forceinline__ void floyd_sample_regs(uint64_t deg, int k, uint64_t seed, uint64_t v,
-                                                  uint64_t m, uint64_t l, const int32_t* adj,
-                                                  int32_t* out) {
-    uint32_t pos[MAXK];
+__device__ __forceinline__ void floyd_positions(uint64_t deg, int k, uint64_t seed, uint64_t v, uint64_t m,
+                                                uint64_t l, uint32_t (&pos)[MAXK]) {
     Words4 words;
 #pragma unroll
     for (int i = 0; i < MAXK; i++) {
@@ -142,7 +141,18 @@ __device__ __forceinline__ void floyd_sample_regs(uint64_t deg, int k, uint64_t 
             pos[i] = seen ? (uint32_t)t : d;
         }
     }
-    // the output slot of a position is its rank among the chosen positions
+}
+
+// Neighbours at positions pos[0..k) of row adj written to out[0..k) in
+// ascending position order (the slot of a position is its rank).  Every load is
+// issued before the first store, so a request waits for one memory round trip.
+template <int MAXK>
+__device__ __forceinline__ void write_ranked(const uint32_t (&pos)[MAXK], int k, const int32_t* adj,
+                                             int32_t* out) {
+    int32_t val[MAXK];
+#pragma unroll
+    for (int a = 0; a < MAXK; a++)
+        if (a < k) val[a] = adj[pos[a]];
 #pragma unroll
     for (int a = 0; a < MAXK; a++) {
         if (a < k) {
@@ -150,12 +160,13 @@ __device__ __forceinline__ void floyd_sample_regs(uint64_t deg, int k, uint64_t 
 #pragma unroll
             for (int b = 0; b < MAXK; b++)
                 if (b < k) rank += (pos[b] < pos[a]) ? 1 : 0;
-            out[rank] = adj[pos[a]];
+            out[rank] = val[a];
         }
     }
 }
 
-// Same sampler for any k: the positions are staged in out[0..k) itself.
+// Any k: the positions are staged in out[0..k) itself, sorted, then replaced by
+// the neighbours eight at a time.
 __device__ __forceinline__ void floyd_sample_mem(uint64_t deg, int k, uint64_t seed, uint64_t v,
                                                  uint64_t m, uint64_t l, const int32_t* adj,
                                                  int32_t* out) {
@@ -174,7 +185,31 @@ __device__ __forceinline__ void floyd_sample_mem(uint64_t deg, int k, uint64_t s
         while (s >= 0 && out[s] > x) { out[s + 1] = out[s]; s--; }
         out[s + 1] = x;
     }
-    for (int i = 0; i < k; i++) out[i] = adj[out[i]];
+    for (int i0 = 0; i0 < k; i0 += 8) {
+        int32_t p[8], x[8];
+#pragma unroll
+        for (int t = 0; t < 8; t++)
+            if (i0 + t < k) p[t] = out[i0 + t];
+#pragma unroll
+        for (int t = 0; t < 8; t++)
+            if (i0 + t < k) x[t] = adj[p[t]];
+#pragma unroll
+        for (int t = 0; t < 8; t++)
+            if (i0 + t < k) out[i0 + t] = x[t];
+    }
+}
+
+// A whole row (k == deg), eight neighbours at a time.
+__device__ __forceinline__ void copy_row(const int32_t* adj, int k, int32_t* out) {
+    for (int i0 = 0; i0 < k; i0 += 8) {
+        int32_t x[8];
+#pragma unroll
+        for (int t = 0; t < 8; t++)
+            if (i0 + t < k) x[t] = adj[i0 + t];
+#pragma unroll
+        for (int t = 0; t < 8; t++)
+            if (i0 + t < k) out[i0 + t] = x[t];
+    }
 }
 
 }  // namespace agnes

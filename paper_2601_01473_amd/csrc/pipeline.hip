@@ -12,14 +12,11 @@
 //   k_sample    walks the list in block order: Floyd subsets from Philox words,
 //               neighbours written at the request's edge offset
 //   radix sort  the sampled neighbours by node id (stable: minibatch order kept)
-//   k_heads     runs of equal (node, minibatch); a run is a new node unless the
-//               list already holds it (merge-join search)
-//   scan        run numbers and new-node numbers
-//   k_runs      new nodes in (node, minibatch) order; local ids of old nodes
-//   group rank  stable count by minibatch: the rank of a new node among its
-//               minibatch's new nodes in id order gives its local id
-//   k_relabel   hop columns in local ids
-//   k_merge     new (node, minibatch) pairs merged into the sorted list
+//   join        merge path of the list with the sorted neighbours: a run of
+//               equal (node, minibatch) keys is an old node when the list holds
+//               the pair, else a new node; new nodes get local ids in id order
+//               per minibatch, every edge gets its column, and the new pairs
+//               are merged into the list (split, count, scan, write)
 // Gather (Alg. 1, gathering loop): the final list is the feature bucket in block
 // order; k_gather copies each row to every minibatch that needs it.
 //
@@ -60,9 +57,6 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
     g.jbits = jb;
     return g;
 }
-
-constexpr int kGroupWGs = 512;          // workgroups of the by-minibatch counting pass
-constexpr int kSortTileR = 2048;        // entries per tile of the by-minibatch ranking
 
 // ----------------------------------------------------------------- small kernels
 
@@ -193,16 +187,9 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, uint
                                                    const OffT* off, const int32_t* adj, int e_blk_log2,
                                                    int64_t nblk, const uint64_t* rl_key, const int32_t* rl_val,
                                                    const int64_t* req_off_g, const int64_t* e_off,
-                                                   int32_t* cg, int32_t* row_ptr,
-                                                   Ctl* ctl) {
-    extern __shared__ int64_t req_off[];      // [H+1] request offsets, then [H+1] edge offsets
-    int64_t* mb_e = req_off + (H + 1);
-    for (int i = threadIdx.x; i <= H; i += kBlock) {
-        int64_t ro = req_off_g[i];
-        req_off[i] = ro;
-        mb_e[i] = e_off[ro];
-    }
-    __syncthreads();
+                                                   int32_t* cg, Ctl* ctl) {
+    extern __shared__ int64_t req_off[];      // [H+1] request offsets
+    load_offsets(req_off, req_off_g, H);
     const int64_t R = ctl->R;
     for (int64_t base = (int64_t)blockIdx.x * kBlock; base < R; base += (int64_t)gridDim.x * kBlock) {
         int64_t p = base + threadIdx.x;
@@ -220,20 +207,25 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, uint
             if (blk >= nblk) blk = nblk - 1;
             int k = (int)(deg < f ? deg : f);
             int64_t eo = e_off[q];
-            int64_t mb_e0 = mb_e[j];
             int32_t* out = cg + eo;
             const int32_t* a = adj + o0;
-            if (k == deg) {
-                for (int t = 0; t < k; t++) out[t] = a[t];
-            } else if (MAXK > 0) {
-                floyd_sample_regs<(MAXK > 0 ? MAXK : 1)>((uint64_t)deg, k, seed, (uint64_t)v,
-                                                         (uint64_t)(mb_base + j), (uint64_t)l, a, out);
+            if (MAXK > 0) {
+                // positions (all of them for a take-all row), then one round of loads
+                constexpr int MK = MAXK > 0 ? MAXK : 1;
+                uint32_t pos[MK];
+                if (k == deg) {
+#pragma unroll
+                    for (int i = 0; i < MK; i++) pos[i] = (uint32_t)i;
+                } else {
+                    floyd_positions<MK>((uint64_t)deg, k, seed, (uint64_t)v, (uint64_t)(mb_base + j),
+                                        (uint64_t)l, pos);
+                }
+                write_ranked<MK>(pos, k, a, out);
+            } else if (k == deg) {
+                copy_row(a, k, out);
             } else {
                 floyd_sample_mem((uint64_t)deg, k, seed, (uint64_t)v, (uint64_t)(mb_base + j), (uint64_t)l, a, out);
             }
-            int64_t rp = req_off[j] + j + r;
-            row_ptr[rp] = (int32_t)(eo - mb_e0);
-            if (q + 1 == req_off[j + 1]) row_ptr[rp + 1] = (int32_t)(eo + k - mb_e0);
         }
         // a request opens a new Bck row when its block differs from the previous request's
         int64_t prev = (int64_t)shfl64((uint64_t)blk, lane_id() > 0 ? lane_id() - 1 : 0);
@@ -248,282 +240,384 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, uint
     }
 }
 
-// Runs of the sorted sampled neighbours.  For sorted edge p: (u, j) = (node,
-// minibatch of the edge); a run head is the first edge of a (u, j) pair.  A head
-// looks its pair up in the list (sorted the same way): found = an old node with
-// local id hl[p]; not found = a new node.  pk[p] = (head << 32) | new.
-// Each workgroup takes tiles of 2048 sorted edges, narrows the list to the key
-// range of the tile with two searches and stages that range in LDS.
-constexpr int kHeadTile = 2048;
-constexpr int kHeadCap = 2048;
+// ----------------------------------------------------------------- join
+//
+// After the sort, the hop's sampled edges B (keys (node, minibatch), sorted,
+// equal keys in edge order) are joined with the list A of the pairs already
+// held (sorted, unique keys, value = local id).  Both are ordered by key with A
+// first on equal keys, so the pair of a run of equal edge keys, if A holds it,
+// sits right before the run.  Merge path cuts the merged sequence into tiles of
+// kJoinTile entries: tile t holds A[a_t, a_{t+1}) and B[t*T - a_t, ...) with
+// a_t from k_join_split.  An edge whose key differs from the previous edge's
+// is a run head; a head whose pair A holds is an old node (the pair is in the
+// tile's A part or is A[a_t - 1]), otherwise a new one.  New nodes take local
+// ids |S_{j,l-1}| + (rank among the new nodes of minibatch j in key order), so
+// each minibatch's new nodes are ascending by id.  G workgroups take
+// consecutive runs of tiles: k_join_count counts the new nodes per minibatch
+// and the merged-list entries of every group, k_join_scan turns the counts into
+// offsets, k_join_write emits the merged list (A's entries and one entry per
+// new pair, in key order), the new nodes' ids and every edge's column.  The
+// number of groups G is a multiple of 256 chosen by the host (join_groups).
+constexpr int kJoinTile = 1024;                               // merged entries per tile
+constexpr int kJoinWaveItems = kJoinTile / kWavesPerBlock;    // edges of a tile per wave
+constexpr int kJoinRounds = kJoinWaveItems / kWave;
+constexpr uint64_t kNoKey = ~0ull;                            // no pair has this key (node < 2^31)
 
-__global__ __launch_bounds__(kBlock) void k_heads(int H, const int64_t* req_off, const int64_t* e_off,
-                                                  const uint32_t* su, const uint32_t* se,
-                                                  const uint64_t* rl_key, const int32_t* rl_val,
-                                                  int64_t* pk, int32_t* hl, const Ctl* ctl) {
+__device__ __forceinline__ uint64_t edge_key(const uint32_t* su, const uint32_t* se, const int64_t* mb_e, int H,
+                                             int64_t p) {
+    return ((uint64_t)su[p] << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)se[p]);
+}
+
+// a_t for every tile boundary t (one wave each): the number of A entries among
+// the first t * kJoinTile merged entries.
+__global__ __launch_bounds__(kBlock) void k_join_split(int H, const int64_t* req_off, const int64_t* e_off,
+                                                       const uint64_t* ak, const uint32_t* su, const uint32_t* se,
+                                                       int64_t* split, const Ctl* ctl) {
     extern __shared__ int64_t mb_e[];
-    __shared__ uint64_t tk[kHeadTile];
-    __shared__ uint64_t lk[kHeadCap];
-    __shared__ int32_t lv[kHeadCap];
-    __shared__ int64_t range[2];
-    __shared__ uint64_t prevk;
     load_mb_edges(mb_e, req_off, e_off, H);
-    const int t = threadIdx.x;
-    const int64_t S = ctl->S, R = ctl->R;
-    for (int64_t t0 = (int64_t)blockIdx.x * kHeadTile; t0 < S; t0 += (int64_t)gridDim.x * kHeadTile) {
-        const int cnt = (int)((S - t0) < kHeadTile ? (S - t0) : kHeadTile);
-        for (int i = t; i < cnt; i += kBlock)
-            tk[i] = ((uint64_t)su[t0 + i] << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)se[t0 + i]);
-        if (t == 0)
-            prevk = t0 > 0 ? (((uint64_t)su[t0 - 1] << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)se[t0 - 1]))
-                           : ~0ull;
-        __syncthreads();
-        {
-            // the list range holding the tile's keys: [lower_bound(first), upper_bound(last))
-            const uint64_t kf = tk[0], kl = tk[cnt - 1];
-            const int64_t a = block_partition_point(0, R, [&](int64_t i) { return rl_key[i] < kf; });
-            const int64_t b = block_partition_point(a, R, [&](int64_t i) { return rl_key[i] <= kl; });
-            if (t == 0) { range[0] = a; range[1] = b; }
-        }
-        __syncthreads();
-        const int64_t lo = range[0], hi = range[1];
-        const int64_t m = hi - lo;
-        const bool staged = m <= kHeadCap;
-        if (staged)
-            for (int i = t; i < m; i += kBlock) {
-                lk[i] = rl_key[lo + i];
-                lv[i] = rl_val[lo + i];
-            }
-        __syncthreads();
-        for (int i = t; i < cnt; i += kBlock) {
-            const uint64_t key = tk[i];
-            const bool head = key != (i > 0 ? tk[i - 1] : prevk);
-            bool found = false;
-            int32_t local = -1;
-            if (head) {
-                if (staged) {
-                    int a = 0, b = (int)m;
-                    while (a < b) {
-                        int mid = (a + b) >> 1;
-                        if (lk[mid] < key) a = mid + 1; else b = mid;
-                    }
-                    if (a < m && lk[a] == key) { found = true; local = lv[a]; }
-                } else {
-                    int64_t a = lo, b = hi;
-                    while (a < b) {
-                        int64_t mid = (a + b) >> 1;
-                        if (rl_key[mid] < key) a = mid + 1; else b = mid;
-                    }
-                    if (a < hi && rl_key[a] == key) { found = true; local = rl_val[a]; }
-                }
-            }
-            pk[t0 + i] = ((int64_t)(head ? 1 : 0) << 32) | (int64_t)((head && !found) ? 1 : 0);
-            hl[t0 + i] = local;
-        }
-        __syncthreads();
+    const int64_t na = ctl->R, nb = ctl->S, n = na + nb;
+    const int64_t tiles = (n + kJoinTile - 1) / kJoinTile;
+    const int64_t nw = (int64_t)gridDim.x * kWavesPerBlock;
+    for (int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave_id(); t <= tiles; t += nw) {
+        const int64_t d = std::min<int64_t>(t * kJoinTile, n);
+        const int64_t lo = d > nb ? d - nb : 0, hi = d < na ? d : na;
+        // A[i] goes before B[d-1-i] when A[i] <= B[d-1-i] (A first on equal keys)
+        const int64_t x = wave_partition_point(
+            lo, hi, [&](int64_t i) { return ak[i] <= edge_key(su, se, mb_e, H, d - 1 - i); });
+        if (lane_id() == 0) split[t] = x;
     }
 }
 
-// Heads of new pairs go to the new-node list (in (node, minibatch) order) with
-// their run number; heads of old pairs give their run its local id.
-__global__ __launch_bounds__(kBlock) void k_runs(int H, const int64_t* req_off, const int64_t* e_off,
-                                                 const uint32_t* su, const uint32_t* se, const int64_t* pk,
-                                                 const int64_t* pkx, const int32_t* hl, uint64_t* nl_key,
-                                                 int32_t* nl_run, int32_t* run_local, Ctl* ctl) {
-    extern __shared__ int64_t mb_e[];
-    load_mb_edges(mb_e, req_off, e_off, H);
-    const int64_t S = ctl->S;
-    if (blockIdx.x == 0 && threadIdx.x == 0) ctl->n_new = ctl->pktot & 0xFFFFFFFFll;
-    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < S; p += (int64_t)gridDim.x * kBlock) {
-        int64_t f = pk[p];
-        if (!(f >> 32)) continue;
-        int64_t x = pkx[p];
-        int32_t run = (int32_t)(x >> 32);
-        if (f & 1) {
-            int64_t ni = x & 0xFFFFFFFFll;
-            nl_key[ni] = ((uint64_t)su[p] << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)se[p]);
-            nl_run[ni] = run;
-        } else {
-            run_local[run] = hl[p];
-        }
+struct JoinSpan {
+    int64_t a0, b0;
+    int nA, nB;
+};
+
+__device__ __forceinline__ JoinSpan join_span(int64_t t, int64_t n, const int64_t* split) {
+    JoinSpan s;
+    const int64_t d0 = t * kJoinTile, d1 = std::min<int64_t>(d0 + kJoinTile, n);
+    s.a0 = split[t];
+    const int64_t a1 = split[t + 1];
+    s.b0 = d0 - s.a0;
+    s.nA = (int)(a1 - s.a0);
+    s.nB = (int)((d1 - a1) - s.b0);
+    return s;
+}
+
+// The tile in LDS: sk[0, nA) = A keys, sk[nA, nA + nB) = edge keys; sv = A local
+// ids, then edge numbers.  pre = {key of the edge before the tile, key of the A
+// entry before the tile} (kNoKey if none), pre_val = that A entry's local id.
+__device__ __forceinline__ void join_stage(const JoinSpan& s, const uint64_t* ak, const int32_t* av,
+                                           const uint32_t* su, const uint32_t* se, const int64_t* mb_e, int H,
+                                           uint64_t* sk, int32_t* sv, uint64_t* pre, int32_t* pre_val) {
+    for (int i = threadIdx.x; i < s.nA; i += kBlock) {
+        sk[i] = ak[s.a0 + i];
+        sv[i] = av[s.a0 + i];
+    }
+    for (int i = threadIdx.x; i < s.nB; i += kBlock) {
+        sk[s.nA + i] = edge_key(su, se, mb_e, H, s.b0 + i);
+        sv[s.nA + i] = (int32_t)se[s.b0 + i];
+    }
+    if (threadIdx.x == 0) {
+        pre[0] = s.b0 > 0 ? edge_key(su, se, mb_e, H, s.b0 - 1) : kNoKey;
+        pre[1] = s.a0 > 0 ? ak[s.a0 - 1] : kNoKey;
+        *pre_val = s.a0 > 0 ? av[s.a0 - 1] : 0;
     }
 }
 
-__device__ __forceinline__ void group_range(int64_t n, int g, int64_t& lo, int64_t& hi) {
-    int64_t chunk = (n + kGroupWGs - 1) / kGroupWGs;
-    lo = (int64_t)g * chunk;
-    if (lo > n) lo = n;
-    hi = lo + chunk;
-    if (hi > n) hi = n;
+__device__ __forceinline__ int lds_lower_bound(const uint64_t* sk, int lo, int hi, uint64_t key) {
+    while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        if (sk[mid] < key) lo = mid + 1; else hi = mid;
+    }
+    return lo;
 }
 
-// Per workgroup range of the new-node list: how many new nodes each minibatch has.
-__global__ __launch_bounds__(kBlock) void k_grp_hist(const uint64_t* nl_key, int H, int64_t* ghist,
-                                                     const Ctl* ctl) {
-    extern __shared__ uint32_t h[];
-    for (int j = threadIdx.x; j < H; j += kBlock) h[j] = 0;
-    __syncthreads();
-    int64_t lo, hi;
-    group_range(ctl->n_new, blockIdx.x, lo, hi);
-    for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock) atomicAdd(&h[(uint32_t)nl_key[i]], 1u);
-    __syncthreads();
-    for (int j = threadIdx.x; j < H; j += kBlock) ghist[(int64_t)j * kGroupWGs + blockIdx.x] = h[j];
+// Edge i of the tile (key K): head?  For a head, idx = lower bound of K in the
+// tile's A part, and found / floc = whether A holds K and its local id.
+struct EdgeFlags {
+    bool head, found;
+    int idx;
+    int32_t floc;
+};
+
+__device__ __forceinline__ EdgeFlags edge_flags(const uint64_t* sk, const int32_t* sv, int nA, int i, uint64_t K,
+                                                const uint64_t* pre, int32_t pre_val) {
+    EdgeFlags f{false, false, 0, 0};
+    const uint64_t prevK = i > 0 ? sk[nA + i - 1] : pre[0];
+    f.head = K != prevK;
+    if (f.head) {
+        f.idx = lds_lower_bound(sk, 0, nA, K);
+        if (f.idx < nA && sk[f.idx] == K) {
+            f.found = true;
+            f.floc = sv[f.idx];
+        } else if (pre[1] == K) {
+            f.found = true;
+            f.floc = pre_val;
+        }
+    }
+    return f;
 }
 
-// Per minibatch j (one workgroup each): offsets of each workgroup's range; the
-// minibatch's new-node count.
-__global__ __launch_bounds__(kBlock) void k_grp_scan(int64_t* ghist, int64_t* newcnt) {
+__device__ __forceinline__ void group_tiles(int64_t n, int g, int G, int64_t& t0, int64_t& t1) {
+    const int64_t tiles = (n + kJoinTile - 1) / kJoinTile;
+    const int64_t per = (tiles + G - 1) / G;
+    t0 = std::min<int64_t>(tiles, (int64_t)g * per);
+    t1 = std::min<int64_t>(tiles, t0 + per);
+}
+
+// Pass 1: per group, new nodes per minibatch (ghist[j][g]) and merged entries
+// (gemit[g]).  Also writes the hop's row pointers in request order: row r of
+// minibatch j starts at its edge offset minus the minibatch's first edge.
+// Dynamic LDS: mb_e[H+1], ro[H+1], sk[T], sv[T], count[H].
+__global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req_off, const int64_t* e_off,
+                                                       const uint64_t* ak, const int32_t* av, const uint32_t* su,
+                                                       const uint32_t* se, const int64_t* split, int G,
+                                                       int64_t* ghist, int64_t* gemit, int32_t* row_ptr,
+                                                       const Ctl* ctl) {
+    extern __shared__ int64_t lds[];
+    int64_t* mb_e = lds;
+    int64_t* ro = mb_e + H + 1;
+    uint64_t* sk = (uint64_t*)(ro + H + 1);
+    int32_t* sv = (int32_t*)(sk + kJoinTile);
+    uint32_t* count = (uint32_t*)(sv + kJoinTile);
+    __shared__ uint64_t pre[2];
+    __shared__ int32_t pre_val;
+    __shared__ uint32_t nh_total;
+    const int tid = threadIdx.x, g = blockIdx.x;
+    for (int j = tid; j < H; j += kBlock) count[j] = 0;
+    if (tid == 0) nh_total = 0;
+    for (int i = tid; i <= H; i += kBlock) ro[i] = req_off[i];
+    load_mb_edges(mb_e, req_off, e_off, H);
+    const int64_t R = ctl->R;
+    for (int64_t q = (int64_t)g * kBlock + tid; q < R; q += (int64_t)G * kBlock) {
+        const int j = upper_segment(ro, H, q);
+        row_ptr[q + j] = (int32_t)(e_off[q] - mb_e[j]);
+        if (q + 1 == ro[j + 1]) row_ptr[q + j + 1] = (int32_t)(e_off[q + 1] - mb_e[j]);
+    }
+    const int64_t n = R + ctl->S;
+    int64_t t0, t1;
+    group_tiles(n, g, G, t0, t1);
+    int64_t a_total = 0;
+    uint32_t nh = 0;
+    for (int64_t t = t0; t < t1; t++) {
+        const JoinSpan s = join_span(t, n, split);
+        join_stage(s, ak, av, su, se, mb_e, H, sk, sv, pre, &pre_val);
+        a_total += s.nA;
+        __syncthreads();
+        for (int i = tid; i < s.nB; i += kBlock) {
+            const uint64_t K = sk[s.nA + i];
+            const EdgeFlags f = edge_flags(sk, sv, s.nA, i, K, pre, pre_val);
+            if (f.head && !f.found) {
+                atomicAdd(&count[(uint32_t)K], 1u);
+                nh++;
+            }
+        }
+        __syncthreads();
+    }
+    if (nh) atomicAdd(&nh_total, nh);
+    __syncthreads();
+    for (int j = tid; j < H; j += kBlock) ghist[(int64_t)j * G + g] = count[j];
+    if (tid == 0) gemit[g] = a_total + nh_total;
+}
+
+// Workgroup j < H: exclusive scan of minibatch j's counts over the groups and
+// its new-node total; workgroup H: the same for the merged entries, and the
+// hop's new-node total (merged entries minus the old list).
+__global__ __launch_bounds__(kBlock) void k_join_scan(int H, int G, int64_t* ghist, int64_t* gemit,
+                                                      int64_t* newcnt, Ctl* ctl) {
     __shared__ int64_t lds[kWavesPerBlock];
-    int64_t* row = ghist + (int64_t)blockIdx.x * kGroupWGs;
-    constexpr int per = kGroupWGs / kBlock;
-    int64_t v[per];
+    const int x = blockIdx.x;
+    int64_t* row = x < H ? ghist + (int64_t)x * G : gemit;
+    const int per = G / kBlock;                // G is a multiple of kBlock
+    int64_t* mine = row + (int64_t)threadIdx.x * per;
     int64_t local = 0;
-#pragma unroll
-    for (int k = 0; k < per; k++) {
-        v[k] = row[threadIdx.x * per + k];
-        local += v[k];
-    }
+    for (int k = 0; k < per; k++) local += mine[k];
     int64_t total;
     int64_t ex = block_exclusive_scan(local, lds, total);
-#pragma unroll
     for (int k = 0; k < per; k++) {
-        row[threadIdx.x * per + k] = ex;
-        ex += v[k];
+        const int64_t v = mine[k];
+        mine[k] = ex;
+        ex += v;
     }
-    if (threadIdx.x == 0) newcnt[blockIdx.x] = total;
+    if (threadIdx.x == 0) {
+        if (x < H) newcnt[x] = total;
+        else ctl->n_new = total - ctl->R;
+    }
 }
 
-// Stable rank of each new node among the new nodes of its minibatch (the list
-// is in id order within a minibatch): local id = |S_{j,l-1}| + rank.  A
-// workgroup walks its range in tiles of 2048: wave w counts its 512 entries per
-// minibatch with ballots (lane order, then round order), the waves' counts are
-// stacked per minibatch (wave order), then every entry gets its local id.
-// Dynamic LDS: H int64 cursors + 4 x H int32 counts.
-__global__ __launch_bounds__(kBlock) void k_grp_rank(const uint64_t* nl_key, const int32_t* nl_run, int H,
-                                                     int jbits, const int64_t* ghist, const int32_t* size,
-                                                     int64_t capN, int32_t* nodes, int32_t* run_local,
-                                                     int32_t* nl_val, Ctl* ctl) {
-    extern __shared__ int64_t cursor[];
-    int32_t* wc = (int32_t*)(cursor + H);           // [kWavesPerBlock][H]
-    const int t = threadIdx.x, w = wave_id(), lane = lane_id();
-    for (int j = t; j < H; j += kBlock) cursor[j] = ghist[(int64_t)j * kGroupWGs + blockIdx.x] + size[j];
-    int64_t lo, hi;
-    group_range(ctl->n_new, blockIdx.x, lo, hi);
-    for (int64_t t0 = lo; t0 < hi; t0 += kSortTileR) {
-        for (int x = t; x < kWavesPerBlock * H; x += kBlock) wc[x] = 0;
+// Pass 2.  Wave w takes a quarter of the tile's edges in rounds of 64;
+// ballots give each edge the new heads before it in the wave and, for a new
+// head, its rank among the wave's new heads of the same minibatch (wave-private
+// counts wcnt[w][j]); after a barrier the waves' totals are stacked.  An edge
+// takes the local id of the last head at or before it (a head before the tile:
+// the old pair A[a_t - 1], or the newest new node of its minibatch so far).
+// Dynamic LDS: mb_e[H+1], sk[T], sv[T], loc[T], nhx[T+1], cursor[H], wcnt[4][H] (16-bit).
+__global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t capN, int64_t rows_cap,
+                                                       const int64_t* req_off, const int64_t* e_off,
+                                                       const uint64_t* ak, const int32_t* av, const uint32_t* su,
+                                                       const uint32_t* se, const int64_t* split, int G,
+                                                       const int64_t* ghist, const int64_t* gemit,
+                                                       const int32_t* size, int32_t* nodes, uint64_t* ck,
+                                                       int32_t* cv, int32_t* col, Ctl* ctl) {
+    extern __shared__ int64_t lds[];
+    int64_t* mb_e = lds;
+    uint64_t* sk = (uint64_t*)(mb_e + H + 1);
+    int32_t* sv = (int32_t*)(sk + kJoinTile);
+    int32_t* loc = sv + kJoinTile;
+    int32_t* nhx = loc + kJoinTile;
+    int32_t* cursor = nhx + kJoinTile + 1;
+    uint16_t* wcnt = (uint16_t*)(cursor + H);
+    __shared__ uint64_t pre[2];
+    __shared__ int32_t pre_val, cont_local;
+    __shared__ int32_t wnh[kWavesPerBlock], wanc[kWavesPerBlock];
+    const int tid = threadIdx.x, w = wave_id(), lane = lane_id(), g = blockIdx.x;
+    for (int j = tid; j < H; j += kBlock) {
+        cursor[j] = size[j] + (int32_t)ghist[(int64_t)j * G + g];
+        for (int x = 0; x < kWavesPerBlock; x++) wcnt[x * H + j] = 0;
+    }
+    load_mb_edges(mb_e, req_off, e_off, H);
+    const int64_t n = ctl->R + ctl->S;
+    int64_t t0, t1;
+    group_tiles(n, g, G, t0, t1);
+    int64_t run = gemit[g];                  // merged entries before the tile
+    const uint64_t lane_le = lanemask_lt() | (1ull << lane);
+    for (int64_t t = t0; t < t1; t++) {
+        const JoinSpan s = join_span(t, n, split);
+        join_stage(s, ak, av, su, se, mb_e, H, sk, sv, pre, &pre_val);
         __syncthreads();
-        int jr[8], rk[8];
+        if (tid == 0) {
+            // edges at the start of the tile that continue a run begun before it
+            int32_t c = 0;
+            if (s.nB > 0 && sk[s.nA] == pre[0]) c = (pre[1] == pre[0]) ? pre_val : cursor[(uint32_t)pre[0]] - 1;
+            cont_local = c;
+        }
+        uint64_t key[kJoinRounds];
+        int32_t nhw[kJoinRounds], jrk[kJoinRounds], anc[kJoinRounds], idx[kJoinRounds], floc[kJoinRounds];
+        uint32_t kind = 0;                   // per round: bit 2r = head, bit 2r+1 = new
+        int nh_run = 0, anc_run = -1;
 #pragma unroll
-        for (int r = 0; r < 8; r++) {
-            const int64_t i = t0 + w * 512 + r * kWave + lane;
-            const bool valid = i < hi;
-            const int j = valid ? (int)(uint32_t)nl_key[i] : 0;
-            uint64_t peers = __ballot(valid);
-            for (int b = 0; b < jbits; b++) {
-                uint64_t m = __ballot((j >> b) & 1);
-                peers &= ((j >> b) & 1) ? m : ~m;
+        for (int r = 0; r < kJoinRounds; r++) {
+            const int i = w * kJoinWaveItems + r * kWave + lane;
+            const bool valid = i < s.nB;
+            const uint64_t K = valid ? sk[s.nA + i] : 0;
+            EdgeFlags f{false, false, 0, 0};
+            if (valid) f = edge_flags(sk, sv, s.nA, i, K, pre, pre_val);
+            const bool nh = f.head && !f.found;
+            const uint64_t nhm = __ballot(nh);
+            nhw[r] = nh_run + __popcll(nhm & lanemask_lt());
+            nh_run += __popcll(nhm);
+            // rank among this wave's new heads of the same minibatch (lane order, then round order)
+            const int j = (int)(uint32_t)K;
+            uint64_t peers = nhm;
+            for (int bit = 0; bit < jbits; bit++) {
+                const uint64_t m = __ballot((j >> bit) & 1);
+                peers &= ((j >> bit) & 1) ? m : ~m;
             }
             const int rank = __popcll(peers & lanemask_lt());
-            const int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
+            const int leader = nh ? (__ffsll((unsigned long long)peers) - 1) : lane;
             int old = 0;
-            if (valid && rank == 0) {
-                old = wc[w * H + j];
-                wc[w * H + j] = old + __popcll(peers);
+            if (nh && rank == 0) {
+                old = wcnt[w * H + j];
+                wcnt[w * H + j] = (uint16_t)(old + __popcll(peers));
             }
             old = __shfl(old, leader, kWave);
-            jr[r] = valid ? j : -1;
-            rk[r] = old + rank;
+            jrk[r] = old + rank;
+            // last head at or before this edge in the wave
+            const uint64_t hm = __ballot(f.head);
+            const uint64_t le = hm & lane_le;
+            const int base = w * kJoinWaveItems + r * kWave;
+            anc[r] = le ? base + 63 - __clzll(le) : anc_run;
+            if (hm) anc_run = base + 63 - __clzll(hm);
+            key[r] = K;
+            idx[r] = f.idx;
+            floc[r] = f.floc;
+            kind |= ((f.head ? 1u : 0u) | (nh ? 2u : 0u)) << (2 * r);
+        }
+        if (lane == 0) {
+            wnh[w] = nh_run;
+            wanc[w] = anc_run;
         }
         __syncthreads();
-        for (int j = t; j < H; j += kBlock) {
-            int64_t c = cursor[j];
-            for (int ww = 0; ww < kWavesPerBlock; ww++) {
-                int n = wc[ww * H + j];
-                wc[ww * H + j] = (int32_t)c;
-                c += n;
-            }
-            cursor[j] = c;
-        }
-        __syncthreads();
+        int nh_base = 0, nh_total = 0, anc_carry = -1;
 #pragma unroll
-        for (int r = 0; r < 8; r++) {
-            if (jr[r] < 0) continue;
-            const int64_t i = t0 + w * 512 + r * kWave + lane;
-            const int j = jr[r];
-            const int64_t local = (int64_t)wc[w * H + j] + rk[r];
-            if (local >= capN) {
-                atomicOr((unsigned long long*)&ctl->err, 4ull);
-            } else {
-                nodes[(int64_t)j * capN + local] = (int32_t)(nl_key[i] >> 32);
-                run_local[nl_run[i]] = (int32_t)local;
-                nl_val[i] = (int32_t)local;
+        for (int x = 0; x < kWavesPerBlock; x++) {
+            if (x < w) {
+                nh_base += wnh[x];
+                anc_carry = std::max(anc_carry, wanc[x]);
+            }
+            nh_total += wnh[x];
+        }
+#pragma unroll
+        for (int r = 0; r < kJoinRounds; r++) {
+            const int i = w * kJoinWaveItems + r * kWave + lane;
+            if (i >= s.nB) continue;
+            nhx[i] = nh_base + nhw[r];
+            if (anc[r] < 0) anc[r] = anc_carry;
+            if ((kind >> (2 * r)) & 1u) {
+                int32_t lc = floc[r];
+                if ((kind >> (2 * r)) & 2u) {
+                    const int j = (int)(uint32_t)key[r];
+                    int rank = jrk[r];
+                    for (int x = 0; x < w; x++) rank += wcnt[x * H + j];
+                    lc = cursor[j] + rank;
+                    const int64_t pos = run + idx[r] + nh_base + nhw[r];
+                    if (lc >= capN || pos >= rows_cap) {
+                        atomicOr((unsigned long long*)&ctl->err, 4ull);
+                    } else {
+                        nodes[(int64_t)j * capN + lc] = (int32_t)(key[r] >> 32);
+                        ck[pos] = key[r];
+                        cv[pos] = lc;
+                    }
+                }
+                loc[i] = lc;
             }
         }
+        if (tid == 0) nhx[s.nB] = nh_total;
+        __syncthreads();
+        // every edge's column; A's entries at their merged positions
+#pragma unroll
+        for (int r = 0; r < kJoinRounds; r++) {
+            const int i = w * kJoinWaveItems + r * kWave + lane;
+            if (i < s.nB) col[sv[s.nA + i]] = anc[r] >= 0 ? loc[anc[r]] : cont_local;
+        }
+        for (int ia = tid; ia < s.nA; ia += kBlock) {
+            const uint64_t K = sk[ia];
+            const int lb = lds_lower_bound(sk, s.nA, s.nA + s.nB, K) - s.nA;
+            const int64_t pos = run + ia + nhx[lb];
+            if (pos < rows_cap) {
+                ck[pos] = K;
+                cv[pos] = sv[ia];
+            }
+        }
+        for (int j = tid; j < H; j += kBlock) {
+            int tot = 0;
+            for (int x = 0; x < kWavesPerBlock; x++) {
+                tot += wcnt[x * H + j];
+                wcnt[x * H + j] = 0;
+            }
+            cursor[j] += tot;
+        }
+        run += s.nA + nh_total;
         __syncthreads();
     }
 }
 
-// Every sampled edge takes the local id of its run.
-__global__ __launch_bounds__(kBlock) void k_relabel(const int64_t* pk, const int64_t* pkx, const uint32_t* se,
-                                                    const int32_t* run_local, int32_t* col, const Ctl* ctl) {
-    const int64_t S = ctl->S;
-    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < S; p += (int64_t)gridDim.x * kBlock) {
-        int32_t run = (int32_t)((pkx[p] + pk[p]) >> 32) - 1;
-        col[se[p]] = run_local[run];
-    }
+// Tiles of the join at any hop: the list and the edges together fit the maxima.
+static int64_t join_tiles_max(const Geometry& g) { return (g.Rmax + g.Smax) / kJoinTile + 1; }
+
+// Workgroups of the join passes: enough for one tile each on large hops, while
+// the per-minibatch count table (H x G) stays near 4M entries.
+static int join_groups(const Geometry& g) {
+    int64_t G = std::min<int64_t>(4096, std::max<int64_t>(256, (int64_t)(4 << 20) / g.H));
+    G = std::min<int64_t>(G, std::max<int64_t>(256, join_tiles_max(g)));
+    return (int)((G + kBlock - 1) / kBlock * kBlock);
 }
 
-// Merge of the list (R pairs) with the hop's new pairs (n_new), both sorted and
-// disjoint, by merge path: a workgroup takes 2048 outputs, finds where they
-// start and end on the two inputs (two searches), stages both pieces in LDS and
-// every thread merges 8 outputs after a local search.
-constexpr int kMergeTile = 2048;
-constexpr int kMergeItems = kMergeTile / kBlock;
-
-__global__ __launch_bounds__(kBlock) void k_merge(const uint64_t* ak, const int32_t* av, const uint64_t* bk,
-                                                  const int32_t* bv, uint64_t* ck, int32_t* cv, const Ctl* ctl) {
-    __shared__ uint64_t sk[kMergeTile];
-    __shared__ int32_t sv[kMergeTile];
-    __shared__ int64_t split[2];
-    const int t = threadIdx.x;
-    const int64_t na = ctl->R, nb = ctl->n_new, n = na + nb;
-    for (int64_t d0 = (int64_t)blockIdx.x * kMergeTile; d0 < n; d0 += (int64_t)gridDim.x * kMergeTile) {
-        const int64_t d1 = (n - d0) < kMergeTile ? n : d0 + kMergeTile;
-        if (t < 2) {
-            // merge path: number of A elements among the first d outputs
-            const int64_t d = t == 0 ? d0 : d1;
-            int64_t lo = d > nb ? d - nb : 0, hi = d < na ? d : na;
-            while (lo < hi) {
-                int64_t mid = (lo + hi) >> 1;
-                if (ak[mid] < bk[d - 1 - mid]) lo = mid + 1; else hi = mid;
-            }
-            split[t] = lo;
-        }
-        __syncthreads();
-        const int64_t a0 = split[0], a1 = split[1];
-        const int64_t b0 = d0 - a0, b1 = d1 - a1;
-        const int nA = (int)(a1 - a0), nB = (int)(b1 - b0);
-        for (int i = t; i < nA; i += kBlock) { sk[i] = ak[a0 + i]; sv[i] = av[a0 + i]; }
-        for (int i = t; i < nB; i += kBlock) { sk[nA + i] = bk[b0 + i]; sv[nA + i] = bv[b0 + i]; }
-        __syncthreads();
-        const int dl = t * kMergeItems;
-        const int total = nA + nB;
-        if (dl < total) {
-            int lo = dl > nB ? dl - nB : 0, hi = dl < nA ? dl : nA;
-            while (lo < hi) {
-                int mid = (lo + hi) >> 1;
-                if (sk[mid] < sk[nA + dl - 1 - mid]) lo = mid + 1; else hi = mid;
-            }
-            int ai = lo, bi = dl - lo;
-            for (int k = 0; k < kMergeItems && dl + k < total; k++) {
-                const bool takea = bi >= nB || (ai < nA && sk[ai] < sk[nA + bi]);
-                const int src = takea ? ai++ : nA + bi++;
-                ck[d0 + dl + k] = sk[src];
-                cv[d0 + dl + k] = sv[src];
-            }
-        }
-        __syncthreads();
-    }
+static size_t join_count_lds(int H) { return (size_t)(H + 1) * 16 + (size_t)kJoinTile * 12 + (size_t)H * 4; }
+static size_t join_write_lds(int H) {
+    return (size_t)(H + 1) * 8 + (size_t)kJoinTile * 8 + (size_t)kJoinTile * 4 * 3 + 4 + (size_t)H * 4 +
+           (size_t)kWavesPerBlock * H * 2;
 }
 
 // ----------------------------------------------------------------- gather
@@ -534,12 +628,13 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // gathering loop in block order: the requests of a feature block are contiguous
 // and those of one node are neighbours, so each row is loaded from HBM once and
 // written to every minibatch that needs it (dest = node_off[j] + local id).
-// LPR lanes share a row (16-byte or 4-byte units).  Each lane group loads the
-// keys of U rows, then U row pieces, then stores them, so U rows are in flight
-// per group.  Workgroup b takes a contiguous range; ranges are dealt so that
-// neighbouring ranges (the same blocks) run on the same XCD.  Also counts the
-// distinct rows and the non-empty feature-block rows.
-template <typename Unit, int LPR, int U>
+// LPR lanes share a row (16-byte or 4-byte units).  A lane group keeps U rows in
+// flight: it loads the U rows' pieces, fetches the list entries of its next U
+// rows while those loads are outstanding, then stores.  Workgroup b takes a
+// contiguous range of the list; ranges are dealt so that neighbouring ranges
+// (the same blocks) run on the same XCD.  Also counts the distinct rows and the
+// non-empty feature-block rows.
+template <typename Unit, int LPR, int U, bool NT>
 __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat, Unit* __restrict__ out,
                                                    int32_t* __restrict__ nodes_out,
                                                    const uint64_t* __restrict__ rl_key,
@@ -548,6 +643,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
                                                    Ctl* ctl) {
     constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
     constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
+    constexpr int64_t STEP = (int64_t)GPB * U;   // list entries per workgroup iteration
     extern __shared__ int64_t node_off[];
     __shared__ unsigned long long cnt[2];
     if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
@@ -561,28 +657,38 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
     const int li = lane_id() % LPR;
     const int gid = wave_id() * RPW + lane_id() / LPR;
     unsigned long long nd = 0, nf = 0;
-    for (int64_t e0 = lo + gid; e0 < hi; e0 += (int64_t)GPB * U) {
+    uint64_t key[U];
+    int32_t val[U];
+#pragma unroll
+    for (int k = 0; k < U; k++) {
+        const int64_t e = lo + gid + (int64_t)k * GPB;
+        key[k] = e < hi ? rl_key[e] : 0;
+        val[k] = e < hi ? rl_val[e] : 0;
+    }
+    for (int64_t e0 = lo + gid; e0 < hi; e0 += STEP) {
         int64_t src[U], dst[U];
         bool ok[U];
 #pragma unroll
         for (int k = 0; k < U; k++) {
             const int64_t e = e0 + (int64_t)k * GPB;
             ok[k] = e < hi;
-            src[k] = 0;
-            dst[k] = 0;
-            if (ok[k]) {
-                const uint64_t key = rl_key[e];
-                const uint32_t u = (uint32_t)(key >> 32);
-                src[k] = (int64_t)u * row_units;
-                const int64_t d = node_off[(uint32_t)key] + rl_val[e];
-                dst[k] = d * row_units;
-                if (li == 0) {
-                    nodes_out[d] = (int32_t)u;
-                    const uint32_t pu = e > 0 ? (uint32_t)(rl_key[e - 1] >> 32) : 0xFFFFFFFFu;
-                    nd += (pu != u);
-                    nf += (e == 0 || pu / rpb != u / rpb);
-                }
+            const uint32_t u = (uint32_t)(key[k] >> 32);
+            const int64_t d = node_off[(uint32_t)key[k]] + val[k];
+            src[k] = ok[k] ? (int64_t)u * row_units : 0;
+            dst[k] = ok[k] ? d * row_units : 0;
+            if (ok[k] && li == 0) {
+                nodes_out[d] = (int32_t)u;
+                const uint32_t pu = e > 0 ? (uint32_t)(rl_key[e - 1] >> 32) : 0xFFFFFFFFu;
+                nd += (pu != u);
+                nf += (e == 0 || pu / rpb != u / rpb);
             }
+        }
+        // list entries of the next iteration, fetched while this one's rows load
+#pragma unroll
+        for (int k = 0; k < U; k++) {
+            const int64_t e = e0 + STEP + (int64_t)k * GPB;
+            key[k] = e < hi ? rl_key[e] : 0;
+            val[k] = e < hi ? rl_val[e] : 0;
         }
         for (int64_t c = li; c < row_units; c += LPR) {
             Unit x[U];
@@ -590,8 +696,11 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             for (int k = 0; k < U; k++)
                 if (ok[k]) x[k] = feat[src[k] + c];
 #pragma unroll
-            for (int k = 0; k < U; k++)
-                if (ok[k]) __builtin_nontemporal_store(x[k], out + dst[k] + c);
+            for (int k = 0; k < U; k++) {
+                if (!ok[k]) continue;
+                if (NT) __builtin_nontemporal_store(x[k], out + dst[k] + c);
+                else out[dst[k] + c] = x[k];
+            }
         }
     }
     if (nd) atomicAdd(&cnt[0], nd);
@@ -603,42 +712,48 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
     }
 }
 
-template <typename Unit, int LPR>
-static void launch_gather_u(int unroll, dim3 grid, size_t lds, hipStream_t st, const Unit* f, Unit* o,
-                            int32_t* nodes_out, const uint64_t* rl_key, const int32_t* rl_val,
-                            const int64_t* node_off, int H, int64_t rows, int64_t row_units, uint32_t rpb,
-                            Ctl* ctl) {
-    if (unroll >= 8)
-        hipLaunchKernelGGL((k_gather<Unit, LPR, 8>), grid, dim3(kBlock), lds, st, f, o, nodes_out, rl_key, rl_val,
-                           node_off, H, rows, row_units, rpb, ctl);
-    else if (unroll >= 4)
-        hipLaunchKernelGGL((k_gather<Unit, LPR, 4>), grid, dim3(kBlock), lds, st, f, o, nodes_out, rl_key, rl_val,
-                           node_off, H, rows, row_units, rpb, ctl);
-    else
-        hipLaunchKernelGGL((k_gather<Unit, LPR, 2>), grid, dim3(kBlock), lds, st, f, o, nodes_out, rl_key, rl_val,
-                           node_off, H, rows, row_units, rpb, ctl);
+struct GatherArgs {
+    const void* feat;
+    void* out;
+    int32_t* nodes_out;
+    const uint64_t* rl_key;
+    const int32_t* rl_val;
+    const int64_t* node_off;
+    int H;
+    int64_t rows, row_units;
+    uint32_t rpb;
+    Ctl* ctl;
+};
+
+template <typename Unit, int LPR, int U, bool NT>
+static void launch_gather_k(const GatherArgs& a, int G, hipStream_t st) {
+    const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
+    hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
+                       (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.rows, a.row_units,
+                       a.rpb, a.ctl);
 }
 
+template <typename Unit, int LPR>
+static void launch_gather_lpr(const GatherArgs& a, int G, int unroll, bool nt, hipStream_t st) {
+    if (unroll >= 16) {
+        if (nt) launch_gather_k<Unit, LPR, 16, true>(a, G, st); else launch_gather_k<Unit, LPR, 16, false>(a, G, st);
+    } else if (unroll >= 8) {
+        if (nt) launch_gather_k<Unit, LPR, 8, true>(a, G, st); else launch_gather_k<Unit, LPR, 8, false>(a, G, st);
+    } else {
+        if (nt) launch_gather_k<Unit, LPR, 4, true>(a, G, st); else launch_gather_k<Unit, LPR, 4, false>(a, G, st);
+    }
+}
+
+// LPR = the power of two lanes that covers a row best (at most a wave).
 template <typename Unit>
-static void launch_gather(const void* feat, void* out, int32_t* nodes_out, const uint64_t* rl_key,
-                          const int32_t* rl_val, const int64_t* node_off, int H, int64_t rows,
-                          int64_t row_units, uint32_t rpb, Ctl* ctl, int groups, int unroll, hipStream_t st) {
-    int G = grid_for(rows * row_units / 64 + 1, groups);
+static void launch_gather(const GatherArgs& a, int groups, int unroll, bool nt, hipStream_t st) {
+    int G = grid_for(a.rows * a.row_units / 64 + 1, groups);
     G = std::max(8, (G + 7) / 8 * 8);
-    const Unit* f = (const Unit*)feat;
-    Unit* o = (Unit*)out;
-    const size_t lds = (size_t)(H + 1) * sizeof(int64_t);
-    const dim3 grid(G);
-    if (row_units >= 64)
-        launch_gather_u<Unit, 64>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
-    else if (row_units > 16)
-        launch_gather_u<Unit, 32>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
-    else if (row_units > 8)
-        launch_gather_u<Unit, 16>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
-    else if (row_units > 4)
-        launch_gather_u<Unit, 8>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
-    else
-        launch_gather_u<Unit, 4>(unroll, grid, lds, st, f, o, nodes_out, rl_key, rl_val, node_off, H, rows, row_units, rpb, ctl);
+    if (a.row_units >= 64) launch_gather_lpr<Unit, 64>(a, G, unroll, nt, st);
+    else if (a.row_units > 16) launch_gather_lpr<Unit, 32>(a, G, unroll, nt, st);
+    else if (a.row_units > 8) launch_gather_lpr<Unit, 16>(a, G, unroll, nt, st);
+    else if (a.row_units > 4) launch_gather_lpr<Unit, 8>(a, G, unroll, nt, st);
+    else launch_gather_lpr<Unit, 4>(a, G, unroll, nt, st);
 }
 
 // ----------------------------------------------------------------- host orchestration
@@ -676,14 +791,9 @@ static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout&
     w.sval.reserve((size_t)g.sort_max * 4);
     w.skey2.reserve((size_t)g.sort_max * 4);
     w.sval2.reserve((size_t)g.sort_max * 4);
-    w.pk.reserve((size_t)g.Smax * 8);
-    w.pkx.reserve((size_t)(g.Smax + 1) * 8);
-    w.hl.reserve((size_t)g.Smax * 4);
-    w.nl_key.reserve((size_t)g.Smax * 8);
-    w.nl_run.reserve((size_t)g.Smax * 4);
-    w.nl_val.reserve((size_t)g.Smax * 4);
-    w.run_local.reserve((size_t)g.Smax * 4);
-    w.ghist.reserve((size_t)H * kGroupWGs * 8);
+    w.split.reserve((size_t)(join_tiles_max(g) + 2) * 8);
+    w.ghist.reserve((size_t)H * join_groups(g) * 8);
+    w.gemit.reserve((size_t)join_groups(g) * 8);
     w.rs_hist.reserve((size_t)radix_hist_entries(g.sort_max) * 4);
     w.rs_dtot.reserve((size_t)radix_dtot_entries() * 4);
     w.scan_part.reserve((size_t)scan_partials_needed() * 8);
@@ -700,7 +810,6 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     const OffT* off = s.offsets.as<OffT>();
     const size_t lds_h = (size_t)(g.H + 1) * sizeof(int64_t);
     const int gR = grid_for(g.Rmax, 2048);
-    const int gS = grid_for(g.Smax, 4096);
     int64_t* part = w.scan_part.as<int64_t>();
     const uint64_t* rlk = w.rl_key[cur].as<uint64_t>();
     const int32_t* rlv = w.rl_val[cur].as<int32_t>();
@@ -711,13 +820,12 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     hipLaunchKernelGGL(k_count<OffT>, dim3(gR), dim3(kBlock), lds_h, st, g.H, g.capN, f, off,
                        w.nodes.as<int32_t>(), w.req_off.as<int64_t>(), w.cnt.as<int32_t>(), ctl);
     scan_counts(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, g.Rmax, &ctl->S, part, st);
-    int32_t* rp = b.row_ptr[l].as<int32_t>();
     const int32_t* adj = s.indices.as<int32_t>();
     int32_t* cg = w.skey.as<int32_t>();
 #define AGNES_SAMPLE(MK)                                                                               \
-    hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), 2 * lds_h, st, l, g.H, f, seed,     \
+    hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, seed,     \
                        mb_base, off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),      \
-                       w.e_off.as<int64_t>(), cg, rp, ctl)
+                       w.e_off.as<int64_t>(), cg, ctl)
     if (f <= 4) AGNES_SAMPLE(4);
     else if (f <= 8) AGNES_SAMPLE(8);
     else if (f <= 16) AGNES_SAMPLE(16);
@@ -730,27 +838,22 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
                                     w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
     const uint32_t* su = in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>();
     const uint32_t* se = in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>();
-    const int gH = (int)std::min<int64_t>(4096, std::max<int64_t>(1, (g.Smax + kHeadTile - 1) / kHeadTile));
-    hipLaunchKernelGGL(k_heads, dim3(gH), dim3(kBlock), lds_h, st, g.H, w.req_off.as<int64_t>(),
-                       w.e_off.as<int64_t>(), su, se, rlk, rlv, w.pk.as<int64_t>(), w.hl.as<int32_t>(), ctl);
-    scan_counts64(w.pk.as<int64_t>(), w.pkx.as<int64_t>(), &ctl->S, g.Smax, &ctl->pktot, part, st);
-    hipLaunchKernelGGL(k_runs, dim3(gS), dim3(kBlock), lds_h, st, g.H, w.req_off.as<int64_t>(),
-                       w.e_off.as<int64_t>(), su, se, w.pk.as<int64_t>(), w.pkx.as<int64_t>(),
-                       w.hl.as<int32_t>(), w.nl_key.as<uint64_t>(), w.nl_run.as<int32_t>(),
-                       w.run_local.as<int32_t>(), ctl);
-    hipLaunchKernelGGL(k_grp_hist, dim3(kGroupWGs), dim3(kBlock), (size_t)g.H * 4, st, w.nl_key.as<uint64_t>(),
-                       g.H, w.ghist.as<int64_t>(), ctl);
-    hipLaunchKernelGGL(k_grp_scan, dim3(g.H), dim3(kBlock), 0, st, w.ghist.as<int64_t>(), w.newcnt.as<int64_t>());
-    hipLaunchKernelGGL(k_grp_rank, dim3(kGroupWGs), dim3(kBlock), (size_t)g.H * 8 + (size_t)kWavesPerBlock * g.H * 4,
-                       st, w.nl_key.as<uint64_t>(),
-                       w.nl_run.as<int32_t>(), g.H, g.jbits, w.ghist.as<int64_t>(), w.size.as<int32_t>(), g.capN,
-                       w.nodes.as<int32_t>(), w.run_local.as<int32_t>(), w.nl_val.as<int32_t>(), ctl);
-    hipLaunchKernelGGL(k_relabel, dim3(gS), dim3(kBlock), 0, st, w.pk.as<int64_t>(), w.pkx.as<int64_t>(), se,
-                       w.run_local.as<int32_t>(), b.col[l].as<int32_t>(), ctl);
-    const int gM = (int)std::min<int64_t>(4096, (g.rows_max + kMergeTile - 1) / kMergeTile);
-    hipLaunchKernelGGL(k_merge, dim3(gM), dim3(kBlock), 0, st, rlk, rlv, w.nl_key.as<uint64_t>(),
-                       w.nl_val.as<int32_t>(), w.rl_key[cur ^ 1].as<uint64_t>(), w.rl_val[cur ^ 1].as<int32_t>(),
-                       ctl);
+    // join with the list: the next list, new node ids and the hop's columns
+    const int gJ = (int)std::min<int64_t>(2048, (join_tiles_max(g) + 1 + kWavesPerBlock - 1) / kWavesPerBlock);
+    int64_t* split = w.split.as<int64_t>();
+    hipLaunchKernelGGL(k_join_split, dim3(gJ), dim3(kBlock), lds_h, st, g.H, w.req_off.as<int64_t>(),
+                       w.e_off.as<int64_t>(), rlk, su, se, split, ctl);
+    const int G = join_groups(g);
+    hipLaunchKernelGGL(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H), st, g.H,
+                       w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se, split, G,
+                       w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), b.row_ptr[l].as<int32_t>(), ctl);
+    hipLaunchKernelGGL(k_join_scan, dim3(g.H + 1), dim3(kBlock), 0, st, g.H, G, w.ghist.as<int64_t>(),
+                       w.gemit.as<int64_t>(), w.newcnt.as<int64_t>(), ctl);
+    hipLaunchKernelGGL(k_join_write, dim3(G), dim3(kBlock), join_write_lds(g.H), st, g.H, g.jbits,
+                       g.capN, g.rows_max, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se,
+                       split, G, w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), w.size.as<int32_t>(),
+                       w.nodes.as<int32_t>(), w.rl_key[cur ^ 1].as<uint64_t>(), w.rl_val[cur ^ 1].as<int32_t>(),
+                       b.col[l].as<int32_t>(), ctl);
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
@@ -762,6 +865,8 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
     if (b.state == kGathering) wait_batch(b);
     b.state = kIdle;
     Geometry g = plan(s, H, B, fanouts, L);
+    AGNES_REQUIRE(join_write_lds(H) <= (size_t)s.max_lds && (size_t)(H + 1) * 16 <= (size_t)s.max_lds,
+                  AGNES_ERR_RANGE, "H is too large for the device's workgroup memory");
     SyncLayout y = sync_layout(H, L);
     Workspace& w = b.ws;
     reserve_workspace(w, g, y);
@@ -867,14 +972,15 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     const uint64_t* rlk = w.rl_key[b.cur].as<uint64_t>();
     const int32_t* rlv = w.rl_val[b.cur].as<int32_t>();
     if (rows > 0) {
-        if (s.row_bytes % 16 == 0)
-            launch_gather<u32x4>(s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv,
-                                 w.mb_off.as<int64_t>(), H, rows, s.row_bytes / 16, (uint32_t)s.rpb, ctl,
-                                 s.gather_groups, s.gather_unroll, st);
-        else
-            launch_gather<uint32_t>(s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv,
-                                    w.mb_off.as<int64_t>(), H, rows, s.row_bytes / 4, (uint32_t)s.rpb, ctl,
-                                    s.gather_groups, s.gather_unroll, st);
+        GatherArgs ga{s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv, w.mb_off.as<int64_t>(),
+                      H, rows, 0, (uint32_t)s.rpb, ctl};
+        if (s.row_bytes % 16 == 0) {
+            ga.row_units = s.row_bytes / 16;
+            launch_gather<u32x4>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, st);
+        } else {
+            ga.row_units = s.row_bytes / 4;
+            launch_gather<uint32_t>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, st);
+        }
     }
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));

@@ -145,11 +145,13 @@ void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_
 // ----------------------------------------------------------------- radix sort
 
 // LSD radix sort of 32-bit keys with 32-bit values, 8-bit digits, tiles of
-// 2048 keys.  Per pass: (1) digit histogram of every tile, (2) per digit, an
-// exclusive scan over the tiles, (3) each tile ranks its keys stably, reorders
-// them by digit in LDS and writes every digit's run contiguously.
-constexpr int kSortItems = 8;
-constexpr int kSortTile = kBlock * kSortItems;     // 2048 keys
+// 4096 keys.  Per pass: (1) digit histogram of every tile, stored tile-major
+// (each tile writes its 256 counts contiguously), (2) per digit, an exclusive
+// scan over the tiles (the table is small and stays in L2), (3) each tile ranks
+// its keys stably, reorders them by digit in LDS and writes every digit's run
+// contiguously.
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kBlock * kSortItems;     // 4096 keys
 constexpr int kRadixBits = 8;
 constexpr int kRadixBins = 1 << kRadixBits;
 
@@ -158,56 +160,61 @@ int64_t radix_hist_entries(int64_t n_max) { return (int64_t)kRadixBins * radix_t
 int64_t radix_dtot_entries() { return kRadixBins; }
 
 __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const int64_t* n_dev, int shift,
-                                                    int tiles, uint32_t* hist) {
+                                                    uint32_t* hist) {
     __shared__ uint32_t h[kRadixBins];
     const int64_t n = *n_dev;
     const int64_t t0 = (int64_t)blockIdx.x * kSortTile;
     if (t0 >= n) return;                        // tiles past the end are not scanned
     h[threadIdx.x] = 0;
-    __syncthreads();
-    for (int k = 0; k < kSortItems; k++) {
-        int64_t i = t0 + k * kBlock + threadIdx.x;
-        if (i < n) atomicAdd(&h[(keys[i] >> shift) & (kRadixBins - 1)], 1u);
+    uint32_t k[kSortItems];
+#pragma unroll
+    for (int q = 0; q < kSortItems; q++) {
+        const int64_t i = t0 + q * kBlock + threadIdx.x;
+        k[q] = i < n ? keys[i] : 0u;
     }
     __syncthreads();
-    hist[(int64_t)threadIdx.x * tiles + blockIdx.x] = h[threadIdx.x];
+#pragma unroll
+    for (int q = 0; q < kSortItems; q++)
+        if (t0 + q * kBlock + threadIdx.x < n) atomicAdd(&h[(k[q] >> shift) & (kRadixBins - 1)], 1u);
+    __syncthreads();
+    hist[(int64_t)blockIdx.x * kRadixBins + threadIdx.x] = h[threadIdx.x];
 }
 
-// One workgroup per digit: exclusive scan over the tiles that hold keys (in
-// place), digit total.
-__global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, int tiles_max, const int64_t* n_dev,
-                                                    uint32_t* dtot) {
+// One workgroup per digit: exclusive scan over the tiles that hold keys of
+// column d of the tile-major table (in place), digit total.
+__global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_t* n_dev, uint32_t* dtot) {
     __shared__ uint32_t lds[kWavesPerBlock];
-    uint32_t* row = hist + (int64_t)blockIdx.x * tiles_max;
+    const int d = blockIdx.x;
     const int tiles = (int)((*n_dev + kSortTile - 1) / kSortTile);
     uint32_t carry = 0;
     for (int b0 = 0; b0 < tiles; b0 += kBlock * 4) {
         uint32_t v[4];
         uint32_t local = 0;
+#pragma unroll
         for (int k = 0; k < 4; k++) {
-            int i = b0 + threadIdx.x * 4 + k;
-            v[k] = i < tiles ? row[i] : 0u;
+            const int i = b0 + threadIdx.x * 4 + k;
+            v[k] = i < tiles ? hist[(int64_t)i * kRadixBins + d] : 0u;
             local += v[k];
         }
         uint32_t total;
         uint32_t ex = block_exclusive_scan(local, lds, total) + carry;
+#pragma unroll
         for (int k = 0; k < 4; k++) {
-            int i = b0 + threadIdx.x * 4 + k;
-            if (i < tiles) row[i] = ex;
+            const int i = b0 + threadIdx.x * 4 + k;
+            if (i < tiles) hist[(int64_t)i * kRadixBins + d] = ex;
             ex += v[k];
         }
         carry += total;
     }
-    if (threadIdx.x == 0) dtot[blockIdx.x] = carry;
+    if (threadIdx.x == 0) dtot[d] = carry;
 }
 
-// Wave w ranks the keys [w*512, (w+1)*512) of the tile in 8 rounds of 64; ranks
+// Wave w ranks the keys [w*1024, (w+1)*1024) of the tile in 16 rounds of 64; ranks
 // inside a round follow lane order (ballot match), rounds follow each other, and
 // waves follow each other, so equal digits keep their input order.
 __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, const uint32_t* vin,
                                                        uint32_t* kout, uint32_t* vout, const int64_t* n_dev,
-                                                       int shift, int tiles, const uint32_t* hist,
-                                                       const uint32_t* dtot) {
+                                                       int shift, const uint32_t* hist, const uint32_t* dtot) {
     __shared__ uint32_t wcnt[kWavesPerBlock][kRadixBins];
     __shared__ uint32_t lbase[kRadixBins];
     __shared__ uint32_t gbase[kRadixBins];
@@ -222,19 +229,21 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     {
         uint32_t tot;
         uint32_t ex = block_exclusive_scan(dtot[t], lds, tot);
-        gbase[t] = ex + hist[(int64_t)t * tiles + blockIdx.x];
+        gbase[t] = ex + hist[(int64_t)blockIdx.x * kRadixBins + t];
     }
     __syncthreads();
     uint32_t key[kSortItems], val[kSortItems], rnk[kSortItems];
-    int dig[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; r++) {
+        int64_t i = t0 + w * (kSortItems * kWave) + r * kWave + lane;
+        key[r] = i < n ? kin[i] : 0u;
+        val[r] = i < n ? (vin ? vin[i] : (uint32_t)i) : 0u;
+    }
 #pragma unroll
     for (int r = 0; r < kSortItems; r++) {
         int64_t i = t0 + w * (kSortItems * kWave) + r * kWave + lane;
         bool valid = i < n;
-        key[r] = valid ? kin[i] : 0u;
-        val[r] = valid ? (vin ? vin[i] : (uint32_t)i) : 0u;
         int d = valid ? (int)((key[r] >> shift) & (kRadixBins - 1)) : -1;
-        dig[r] = d;
         uint64_t peers = __ballot(valid);
 #pragma unroll
         for (int b = 0; b < kRadixBits; b++) {
@@ -266,8 +275,8 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kSortItems; r++) {
-        if (dig[r] >= 0) {
-            uint32_t pos = wcnt[w][dig[r]] + rnk[r];
+        if (t0 + w * (kSortItems * kWave) + r * kWave + lane < n) {
+            uint32_t pos = wcnt[w][(key[r] >> shift) & (kRadixBins - 1)] + rnk[r];
             sk[pos] = key[r];
             sv[pos] = val[r];
         }
@@ -294,10 +303,10 @@ int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint3
     for (int p = 0; p < passes; p++) {
         int shift = p * kRadixBits;
         const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
-        hipLaunchKernelGGL(k_rs_hist, dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, tiles, hist);
-        hipLaunchKernelGGL(k_rs_scan, dim3(kRadixBins), dim3(kBlock), 0, st, hist, tiles, n_dev, dtot);
-        hipLaunchKernelGGL(k_rs_scatter, dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev, shift,
-                           tiles, hist, dtot);
+        hipLaunchKernelGGL(k_rs_hist, dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, hist);
+        hipLaunchKernelGGL(k_rs_scan, dim3(kRadixBins), dim3(kBlock), 0, st, hist, n_dev, dtot);
+        hipLaunchKernelGGL(k_rs_scatter, dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev, shift, hist,
+                           dtot);
         uint32_t* tk = ka; ka = kb; kb = tk;
         uint32_t* tv = va; va = vb; vb = tv;
     }

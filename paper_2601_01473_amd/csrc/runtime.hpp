@@ -94,7 +94,6 @@ struct Ctl {
     int64_t distinct;   // distinct gathered rows
     int64_t fblocks;    // non-empty feature-block rows
     int64_t targets;    // H * B
-    int64_t pktot;      // (runs << 32) | new nodes of the current hop
     int64_t requests[AGNES_MAX_LAYERS];
     int64_t sampled[AGNES_MAX_LAYERS];
     int64_t new_nodes[AGNES_MAX_LAYERS];
@@ -111,10 +110,8 @@ struct Workspace {
     DevBuf cnt, e_off;                // per request
     DevBuf rl_key[2], rl_val[2];      // (node, minibatch) list and local ids, two buffers
     DevBuf skey, sval, skey2, sval2;  // sort buffers (sampled neighbours, targets)
-    DevBuf pk, pkx, hl;               // per sorted edge: run/new flags, their scan, old local id
-    DevBuf nl_key, nl_run, nl_val;    // new (node, minibatch) pairs of a hop
-    DevBuf run_local;                 // local id of every run
-    DevBuf ghist;                     // per-minibatch counts of the new-node ranking
+    DevBuf split;                     // join: list entries before every tile boundary
+    DevBuf ghist, gemit;              // join: per group new nodes per minibatch, merged entries
     DevBuf rs_hist, rs_dtot;          // radix-sort histograms
     DevBuf scan_part;                 // scan partial sums
     hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
@@ -123,6 +120,7 @@ struct Workspace {
 struct Store {
     uint32_t magic = kStoreMagic;
     int device = 0;
+    int max_lds = 65536;              // LDS bytes one workgroup may use on the device
     int64_t num_nodes = 0, num_edges = 0;
     int offsets64 = 0;                // 1: int64 offsets, 0: int32
     int64_t e_blk = 0;                // edges per topology block
@@ -137,7 +135,8 @@ struct Store {
     DevBuf offsets, indices, features, first_node, last_node;
     int profile = 0;
     int gather_groups = 2048;         // workgroups of the row-copy kernel (upper bound)
-    int gather_unroll = 4;            // rows in flight per lane group (2, 4 or 8)
+    int gather_unroll = 4;            // rows in flight per lane group (4, 8 or 16)
+    int gather_nt = 1;                // 1 = non-temporal stores of the gathered rows
 };
 
 // A batch: the outputs of one hyperbatch and the scratch memory that produces

@@ -86,6 +86,7 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
 
     std::unique_ptr<Store> s(new Store());
     AGNES_CHECK_HIP(hipGetDevice(&s->device));
+    AGNES_CHECK_HIP(hipDeviceGetAttribute(&s->max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, s->device));
     s->num_nodes = n;
     s->num_edges = e;
     s->offsets64 = o64 ? 1 : 0;

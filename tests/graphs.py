@@ -40,3 +40,17 @@ def distinct_targets(n, H, B, seed):
 def features(n, dim, seed, dtype=np.float32):
     rng = np.random.default_rng(seed)
     return rng.standard_normal((n, dim)).astype(dtype)
+
+
+def star_graph(n, extra, seed):
+    """Every node links to node 0 (first in its row) plus `extra` random others:
+    node 0 is sampled by every request, so one (node, minibatch) run spans many
+    tiles of the join."""
+    rng = np.random.default_rng(seed)
+    rows = [np.sort(rng.choice(np.arange(1, n), size=min(extra, n - 1), replace=False)).astype(np.int32)]
+    for v in range(1, n):
+        others = rng.choice(np.arange(1, n), size=extra, replace=False)
+        rows.append(np.concatenate([[0], np.sort(others)]).astype(np.int32))
+    offsets = np.zeros(n + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum([len(r) for r in rows])
+    return offsets, np.concatenate(rows).astype(np.int32)

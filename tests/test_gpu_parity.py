@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import oracle
-from tests.graphs import distinct_targets, features, hand_graph, random_graph
+from tests.graphs import distinct_targets, features, hand_graph, random_graph, star_graph
 from tests.parity import compare_minibatch, feature_bytes, log
 
 pytestmark = pytest.mark.gpu
@@ -267,9 +267,10 @@ def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim):
     ref = oracle.Oracle(off, idx).hyperbatch(tg, fan, 9, 0)
     fb = feature_bytes(feat)
     want = oracle.hyperbatch_stats(off, 256, fb.shape[1], ref, len(fan))
-    for groups, unroll in [(8, 2), (8, 8), (24, 4), (2048, 4), (65536, 8), (1000, 2)]:
-        log("gather shape", rows_dim, groups, unroll)
-        store.set_gather_shape(groups, unroll)
+    for groups, unroll, nt in [(8, 4, True), (8, 16, False), (24, 8, True), (2048, 4, False),
+                               (65536, 8, True), (1000, 16, True)]:
+        log("gather shape", rows_dim, groups, unroll, nt)
+        store.set_gather_shape(groups, unroll, nt)
         b = store.prepare(t, fan, seed=9, mb_base=0)
         got = b.to_host()
         for j in range(tg.shape[0]):
@@ -278,7 +279,33 @@ def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim):
         for k, v in want.items():
             assert st[k] == v, (groups, unroll, k, st[k], v)
         b.close()
-    for bad in [(7, None), (65537, None), (None, 3), (None, 16)]:
+    for bad in [(7, None), (65537, None), (None, 3), (None, 2), (None, 32)]:
         with pytest.raises(agnes.AgnesError):
             store.set_gather_shape(*bad)
     store.close()
+
+
+def test_runs_spanning_join_tiles(agnes):
+    """Node 0 is a neighbour of every request: with take-all rows, minibatch j
+    holds a run of thousands of equal (0, j) edges, longer than a join tile, and
+    the long runs of hop 1 continue across tile and group boundaries."""
+    off, idx = star_graph(9000, 2, 3)
+    tg = (np.random.default_rng(9).permutation(8999)[:6000] + 1).reshape(2, 3000).astype(np.int32)
+    feat = features(9000, 8, 8)
+    run_case(agnes, off, idx, feat, tg, [4, 3], 5, 0, 512, tag="star")
+
+
+def test_many_minibatches(agnes):
+    """H = 4096 minibatches of 2 targets: the widest per-minibatch LDS tables."""
+    off, idx = random_graph(20000, 6, 12, hubs=2, hub_deg=3000)
+    tg = distinct_targets(20000, 4096, 2, 10)
+    feat = features(20000, 4, 9)
+    run_case(agnes, off, idx, feat, tg, [3, 2], 6, 11, 256, tag="H4096")
+
+
+def test_single_minibatch_many_targets(agnes):
+    """H = 1: minibatch ranking without minibatch bits; ragged last tile."""
+    off, idx = random_graph(30000, 9, 13, hubs=3, hub_deg=5000)
+    tg = distinct_targets(30000, 1, 7001, 11)
+    feat = features(30000, 8, 10)
+    run_case(agnes, off, idx, feat, tg, [6, 4], 7, 2, 1024, tag="H1")
