@@ -25,6 +25,38 @@ import numpy as np
 HBM_PEAK_GBPS = 8000.0
 
 
+GATHER_TRAFFIC_FILE = os.path.join("profiles", "k_gather.rmat-2^23.hbm-traffic.md")
+
+
+def gather_fingerprint(root: str) -> str:
+    """sha256 of the row-copy kernel's source and its default launch shape: the
+    measured HBM traffic stays valid only while these are unchanged."""
+    import hashlib
+    src = open(os.path.join(root, "paper_2601_01473_amd", "csrc", "pipeline.hip")).read()
+    a = src.index("template <typename Unit, int LPR, int U, bool NT>\n__global__")
+    b = src.index("struct GatherArgs {", a)
+    rt = open(os.path.join(root, "paper_2601_01473_amd", "csrc", "runtime.hpp")).read()
+    shape = [ln.strip() for ln in rt.splitlines() if ln.strip().startswith(("int gather_groups", "int gather_unroll",
+                                                                             "int gather_nt"))]
+    return hashlib.sha256((src[a:b] + "\n".join(shape)).encode()).hexdigest()
+
+
+def measured_traffic(root: str):
+    """(GB per launch, algorithmic GB per launch) of the row-copy kernel from the
+    committed counter summary, or None when the kernel changed since."""
+    path = os.path.join(root, GATHER_TRAFFIC_FILE)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for ln in open(path):
+        if ln.startswith("- ") and ": " in ln:
+            k, v = ln[2:].split(": ", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("kernel_fingerprint") != gather_fingerprint(root):
+        return None
+    return float(vals["traffic_GB_per_launch"]), float(vals["algorithmic_GB_per_launch"])
+
+
 def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int) -> tuple:
     """Bytes the method must move (exact counts from the batch statistics).
 
@@ -55,6 +87,7 @@ def cpu_baseline(w, cfg, steps_targets, budget_s=20.0):
     t0 = time.perf_counter()
     H = w["H"]
     for s, tg in enumerate(steps_targets):
+        seen_rows = set()                       # distinct rows are counted per hyperbatch
         for j in range(H):
             mb = o.minibatch(tg[j], cfg.fanouts, cfg.seed, s * H + j)
             feats = oracle.gather(fb, mb.nodes)
@@ -229,6 +262,7 @@ def main():
     torch.cuda.synchronize()
     serial_ms = (time.perf_counter() - t1) / nser * 1e3
 
+    traffic = measured_traffic(root)
     tot_bytes, tot_sample, tot_gather = acc["bytes"], acc["sample"], acc["gather"]
     tot_copy_bytes, edges, rows = acc["copy_bytes"], acc["edges"], acc["rows"]
     sample_ms, gather_ms, copy_ms = acc["sample_ms"], acc["gather_ms"], acc["copy_ms"]
@@ -266,7 +300,9 @@ def main():
                      "gather_bytes": tot_gather // K, "rows": rows // K, "sampled_edges": edges // K},
         "roofline": {"kernel": "k_gather (row copy)", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": None},
+                     "traffic": traffic[0] if traffic else None,
+                     "traffic_unit": "GB per launch, HBM (FETCH_SIZE x2.0 + WRITE_SIZE x1.0, copy-calibrated)",
+                     "traffic_algorithmic": traffic[1] if traffic else None},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, cfg, step_targets[args.warmup:], args.cpu_budget)

@@ -628,12 +628,13 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // gathering loop in block order: the requests of a feature block are contiguous
 // and those of one node are neighbours, so each row is loaded from HBM once and
 // written to every minibatch that needs it (dest = node_off[j] + local id).
-// LPR lanes share a row (16-byte or 4-byte units).  A lane group keeps U rows in
-// flight: it loads the U rows' pieces, fetches the list entries of its next U
-// rows while those loads are outstanding, then stores.  Workgroup b takes a
-// contiguous range of the list; ranges are dealt so that neighbouring ranges
-// (the same blocks) run on the same XCD.  Also counts the distinct rows and the
-// non-empty feature-block rows.
+// LPR lanes share a row (16-byte or 4-byte units).  Workgroup b takes a
+// contiguous range of the list (ranges are dealt so that neighbouring ranges,
+// the same blocks, run on the same XCD) and each lane group a contiguous piece
+// of it, U entries at a time: an entry whose node equals the previous entry's
+// reuses the row already in registers, the others load theirs (U rows in
+// flight), and the list entries of the next U are fetched while the rows load.
+// Also counts the distinct rows and the non-empty feature-block rows.
 template <typename Unit, int LPR, int U, bool NT>
 __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat, Unit* __restrict__ out,
                                                    int32_t* __restrict__ nodes_out,
@@ -643,7 +644,6 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
                                                    Ctl* ctl) {
     constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
     constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
-    constexpr int64_t STEP = (int64_t)GPB * U;   // list entries per workgroup iteration
     extern __shared__ int64_t node_off[];
     __shared__ unsigned long long cnt[2];
     if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
@@ -652,41 +652,46 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
     const int b = blockIdx.x;
     const int lb = (G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
     const int64_t chunk = (rows + G - 1) / G;
-    const int64_t lo = std::min<int64_t>(rows, (int64_t)lb * chunk);
-    const int64_t hi = std::min<int64_t>(rows, lo + chunk);
+    const int64_t wlo = std::min<int64_t>(rows, (int64_t)lb * chunk);
+    const int64_t whi = std::min<int64_t>(rows, wlo + chunk);
     const int li = lane_id() % LPR;
     const int gid = wave_id() * RPW + lane_id() / LPR;
+    const int64_t sub = (whi - wlo + GPB - 1) / GPB;
+    const int64_t lo = std::min<int64_t>(whi, wlo + gid * sub);
+    const int64_t hi = std::min<int64_t>(whi, lo + sub);
     unsigned long long nd = 0, nf = 0;
+    uint32_t prev_u = (lo > 0 && lo < hi) ? (uint32_t)(rl_key[lo - 1] >> 32) : 0xFFFFFFFFu;
     uint64_t key[U];
     int32_t val[U];
 #pragma unroll
     for (int k = 0; k < U; k++) {
-        const int64_t e = lo + gid + (int64_t)k * GPB;
-        key[k] = e < hi ? rl_key[e] : 0;
-        val[k] = e < hi ? rl_val[e] : 0;
+        key[k] = lo + k < hi ? rl_key[lo + k] : 0;
+        val[k] = lo + k < hi ? rl_val[lo + k] : 0;
     }
-    for (int64_t e0 = lo + gid; e0 < hi; e0 += STEP) {
+    for (int64_t e0 = lo; e0 < hi; e0 += U) {
         int64_t src[U], dst[U];
-        bool ok[U];
+        bool ok[U], fresh[U];
 #pragma unroll
         for (int k = 0; k < U; k++) {
-            const int64_t e = e0 + (int64_t)k * GPB;
+            const int64_t e = e0 + k;
             ok[k] = e < hi;
             const uint32_t u = (uint32_t)(key[k] >> 32);
+            const uint32_t pu = k > 0 ? (uint32_t)(key[k - 1] >> 32) : prev_u;
             const int64_t d = node_off[(uint32_t)key[k]] + val[k];
+            fresh[k] = ok[k] && (k == 0 || u != pu);
             src[k] = ok[k] ? (int64_t)u * row_units : 0;
             dst[k] = ok[k] ? d * row_units : 0;
             if (ok[k] && li == 0) {
                 nodes_out[d] = (int32_t)u;
-                const uint32_t pu = e > 0 ? (uint32_t)(rl_key[e - 1] >> 32) : 0xFFFFFFFFu;
-                nd += (pu != u);
+                nd += (e == 0 || pu != u);
                 nf += (e == 0 || pu / rpb != u / rpb);
             }
         }
-        // list entries of the next iteration, fetched while this one's rows load
+        prev_u = (uint32_t)(key[U - 1] >> 32);
+        // list entries of the next U, fetched while these rows load
 #pragma unroll
         for (int k = 0; k < U; k++) {
-            const int64_t e = e0 + STEP + (int64_t)k * GPB;
+            const int64_t e = e0 + U + k;
             key[k] = e < hi ? rl_key[e] : 0;
             val[k] = e < hi ? rl_val[e] : 0;
         }
@@ -694,7 +699,10 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             Unit x[U];
 #pragma unroll
             for (int k = 0; k < U; k++)
-                if (ok[k]) x[k] = feat[src[k] + c];
+                if (fresh[k]) x[k] = feat[src[k] + c];
+#pragma unroll
+            for (int k = 1; k < U; k++)
+                if (!fresh[k]) x[k] = x[k - 1];
 #pragma unroll
             for (int k = 0; k < U; k++) {
                 if (!ok[k]) continue;
