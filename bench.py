@@ -1,10 +1,14 @@
 #!/usr/bin/env python3
 """Benchmark: hyperbatch data preparation on one MI355X.
 
-A step is one call of agnes_hyperbatch_prepare: L hops of block-bucketed
-sampling for H minibatches plus the block-bucketed feature gather, on a fresh
-hyperbatch of targets (step s uses targets s and mb_base = s * H).  All inputs
-(graph, features, every step's targets) are resident in HBM before timing.
+A step is one hyperbatch: L hops of block-bucketed sampling for H minibatches
+plus the block-bucketed feature gather, on a fresh hyperbatch of targets (step
+s uses targets s and mb_base = s * H).  All inputs (graph, features, every
+step's targets) are resident in HBM before timing.  Steps are pipelined with
+the two-phase API: the sampling of the next --depth hyperbatches runs on
+--sample-streams streams (alternating) while one hyperbatch gathers on its own
+stream; every step's outputs are complete when the timed region ends.  A
+serial reference (prepare after prepare) is reported beside it.
 
 Default workload: R-MAT 2^23 nodes, average degree 30, fp32 features of 256
 dims, fanouts [25, 10], 64 minibatches of 1024 targets, 64 KiB blocks.
@@ -12,7 +16,8 @@ dims, fanouts [25, 10], 64 minibatches of 1024 targets, 64 KiB blocks.
 Printed (one JSON line): value = algorithmic bytes of sampling + gather per
 second (GB/s), with sampled edges/s, gathered feature GB/s and the fraction of
 the 8 TB/s HBM peak; the roofline of the row-copy kernel (HIP events on the
-prepare stream); the CPU oracle timed on a bounded sample of the same work.
+gather stream, counter-measured HBM traffic from profiles/); the CPU oracle
+timed on a bounded sample of the same work.
 """
 import argparse
 import json
@@ -140,7 +145,9 @@ def main():
     ap.add_argument("--H", type=int, default=None, help="minibatches per hyperbatch (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
-    ap.add_argument("--depth", type=int, default=1, help="hyperbatches sampled ahead of the one gathering")
+    ap.add_argument("--depth", type=int, default=2, help="hyperbatches sampled ahead of the one gathering")
+    ap.add_argument("--sample-streams", type=int, default=2,
+                    help="streams the sampling of consecutive hyperbatches alternates between")
     ap.add_argument("--gather-first", action="store_true",
                     help="queue each gather before waiting for the previous one")
     ap.add_argument("--gather-groups", type=int, default=None, help="row-copy kernel workgroups")
@@ -187,8 +194,9 @@ def main():
     ob = 8 if w["offsets"].dtype == np.int64 else 4
     rb = cfg.row_bytes
 
-    # sampling runs on one stream, gathers on another (both default priority)
-    s_stream, g_stream = torch.cuda.Stream(), torch.cuda.Stream()
+    # sampling runs on one or more streams, gathers on another (all default priority)
+    s_streams = [torch.cuda.Stream() for _ in range(max(1, args.sample_streams))]
+    s_stream, g_stream = s_streams[0], torch.cuda.Stream()
     acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, sample_ms=0.0, gather_ms=0.0,
                copy_ms=0.0, steps=0)
 
@@ -213,7 +221,7 @@ def main():
     def begin(s):
         k = s % NSLOT
         slots[k] = store.begin(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[k],
-                               stream=s_stream)
+                               stream=s_streams[s % len(s_streams)])
 
     def pipeline(first, n, record):
         """Steps first .. first+n-1 with the sampling of steps s+1 .. s+D in flight
@@ -294,7 +302,8 @@ def main():
                      "copy_kernel": round(copy_avg_ms, 4)},
         "mode": f"pipelined: {NSLOT} batch slots, a sampling stream and a gather stream; "
                 f"hyperbatches t+1..t+{D} sample while t gathers"
-                + ("; gathers queued back to back" if args.gather_first else "; sampling enqueued first"),
+                + ("; gathers queued back to back" if args.gather_first else "; sampling enqueued first")
+                + f"; {len(s_streams)} sampling stream(s)",
         "serial_ms_per_step": round(serial_ms, 4),
         "per_step": {"algorithmic_bytes": tot_bytes // K, "sample_bytes": tot_sample // K,
                      "gather_bytes": tot_gather // K, "rows": rows // K, "sampled_edges": edges // K},

@@ -67,6 +67,28 @@ __device__ __forceinline__ int upper_segment(const T* off, int n, T x) {
     return lo;
 }
 
+// The same search by a group of P lanes (P divides 64; lanes [g*P, (g+1)*P)
+// form group g and the groups of a wave search independently): log_P(n) rounds
+// of P probes.  All lanes of a group must call it together.
+template <int P, typename Pred>
+__device__ __forceinline__ int64_t group_partition_point(int64_t lo, int64_t hi, Pred before) {
+    const int gl = lane_id() % P;
+    const uint64_t gmask = (P == kWave) ? ~0ull : (((1ull << P) - 1) << (lane_id() - gl));
+    while (lo < hi) {
+        const int64_t n = hi - lo;
+        const int64_t step = (n + P - 1) / P;
+        const int64_t p = lo + (int64_t)gl * step;
+        const bool probe = p < hi;
+        const int c = __popcll(__ballot(probe && before(p)) & gmask);
+        if (c == 0) return lo;
+        const int probes = (int)((n + step - 1) / step);
+        const int64_t nhi = c < probes ? lo + (int64_t)c * step : hi;
+        lo = lo + (int64_t)(c - 1) * step + 1;
+        hi = nhi;
+    }
+    return lo;
+}
+
 // First index in [lo, hi) where before() is false, for a predicate that is true
 // on a prefix of the range, searched by one wave: every round the 64 lanes test
 // 64 evenly spaced indices, which narrows the range by a factor of ~64, so a

@@ -268,8 +268,11 @@ __device__ __forceinline__ uint64_t edge_key(const uint32_t* su, const uint32_t*
     return ((uint64_t)su[p] << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)se[p]);
 }
 
-// a_t for every tile boundary t (one wave each): the number of A entries among
-// the first t * kJoinTile merged entries.
+// a_t for every tile boundary t: the number of A entries among the first
+// t * kJoinTile merged entries.  Groups of kSplitLanes lanes search one boundary
+// each (a few rounds of 16 probes).
+constexpr int kSplitLanes = 16;
+
 __global__ __launch_bounds__(kBlock) void k_join_split(int H, const int64_t* req_off, const int64_t* e_off,
                                                        const uint64_t* ak, const uint32_t* su, const uint32_t* se,
                                                        int64_t* split, const Ctl* ctl) {
@@ -277,14 +280,14 @@ __global__ __launch_bounds__(kBlock) void k_join_split(int H, const int64_t* req
     load_mb_edges(mb_e, req_off, e_off, H);
     const int64_t na = ctl->R, nb = ctl->S, n = na + nb;
     const int64_t tiles = (n + kJoinTile - 1) / kJoinTile;
-    const int64_t nw = (int64_t)gridDim.x * kWavesPerBlock;
-    for (int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + wave_id(); t <= tiles; t += nw) {
+    const int64_t ng = (int64_t)gridDim.x * kBlock / kSplitLanes;
+    for (int64_t t = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kSplitLanes; t <= tiles; t += ng) {
         const int64_t d = std::min<int64_t>(t * kJoinTile, n);
         const int64_t lo = d > nb ? d - nb : 0, hi = d < na ? d : na;
         // A[i] goes before B[d-1-i] when A[i] <= B[d-1-i] (A first on equal keys)
-        const int64_t x = wave_partition_point(
+        const int64_t x = group_partition_point<kSplitLanes>(
             lo, hi, [&](int64_t i) { return ak[i] <= edge_key(su, se, mb_e, H, d - 1 - i); });
-        if (lane_id() == 0) split[t] = x;
+        if (lane_id() % kSplitLanes == 0) split[t] = x;
     }
 }
 
@@ -452,8 +455,12 @@ __global__ __launch_bounds__(kBlock) void k_join_scan(int H, int G, int64_t* ghi
 // counts wcnt[w][j]); after a barrier the waves' totals are stacked.  An edge
 // takes the local id of the last head at or before it (a head before the tile:
 // the old pair A[a_t - 1], or the newest new node of its minibatch so far).
+// nodes (the per-minibatch lists that the next hop's requests read) is
+// written only when another hop follows (write_nodes); the gather writes the
+// final lists itself.
 // Dynamic LDS: mb_e[H+1], sk[T], sv[T], loc[T], nhx[T+1], cursor[H], wcnt[4][H] (16-bit).
 __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t capN, int64_t rows_cap,
+                                                       int write_nodes,
                                                        const int64_t* req_off, const int64_t* e_off,
                                                        const uint64_t* ak, const int32_t* av, const uint32_t* su,
                                                        const uint32_t* se, const int64_t* split, int G,
@@ -565,7 +572,7 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
                     if (lc >= capN || pos >= rows_cap) {
                         atomicOr((unsigned long long*)&ctl->err, 4ull);
                     } else {
-                        nodes[(int64_t)j * capN + lc] = (int32_t)(key[r] >> 32);
+                        if (write_nodes) nodes[(int64_t)j * capN + lc] = (int32_t)(key[r] >> 32);
                         ck[pos] = key[r];
                         cv[pos] = lc;
                     }
@@ -606,11 +613,11 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
 // Tiles of the join at any hop: the list and the edges together fit the maxima.
 static int64_t join_tiles_max(const Geometry& g) { return (g.Rmax + g.Smax) / kJoinTile + 1; }
 
-// Workgroups of the join passes: enough for one tile each on large hops, while
-// the per-minibatch count table (H x G) stays near 4M entries.
-static int join_groups(const Geometry& g) {
-    int64_t G = std::min<int64_t>(4096, std::max<int64_t>(256, (int64_t)(4 << 20) / g.H));
-    G = std::min<int64_t>(G, std::max<int64_t>(256, join_tiles_max(g)));
+// Workgroups of the join passes: one tile each up to 4096 groups, while the
+// per-minibatch count table (H x G) stays near 4M entries.
+static int join_groups(int H, int64_t tiles) {
+    int64_t G = std::min<int64_t>(4096, std::max<int64_t>(256, (int64_t)(4 << 20) / H));
+    G = std::min<int64_t>(G, std::max<int64_t>(256, tiles));
     return (int)((G + kBlock - 1) / kBlock * kBlock);
 }
 
@@ -800,8 +807,8 @@ static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout&
     w.skey2.reserve((size_t)g.sort_max * 4);
     w.sval2.reserve((size_t)g.sort_max * 4);
     w.split.reserve((size_t)(join_tiles_max(g) + 2) * 8);
-    w.ghist.reserve((size_t)H * join_groups(g) * 8);
-    w.gemit.reserve((size_t)join_groups(g) * 8);
+    w.ghist.reserve((size_t)H * join_groups(g.H, join_tiles_max(g)) * 8);
+    w.gemit.reserve((size_t)join_groups(g.H, join_tiles_max(g)) * 8);
     w.rs_hist.reserve((size_t)radix_hist_entries(g.sort_max) * 4);
     w.rs_dtot.reserve((size_t)radix_dtot_entries() * 4);
     w.scan_part.reserve((size_t)scan_partials_needed() * 8);
@@ -847,18 +854,19 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     const uint32_t* su = in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>();
     const uint32_t* se = in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>();
     // join with the list: the next list, new node ids and the hop's columns
-    const int gJ = (int)std::min<int64_t>(2048, (join_tiles_max(g) + 1 + kWavesPerBlock - 1) / kWavesPerBlock);
+    const int64_t tiles_l = ((int64_t)g.H * g.cap[l] * (1 + (int64_t)f)) / kJoinTile + 1;
+    const int gJ = (int)std::min<int64_t>(2048, (tiles_l + 1) * kSplitLanes / kBlock + 1);
     int64_t* split = w.split.as<int64_t>();
     hipLaunchKernelGGL(k_join_split, dim3(gJ), dim3(kBlock), lds_h, st, g.H, w.req_off.as<int64_t>(),
                        w.e_off.as<int64_t>(), rlk, su, se, split, ctl);
-    const int G = join_groups(g);
+    const int G = join_groups(g.H, tiles_l);
     hipLaunchKernelGGL(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H), st, g.H,
                        w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se, split, G,
                        w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), b.row_ptr[l].as<int32_t>(), ctl);
     hipLaunchKernelGGL(k_join_scan, dim3(g.H + 1), dim3(kBlock), 0, st, g.H, G, w.ghist.as<int64_t>(),
                        w.gemit.as<int64_t>(), w.newcnt.as<int64_t>(), ctl);
     hipLaunchKernelGGL(k_join_write, dim3(G), dim3(kBlock), join_write_lds(g.H), st, g.H, g.jbits,
-                       g.capN, g.rows_max, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se,
+                       g.capN, g.rows_max, (int)(l + 1 < g.L), w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se,
                        split, G, w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), w.size.as<int32_t>(),
                        w.nodes.as<int32_t>(), w.rl_key[cur ^ 1].as<uint64_t>(), w.rl_val[cur ^ 1].as<int32_t>(),
                        b.col[l].as<int32_t>(), ctl);

@@ -145,36 +145,42 @@ void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_
 // ----------------------------------------------------------------- radix sort
 
 // LSD radix sort of 32-bit keys with 32-bit values, 8-bit digits, tiles of
-// 4096 keys.  Per pass: (1) digit histogram of every tile, stored tile-major
+// 256 x ITEMS keys (2048 for sorts of at most 2M keys, where more and shorter
+// workgroups hide latency better; 4096 above, for longer runs per digit).
+// Per pass: (1) digit histogram of every tile, stored tile-major
 // (each tile writes its 256 counts contiguously), (2) per digit, an exclusive
 // scan over the tiles (the table is small and stays in L2), (3) each tile ranks
 // its keys stably, reorders them by digit in LDS and writes every digit's run
 // contiguously.
-constexpr int kSortItems = 16;
-constexpr int kSortTile = kBlock * kSortItems;     // 4096 keys
+constexpr int64_t kSmallSort = 1 << 21;
+static int sort_items(int64_t n_max) { return n_max <= kSmallSort ? 8 : 16; }
 constexpr int kRadixBits = 8;
 constexpr int kRadixBins = 1 << kRadixBits;
 
-int64_t radix_tiles(int64_t n_max) { return (n_max + kSortTile - 1) / kSortTile + 1; }
+int64_t radix_tiles(int64_t n_max) {
+    const int64_t tile = (int64_t)kBlock * sort_items(n_max);
+    return (n_max + tile - 1) / tile + 1;
+}
 int64_t radix_hist_entries(int64_t n_max) { return (int64_t)kRadixBins * radix_tiles(n_max); }
 int64_t radix_dtot_entries() { return kRadixBins; }
 
+template <int ITEMS>
 __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const int64_t* n_dev, int shift,
                                                     uint32_t* hist) {
     __shared__ uint32_t h[kRadixBins];
     const int64_t n = *n_dev;
-    const int64_t t0 = (int64_t)blockIdx.x * kSortTile;
+    const int64_t t0 = (int64_t)blockIdx.x * (kBlock * ITEMS);
     if (t0 >= n) return;                        // tiles past the end are not scanned
     h[threadIdx.x] = 0;
-    uint32_t k[kSortItems];
+    uint32_t k[ITEMS];
 #pragma unroll
-    for (int q = 0; q < kSortItems; q++) {
+    for (int q = 0; q < ITEMS; q++) {
         const int64_t i = t0 + q * kBlock + threadIdx.x;
         k[q] = i < n ? keys[i] : 0u;
     }
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < kSortItems; q++)
+    for (int q = 0; q < ITEMS; q++)
         if (t0 + q * kBlock + threadIdx.x < n) atomicAdd(&h[(k[q] >> shift) & (kRadixBins - 1)], 1u);
     __syncthreads();
     hist[(int64_t)blockIdx.x * kRadixBins + threadIdx.x] = h[threadIdx.x];
@@ -182,10 +188,11 @@ __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const 
 
 // One workgroup per digit: exclusive scan over the tiles that hold keys of
 // column d of the tile-major table (in place), digit total.
+template <int ITEMS>
 __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_t* n_dev, uint32_t* dtot) {
     __shared__ uint32_t lds[kWavesPerBlock];
     const int d = blockIdx.x;
-    const int tiles = (int)((*n_dev + kSortTile - 1) / kSortTile);
+    const int tiles = (int)((*n_dev + (kBlock * ITEMS) - 1) / (kBlock * ITEMS));
     uint32_t carry = 0;
     for (int b0 = 0; b0 < tiles; b0 += kBlock * 4) {
         uint32_t v[4];
@@ -209,9 +216,10 @@ __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_
     if (threadIdx.x == 0) dtot[d] = carry;
 }
 
-// Wave w ranks the keys [w*1024, (w+1)*1024) of the tile in 16 rounds of 64; ranks
+// Wave w ranks a quarter of the tile's keys in ITEMS rounds of 64; ranks
 // inside a round follow lane order (ballot match), rounds follow each other, and
 // waves follow each other, so equal digits keep their input order.
+template <int ITEMS>
 __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, const uint32_t* vin,
                                                        uint32_t* kout, uint32_t* vout, const int64_t* n_dev,
                                                        int shift, const uint32_t* hist, const uint32_t* dtot) {
@@ -219,10 +227,10 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     __shared__ uint32_t lbase[kRadixBins];
     __shared__ uint32_t gbase[kRadixBins];
     __shared__ uint32_t lds[kWavesPerBlock];
-    __shared__ uint32_t sk[kSortTile];
-    __shared__ uint32_t sv[kSortTile];
+    __shared__ uint32_t sk[kBlock * ITEMS];
+    __shared__ uint32_t sv[kBlock * ITEMS];
     const int64_t n = *n_dev;
-    const int64_t t0 = (int64_t)blockIdx.x * kSortTile;
+    const int64_t t0 = (int64_t)blockIdx.x * (kBlock * ITEMS);
     if (t0 >= n) return;
     const int t = threadIdx.x, w = wave_id(), lane = lane_id();
     for (int x = t; x < kWavesPerBlock * kRadixBins; x += kBlock) (&wcnt[0][0])[x] = 0;
@@ -232,16 +240,16 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
         gbase[t] = ex + hist[(int64_t)blockIdx.x * kRadixBins + t];
     }
     __syncthreads();
-    uint32_t key[kSortItems], val[kSortItems], rnk[kSortItems];
+    uint32_t key[ITEMS], val[ITEMS], rnk[ITEMS];
 #pragma unroll
-    for (int r = 0; r < kSortItems; r++) {
-        int64_t i = t0 + w * (kSortItems * kWave) + r * kWave + lane;
+    for (int r = 0; r < ITEMS; r++) {
+        int64_t i = t0 + w * (ITEMS * kWave) + r * kWave + lane;
         key[r] = i < n ? kin[i] : 0u;
         val[r] = i < n ? (vin ? vin[i] : (uint32_t)i) : 0u;
     }
 #pragma unroll
-    for (int r = 0; r < kSortItems; r++) {
-        int64_t i = t0 + w * (kSortItems * kWave) + r * kWave + lane;
+    for (int r = 0; r < ITEMS; r++) {
+        int64_t i = t0 + w * (ITEMS * kWave) + r * kWave + lane;
         bool valid = i < n;
         int d = valid ? (int)((key[r] >> shift) & (kRadixBins - 1)) : -1;
         uint64_t peers = __ballot(valid);
@@ -274,15 +282,15 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     }
     __syncthreads();
 #pragma unroll
-    for (int r = 0; r < kSortItems; r++) {
-        if (t0 + w * (kSortItems * kWave) + r * kWave + lane < n) {
+    for (int r = 0; r < ITEMS; r++) {
+        if (t0 + w * (ITEMS * kWave) + r * kWave + lane < n) {
             uint32_t pos = wcnt[w][(key[r] >> shift) & (kRadixBins - 1)] + rnk[r];
             sk[pos] = key[r];
             sv[pos] = val[r];
         }
     }
     __syncthreads();
-    const int cnt = (int)((n - t0) < kSortTile ? (n - t0) : kSortTile);
+    const int cnt = (int)((n - t0) < (kBlock * ITEMS) ? (n - t0) : (kBlock * ITEMS));
     for (int i = t; i < cnt; i += kBlock) {
         uint32_t k = sk[i];
         int d = (int)((k >> shift) & (kRadixBins - 1));
@@ -292,24 +300,34 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     }
 }
 
+template <int ITEMS>
+static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
+                         const int64_t* n_dev, int tiles, int passes, uint32_t* hist, uint32_t* dtot,
+                         hipStream_t st, bool vals_iota) {
+    uint32_t *ka = keys, *kb = keys_tmp;
+    uint32_t *va = vals, *vb = vals_tmp;
+    for (int p = 0; p < passes; p++) {
+        int shift = p * kRadixBits;
+        const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
+        hipLaunchKernelGGL(k_rs_hist<ITEMS>, dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, hist);
+        hipLaunchKernelGGL(k_rs_scan<ITEMS>, dim3(kRadixBins), dim3(kBlock), 0, st, hist, n_dev, dtot);
+        hipLaunchKernelGGL(k_rs_scatter<ITEMS>, dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev, shift,
+                           hist, dtot);
+        uint32_t* tk = ka; ka = kb; kb = tk;
+        uint32_t* tv = va; va = vb; vb = tv;
+    }
+}
+
 int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                        const int64_t* n_dev, int64_t n_max, int bits, uint32_t* hist,
                        uint32_t* dtot, hipStream_t st, bool vals_iota) {
     if (bits < 1) bits = 1;
     const int passes = (bits + kRadixBits - 1) / kRadixBits;
     const int tiles = (int)radix_tiles(n_max);
-    uint32_t *ka = keys, *kb = keys_tmp;
-    uint32_t *va = vals, *vb = vals_tmp;
-    for (int p = 0; p < passes; p++) {
-        int shift = p * kRadixBits;
-        const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
-        hipLaunchKernelGGL(k_rs_hist, dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, hist);
-        hipLaunchKernelGGL(k_rs_scan, dim3(kRadixBins), dim3(kBlock), 0, st, hist, n_dev, dtot);
-        hipLaunchKernelGGL(k_rs_scatter, dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev, shift, hist,
-                           dtot);
-        uint32_t* tk = ka; ka = kb; kb = tk;
-        uint32_t* tv = va; va = vb; vb = tv;
-    }
+    if (sort_items(n_max) == 8)
+        radix_passes<8>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+    else
+        radix_passes<16>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
     AGNES_CHECK_HIP(hipGetLastError());
     return passes & 1;   // 1: the sorted pairs are in keys_tmp / vals_tmp
 }

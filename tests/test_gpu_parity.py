@@ -230,6 +230,43 @@ def test_two_batches_in_flight_on_two_streams(agnes):
             compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=("async", k, j))
 
 
+def test_three_batches_two_sampling_streams_one_gather_stream(agnes):
+    """The loader schedule of bench.py: hyperbatches t+1 and t+2 sample on two
+    streams (alternating) while t gathers on a third; every batch is checked."""
+    off, idx = random_graph(4000, 10, 31, hubs=3, hub_deg=1200)
+    feat = features(4000, 16, 12)
+    store = agnes.Store(off, idx, feat, 256)
+    s_streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    g_stream = torch.cuda.Stream()
+    fan = [5, 4]
+    n, D = 8, 2
+    tgs = [distinct_targets(4000, 4, 50, 200 + k) for k in range(n)]
+    dev = [torch.from_numpy(t).cuda() for t in tgs]
+    o = oracle.Oracle(off, idx)
+    fb = feature_bytes(feat)
+    slots = [None] * (D + 1)
+    done = []
+
+    def begin(s):
+        k = s % (D + 1)
+        slots[k] = store.begin(dev[s], fan, seed=7, mb_base=s * 4, batch=slots[k], stream=s_streams[s % 2])
+
+    for s in range(D):
+        begin(s)
+    for s in range(n):
+        if s >= 1:
+            done.append((s - 1, slots[(s - 1) % (D + 1)].to_host()))
+        if s + D < n:
+            begin(s + D)
+        slots[s % (D + 1)].finish(stream=g_stream)
+    done.append((n - 1, slots[(n - 1) % (D + 1)].to_host()))
+    assert sorted(k for k, _ in done) == list(range(n))
+    for k, got in done:
+        ref = o.hyperbatch(tgs[k], fan, 7, k * 4)
+        for j in range(4):
+            compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=("3slot", k, j))
+
+
 def test_finish_on_other_stream_and_errors(agnes):
     off, idx = random_graph(800, 8, 3)
     feat = features(800, 8, 1)
