@@ -37,8 +37,12 @@ def gather_fingerprint(root: str) -> str:
     """sha256 of the row-copy kernel's source and its default launch shape: the
     measured HBM traffic stays valid only while these are unchanged."""
     import hashlib
+    import re
     src = open(os.path.join(root, "paper_2601_01473_amd", "csrc", "pipeline.hip")).read()
-    a = src.index("template <typename Unit, int LPR, int U, bool NT>\n__global__")
+    m = re.search(r"template <[^>]*>\n__global__ __launch_bounds__\(kBlock\) void k_gather\(", src)
+    if m is None or "struct GatherArgs {" not in src[m.start():]:
+        return ""
+    a = m.start()
     b = src.index("struct GatherArgs {", a)
     rt = open(os.path.join(root, "paper_2601_01473_amd", "csrc", "runtime.hpp")).read()
     shape = [ln.strip() for ln in rt.splitlines() if ln.strip().startswith(("int gather_groups", "int gather_unroll",
@@ -57,7 +61,8 @@ def measured_traffic(root: str):
         if ln.startswith("- ") and ": " in ln:
             k, v = ln[2:].split(": ", 1)
             vals[k.strip()] = v.strip().strip("`")
-    if vals.get("kernel_fingerprint") != gather_fingerprint(root):
+    fp = gather_fingerprint(root)
+    if not fp or vals.get("kernel_fingerprint") != fp:
         return None
     return float(vals["traffic_GB_per_launch"]), float(vals["algorithmic_GB_per_launch"])
 

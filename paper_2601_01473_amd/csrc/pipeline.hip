@@ -642,7 +642,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // reuses the row already in registers, the others load theirs (U rows in
 // flight), and the list entries of the next U are fetched while the rows load.
 // Also counts the distinct rows and the non-empty feature-block rows.
-template <typename Unit, int LPR, int U, bool NT>
+template <typename Unit, int LPR, int U, bool NT, bool ONE>
 __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat, Unit* __restrict__ out,
                                                    int32_t* __restrict__ nodes_out,
                                                    const uint64_t* __restrict__ rl_key,
@@ -676,7 +676,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
         val[k] = lo + k < hi ? rl_val[lo + k] : 0;
     }
     for (int64_t e0 = lo; e0 < hi; e0 += U) {
-        int64_t src[U], dst[U];
+        uint32_t src[U], dst[U];             // row numbers (node, output row); < 2^31
         bool ok[U], fresh[U];
 #pragma unroll
         for (int k = 0; k < U; k++) {
@@ -684,10 +684,10 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             ok[k] = e < hi;
             const uint32_t u = (uint32_t)(key[k] >> 32);
             const uint32_t pu = k > 0 ? (uint32_t)(key[k - 1] >> 32) : prev_u;
-            const int64_t d = node_off[(uint32_t)key[k]] + val[k];
+            const uint32_t d = (uint32_t)(node_off[(uint32_t)key[k]] + val[k]);
             fresh[k] = ok[k] && (k == 0 || u != pu);
-            src[k] = ok[k] ? (int64_t)u * row_units : 0;
-            dst[k] = ok[k] ? d * row_units : 0;
+            src[k] = u;
+            dst[k] = d;
             if (ok[k] && li == 0) {
                 nodes_out[d] = (int32_t)u;
                 nd += (e == 0 || pu != u);
@@ -702,19 +702,22 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             key[k] = e < hi ? rl_key[e] : 0;
             val[k] = e < hi ? rl_val[e] : 0;
         }
-        for (int64_t c = li; c < row_units; c += LPR) {
+        // a row of at most LPR units is one piece per lane (the common case: no loop)
+        const int64_t c_end = ONE ? std::min<int64_t>(row_units, li + 1) : row_units;
+        for (int64_t c = li; c < c_end; c += LPR) {
             Unit x[U];
 #pragma unroll
             for (int k = 0; k < U; k++)
-                if (fresh[k]) x[k] = feat[src[k] + c];
+                if (fresh[k]) x[k] = feat[(int64_t)src[k] * row_units + c];
 #pragma unroll
             for (int k = 1; k < U; k++)
                 if (!fresh[k]) x[k] = x[k - 1];
 #pragma unroll
             for (int k = 0; k < U; k++) {
                 if (!ok[k]) continue;
-                if (NT) __builtin_nontemporal_store(x[k], out + dst[k] + c);
-                else out[dst[k] + c] = x[k];
+                Unit* o = out + (int64_t)dst[k] * row_units + c;
+                if (NT) __builtin_nontemporal_store(x[k], o);
+                else *o = x[k];
             }
         }
     }
@@ -743,9 +746,14 @@ struct GatherArgs {
 template <typename Unit, int LPR, int U, bool NT>
 static void launch_gather_k(const GatherArgs& a, int G, hipStream_t st) {
     const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
-    hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
-                       (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.rows, a.row_units,
-                       a.rpb, a.ctl);
+    if (a.row_units <= LPR)
+        hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, true>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
+                           (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.rows, a.row_units,
+                           a.rpb, a.ctl);
+    else
+        hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, false>), dim3(G), dim3(kBlock), lds, st,
+                           (const Unit*)a.feat, (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H,
+                           a.rows, a.row_units, a.rpb, a.ctl);
 }
 
 template <typename Unit, int LPR>
