@@ -150,14 +150,18 @@ def main():
     ap.add_argument("--H", type=int, default=None, help="minibatches per hyperbatch (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
-    ap.add_argument("--depth", type=int, default=2, help="hyperbatches sampled ahead of the one gathering")
-    ap.add_argument("--sample-streams", type=int, default=2,
+    ap.add_argument("--depth", type=int, default=3, help="hyperbatches sampled ahead of the one gathering")
+    ap.add_argument("--sample-streams", type=int, default=3,
                     help="streams the sampling of consecutive hyperbatches alternates between")
+    ap.add_argument("--gather-stream", choices=["default", "own"], default="default",
+                    help="gather on the default stream (default: the process's other hardware queues, "
+                         "4 per process on this platform, then serve the sampling streams) or on its own")
     ap.add_argument("--gather-first", action="store_true",
                     help="queue each gather before waiting for the previous one")
     ap.add_argument("--gather-groups", type=int, default=None, help="row-copy kernel workgroups")
     ap.add_argument("--gather-unroll", type=int, default=None, help="rows in flight per lane group")
     ap.add_argument("--gather-nt", type=int, default=None, help="1 = non-temporal row stores, 0 = ordinary")
+    ap.add_argument("--gather-chunks", type=int, default=None, help="launches the row copy is split into")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
     args = ap.parse_args()
@@ -194,14 +198,17 @@ def main():
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
     store.set_profiling(True)
     store.set_gather_shape(args.gather_groups, args.gather_unroll,
-                           None if args.gather_nt is None else bool(args.gather_nt))
+                           None if args.gather_nt is None else bool(args.gather_nt), args.gather_chunks)
     stream = torch.cuda.current_stream()
     ob = 8 if w["offsets"].dtype == np.int64 else 4
     rb = cfg.row_bytes
 
     # sampling runs on one or more streams, gathers on another (all default priority)
     s_streams = [torch.cuda.Stream() for _ in range(max(1, args.sample_streams))]
-    s_stream, g_stream = s_streams[0], torch.cuda.Stream()
+    # the gather may run on the default stream, leaving the process's other
+    # hardware queues to sampling
+    g_stream = torch.cuda.default_stream() if args.gather_stream == "default" else torch.cuda.Stream()
+    s_stream = s_streams[0]
     acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, sample_ms=0.0, gather_ms=0.0,
                copy_ms=0.0, steps=0)
 
@@ -308,7 +315,7 @@ def main():
         "mode": f"pipelined: {NSLOT} batch slots, a sampling stream and a gather stream; "
                 f"hyperbatches t+1..t+{D} sample while t gathers"
                 + ("; gathers queued back to back" if args.gather_first else "; sampling enqueued first")
-                + f"; {len(s_streams)} sampling stream(s)",
+                + f"; {len(s_streams)} sampling stream(s); gather on the {args.gather_stream} stream",
         "serial_ms_per_step": round(serial_ms, 4),
         "per_step": {"algorithmic_bytes": tot_bytes // K, "sample_bytes": tot_sample // K,
                      "gather_bytes": tot_gather // K, "rows": rows // K, "sampled_edges": edges // K},

@@ -207,12 +207,16 @@ agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);   /*
  *     16 (default 4).
  *   AGNES_OPT_GATHER_NONTEMPORAL: 1 = write gathered rows with non-temporal
  *     stores (default), 0 = ordinary stores.
+ *   AGNES_OPT_GATHER_CHUNKS: the row copy runs as this many consecutive
+ *     launches over consecutive parts of the bucket, in [1, 64] (default 1);
+ *     kernels of other streams are dispatched between them.
  * Options change launch shapes and store kinds only, never results. */
 typedef enum {
     AGNES_OPT_PROFILE = 1,
     AGNES_OPT_GATHER_GROUPS = 2,
     AGNES_OPT_GATHER_UNROLL = 3,
-    AGNES_OPT_GATHER_NONTEMPORAL = 4
+    AGNES_OPT_GATHER_NONTEMPORAL = 4,
+    AGNES_OPT_GATHER_CHUNKS = 5
 } agnes_option;
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value);
 

@@ -94,8 +94,10 @@ class Store:
         agnes_store_set_option(self.handle, B.AGNES_OPT_PROFILE, 1 if on else 0)
 
     def set_gather_shape(self, groups: int | None = None, unroll: int | None = None,
-                         nontemporal: bool | None = None) -> None:
+                         nontemporal: bool | None = None, chunks: int | None = None) -> None:
         """Launch shape and store kind of the row-copy kernel (never change results)."""
+        if chunks is not None:
+            agnes_store_set_option(self.handle, B.AGNES_OPT_GATHER_CHUNKS, int(chunks))
         if groups is not None:
             agnes_store_set_option(self.handle, B.AGNES_OPT_GATHER_GROUPS, int(groups))
         if unroll is not None:

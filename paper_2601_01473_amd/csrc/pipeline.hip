@@ -641,14 +641,16 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // of it, U entries at a time: an entry whose node equals the previous entry's
 // reuses the row already in registers, the others load theirs (U rows in
 // flight), and the list entries of the next U are fetched while the rows load.
-// Also counts the distinct rows and the non-empty feature-block rows.
+// A launch covers list entries [base, base + rows); the host may split the list
+// into several launches so that other streams' kernels are dispatched between
+// them.  Also counts the distinct rows and the non-empty feature-block rows.
 template <typename Unit, int LPR, int U, bool NT, bool ONE>
 __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat, Unit* __restrict__ out,
                                                    int32_t* __restrict__ nodes_out,
                                                    const uint64_t* __restrict__ rl_key,
                                                    const int32_t* __restrict__ rl_val, const int64_t* node_off_g,
-                                                   int H, int64_t rows, int64_t row_units, uint32_t rpb,
-                                                   Ctl* ctl) {
+                                                   int H, int64_t base, int64_t rows, int64_t row_units,
+                                                   uint32_t rpb, Ctl* ctl) {
     constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
     constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
     extern __shared__ int64_t node_off[];
@@ -659,8 +661,8 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
     const int b = blockIdx.x;
     const int lb = (G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
     const int64_t chunk = (rows + G - 1) / G;
-    const int64_t wlo = std::min<int64_t>(rows, (int64_t)lb * chunk);
-    const int64_t whi = std::min<int64_t>(rows, wlo + chunk);
+    const int64_t wlo = base + std::min<int64_t>(rows, (int64_t)lb * chunk);
+    const int64_t whi = base + std::min<int64_t>(rows, (int64_t)lb * chunk + chunk);
     const int li = lane_id() % LPR;
     const int gid = wave_id() * RPW + lane_id() / LPR;
     const int64_t sub = (whi - wlo + GPB - 1) / GPB;
@@ -738,7 +740,7 @@ struct GatherArgs {
     const int32_t* rl_val;
     const int64_t* node_off;
     int H;
-    int64_t rows, row_units;
+    int64_t base, rows, row_units;   // entries [base, base + rows) of the list
     uint32_t rpb;
     Ctl* ctl;
 };
@@ -748,12 +750,12 @@ static void launch_gather_k(const GatherArgs& a, int G, hipStream_t st) {
     const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
     if (a.row_units <= LPR)
         hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, true>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
-                           (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.rows, a.row_units,
-                           a.rpb, a.ctl);
+                           (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
+                           a.row_units, a.rpb, a.ctl);
     else
         hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, false>), dim3(G), dim3(kBlock), lds, st,
                            (const Unit*)a.feat, (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H,
-                           a.rows, a.row_units, a.rpb, a.ctl);
+                           a.base, a.rows, a.row_units, a.rpb, a.ctl);
 }
 
 template <typename Unit, int LPR>
@@ -767,16 +769,23 @@ static void launch_gather_lpr(const GatherArgs& a, int G, int unroll, bool nt, h
     }
 }
 
-// LPR = the power of two lanes that covers a row best (at most a wave).
+// LPR = the power of two lanes that covers a row best (at most a wave).  The
+// list is copied in `chunks` consecutive launches of groups/chunks workgroups.
 template <typename Unit>
-static void launch_gather(const GatherArgs& a, int groups, int unroll, bool nt, hipStream_t st) {
-    int G = grid_for(a.rows * a.row_units / 64 + 1, groups);
-    G = std::max(8, (G + 7) / 8 * 8);
-    if (a.row_units >= 64) launch_gather_lpr<Unit, 64>(a, G, unroll, nt, st);
-    else if (a.row_units > 16) launch_gather_lpr<Unit, 32>(a, G, unroll, nt, st);
-    else if (a.row_units > 8) launch_gather_lpr<Unit, 16>(a, G, unroll, nt, st);
-    else if (a.row_units > 4) launch_gather_lpr<Unit, 8>(a, G, unroll, nt, st);
-    else launch_gather_lpr<Unit, 4>(a, G, unroll, nt, st);
+static void launch_gather(const GatherArgs& all, int groups, int unroll, bool nt, int chunks, hipStream_t st) {
+    chunks = (int)std::max<int64_t>(1, std::min<int64_t>(chunks, all.rows));
+    for (int c = 0; c < chunks; c++) {
+        GatherArgs a = all;
+        a.base = all.rows * c / chunks;
+        a.rows = all.rows * (c + 1) / chunks - a.base;
+        int G = grid_for(a.rows * a.row_units / 64 + 1, std::max(8, groups / chunks));
+        G = std::max(8, (G + 7) / 8 * 8);
+        if (a.row_units >= 64) launch_gather_lpr<Unit, 64>(a, G, unroll, nt, st);
+        else if (a.row_units > 16) launch_gather_lpr<Unit, 32>(a, G, unroll, nt, st);
+        else if (a.row_units > 8) launch_gather_lpr<Unit, 16>(a, G, unroll, nt, st);
+        else if (a.row_units > 4) launch_gather_lpr<Unit, 8>(a, G, unroll, nt, st);
+        else launch_gather_lpr<Unit, 4>(a, G, unroll, nt, st);
+    }
 }
 
 // ----------------------------------------------------------------- host orchestration
@@ -997,13 +1006,13 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     const int32_t* rlv = w.rl_val[b.cur].as<int32_t>();
     if (rows > 0) {
         GatherArgs ga{s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv, w.mb_off.as<int64_t>(),
-                      H, rows, 0, (uint32_t)s.rpb, ctl};
+                      H, 0, rows, 0, (uint32_t)s.rpb, ctl};
         if (s.row_bytes % 16 == 0) {
             ga.row_units = s.row_bytes / 16;
-            launch_gather<u32x4>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, st);
+            launch_gather<u32x4>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, s.gather_chunks, st);
         } else {
             ga.row_units = s.row_bytes / 4;
-            launch_gather<uint32_t>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, st);
+            launch_gather<uint32_t>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, s.gather_chunks, st);
         }
     }
     AGNES_CHECK_HIP(hipGetLastError());

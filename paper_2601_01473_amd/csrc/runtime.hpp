@@ -137,6 +137,7 @@ struct Store {
     int gather_groups = 16384;        // workgroups of the row-copy kernel (upper bound)
     int gather_unroll = 4;            // rows in flight per lane group (4, 8 or 16)
     int gather_nt = 1;                // 1 = non-temporal stores of the gathered rows
+    int gather_chunks = 1;            // consecutive launches the row copy is split into
 };
 
 // A batch: the outputs of one hyperbatch and the scratch memory that produces

@@ -304,10 +304,10 @@ def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim):
     ref = oracle.Oracle(off, idx).hyperbatch(tg, fan, 9, 0)
     fb = feature_bytes(feat)
     want = oracle.hyperbatch_stats(off, 256, fb.shape[1], ref, len(fan))
-    for groups, unroll, nt in [(8, 4, True), (8, 16, False), (24, 8, True), (2048, 4, False),
-                               (65536, 8, True), (1000, 16, True)]:
-        log("gather shape", rows_dim, groups, unroll, nt)
-        store.set_gather_shape(groups, unroll, nt)
+    for groups, unroll, nt, chunks in [(8, 4, True, 1), (8, 16, False, 3), (24, 8, True, 1),
+                                       (2048, 4, False, 7), (65536, 8, True, 64), (1000, 16, True, 2)]:
+        log("gather shape", rows_dim, groups, unroll, nt, chunks)
+        store.set_gather_shape(groups, unroll, nt, chunks)
         b = store.prepare(t, fan, seed=9, mb_base=0)
         got = b.to_host()
         for j in range(tg.shape[0]):
@@ -319,6 +319,9 @@ def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim):
     for bad in [(7, None), (65537, None), (None, 3), (None, 2), (None, 32)]:
         with pytest.raises(agnes.AgnesError):
             store.set_gather_shape(*bad)
+    for bad_chunks in [0, 65]:
+        with pytest.raises(agnes.AgnesError):
+            store.set_gather_shape(chunks=bad_chunks)
     store.close()
 
 
