@@ -635,12 +635,13 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // gathering loop in block order: the requests of a feature block are contiguous
 // and those of one node are neighbours, so each row is loaded from HBM once and
 // written to every minibatch that needs it (dest = node_off[j] + local id).
-// LPR lanes share a row (16-byte or 4-byte units).  Workgroup b takes a
-// contiguous range of the list (ranges are dealt so that neighbouring ranges,
-// the same blocks, run on the same XCD) and each lane group a contiguous piece
-// of it, U entries at a time: an entry whose node equals the previous entry's
-// reuses the row already in registers, the others load theirs (U rows in
-// flight), and the list entries of the next U are fetched while the rows load.
+// LPR lanes share a row (16-byte or 4-byte units).  Lane groups take blocks of
+// U consecutive entries in grid-stride order, so the waves in flight work on
+// one compact window of the list: a minibatch's rows are written in ascending
+// address order (the list is sorted by node, and so are the local ids of each
+// hop's new nodes), and a compact window keeps those writes close together in
+// DRAM.  Within a block, an entry whose node equals the previous entry's reuses
+// the row already in registers; the others load theirs (U rows in flight).
 // A launch covers list entries [base, base + rows); the host may split the list
 // into several launches so that other streams' kernels are dispatched between
 // them.  Also counts the distinct rows and the non-empty feature-block rows.
@@ -658,27 +659,21 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
     if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
     load_offsets(node_off, node_off_g, H);
     const int G = gridDim.x;
-    const int b = blockIdx.x;
-    const int lb = (G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
-    const int64_t chunk = (rows + G - 1) / G;
-    const int64_t wlo = base + std::min<int64_t>(rows, (int64_t)lb * chunk);
-    const int64_t whi = base + std::min<int64_t>(rows, (int64_t)lb * chunk + chunk);
     const int li = lane_id() % LPR;
     const int gid = wave_id() * RPW + lane_id() / LPR;
-    const int64_t sub = (whi - wlo + GPB - 1) / GPB;
-    const int64_t lo = std::min<int64_t>(whi, wlo + gid * sub);
-    const int64_t hi = std::min<int64_t>(whi, lo + sub);
     unsigned long long nd = 0, nf = 0;
-    uint32_t prev_u = (lo > 0 && lo < hi) ? (uint32_t)(rl_key[lo - 1] >> 32) : 0xFFFFFFFFu;
-    uint64_t key[U];
-    int32_t val[U];
+    const int64_t lo = base, hi = base + rows;
+    const int64_t stride = (int64_t)G * GPB * U;
+    for (int64_t e0 = lo + ((int64_t)blockIdx.x * GPB + gid) * U; e0 < hi; e0 += stride) {
+        uint64_t key[U];
+        int32_t val[U];
 #pragma unroll
-    for (int k = 0; k < U; k++) {
-        key[k] = lo + k < hi ? rl_key[lo + k] : 0;
-        val[k] = lo + k < hi ? rl_val[lo + k] : 0;
-    }
-    for (int64_t e0 = lo; e0 < hi; e0 += U) {
-        uint32_t src[U], dst[U];             // row numbers (node, output row); < 2^31
+        for (int k = 0; k < U; k++) {
+            key[k] = e0 + k < hi ? rl_key[e0 + k] : 0;
+            val[k] = e0 + k < hi ? rl_val[e0 + k] : 0;
+        }
+        uint32_t prev_u = e0 > 0 ? (uint32_t)(rl_key[e0 - 1] >> 32) : 0xFFFFFFFFu;
+        uint32_t src[U], dst[U];
         bool ok[U], fresh[U];
 #pragma unroll
         for (int k = 0; k < U; k++) {
@@ -696,15 +691,6 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
                 nf += (e == 0 || pu / rpb != u / rpb);
             }
         }
-        prev_u = (uint32_t)(key[U - 1] >> 32);
-        // list entries of the next U, fetched while these rows load
-#pragma unroll
-        for (int k = 0; k < U; k++) {
-            const int64_t e = e0 + U + k;
-            key[k] = e < hi ? rl_key[e] : 0;
-            val[k] = e < hi ? rl_val[e] : 0;
-        }
-        // a row of at most LPR units is one piece per lane (the common case: no loop)
         const int64_t c_end = ONE ? std::min<int64_t>(row_units, li + 1) : row_units;
         for (int64_t c = li; c < c_end; c += LPR) {
             Unit x[U];
