@@ -120,14 +120,26 @@ __device__ __forceinline__ int64_t wave_partition_point(int64_t lo, int64_t hi, 
 // published Weyl increments between rounds.
 struct Words4 { uint64_t w[4]; };
 
+// Full 128-bit product of a 64-bit constant and a 64-bit value from four
+// 32 x 32 -> 64 multiply-adds (each partial sum fits in 64 bits).
+__device__ __forceinline__ void mul64_wide(uint64_t a, uint64_t b, uint64_t& hi, uint64_t& lo) {
+    const uint64_t al = (uint32_t)a, ah = a >> 32, bl = (uint32_t)b, bh = b >> 32;
+    const uint64_t t0 = al * bl;
+    const uint64_t t1 = al * bh + (t0 >> 32);
+    const uint64_t t2 = ah * bl + (uint32_t)t1;
+    hi = ah * bh + (t1 >> 32) + (t2 >> 32);
+    lo = (t2 << 32) | (uint32_t)t0;
+}
+
 __device__ __forceinline__ Words4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
                                                 uint64_t k0, uint64_t k1) {
     const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
     const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
 #pragma unroll
     for (int r = 0; r < 10; r++) {
-        uint64_t hi0 = __umul64hi(M0, c0), lo0 = M0 * c0;
-        uint64_t hi1 = __umul64hi(M1, c2), lo1 = M1 * c2;
+        uint64_t hi0, lo0, hi1, lo1;
+        mul64_wide(M0, c0, hi0, lo0);
+        mul64_wide(M1, c2, hi1, lo1);
         uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
         c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
         k0 += W0; k1 += W1;

@@ -654,6 +654,11 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
                                                    uint32_t rpb, Ctl* ctl) {
     constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
     constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
+    // Hold at least 88 VGPRs, i.e. at most 5 of the 8 wave slots of a SIMD (512
+    // VGPRs each).  The copy alone runs as fast this way, and kernels of other
+    // streams (the sampling of the next hyperbatches) always find free slots
+    // instead of waiting for the copy's backlog of workgroups to drain.
+    asm volatile("" ::: "v87");
     extern __shared__ int64_t node_off[];
     __shared__ unsigned long long cnt[2];
     if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
@@ -844,9 +849,14 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, seed,     \
                        mb_base, off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),      \
                        w.e_off.as<int64_t>(), cg, ctl)
+    // the register sampler's work grows with MAXK^2 (ranks) and MAXK/4 (Philox
+    // calls), so common fanouts get a bound of their own
     if (f <= 4) AGNES_SAMPLE(4);
     else if (f <= 8) AGNES_SAMPLE(8);
+    else if (f <= 10) AGNES_SAMPLE(10);
     else if (f <= 16) AGNES_SAMPLE(16);
+    else if (f <= 20) AGNES_SAMPLE(20);
+    else if (f <= 25) AGNES_SAMPLE(25);
     else if (f <= 32) AGNES_SAMPLE(32);
     else AGNES_SAMPLE(0);
 #undef AGNES_SAMPLE
