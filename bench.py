@@ -30,7 +30,7 @@ import numpy as np
 HBM_PEAK_GBPS = 8000.0
 
 
-GATHER_TRAFFIC_FILE = os.path.join("profiles", "k_gather.rmat-2^23.hbm-traffic.md")
+GATHER_TRAFFIC_FILE = os.path.join("profiles", "k_gather_rows.rmat-2^23.hbm-traffic.md")
 
 
 def gather_fingerprint(root: str) -> str:
@@ -39,7 +39,7 @@ def gather_fingerprint(root: str) -> str:
     import hashlib
     import re
     src = open(os.path.join(root, "paper_2601_01473_amd", "csrc", "pipeline.hip")).read()
-    m = re.search(r"template <[^>]*>\n__global__ __launch_bounds__\(kBlock\) void k_gather\(", src)
+    m = re.search(r"template <[^>]*>\n__global__ __launch_bounds__\(kBlock\) void k_gather_rows\(", src)
     if m is None or "struct GatherArgs {" not in src[m.start():]:
         return ""
     a = m.start()
@@ -156,8 +156,11 @@ def main():
     ap.add_argument("--gather-stream", choices=["default", "own"], default="default",
                     help="gather on the default stream (default: the process's other hardware queues, "
                          "4 per process on this platform, then serve the sampling streams) or on its own")
-    ap.add_argument("--gather-first", action="store_true",
-                    help="queue each gather before waiting for the previous one")
+    ap.add_argument("--schedule", choices=["ahead", "sample-first", "gather-first"], default="ahead",
+                    help="ahead: each gather is queued behind the running one and a step's statistics are "
+                         "read two steps later, so the host never waits for a gather before queuing work; "
+                         "sample-first: the next sampling is enqueued before each gather; gather-first: each "
+                         "gather is queued before the previous one is waited for")
     ap.add_argument("--gather-groups", type=int, default=None, help="row-copy kernel workgroups")
     ap.add_argument("--gather-unroll", type=int, default=None, help="rows in flight per lane group")
     ap.add_argument("--gather-nt", type=int, default=None, help="1 = non-temporal row stores, 0 = ordinary")
@@ -185,7 +188,7 @@ def main():
     w = synth.workload(cfg, H=args.H)
     H, B = w["H"], w["B"]
     print(f"# inputs ready in {time.time() - t0:.1f}s (E={len(w['indices'])})", file=sys.stderr, flush=True)
-    args.warmup = max(args.depth + 1, args.warmup)   # every batch slot is allocated before timing
+    args.warmup = max(args.depth + 2, args.warmup)   # every batch slot is allocated before timing
     nsteps = args.steps + args.warmup
     # distinct targets per step: consecutive slices of one permutation of the nodes
     perm = synth.targets(cfg.num_nodes, min(cfg.num_nodes, nsteps * H * B), cfg.data_seed + 7)
@@ -209,7 +212,7 @@ def main():
     # hardware queues to sampling
     g_stream = torch.cuda.default_stream() if args.gather_stream == "default" else torch.cuda.Stream()
     s_stream = s_streams[0]
-    acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, sample_ms=0.0, gather_ms=0.0,
+    acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, distinct=0, sample_ms=0.0, gather_ms=0.0,
                copy_ms=0.0, steps=0)
 
     def account(batch):
@@ -221,13 +224,16 @@ def main():
         acc["bytes"] += bs + bg
         acc["edges"] += sum(st["sampled"])
         acc["rows"] += st["rows"]
+        acc["distinct"] += st["distinct_rows"]
         acc["sample_ms"] += st["sample_ms"]
         acc["gather_ms"] += st["gather_ms"]
         acc["copy_ms"] += st["copy_ms"]
         acc["steps"] += 1
 
     D = max(1, args.depth)                      # hyperbatches sampled ahead of the one gathering
-    NSLOT = D + 1
+    # "ahead" keeps two finished steps unread, so it holds two more slots than
+    # the hyperbatches in flight
+    NSLOT = D + (2 if args.schedule == "ahead" else 1)
     slots = [None] * NSLOT
 
     def begin(s):
@@ -235,27 +241,33 @@ def main():
         slots[k] = store.begin(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[k],
                                stream=s_streams[s % len(s_streams)])
 
+    def retire(s, record):
+        b = slots[s % NSLOT]
+        account(b) if record else b.wait()
+
     def pipeline(first, n, record):
         """Steps first .. first+n-1 with the sampling of steps s+1 .. s+D in flight
-        while step s gathers.  Default order: the sampling of step s+D is enqueued
-        before the gather of step s, so it starts on an idle GPU; with
-        --gather-first the gather of step s is queued before step s-1 is waited
-        for, so the gather stream never drains."""
+        while step s gathers.
+        ahead: gather s is queued (behind gather s-1) as soon as step s's sizes
+          are known; only then is step s-2 retired and step s+D begun in its slot,
+          so the gather stream never drains while the host enqueues sampling.
+        sample-first: step s-1 is retired, step s+D begun, then gather s queued.
+        gather-first: gather s queued, step s-1 retired, step s+D begun."""
         for s in range(first, first + min(D, n)):
             begin(s)
+        lag = 2 if args.schedule == "ahead" else 1
         for i in range(n):
             s = first + i
-            if args.gather_first:
+            if args.schedule != "sample-first":
                 slots[s % NSLOT].finish(stream=g_stream)   # waits for step s's sizes only
-            if i >= 1:
-                b = slots[(s - 1) % NSLOT]
-                account(b) if record else b.wait()          # step s-1 done: its slot is free
+            if i >= lag:
+                retire(s - lag, record)                    # its slot is free for step s+D
             if i + D < n:
                 begin(s + D)
-            if not args.gather_first:
+            if args.schedule == "sample-first":
                 slots[s % NSLOT].finish(stream=g_stream)
-        last = slots[(first + n - 1) % NSLOT]
-        account(last) if record else last.wait()
+        for s in range(first + max(0, n - lag), first + n):
+            retire(s, record)
 
     # warm-up: every slot allocated at the largest shape seen so far
     pipeline(0, args.warmup, record=False)
@@ -312,14 +324,14 @@ def main():
         "gather_phase_GBps": round(rows * rb / (gather_ms * 1e-3) / 1e9, 2) if gather_ms > 0 else None,
         "phase_ms": {"sample": round(sample_ms / K, 4), "gather": round(gather_ms / K, 4),
                      "copy_kernel": round(copy_avg_ms, 4)},
-        "mode": f"pipelined: {NSLOT} batch slots, a sampling stream and a gather stream; "
+        "mode": f"pipelined ({args.schedule}): {NSLOT} batch slots; "
                 f"hyperbatches t+1..t+{D} sample while t gathers"
-                + ("; gathers queued back to back" if args.gather_first else "; sampling enqueued first")
-                + f"; {len(s_streams)} sampling stream(s); gather on the {args.gather_stream} stream",
+                f"; {len(s_streams)} sampling stream(s); gather on the {args.gather_stream} stream",
         "serial_ms_per_step": round(serial_ms, 4),
         "per_step": {"algorithmic_bytes": tot_bytes // K, "sample_bytes": tot_sample // K,
-                     "gather_bytes": tot_gather // K, "rows": rows // K, "sampled_edges": edges // K},
-        "roofline": {"kernel": "k_gather (row copy)", "bound": "hbm", "achieved": round(achieved, 1),
+                     "gather_bytes": tot_gather // K, "rows": rows // K,
+                     "distinct_rows": acc["distinct"] // K, "sampled_edges": edges // K},
+        "roofline": {"kernel": "k_gather_rows (row copy)", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic[0] if traffic else None,
                      "traffic_unit": "GB per launch, HBM (FETCH_SIZE x2.0 + WRITE_SIZE x1.0, copy-calibrated)",

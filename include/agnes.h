@@ -202,7 +202,8 @@ agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);   /*
  *   AGNES_OPT_PROFILE: 1 = record HIP events around the phases of every
  *     hyperbatch (reported by agnes_batch_stats), 0 = off (default).
  *   AGNES_OPT_GATHER_GROUPS: most workgroups of the row-copy kernel, in
- *     [8, 65536] (default 16384).  Fewer leave room for another stream's work.
+ *     [8, 2^22] (default 2^22); a launch never takes more workgroups than it
+ *     has blocks of rows.  Fewer leave room for another stream's work.
  *   AGNES_OPT_GATHER_UNROLL: rows each lane group keeps in flight, 4, 8 or
  *     16 (default 4).
  *   AGNES_OPT_GATHER_NONTEMPORAL: 1 = write gathered rows with non-temporal

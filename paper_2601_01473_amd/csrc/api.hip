@@ -193,7 +193,7 @@ agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_
         if (opt == AGNES_OPT_PROFILE) {
             s->profile = value ? 1 : 0;
         } else if (opt == AGNES_OPT_GATHER_GROUPS) {
-            AGNES_REQUIRE(value >= 8 && value <= 65536, AGNES_ERR_INVALID, "gather groups must be in [8, 65536]");
+            AGNES_REQUIRE(value >= 8 && value <= (1 << 22), AGNES_ERR_INVALID, "gather groups must be in [8, 2^22]");
             s->gather_groups = (int)value;
         } else if (opt == AGNES_OPT_GATHER_UNROLL) {
             AGNES_REQUIRE(value == 4 || value == 8 || value == 16, AGNES_ERR_INVALID,

@@ -627,6 +627,34 @@ static size_t join_write_lds(int H) {
            (size_t)kWavesPerBlock * H * 2;
 }
 
+// Statistics of the final list (the feature bucket): distinct rows (runs of one
+// node) and non-empty feature-block rows (runs of one feature block).  Runs on
+// the sampling stream so that the row copy does nothing but copy.
+__global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, uint32_t rpb, Ctl* ctl) {
+    __shared__ unsigned long long cnt[2];
+    if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t n = ctl->rows;
+    unsigned long long nd = 0, nf = 0;
+    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n; e += (int64_t)gridDim.x * kBlock) {
+        const uint32_t u = (uint32_t)(rl_key[e] >> 32);
+        const uint32_t pu = e > 0 ? (uint32_t)(rl_key[e - 1] >> 32) : 0xFFFFFFFFu;
+        nd += (e == 0 || pu != u);
+        nf += (e == 0 || pu / rpb != u / rpb);
+    }
+    nd = wave_inclusive_scan(nd);
+    nf = wave_inclusive_scan(nf);
+    if (lane_id() == kWave - 1) {
+        if (nd) atomicAdd(&cnt[0], nd);
+        if (nf) atomicAdd(&cnt[1], nf);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        if (cnt[0]) atomicAdd((unsigned long long*)&ctl->distinct, cnt[0]);
+        if (cnt[1]) atomicAdd((unsigned long long*)&ctl->fblocks, cnt[1]);
+    }
+}
+
 // ----------------------------------------------------------------- gather
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -650,8 +678,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
                                                    int32_t* __restrict__ nodes_out,
                                                    const uint64_t* __restrict__ rl_key,
                                                    const int32_t* __restrict__ rl_val, const int64_t* node_off_g,
-                                                   int H, int64_t base, int64_t rows, int64_t row_units,
-                                                   uint32_t rpb, Ctl* ctl) {
+                                                   int H, int64_t base, int64_t rows, int64_t row_units) {
     constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
     constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
     // Hold at least 88 VGPRs, i.e. at most 5 of the 8 wave slots of a SIMD (512
@@ -660,13 +687,10 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
     // instead of waiting for the copy's backlog of workgroups to drain.
     asm volatile("" ::: "v87");
     extern __shared__ int64_t node_off[];
-    __shared__ unsigned long long cnt[2];
-    if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
     load_offsets(node_off, node_off_g, H);
     const int G = gridDim.x;
     const int li = lane_id() % LPR;
     const int gid = wave_id() * RPW + lane_id() / LPR;
-    unsigned long long nd = 0, nf = 0;
     const int64_t lo = base, hi = base + rows;
     const int64_t stride = (int64_t)G * GPB * U;
     for (int64_t e0 = lo + ((int64_t)blockIdx.x * GPB + gid) * U; e0 < hi; e0 += stride) {
@@ -690,11 +714,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             fresh[k] = ok[k] && (k == 0 || u != pu);
             src[k] = u;
             dst[k] = d;
-            if (ok[k] && li == 0) {
-                nodes_out[d] = (int32_t)u;
-                nd += (e == 0 || pu != u);
-                nf += (e == 0 || pu / rpb != u / rpb);
-            }
+            if (ok[k] && li == 0) nodes_out[d] = (int32_t)u;
         }
         const int64_t c_end = ONE ? std::min<int64_t>(row_units, li + 1) : row_units;
         for (int64_t c = li; c < c_end; c += LPR) {
@@ -714,12 +734,76 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             }
         }
     }
-    if (nd) atomicAdd(&cnt[0], nd);
-    if (nf) atomicAdd(&cnt[1], nf);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        if (cnt[0]) atomicAdd((unsigned long long*)&ctl->distinct, cnt[0]);
-        if (cnt[1]) atomicAdd((unsigned long long*)&ctl->fblocks, cnt[1]);
+}
+
+// Row copy for rows of at least 64 16-byte units (1 KiB and up): one wave per
+// row.  A wave takes U consecutive entries of the list; lane k < U reads entry
+// k and resolves its source row (the node) and destination row (node_off[j] +
+// local id), and the wave then broadcasts them with readlane, so each row's
+// addresses live in scalar registers and a lane holds only the data: U rows x
+// UPR units in flight per lane.  Chunks of 64 * UPR units cover longer rows.
+// An entry whose node repeats the previous entry's (within the wave's U) reuses
+// the row already in registers.  Waves take blocks of U entries in grid-stride
+// order (wave w of the grid, then w + all waves, ...).
+template <int U, int UPR, bool NT>
+__global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict__ feat, u32x4* __restrict__ out,
+                                                        int32_t* __restrict__ nodes_out,
+                                                        const uint64_t* __restrict__ rl_key,
+                                                        const int32_t* __restrict__ rl_val,
+                                                        const int64_t* node_off_g, int H, int64_t base,
+                                                        int64_t rows, int64_t row_units) {
+    static_assert(U <= kWave, "one lane per entry");
+    extern __shared__ int64_t node_off[];
+    load_offsets(node_off, node_off_g, H);
+    const int lane = lane_id();
+    const int64_t hi = base + rows;
+    const int64_t nw = (int64_t)gridDim.x * kWavesPerBlock;
+    for (int64_t e0 = base + ((int64_t)blockIdx.x * kWavesPerBlock + wave_id()) * U; e0 < hi; e0 += nw * U) {
+        const int64_t e = e0 + lane;
+        const bool mine = lane < U && e < hi;
+        uint32_t u = 0xFFFFFFFFu, d = 0;
+        if (mine) {
+            const uint64_t key = rl_key[e];
+            u = (uint32_t)(key >> 32);
+            d = (uint32_t)(node_off[(uint32_t)key] + rl_val[e]);
+            nodes_out[d] = (int32_t)u;
+        }
+        const uint32_t pu = (uint32_t)__shfl_up((int)u, 1, kWave);
+        const uint64_t okm = __ballot(mine);
+        const uint64_t fresh = __ballot(mine && (lane == 0 || pu != u));
+        uint32_t src[U], dst[U];
+#pragma unroll
+        for (int k = 0; k < U; k++) {
+            src[k] = (uint32_t)__builtin_amdgcn_readlane((int)u, k);
+            dst[k] = (uint32_t)__builtin_amdgcn_readlane((int)d, k);
+        }
+        for (int64_t c0 = 0; c0 < row_units; c0 += (int64_t)kWave * UPR) {
+            u32x4 x[U][UPR];
+#pragma unroll
+            for (int k = 0; k < U; k++) {
+                if ((fresh >> k) & 1) {
+                    const u32x4* p = feat + (int64_t)src[k] * row_units + c0 + lane;
+#pragma unroll
+                    for (int q = 0; q < UPR; q++)
+                        if (c0 + lane + q * kWave < row_units) x[k][q] = p[q * kWave];
+                } else if (k > 0) {
+#pragma unroll
+                    for (int q = 0; q < UPR; q++) x[k][q] = x[k - 1][q];
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < U; k++) {
+                if (!((okm >> k) & 1)) continue;
+                u32x4* o = out + (int64_t)dst[k] * row_units + c0 + lane;
+#pragma unroll
+                for (int q = 0; q < UPR; q++) {
+                    if (c0 + lane + q * kWave < row_units) {
+                        if (NT) __builtin_nontemporal_store(x[k][q], o + q * kWave);
+                        else o[q * kWave] = x[k][q];
+                    }
+                }
+            }
+        }
     }
 }
 
@@ -732,21 +816,24 @@ struct GatherArgs {
     const int64_t* node_off;
     int H;
     int64_t base, rows, row_units;   // entries [base, base + rows) of the list
-    uint32_t rpb;
-    Ctl* ctl;
 };
 
 template <typename Unit, int LPR, int U, bool NT>
-static void launch_gather_k(const GatherArgs& a, int G, hipStream_t st) {
+static void launch_gather_k(const GatherArgs& a, int groups, hipStream_t st) {
     const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
+    // at most one workgroup per U rows of each lane group: with enough groups
+    // every workgroup copies one block and the blocks in flight follow the
+    // dispatch order through the list
+    constexpr int64_t per_wg = (int64_t)kWavesPerBlock * (kWave / LPR) * U;
+    const int G = (int)std::max<int64_t>(1, std::min<int64_t>(groups, (a.rows + per_wg - 1) / per_wg));
     if (a.row_units <= LPR)
         hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, true>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
                            (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
-                           a.row_units, a.rpb, a.ctl);
+                           a.row_units);
     else
         hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, false>), dim3(G), dim3(kBlock), lds, st,
                            (const Unit*)a.feat, (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H,
-                           a.base, a.rows, a.row_units, a.rpb, a.ctl);
+                           a.base, a.rows, a.row_units);
 }
 
 template <typename Unit, int LPR>
@@ -760,6 +847,28 @@ static void launch_gather_lpr(const GatherArgs& a, int G, int unroll, bool nt, h
     }
 }
 
+template <int U, int UPR, bool NT>
+static void launch_gather_rows_k(const GatherArgs& a, int groups, hipStream_t st) {
+    const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
+    constexpr int64_t per_wg = (int64_t)kWavesPerBlock * U;
+    const int G = (int)std::max<int64_t>(1, std::min<int64_t>(groups, (a.rows + per_wg - 1) / per_wg));
+    hipLaunchKernelGGL((k_gather_rows<U, UPR, NT>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
+                       (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
+                       a.row_units);
+}
+
+template <int UPR>
+static void launch_gather_rows_upr(const GatherArgs& a, int groups, int unroll, bool nt, hipStream_t st) {
+    if (unroll >= 16) {
+        if (nt) launch_gather_rows_k<16, UPR, true>(a, groups, st); else launch_gather_rows_k<16, UPR, false>(a, groups, st);
+    } else if (unroll >= 8) {
+        if (nt) launch_gather_rows_k<8, UPR, true>(a, groups, st); else launch_gather_rows_k<8, UPR, false>(a, groups, st);
+    } else {
+        if (nt) launch_gather_rows_k<4, UPR, true>(a, groups, st); else launch_gather_rows_k<4, UPR, false>(a, groups, st);
+    }
+}
+
+
 // LPR = the power of two lanes that covers a row best (at most a wave).  The
 // list is copied in `chunks` consecutive launches of groups/chunks workgroups.
 template <typename Unit>
@@ -769,9 +878,11 @@ static void launch_gather(const GatherArgs& all, int groups, int unroll, bool nt
         GatherArgs a = all;
         a.base = all.rows * c / chunks;
         a.rows = all.rows * (c + 1) / chunks - a.base;
-        int G = grid_for(a.rows * a.row_units / 64 + 1, std::max(8, groups / chunks));
-        G = std::max(8, (G + 7) / 8 * 8);
-        if (a.row_units >= 64) launch_gather_lpr<Unit, 64>(a, G, unroll, nt, st);
+        const int G = std::max(8, groups / chunks);
+        if (a.row_units >= 64 && sizeof(Unit) == 16) {
+            if (a.row_units >= 128) launch_gather_rows_upr<2>(a, G, unroll, nt, st);
+            else launch_gather_rows_upr<1>(a, G, unroll, nt, st);
+        } else if (a.row_units >= 64) launch_gather_lpr<Unit, 64>(a, G, unroll, nt, st);
         else if (a.row_units > 16) launch_gather_lpr<Unit, 32>(a, G, unroll, nt, st);
         else if (a.row_units > 8) launch_gather_lpr<Unit, 16>(a, G, unroll, nt, st);
         else if (a.row_units > 4) launch_gather_lpr<Unit, 8>(a, G, unroll, nt, st);
@@ -937,6 +1048,8 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
     hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
                        w.mb_off.as<int64_t>());
+    hipLaunchKernelGGL(k_list_stats, dim3(grid_for(g.rows_max, 1024)), dim3(kBlock), 0, st,
+                       w.rl_key[cur].as<uint64_t>(), (uint32_t)s.rpb, ctl);
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
     // sizes of the outputs travel to pinned host memory; finish reads them
@@ -970,6 +1083,8 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
         b.stats.new_nodes[l] = hc.new_nodes[l];
         b.stats.topo_blocks[l] = hc.topo_blocks[l];
     }
+    b.stats.distinct_rows = hc.distinct;
+    b.stats.feat_blocks = hc.fblocks;
 
     // host view offsets
     b.node_off.assign((size_t)H + 1, 0);
@@ -1002,7 +1117,7 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     const int32_t* rlv = w.rl_val[b.cur].as<int32_t>();
     if (rows > 0) {
         GatherArgs ga{s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv, w.mb_off.as<int64_t>(),
-                      H, 0, rows, 0, (uint32_t)s.rpb, ctl};
+                      H, 0, rows, 0};
         if (s.row_bytes % 16 == 0) {
             ga.row_units = s.row_bytes / 16;
             launch_gather<u32x4>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, s.gather_chunks, st);
@@ -1023,10 +1138,6 @@ void wait_batch(Batch& b) {
     if (b.state == kDone) return;
     AGNES_REQUIRE(b.state == kGathering, AGNES_ERR_INVALID, "the batch holds no finished hyperbatch");
     AGNES_CHECK_HIP(hipEventSynchronize(b.gathered));
-    Ctl hc;
-    memcpy(&hc, b.ws.sync_host.ptr, sizeof(Ctl));
-    b.stats.distinct_rows = hc.distinct;
-    b.stats.feat_blocks = hc.fblocks;
     b.stats.sample_ms = b.stats.gather_ms = b.stats.copy_ms = -1.0f;
     if (b.store->profile) {
         Workspace& w = b.ws;

@@ -134,7 +134,7 @@ struct Store {
     int node_bits = 0;                // bits of a node id (ceil log2 num_nodes)
     DevBuf offsets, indices, features, first_node, last_node;
     int profile = 0;
-    int gather_groups = 16384;        // workgroups of the row-copy kernel (upper bound)
+    int gather_groups = 1 << 22;      // workgroups of the row-copy kernel (upper bound)
     int gather_unroll = 4;            // rows in flight per lane group (4, 8 or 16)
     int gather_nt = 1;                // 1 = non-temporal stores of the gathered rows
     int gather_chunks = 1;            // consecutive launches the row copy is split into

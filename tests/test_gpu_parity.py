@@ -291,21 +291,31 @@ def test_finish_on_other_stream_and_errors(agnes):
         compare_minibatch(got[j], ref[j], oracle.gather(feature_bytes(feat), ref[j].nodes))
 
 
-@pytest.mark.parametrize("rows_dim", [20, 3, 64])
-def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim):
+@pytest.mark.parametrize("rows_dim,dtype", [(20, np.float32), (3, np.float32), (64, np.float32),
+                                            (256, np.float32), (384, np.float32), (1024, np.float16),
+                                            (1280, np.float32)])
+def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim, dtype):
     """Every row-copy launch shape (workgroups, rows in flight) gives the same
-    bytes; small workgroup counts force many rows per lane group and ragged ends."""
+    bytes; small workgroup counts force many rows per lane group and ragged ends.
+    Rows of 12, 80 and 256 bytes take the lane-group copy; 1 KiB, 1.5 KiB, 2 KiB
+    and 5 KiB rows take the wave-per-row copy (one or two units per lane, one to
+    three chunks per row, a partial last chunk for 1.5 and 5 KiB)."""
     off, idx = random_graph(2500, 8, 21, hubs=2, hub_deg=600)
     tg = distinct_targets(2500, 4, 45, 3)
-    feat = features(2500, rows_dim, 4)
+    feat = features(2500, rows_dim, 4, dtype)
     fan = [6, 3]
-    store = agnes.Store(off, idx, feat, 256)
+    row_bytes = feat.shape[1] * feat.itemsize
+    block = 256
+    while block < row_bytes:
+        block *= 2
+    store = agnes.Store(off, idx, feat, block)
     t = torch.from_numpy(np.ascontiguousarray(tg, dtype=np.int32)).cuda()
     ref = oracle.Oracle(off, idx).hyperbatch(tg, fan, 9, 0)
     fb = feature_bytes(feat)
-    want = oracle.hyperbatch_stats(off, 256, fb.shape[1], ref, len(fan))
+    want = oracle.hyperbatch_stats(off, block, fb.shape[1], ref, len(fan))
     for groups, unroll, nt, chunks in [(8, 4, True, 1), (8, 16, False, 3), (24, 8, True, 1),
-                                       (2048, 4, False, 7), (65536, 8, True, 64), (1000, 16, True, 2)]:
+                                       (2048, 4, False, 7), (65536, 8, True, 64), (1000, 16, True, 2),
+                                       (1 << 22, 4, True, 1), (1 << 22, 16, False, 5)]:
         log("gather shape", rows_dim, groups, unroll, nt, chunks)
         store.set_gather_shape(groups, unroll, nt, chunks)
         b = store.prepare(t, fan, seed=9, mb_base=0)
@@ -316,7 +326,7 @@ def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim):
         for k, v in want.items():
             assert st[k] == v, (groups, unroll, k, st[k], v)
         b.close()
-    for bad in [(7, None), (65537, None), (None, 3), (None, 2), (None, 32)]:
+    for bad in [(7, None), ((1 << 22) + 1, None), (None, 3), (None, 2), (None, 32)]:
         with pytest.raises(agnes.AgnesError):
             store.set_gather_shape(*bad)
     for bad_chunks in [0, 65]:
