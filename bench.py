@@ -82,6 +82,70 @@ def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int) -> tuple:
     return bs, bg, copy
 
 
+def block_model_bytes(st: dict, block_bytes: int) -> int:
+    """Bytes the paper's I/O model reads: every non-empty topology block row of
+    every hop and every non-empty feature block row, one whole block each."""
+    return (sum(st["topo_blocks"]) + st["feat_blocks"]) * block_bytes
+
+
+def ablation(store, cfg, targets_dev, H, reps, ob, rb, torch):
+    """The hyperbatch against the same minibatches prepared one at a time (the
+    paper's AGNES-No): time, algorithmic bytes and block reads of both modes.
+    Minibatch j alone uses mb_base j, so its output equals its part of the
+    hyperbatch; block reads of the one-at-a-time mode are summed over j."""
+    def run_hb(batch):
+        return store.prepare(targets_dev, cfg.fanouts, seed=cfg.seed, mb_base=0, batch=batch)
+
+    def run_no(batches):
+        return [store.prepare(targets_dev[j:j + 1], cfg.fanouts, seed=cfg.seed, mb_base=j, batch=batches[j])
+                for j in range(H)]
+
+    b = run_hb(None)
+    bs = run_no([None] * H)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        b = run_hb(b)
+    torch.cuda.synchronize()
+    t_hb = (time.perf_counter() - t0) / reps
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        bs = run_no(bs)
+    torch.cuda.synchronize()
+    t_no = (time.perf_counter() - t0) / reps
+
+    def summary(stats, t):
+        tot = {"topo_block_reads": 0, "feat_block_reads": 0, "algorithmic_bytes": 0, "rows": 0,
+               "distinct_rows": 0, "sampled_edges": 0}
+        for st in stats:
+            s_, g_, _ = algorithmic_bytes(st, ob, rb)
+            tot["topo_block_reads"] += sum(st["topo_blocks"])
+            tot["feat_block_reads"] += st["feat_blocks"]
+            tot["algorithmic_bytes"] += s_ + g_
+            tot["rows"] += st["rows"]
+            tot["distinct_rows"] += st["distinct_rows"]
+            tot["sampled_edges"] += sum(st["sampled"])
+        tot["block_model_bytes"] = (tot["topo_block_reads"] + tot["feat_block_reads"]) * cfg.block_bytes
+        tot["ms"] = round(t * 1e3, 4)
+        tot["algorithmic_GBps"] = round(tot["algorithmic_bytes"] / t / 1e9, 2)
+        return tot
+
+    hb = summary([b.stats()], t_hb)
+    no = summary([x.stats() for x in bs], t_no)
+    out = {"mode": "ablation: hyperbatch vs one minibatch at a time (synchronous prepare calls)",
+           "config": {"workload": cfg.describe(), "hyperbatch": H, "minibatch": cfg.B,
+                      "fanouts": list(cfg.fanouts), "block_bytes": cfg.block_bytes},
+           "reps": reps, "hyperbatch": hb, "one_at_a_time": no,
+           "time_ratio": round(t_no / t_hb, 3),
+           "block_read_ratio": round((no["topo_block_reads"] + no["feat_block_reads"]) /
+                                     max(1, hb["topo_block_reads"] + hb["feat_block_reads"]), 3),
+           "feature_row_read_ratio": round(no["distinct_rows"] / max(1, hb["distinct_rows"]), 3)}
+    for x in bs:
+        x.close()
+    b.close()
+    return out
+
+
 def cpu_baseline(w, cfg, steps_targets, budget_s=20.0):
     """The plain oracle on the host: whole minibatches (sampling + gather) of the
     benchmark's hyperbatches, in order, until about budget_s seconds of work."""
@@ -165,6 +229,9 @@ def main():
     ap.add_argument("--gather-unroll", type=int, default=None, help="rows in flight per lane group")
     ap.add_argument("--gather-nt", type=int, default=None, help="1 = non-temporal row stores, 0 = ordinary")
     ap.add_argument("--gather-chunks", type=int, default=None, help="launches the row copy is split into")
+    ap.add_argument("--ablation", action="store_true",
+                    help="instead of the benchmark line, compare the hyperbatch with its minibatches "
+                         "prepared one at a time (time, bytes, block reads)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
     args = ap.parse_args()
@@ -199,6 +266,13 @@ def main():
     dev_targets = [torch.from_numpy(np.ascontiguousarray(t)).cuda() for t in step_targets]
 
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
+    if args.ablation:
+        tg = torch.from_numpy(np.ascontiguousarray(step_targets[0])).cuda()
+        ob_ = 8 if w["offsets"].dtype == np.int64 else 4
+        print(json.dumps(ablation(store, cfg, tg, H, max(1, min(args.steps, 5)), ob_, cfg.row_bytes, torch)),
+              flush=True)
+        store.close()
+        return
     store.set_profiling(True)
     store.set_gather_shape(args.gather_groups, args.gather_unroll,
                            None if args.gather_nt is None else bool(args.gather_nt), args.gather_chunks)
@@ -212,7 +286,7 @@ def main():
     # hardware queues to sampling
     g_stream = torch.cuda.default_stream() if args.gather_stream == "default" else torch.cuda.Stream()
     s_stream = s_streams[0]
-    acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, distinct=0, sample_ms=0.0, gather_ms=0.0,
+    acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, distinct=0, block_model=0, sample_ms=0.0, gather_ms=0.0,
                copy_ms=0.0, steps=0)
 
     def account(batch):
@@ -225,6 +299,7 @@ def main():
         acc["edges"] += sum(st["sampled"])
         acc["rows"] += st["rows"]
         acc["distinct"] += st["distinct_rows"]
+        acc["block_model"] += block_model_bytes(st, cfg.block_bytes)
         acc["sample_ms"] += st["sample_ms"]
         acc["gather_ms"] += st["gather_ms"]
         acc["copy_ms"] += st["copy_ms"]
@@ -330,7 +405,8 @@ def main():
         "serial_ms_per_step": round(serial_ms, 4),
         "per_step": {"algorithmic_bytes": tot_bytes // K, "sample_bytes": tot_sample // K,
                      "gather_bytes": tot_gather // K, "rows": rows // K,
-                     "distinct_rows": acc["distinct"] // K, "sampled_edges": edges // K},
+                     "distinct_rows": acc["distinct"] // K, "sampled_edges": edges // K,
+                     "block_model_bytes": acc["block_model"] // K},
         "roofline": {"kernel": "k_gather_rows (row copy)", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic[0] if traffic else None,

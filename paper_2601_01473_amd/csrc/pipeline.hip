@@ -630,17 +630,29 @@ static size_t join_write_lds(int H) {
 // Statistics of the final list (the feature bucket): distinct rows (runs of one
 // node) and non-empty feature-block rows (runs of one feature block).  Runs on
 // the sampling stream so that the row copy does nothing but copy.
+constexpr int kStatItems = 8;   // entries per thread per round (independent loads in flight)
+
 __global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, uint32_t rpb, Ctl* ctl) {
     __shared__ unsigned long long cnt[2];
     if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
     __syncthreads();
     const int64_t n = ctl->rows;
     unsigned long long nd = 0, nf = 0;
-    for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n; e += (int64_t)gridDim.x * kBlock) {
-        const uint32_t u = (uint32_t)(rl_key[e] >> 32);
-        const uint32_t pu = e > 0 ? (uint32_t)(rl_key[e - 1] >> 32) : 0xFFFFFFFFu;
-        nd += (e == 0 || pu != u);
-        nf += (e == 0 || pu / rpb != u / rpb);
+    const int64_t step = (int64_t)gridDim.x * kBlock * kStatItems;
+    for (int64_t b = (int64_t)blockIdx.x * kBlock * kStatItems + threadIdx.x; b < n; b += step) {
+        uint32_t u[kStatItems], pu[kStatItems];
+#pragma unroll
+        for (int i = 0; i < kStatItems; i++) {
+            const int64_t e = b + (int64_t)i * kBlock;
+            u[i] = e < n ? (uint32_t)(rl_key[e] >> 32) : 0u;
+            pu[i] = (e > 0 && e < n) ? (uint32_t)(rl_key[e - 1] >> 32) : 0xFFFFFFFFu;
+        }
+#pragma unroll
+        for (int i = 0; i < kStatItems; i++) {
+            if (b + (int64_t)i * kBlock >= n) continue;
+            nd += (pu[i] != u[i]);
+            nf += (pu[i] == 0xFFFFFFFFu || pu[i] / rpb != u[i] / rpb);
+        }
     }
     nd = wave_inclusive_scan(nd);
     nf = wave_inclusive_scan(nf);
@@ -1048,7 +1060,7 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
     hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
                        w.mb_off.as<int64_t>());
-    hipLaunchKernelGGL(k_list_stats, dim3(grid_for(g.rows_max, 1024)), dim3(kBlock), 0, st,
+    hipLaunchKernelGGL(k_list_stats, dim3(grid_for(g.rows_max / kStatItems + 1, 512)), dim3(kBlock), 0, st,
                        w.rl_key[cur].as<uint64_t>(), (uint32_t)s.rpb, ctl);
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
