@@ -146,6 +146,53 @@ def ablation(store, cfg, targets_dev, H, reps, ob, rb, torch):
     return out
 
 
+def staged_tier(ag, w, cfg, dev_targets, H, pool_blocks, warmup, steps, ob, rb, torch):
+    """Hyperbatches on a store whose features sit in pinned host memory, with a
+    pool of pool_blocks feature blocks in HBM: consecutive fresh hyperbatches
+    (synchronous prepare calls), so later ones hit blocks staged earlier."""
+    store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype,
+                     pool_blocks=pool_blocks)
+    store.set_profiling(True)
+    info = store.info()
+    b = None
+    for s in range(warmup):
+        b = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=b)
+    torch.cuda.synchronize()
+    acc = dict(ms=0.0, gather_ms=0.0, bytes=0, staged_blocks=0, hit_blocks=0, needed_blocks=0, rounds=0,
+               staged_bytes=0, rows_bytes=0)
+    for s in range(warmup, warmup + steps):
+        t0 = time.perf_counter()
+        b = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=b)
+        st = b.stats()
+        ts = b.tier_stats()
+        acc["ms"] += (time.perf_counter() - t0) * 1e3
+        bs, bg, _ = algorithmic_bytes(st, ob, rb)
+        acc["bytes"] += bs + bg
+        acc["gather_ms"] += ts["gather_ms"]
+        acc["rows_bytes"] += st["rows"] * rb
+        for k in ("staged_blocks", "hit_blocks", "needed_blocks", "rounds", "staged_bytes"):
+            acc[k] += ts[k]
+    K = steps
+    out = {"mode": "staged feature tier: features in pinned host memory, HBM pool of feature blocks "
+                   "(synchronous prepare calls on fresh hyperbatches)",
+           "config": {"workload": cfg.describe(), "hyperbatch": H, "minibatch": cfg.B,
+                      "pool_blocks": pool_blocks, "pool_bytes": pool_blocks * info["rows_per_block"] * rb,
+                      "feature_blocks": info["feat_blocks"], "rows_per_block": info["rows_per_block"]},
+           "steps": K, "warmup": warmup,
+           "ms_per_step": round(acc["ms"] / K, 3),
+           "algorithmic_GBps": round(acc["bytes"] / (acc["ms"] * 1e-3) / 1e9, 2),
+           "gather_ms": round(acc["gather_ms"] / K, 3),
+           "needed_blocks": acc["needed_blocks"] // K, "staged_blocks": acc["staged_blocks"] // K,
+           "hit_blocks": acc["hit_blocks"] // K, "rounds": acc["rounds"] / K,
+           "hit_rate": round(acc["hit_blocks"] / max(1, acc["needed_blocks"]), 4),
+           "staged_GB": round(acc["staged_bytes"] / K / 1e9, 4),
+           "staged_GBps_over_gather": round(acc["staged_bytes"] / max(1e-9, acc["gather_ms"] * 1e-3) / 1e9, 2),
+           "gathered_rows_GB": round(acc["rows_bytes"] / K / 1e9, 4)}
+    b.close()
+    store.close()
+    return out
+
+
 def cpu_baseline(w, cfg, steps_targets, budget_s=20.0):
     """The plain oracle on the host: whole minibatches (sampling + gather) of the
     benchmark's hyperbatches, in order, until about budget_s seconds of work."""
@@ -232,6 +279,9 @@ def main():
     ap.add_argument("--ablation", action="store_true",
                     help="instead of the benchmark line, compare the hyperbatch with its minibatches "
                          "prepared one at a time (time, bytes, block reads)")
+    ap.add_argument("--staged", type=int, default=None, metavar="POOL_BLOCKS",
+                    help="instead of the benchmark line, run the staged feature tier (features in pinned "
+                         "host memory) with a pool of POOL_BLOCKS feature blocks in HBM")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
     args = ap.parse_args()
@@ -265,6 +315,10 @@ def main():
         step_targets.append(perm[a:a + H * B].reshape(H, B))
     dev_targets = [torch.from_numpy(np.ascontiguousarray(t)).cuda() for t in step_targets]
 
+    if args.staged is not None:
+        print(json.dumps(staged_tier(ag, w, cfg, dev_targets, H, args.staged, args.warmup, args.steps,
+                                     8 if w["offsets"].dtype == np.int64 else 4, cfg.row_bytes, torch)), flush=True)
+        return
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
     if args.ablation:
         tg = torch.from_numpy(np.ascontiguousarray(step_targets[0])).cuda()

@@ -221,6 +221,47 @@ typedef enum {
 } agnes_option;
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value);
 
+/* Staged feature tier (Sec. 3.4(1): blocks pinned in a buffer until the
+ * current iteration has processed them, LRU replacement; Sec. 3.2(1): fixed-size
+ * blocks as the unit of I/O).  Like agnes_build_blocks, but the feature
+ * matrix is kept in library-owned pinned host memory (its padded copy:
+ * ceil(num_nodes / rows_per_block) blocks) and only a pool of `pool_blocks`
+ * feature-block slots (pool_blocks * rows_per_block * row_bytes bytes) is
+ * allocated in HBM.  The topology stays in HBM.
+ *
+ * Every hyperbatch prepared on such a store needs the feature blocks that its
+ * final bucket touches (ascending block ids).  They are taken in rounds of at
+ * most pool_blocks blocks.  Within a round, the blocks already in the pool are
+ * hits: each is used in turn (ascending) and so pinned for the round.  Then
+ * each missing block (ascending) takes the lowest slot that never held a
+ * block, or else the least recently used slot that is not pinned in this
+ * round, and is used.  The GPU copies the missing blocks from host memory into
+ * their slots, then copies the round's rows.  Slots keep their blocks across
+ * hyperbatches, so a later hyperbatch hits blocks staged earlier.  Outputs are
+ * identical to a store with HBM-resident features.
+ * Hyperbatches of one store are gathered one at a time in the order their
+ * finish calls are made (each waits for the previous gather on any stream).
+ * Errors: as agnes_build_blocks; pool_blocks < 1 -> AGNES_ERR_INVALID. */
+agnes_status agnes_build_blocks_staged(const agnes_csr* csr, const agnes_features* feat,
+                                       uint64_t block_bytes, int64_t pool_blocks, void* hip_stream,
+                                       agnes_store** out);
+
+/* Feature-tier counters of a prepared hyperbatch (all zero for a store with
+ * HBM-resident features): needed feature blocks (= agnes_stats.feat_blocks),
+ * blocks copied from host memory, blocks found in the pool, rounds, bytes
+ * copied from host memory, and the device time of the gather including the
+ * staging copies when profiling is on (else -1). */
+typedef struct {
+    int64_t needed_blocks;
+    int64_t staged_blocks;
+    int64_t hit_blocks;
+    int64_t rounds;
+    int64_t staged_bytes;
+    float gather_ms;
+} agnes_tier_stats;
+
+agnes_status agnes_batch_tier_stats(const agnes_batch* batch, agnes_tier_stats* out);  /* waits for the batch */
+
 /* Store facts: out[0] num_nodes, out[1] num_edges, out[2] topology blocks,
  * out[3] edges per topology block, out[4] feature blocks, out[5] rows per
  * feature block, out[6] row_bytes, out[7] device bytes held by the store. */

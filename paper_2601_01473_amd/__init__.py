@@ -20,6 +20,7 @@ from ._binding import AgnesError, agnes_batch_stats, agnes_batch_view_get, agnes
 from ._binding import agnes_batch_finish, agnes_batch_wait, agnes_hyperbatch_begin  # noqa: F401
 from ._binding import agnes_free, agnes_hyperbatch_prepare, agnes_last_error  # noqa: F401
 from ._binding import agnes_store_info, agnes_store_object_table, agnes_store_set_option  # noqa: F401
+from ._binding import agnes_batch_tier_stats, agnes_build_blocks_staged  # noqa: F401
 
 _FEAT_DTYPES = {np.dtype(np.float32): B.AGNES_FLOAT32, np.dtype(np.float16): B.AGNES_FLOAT16}
 
@@ -52,10 +53,13 @@ def _stream_handle(stream) -> int:
 
 
 class Store:
-    """HBM-resident topology and feature blocks (agnes_build_blocks)."""
+    """HBM-resident topology and feature blocks (agnes_build_blocks), or with
+    pool_blocks set, HBM-resident topology and a staged feature tier: features
+    in pinned host memory, a pool of pool_blocks feature blocks in HBM
+    (agnes_build_blocks_staged)."""
 
     def __init__(self, offsets, indices, features, block_bytes: int, feat_dtype: str | None = None,
-                 stream=None):
+                 stream=None, pool_blocks: int | None = None):
         off = np.ascontiguousarray(offsets)
         if off.dtype not in (np.int32, np.int64):
             raise TypeError("offsets must be int32 or int64")
@@ -72,7 +76,11 @@ class Store:
         csr = B.agnes_csr(len(off) - 1, len(idx), B.AGNES_INT64 if off.dtype == np.int64 else B.AGNES_INT32,
                           off.ctypes.data, idx.ctypes.data if len(idx) else None)
         fs = B.agnes_features(feat.ctypes.data, feat.shape[1], fdt)
-        self.handle = agnes_build_blocks(csr, fs, block_bytes, _stream_handle(stream))
+        if pool_blocks is None:
+            self.handle = agnes_build_blocks(csr, fs, block_bytes, _stream_handle(stream))
+        else:
+            self.handle = agnes_build_blocks_staged(csr, fs, block_bytes, int(pool_blocks), _stream_handle(stream))
+        self.pool_blocks = pool_blocks
         self.num_nodes = len(off) - 1
         self.row_bytes = feat.shape[1] * feat.itemsize
         self.block_bytes = block_bytes
@@ -168,6 +176,12 @@ class Batch:
                     new_nodes=list(s.new_nodes[:L]), topo_blocks=list(s.topo_blocks[:L]),
                     rows=s.rows, distinct_rows=s.distinct_rows, feat_blocks=s.feat_blocks,
                     sample_ms=s.sample_ms, gather_ms=s.gather_ms, copy_ms=s.copy_ms)
+
+    def tier_stats(self) -> dict:
+        """Staged-tier counters (all zero for HBM-resident features)."""
+        t = agnes_batch_tier_stats(self.handle)
+        return dict(needed_blocks=t.needed_blocks, staged_blocks=t.staged_blocks, hit_blocks=t.hit_blocks,
+                    rounds=t.rounds, staged_bytes=t.staged_bytes, gather_ms=t.gather_ms)
 
     def view(self) -> B.agnes_batch_view:
         return agnes_batch_view_get(self.handle)

@@ -22,9 +22,9 @@ AGNES_OPT_GATHER_UNROLL = 3
 AGNES_OPT_GATHER_NONTEMPORAL = 4
 AGNES_OPT_GATHER_CHUNKS = 5
 
-EXPORTED = ["agnes_build_blocks", "agnes_hyperbatch_prepare", "agnes_hyperbatch_begin",
-            "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
-            "agnes_batch_stats", "agnes_store_set_option", "agnes_store_info",
+EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_hyperbatch_prepare",
+            "agnes_hyperbatch_begin", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
+            "agnes_batch_stats", "agnes_batch_tier_stats", "agnes_store_set_option", "agnes_store_info",
             "agnes_store_object_table", "agnes_free", "agnes_last_error"]
 
 
@@ -62,6 +62,12 @@ class agnes_stats(ctypes.Structure):
                 ("copy_ms", ctypes.c_float)]
 
 
+class agnes_tier_stats(ctypes.Structure):
+    _fields_ = [("needed_blocks", ctypes.c_int64), ("staged_blocks", ctypes.c_int64),
+                ("hit_blocks", ctypes.c_int64), ("rounds", ctypes.c_int64),
+                ("staged_bytes", ctypes.c_int64), ("gather_ms", ctypes.c_float)]
+
+
 class AgnesError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), msg))
@@ -85,6 +91,11 @@ def lib():
     L.agnes_build_blocks.restype = st
     L.agnes_build_blocks.argtypes = [ctypes.POINTER(agnes_csr), ctypes.POINTER(agnes_features), u64, vp,
                                      ctypes.POINTER(vp)]
+    L.agnes_build_blocks_staged.restype = st
+    L.agnes_build_blocks_staged.argtypes = [ctypes.POINTER(agnes_csr), ctypes.POINTER(agnes_features), u64, i64,
+                                            vp, ctypes.POINTER(vp)]
+    L.agnes_batch_tier_stats.restype = st
+    L.agnes_batch_tier_stats.argtypes = [vp, ctypes.POINTER(agnes_tier_stats)]
     L.agnes_hyperbatch_prepare.restype = st
     L.agnes_hyperbatch_prepare.argtypes = [vp, vp, i32, i32, vp, i32, u64, i64, vp, ctypes.POINTER(vp)]
     L.agnes_hyperbatch_begin.restype = st
@@ -123,6 +134,20 @@ def agnes_build_blocks(csr: agnes_csr, feat: agnes_features, block_bytes: int, s
     check(lib().agnes_build_blocks(ctypes.byref(csr), ctypes.byref(feat), block_bytes,
                                    ctypes.c_void_p(stream), ctypes.byref(out)))
     return out.value
+
+
+def agnes_build_blocks_staged(csr: agnes_csr, feat: agnes_features, block_bytes: int, pool_blocks: int,
+                              stream: int = 0) -> int:
+    out = ctypes.c_void_p()
+    check(lib().agnes_build_blocks_staged(ctypes.byref(csr), ctypes.byref(feat), block_bytes, pool_blocks,
+                                          ctypes.c_void_p(stream), ctypes.byref(out)))
+    return out.value
+
+
+def agnes_batch_tier_stats(batch: int) -> agnes_tier_stats:
+    s = agnes_tier_stats()
+    check(lib().agnes_batch_tier_stats(ctypes.c_void_p(batch), ctypes.byref(s)))
+    return s
 
 
 def agnes_hyperbatch_prepare(store: int, targets_ptr: int, H: int, B: int, fanouts_arr, L: int,

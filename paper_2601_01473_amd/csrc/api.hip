@@ -51,7 +51,19 @@ agnes_status agnes_build_blocks(const agnes_csr* csr, const agnes_features* feat
     if (out) *out = nullptr;
     return guarded([&] {
         AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
-        Store* s = build_store(csr, feat, block_bytes, (hipStream_t)hip_stream);
+        Store* s = build_store(csr, feat, block_bytes, 0, (hipStream_t)hip_stream);
+        *out = reinterpret_cast<agnes_store*>(s);
+    });
+}
+
+agnes_status agnes_build_blocks_staged(const agnes_csr* csr, const agnes_features* feat,
+                                       uint64_t block_bytes, int64_t pool_blocks, void* hip_stream,
+                                       agnes_store** out) {
+    if (out) *out = nullptr;
+    return guarded([&] {
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        AGNES_REQUIRE(pool_blocks >= 1, AGNES_ERR_INVALID, "pool_blocks must be >= 1");
+        Store* s = build_store(csr, feat, block_bytes, pool_blocks, (hipStream_t)hip_stream);
         *out = reinterpret_cast<agnes_store*>(s);
     });
 }
@@ -187,6 +199,15 @@ agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out) {
     });
 }
 
+agnes_status agnes_batch_tier_stats(const agnes_batch* batch, agnes_tier_stats* out) {
+    return guarded([&] {
+        Batch* b = as_batch((void*)batch);
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        wait_batch(*b);
+        *out = b->tier;
+    });
+}
+
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value) {
     return guarded([&] {
         Store* s = as_store(store);
@@ -222,7 +243,7 @@ agnes_status agnes_store_info(const agnes_store* store, int64_t out[8]) {
         out[5] = s->rpb;
         out[6] = s->row_bytes;
         out[7] = (int64_t)(s->offsets.bytes + s->indices.bytes + s->features.bytes +
-                           s->first_node.bytes + s->last_node.bytes);
+                           s->first_node.bytes + s->last_node.bytes + s->pool.bytes + s->tbuf.bytes);
     });
 }
 

@@ -24,6 +24,8 @@
 // device until one synchronisation before the gather.
 #include <algorithm>
 #include <cstring>
+#include <functional>
+#include <vector>
 
 #include "device.hpp"
 #include "runtime.hpp"
@@ -671,6 +673,13 @@ __global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, u
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// Source row of node u: u itself when the features are in HBM; in the staged
+// tier, row (u mod rpb) of the pool slot that holds u's feature block.
+__device__ __forceinline__ uint32_t source_row(const int32_t* tbuf, uint32_t rpb, uint32_t u) {
+    const uint32_t b = u / rpb;
+    return (uint32_t)tbuf[b] * rpb + (u - b * rpb);
+}
+
 // Row copy over the final list, which is the feature bucket of Alg. 1's
 // gathering loop in block order: the requests of a feature block are contiguous
 // and those of one node are neighbours, so each row is loaded from HBM once and
@@ -685,12 +694,13 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // A launch covers list entries [base, base + rows); the host may split the list
 // into several launches so that other streams' kernels are dispatched between
 // them.  Also counts the distinct rows and the non-empty feature-block rows.
-template <typename Unit, int LPR, int U, bool NT, bool ONE>
+template <typename Unit, int LPR, int U, bool NT, bool ONE, bool TIER>
 __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat, Unit* __restrict__ out,
                                                    int32_t* __restrict__ nodes_out,
                                                    const uint64_t* __restrict__ rl_key,
                                                    const int32_t* __restrict__ rl_val, const int64_t* node_off_g,
-                                                   int H, int64_t base, int64_t rows, int64_t row_units) {
+                                                   int H, int64_t base, int64_t rows, int64_t row_units,
+                                                   const int32_t* __restrict__ tbuf, uint32_t rpb) {
     constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
     constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
     // Hold at least 88 VGPRs, i.e. at most 5 of the 8 wave slots of a SIMD (512
@@ -724,7 +734,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             const uint32_t pu = k > 0 ? (uint32_t)(key[k - 1] >> 32) : prev_u;
             const uint32_t d = (uint32_t)(node_off[(uint32_t)key[k]] + val[k]);
             fresh[k] = ok[k] && (k == 0 || u != pu);
-            src[k] = u;
+            src[k] = (TIER && ok[k]) ? source_row(tbuf, rpb, u) : u;
             dst[k] = d;
             if (ok[k] && li == 0) nodes_out[d] = (int32_t)u;
         }
@@ -757,13 +767,14 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
 // An entry whose node repeats the previous entry's (within the wave's U) reuses
 // the row already in registers.  Waves take blocks of U entries in grid-stride
 // order (wave w of the grid, then w + all waves, ...).
-template <int U, int UPR, bool NT>
+template <int U, int UPR, bool NT, bool TIER>
 __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict__ feat, u32x4* __restrict__ out,
                                                         int32_t* __restrict__ nodes_out,
                                                         const uint64_t* __restrict__ rl_key,
                                                         const int32_t* __restrict__ rl_val,
                                                         const int64_t* node_off_g, int H, int64_t base,
-                                                        int64_t rows, int64_t row_units) {
+                                                        int64_t rows, int64_t row_units,
+                                                        const int32_t* __restrict__ tbuf, uint32_t rpb) {
     static_assert(U <= kWave, "one lane per entry");
     extern __shared__ int64_t node_off[];
     load_offsets(node_off, node_off_g, H);
@@ -773,11 +784,12 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict_
     for (int64_t e0 = base + ((int64_t)blockIdx.x * kWavesPerBlock + wave_id()) * U; e0 < hi; e0 += nw * U) {
         const int64_t e = e0 + lane;
         const bool mine = lane < U && e < hi;
-        uint32_t u = 0xFFFFFFFFu, d = 0;
+        uint32_t u = 0xFFFFFFFFu, d = 0, row = 0;
         if (mine) {
             const uint64_t key = rl_key[e];
             u = (uint32_t)(key >> 32);
             d = (uint32_t)(node_off[(uint32_t)key] + rl_val[e]);
+            row = TIER ? source_row(tbuf, rpb, u) : u;
             nodes_out[d] = (int32_t)u;
         }
         const uint32_t pu = (uint32_t)__shfl_up((int)u, 1, kWave);
@@ -786,7 +798,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict_
         uint32_t src[U], dst[U];
 #pragma unroll
         for (int k = 0; k < U; k++) {
-            src[k] = (uint32_t)__builtin_amdgcn_readlane((int)u, k);
+            src[k] = (uint32_t)__builtin_amdgcn_readlane((int)row, k);
             dst[k] = (uint32_t)__builtin_amdgcn_readlane((int)d, k);
         }
         for (int64_t c0 = 0; c0 < row_units; c0 += (int64_t)kWave * UPR) {
@@ -828,24 +840,33 @@ struct GatherArgs {
     const int64_t* node_off;
     int H;
     int64_t base, rows, row_units;   // entries [base, base + rows) of the list
+    const int32_t* tbuf;             // staged tier: block -> pool slot (feat is then the pool); else null
+    uint32_t rpb;
 };
+
+template <typename Unit, int LPR, int U, bool NT, bool ONE, bool TIER>
+static void launch_gather_k2(const GatherArgs& a, int G, hipStream_t st) {
+    const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
+    hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, ONE, TIER>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
+                       (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
+                       a.row_units, a.tbuf, a.rpb);
+}
 
 template <typename Unit, int LPR, int U, bool NT>
 static void launch_gather_k(const GatherArgs& a, int groups, hipStream_t st) {
-    const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
     // at most one workgroup per U rows of each lane group: with enough groups
     // every workgroup copies one block and the blocks in flight follow the
     // dispatch order through the list
     constexpr int64_t per_wg = (int64_t)kWavesPerBlock * (kWave / LPR) * U;
     const int G = (int)std::max<int64_t>(1, std::min<int64_t>(groups, (a.rows + per_wg - 1) / per_wg));
-    if (a.row_units <= LPR)
-        hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, true>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
-                           (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
-                           a.row_units);
-    else
-        hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, false>), dim3(G), dim3(kBlock), lds, st,
-                           (const Unit*)a.feat, (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H,
-                           a.base, a.rows, a.row_units);
+    const bool one = a.row_units <= LPR;
+    if (a.tbuf) {
+        if (one) launch_gather_k2<Unit, LPR, U, NT, true, true>(a, G, st);
+        else launch_gather_k2<Unit, LPR, U, NT, false, true>(a, G, st);
+    } else {
+        if (one) launch_gather_k2<Unit, LPR, U, NT, true, false>(a, G, st);
+        else launch_gather_k2<Unit, LPR, U, NT, false, false>(a, G, st);
+    }
 }
 
 template <typename Unit, int LPR>
@@ -864,9 +885,14 @@ static void launch_gather_rows_k(const GatherArgs& a, int groups, hipStream_t st
     const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
     constexpr int64_t per_wg = (int64_t)kWavesPerBlock * U;
     const int G = (int)std::max<int64_t>(1, std::min<int64_t>(groups, (a.rows + per_wg - 1) / per_wg));
-    hipLaunchKernelGGL((k_gather_rows<U, UPR, NT>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
-                       (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
-                       a.row_units);
+    if (a.tbuf)
+        hipLaunchKernelGGL((k_gather_rows<U, UPR, NT, true>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
+                           (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
+                           a.row_units, a.tbuf, a.rpb);
+    else
+        hipLaunchKernelGGL((k_gather_rows<U, UPR, NT, false>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
+                           (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
+                           a.row_units, a.tbuf, a.rpb);
 }
 
 template <int UPR>
@@ -888,8 +914,8 @@ static void launch_gather(const GatherArgs& all, int groups, int unroll, bool nt
     chunks = (int)std::max<int64_t>(1, std::min<int64_t>(chunks, all.rows));
     for (int c = 0; c < chunks; c++) {
         GatherArgs a = all;
-        a.base = all.rows * c / chunks;
-        a.rows = all.rows * (c + 1) / chunks - a.base;
+        a.base = all.base + all.rows * c / chunks;
+        a.rows = all.base + all.rows * (c + 1) / chunks - a.base;
         const int G = std::max(8, groups / chunks);
         if (a.row_units >= 64 && sizeof(Unit) == 16) {
             if (a.row_units >= 128) launch_gather_rows_upr<2>(a, G, unroll, nt, st);
@@ -899,6 +925,57 @@ static void launch_gather(const GatherArgs& all, int groups, int unroll, bool nt
         else if (a.row_units > 8) launch_gather_lpr<Unit, 16>(a, G, unroll, nt, st);
         else if (a.row_units > 4) launch_gather_lpr<Unit, 8>(a, G, unroll, nt, st);
         else launch_gather_lpr<Unit, 4>(a, G, unroll, nt, st);
+    }
+}
+
+
+// ----------------------------------------------------------------- staged feature tier
+//
+// The final list is the feature bucket in ascending block order, so the
+// hyperbatch's needed feature blocks are the list's block starts.  Their ids
+// and first list entries are compacted on the device and read by the host,
+// which plans rounds of at most pool_blocks blocks (hits pinned first, misses
+// given the lowest unused slot, else the least recently used unpinned slot).
+// Per round the GPU updates the block -> slot table, copies the missing blocks
+// from pinned host memory into their slots, and copies the round's rows.
+
+__global__ __launch_bounds__(kBlock) void k_block_flags(const uint64_t* rl_key, uint32_t rpb, int32_t* flag,
+                                                        const Ctl* ctl) {
+    const int64_t n = ctl->rows;
+    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < n; p += (int64_t)gridDim.x * kBlock) {
+        const uint32_t b = (uint32_t)(rl_key[p] >> 32) / rpb;
+        flag[p] = (p == 0 || (uint32_t)(rl_key[p - 1] >> 32) / rpb != b) ? 1 : 0;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_block_compact(const uint64_t* rl_key, uint32_t rpb, const int32_t* flag,
+                                                          const int64_t* off, int64_t* need_entry,
+                                                          int32_t* need_block, const Ctl* ctl) {
+    const int64_t n = ctl->rows;
+    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < n; p += (int64_t)gridDim.x * kBlock) {
+        if (flag[p]) {
+            const int64_t k = off[p];
+            need_entry[k] = p;
+            need_block[k] = (int32_t)((uint32_t)(rl_key[p] >> 32) / rpb);
+        }
+    }
+}
+
+// tbuf[block] = slot for every (block, slot) pair of a round (slot -1: evicted).
+__global__ __launch_bounds__(kBlock) void k_tbuf_update(const int32_t* pairs, int n, int32_t* tbuf) {
+    for (int i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) tbuf[pairs[2 * i]] = pairs[2 * i + 1];
+}
+
+// One workgroup per missing block (grid-stride): the block's rows, read from
+// pinned host memory through its mapped address, written to its pool slot.
+template <typename Unit>
+__global__ __launch_bounds__(kBlock) void k_stage(const Unit* __restrict__ host, Unit* __restrict__ pool,
+                                                  const int32_t* __restrict__ misses, int n, int64_t units) {
+    for (int i = blockIdx.x; i < n; i += gridDim.x) {
+        const int64_t b = misses[2 * i], slot = misses[2 * i + 1];
+        const Unit* src = host + b * units;
+        Unit* dst = pool + slot * units;
+        for (int64_t c = threadIdx.x; c < units; c += kBlock) dst[c] = src[c];
     }
 }
 
@@ -1009,6 +1086,125 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
+// ----------------------------------------------------------------- staged tier: host planning
+
+struct TierRound {
+    int64_t e0, e1;              // list entries whose rows the round copies
+    int n_upd, n_miss;           // table updates (block, slot) and blocks to copy (block, slot)
+    size_t upd_at, miss_at;      // their offsets (int32 elements) in the uploaded plan
+};
+
+// Reads the hyperbatch's needed feature blocks (ascending) and plans the rounds:
+// at most pool_blocks blocks per round; blocks in the pool are hits and are
+// used (pinned) first, ascending; every other block of the round, ascending,
+// takes the lowest never-used slot, else the least recently used slot among
+// the slots not used in this round.  Every hit and every staging is one use.
+// The plan is written to the batch's pinned plan buffer; the store's pool view
+// is advanced as if the rounds had run (they are enqueued in the same order).
+static std::vector<TierRound> plan_staging(const Store& s, Batch& b, hipStream_t) {
+    Workspace& w = b.ws;
+    const int64_t nb = b.stats.feat_blocks;
+    const int64_t rows = b.node_off[b.H];
+    AGNES_REQUIRE(nb >= 1 && nb <= b.need_cap, AGNES_ERR_INTERNAL, "needed feature blocks out of range");
+    w.need_host.reserve_slack((size_t)nb * 12);
+    if (!b.needed) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.needed, hipEventDisableTiming));
+    int64_t* need_entry = (int64_t*)w.need_host.ptr;
+    int32_t* need_block = (int32_t*)((char*)w.need_host.ptr + (size_t)nb * 8);
+    AGNES_CHECK_HIP(hipMemcpyAsync(need_entry, w.need.ptr, (size_t)nb * 8, hipMemcpyDeviceToHost, b.stream));
+    AGNES_CHECK_HIP(hipMemcpyAsync(need_block, (char*)w.need.ptr + (size_t)b.need_cap * 8, (size_t)nb * 4,
+                                   hipMemcpyDeviceToHost, b.stream));
+    AGNES_CHECK_HIP(hipEventRecord(b.needed, b.stream));
+    AGNES_CHECK_HIP(hipEventSynchronize(b.needed));
+
+    const int64_t P = s.pool_blocks;
+    std::vector<TierRound> rounds;
+    std::vector<int32_t> upd, miss, plan;
+    int64_t staged = 0, hits = 0;
+    auto touch = [&](int32_t sl) {
+        const int64_t t = ++s.accesses;
+        s.slot_stamp[sl] = t;
+        s.lru.push_back({t, sl});
+    };
+    // the least recently used slot not used since access number t0 (the start
+    // of the current round); stale entries are dropped on the way
+    auto victim = [&](int64_t t0) -> int32_t {
+        for (;;) {
+            AGNES_REQUIRE(!s.lru.empty(), AGNES_ERR_INTERNAL, "no pool slot to replace");
+            const auto e = s.lru.front();
+            s.lru.pop_front();
+            if (s.slot_stamp[e.second] != e.first) continue;
+            AGNES_REQUIRE(e.first <= t0, AGNES_ERR_INTERNAL, "every pool slot is pinned");
+            return e.second;
+        }
+    };
+    for (int64_t i0 = 0; i0 < nb; i0 += P) {
+        const int64_t i1 = std::min<int64_t>(nb, i0 + P);
+        const int64_t t0 = s.accesses;
+        s.tier_clock++;
+        upd.clear();
+        miss.clear();
+        for (int64_t k = i0; k < i1; k++) {                 // hits: pinned for this round
+            const int32_t sl = s.block_slot[need_block[k]];
+            if (sl >= 0) {
+                touch(sl);
+                hits++;
+            }
+        }
+        for (int64_t k = i0; k < i1; k++) {                 // misses, ascending
+            const int32_t blk = need_block[k];
+            if (s.block_slot[blk] >= 0) continue;
+            int32_t sl;
+            if (s.next_free < P) {
+                sl = (int32_t)s.next_free++;
+            } else {
+                sl = victim(t0);
+                const int32_t old = s.slot_block[sl];
+                s.block_slot[old] = -1;
+                upd.push_back(old);
+                upd.push_back(-1);
+            }
+            s.slot_block[sl] = blk;
+            s.block_slot[blk] = sl;
+            touch(sl);
+            upd.push_back(blk);
+            upd.push_back(sl);
+            miss.push_back(blk);
+            miss.push_back(sl);
+            staged++;
+        }
+        TierRound r;
+        r.e0 = need_entry[i0];
+        r.e1 = i1 < nb ? need_entry[i1] : rows;
+        r.n_upd = (int)(upd.size() / 2);
+        r.n_miss = (int)(miss.size() / 2);
+        r.upd_at = plan.size();
+        plan.insert(plan.end(), upd.begin(), upd.end());
+        r.miss_at = plan.size();
+        plan.insert(plan.end(), miss.begin(), miss.end());
+        rounds.push_back(r);
+    }
+    // keep the queue near the pool size: rebuild it from the live stamps
+    if ((int64_t)s.lru.size() > 4 * P + 1024) {
+        std::vector<std::pair<int64_t, int32_t>> all;
+        all.reserve((size_t)s.next_free);
+        for (int64_t sl = 0; sl < s.next_free; sl++) all.push_back({s.slot_stamp[sl], (int32_t)sl});
+        std::sort(all.begin(), all.end());
+        s.lru.assign(all.begin(), all.end());
+    }
+    const size_t bytes = std::max<size_t>(plan.size() * 4, 8);
+    w.plan_host.reserve_slack(bytes);
+    memcpy(w.plan_host.ptr, plan.data(), plan.size() * 4);
+    w.plan.reserve_slack(bytes);
+    w.plan_used = bytes;
+    b.tier.needed_blocks = nb;
+    b.tier.staged_blocks = staged;
+    b.tier.hit_blocks = hits;
+    b.tier.rounds = (int64_t)rounds.size();
+    b.tier.staged_bytes = staged * s.rpb * s.row_bytes;
+    return rounds;
+}
+
+
 void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
                       const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
                       hipStream_t st) {
@@ -1062,6 +1258,21 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
                        w.mb_off.as<int64_t>());
     hipLaunchKernelGGL(k_list_stats, dim3(grid_for(g.rows_max / kStatItems + 1, 512)), dim3(kBlock), 0, st,
                        w.rl_key[cur].as<uint64_t>(), (uint32_t)s.rpb, ctl);
+    if (s.tiered) {
+        // staged tier: the needed feature blocks (block starts of the final list)
+        w.blk_flag.reserve((size_t)g.rows_max * 4);
+        w.blk_off.reserve((size_t)(g.rows_max + 1) * 8);
+        w.need.reserve((size_t)g.rows_max * 12 + 256);
+        const int gl = grid_for(g.rows_max, 4096);
+        hipLaunchKernelGGL(k_block_flags, dim3(gl), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
+                           (uint32_t)s.rpb, w.blk_flag.as<int32_t>(), ctl);
+        scan_counts(w.blk_flag.as<int32_t>(), w.blk_off.as<int64_t>(), &ctl->rows, g.rows_max, nullptr,
+                    w.scan_part.as<int64_t>(), st);
+        hipLaunchKernelGGL(k_block_compact, dim3(gl), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
+                           (uint32_t)s.rpb, w.blk_flag.as<int32_t>(), w.blk_off.as<int64_t>(), w.need.as<int64_t>(),
+                           (int32_t*)((char*)w.need.ptr + (size_t)g.rows_max * 8), ctl);
+        b.need_cap = g.rows_max;
+    }
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
     // sizes of the outputs travel to pinned host memory; finish reads them
@@ -1120,27 +1331,60 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
 
     // gather over the final list, ordered after the sampling phase
     if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.sampled, 0));
-    Ctl* ctl = w.sync.as<Ctl>();
-    if (s.profile) {
-        AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
-        AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
-    }
     const uint64_t* rlk = w.rl_key[b.cur].as<uint64_t>();
     const int32_t* rlv = w.rl_val[b.cur].as<int32_t>();
-    if (rows > 0) {
-        GatherArgs ga{s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv, w.mb_off.as<int64_t>(),
-                      H, 0, rows, 0};
-        if (s.row_bytes % 16 == 0) {
-            ga.row_units = s.row_bytes / 16;
-            launch_gather<u32x4>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, s.gather_chunks, st);
-        } else {
-            ga.row_units = s.row_bytes / 4;
-            launch_gather<uint32_t>(ga, s.gather_groups, s.gather_unroll, s.gather_nt != 0, s.gather_chunks, st);
+    GatherArgs ga{s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv, w.mb_off.as<int64_t>(),
+                  H, 0, rows, 0, nullptr, (uint32_t)s.rpb};
+    const bool wide = s.row_bytes % 16 == 0;
+    ga.row_units = wide ? s.row_bytes / 16 : s.row_bytes / 4;
+    auto copy_rows = [&](const GatherArgs& a) {
+        if (wide) launch_gather<u32x4>(a, s.gather_groups, s.gather_unroll, s.gather_nt != 0, s.gather_chunks, st);
+        else launch_gather<uint32_t>(a, s.gather_groups, s.gather_unroll, s.gather_nt != 0, s.gather_chunks, st);
+    };
+    memset(&b.tier, 0, sizeof(b.tier));
+    if (s.tiered && rows > 0) {
+        std::vector<TierRound> rounds = plan_staging(s, b, st);
+        AGNES_CHECK_HIP(hipStreamWaitEvent(st, s.pool_free, 0));   // the previous tiered gather is done
+        if (s.profile) {
+            AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
+            AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
         }
+        AGNES_CHECK_HIP(hipMemcpyAsync(w.plan.ptr, w.plan_host.ptr, w.plan_used, hipMemcpyHostToDevice, st));
+        const int32_t* plan = w.plan.as<int32_t>();
+        const int64_t blk_bytes = s.rpb * s.row_bytes;
+        ga.feat = s.pool.ptr;
+        ga.tbuf = s.tbuf.as<int32_t>();
+        for (const TierRound& r : rounds) {
+            if (r.n_upd)
+                hipLaunchKernelGGL(k_tbuf_update, dim3(grid_for(r.n_upd, 256)), dim3(kBlock), 0, st, plan + r.upd_at,
+                                   r.n_upd, s.tbuf.as<int32_t>());
+            if (r.n_miss) {
+                const int gs = std::min(r.n_miss, 16384);
+                if (blk_bytes % 16 == 0)
+                    hipLaunchKernelGGL(k_stage<u32x4>, dim3(gs), dim3(kBlock), 0, st, (const u32x4*)s.host_feat_dev,
+                                       s.pool.as<u32x4>(), plan + r.miss_at, r.n_miss, blk_bytes / 16);
+                else
+                    hipLaunchKernelGGL(k_stage<uint32_t>, dim3(gs), dim3(kBlock), 0, st,
+                                       (const uint32_t*)s.host_feat_dev, s.pool.as<uint32_t>(), plan + r.miss_at,
+                                       r.n_miss, blk_bytes / 4);
+            }
+            GatherArgs a = ga;
+            a.base = r.e0;
+            a.rows = r.e1 - r.e0;
+            copy_rows(a);
+        }
+        AGNES_CHECK_HIP(hipGetLastError());
+        if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));
+        AGNES_CHECK_HIP(hipEventRecord(s.pool_free, st));
+    } else {
+        if (s.profile) {
+            AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
+            AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
+        }
+        if (rows > 0) copy_rows(ga);
+        AGNES_CHECK_HIP(hipGetLastError());
+        if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));
     }
-    AGNES_CHECK_HIP(hipGetLastError());
-    if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));
-    AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st));
     AGNES_CHECK_HIP(hipEventRecord(b.gathered, st));
     b.stream = st;
     b.state = kGathering;
@@ -1157,6 +1401,7 @@ void wait_batch(Batch& b) {
         AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.gather_ms, w.ev[2], w.ev[4]));
         AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.copy_ms, w.ev[3], w.ev[4]));
     }
+    if (b.store->tiered) b.tier.gather_ms = b.stats.gather_ms;
     b.state = kDone;
 }
 

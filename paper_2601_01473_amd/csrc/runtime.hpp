@@ -5,7 +5,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <deque>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/agnes.h"
@@ -71,6 +73,11 @@ struct PinnedBuf {
     ~PinnedBuf() {
         if (ptr) (void)hipHostFree(ptr);
     }
+    // Same, with 25% headroom when growing, for sizes that vary call to call.
+    void reserve_slack(size_t need) {
+        if (need <= bytes && ptr) return;
+        reserve(need + need / 4);
+    }
     void reserve(size_t need) {
         if (need <= bytes && ptr) return;
         if (ptr) (void)hipHostFree(ptr);
@@ -114,6 +121,11 @@ struct Workspace {
     DevBuf ghist, gemit;              // join: per group new nodes per minibatch, merged entries
     DevBuf rs_hist, rs_dtot;          // radix-sort histograms
     DevBuf scan_part;                 // scan partial sums
+    DevBuf blk_flag, blk_off;         // staged tier: block starts of the final list, their offsets
+    DevBuf need;                      // staged tier: [needed blocks] first list entry, then block ids
+    DevBuf plan;                      // staged tier: the rounds' (block, slot) updates and misses
+    PinnedBuf need_host, plan_host;
+    size_t plan_used = 0;             // staged tier: bytes of the current plan
     hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
 };
 
@@ -133,6 +145,29 @@ struct Store {
     int64_t max_degree = 0;
     int node_bits = 0;                // bits of a node id (ceil log2 num_nodes)
     DevBuf offsets, indices, features, first_node, last_node;
+    // Staged feature tier (features in pinned host memory, an HBM pool of
+    // feature-block slots).  Not used when tiered == 0 (features in HBM).
+    // The pool's host-side bookkeeping changes with every planned hyperbatch.
+    int tiered = 0;
+    void* host_feat = nullptr;        // pinned host copy of the padded feature matrix
+    void* host_feat_dev = nullptr;    // its device-visible address
+    int64_t pool_blocks = 0;          // slots of the pool (rpb rows each)
+    DevBuf pool;                      // [pool_blocks][rpb][row_bytes]
+    DevBuf tbuf;                      // [nfblk] int32: slot holding feature block b, or -1
+    mutable std::vector<int32_t> slot_block;  // host view of the pool: block in slot s, or -1
+    mutable std::vector<int64_t> slot_stamp;  // access number of slot s's last use (-1: never)
+    mutable std::vector<int32_t> block_slot;  // host mirror of tbuf
+    // Replacement order: (access number, slot) in access order; an entry whose
+    // slot was used again later is stale and skipped.
+    mutable std::deque<std::pair<int64_t, int32_t>> lru;
+    mutable int64_t accesses = 0;     // pool accesses so far (hits and stagings)
+    mutable int64_t next_free = 0;    // lowest never-used slot
+    mutable int64_t tier_clock = 0;   // rounds planned so far
+    hipEvent_t pool_free = nullptr;   // the last enqueued tiered gather is done with the pool
+    ~Store() {
+        if (host_feat) (void)hipHostFree(host_feat);
+        if (pool_free) (void)hipEventDestroy(pool_free);
+    }
     int profile = 0;
     int gather_groups = 1 << 22;      // workgroups of the row-copy kernel (upper bound)
     int gather_unroll = 4;            // rows in flight per lane group (4, 8 or 16)
@@ -152,8 +187,10 @@ struct Batch {
     hipStream_t stream = nullptr;     // stream of the sampling phase
     hipEvent_t sampled = nullptr;     // sizes of the outputs are in ws.sync_host
     hipEvent_t gathered = nullptr;    // outputs and statistics are complete
+    hipEvent_t needed = nullptr;      // staged tier: the needed feature blocks are in ws.need_host
     int64_t capN = 0;
     int cur = 0;                      // which list buffer holds the final list
+    int64_t need_cap = 0;             // staged tier: entries of each array in ws.need
     std::vector<int64_t> node_off;
     std::vector<int32_t> layer_sizes;
     std::vector<int64_t> rp_off[AGNES_MAX_LAYERS];
@@ -162,9 +199,11 @@ struct Batch {
     DevBuf row_ptr[AGNES_MAX_LAYERS], col[AGNES_MAX_LAYERS];
     Workspace ws;
     agnes_stats stats{};
+    agnes_tier_stats tier{};
     ~Batch() {
         if (sampled) (void)hipEventDestroy(sampled);
         if (gathered) (void)hipEventDestroy(gathered);
+        if (needed) (void)hipEventDestroy(needed);
         for (auto& e : ws.ev)
             if (e) (void)hipEventDestroy(e);
     }
@@ -180,8 +219,9 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
 void finish_hyperbatch(Batch& b, hipStream_t stream);
 void wait_batch(Batch& b);
 // Store construction (store.hip).
+// pool_blocks == 0: features in HBM; > 0: staged feature tier with that many slots.
 Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t block_bytes,
-                   hipStream_t stream);
+                   int64_t pool_blocks, hipStream_t stream);
 
 // ----------------------------------------------------------------- primitives (prims.hip)
 

@@ -55,7 +55,8 @@ static int64_t validate_offsets(const OffT* off, int64_t n, int64_t e) {
 }
 
 Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t block_bytes,
-                   hipStream_t st) {
+                   int64_t pool_blocks, hipStream_t st) {
+    AGNES_REQUIRE(pool_blocks >= 0, AGNES_ERR_INVALID, "pool_blocks must not be negative");
     AGNES_REQUIRE(csr && feat, AGNES_ERR_INVALID, "csr and features must not be NULL");
     const int64_t n = csr->num_nodes, e = csr->num_edges;
     AGNES_REQUIRE(n >= 1 && n < 0x7FFFFFFFll, AGNES_ERR_INVALID, "num_nodes must be in [1, 2^31-1)");
@@ -105,9 +106,9 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
     const size_t obytes = (size_t)(n + 1) * (o64 ? 8 : 4);
     const size_t ibytes = (size_t)(s->nblk * s->e_blk) * 4;
     const size_t fbytes = (size_t)(s->nfblk * s->rpb) * (size_t)row_bytes;
+    const size_t fdata = (size_t)n * (size_t)row_bytes;
     s->offsets.reserve(obytes);
     s->indices.reserve(ibytes);
-    s->features.reserve(fbytes);
     s->first_node.reserve((size_t)s->nblk * 4);
     s->last_node.reserve((size_t)s->nblk * 4);
     AGNES_CHECK_HIP(hipMemcpyAsync(s->offsets.ptr, csr->offsets, obytes, hipMemcpyHostToDevice, st));
@@ -115,10 +116,29 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
         AGNES_CHECK_HIP(hipMemcpyAsync(s->indices.ptr, csr->indices, (size_t)e * 4, hipMemcpyHostToDevice, st));
     if (ibytes > (size_t)e * 4)
         AGNES_CHECK_HIP(hipMemsetAsync((char*)s->indices.ptr + (size_t)e * 4, 0, ibytes - (size_t)e * 4, st));
-    const size_t fdata = (size_t)n * (size_t)row_bytes;
-    AGNES_CHECK_HIP(hipMemcpyAsync(s->features.ptr, feat->data, fdata, hipMemcpyHostToDevice, st));
-    if (fbytes > fdata)
-        AGNES_CHECK_HIP(hipMemsetAsync((char*)s->features.ptr + fdata, 0, fbytes - fdata, st));
+    if (pool_blocks > 0) {
+        // the storage tier: the padded feature matrix in pinned host memory,
+        // read by the GPU through its mapped address; HBM holds only the pool
+        s->tiered = 1;
+        s->pool_blocks = pool_blocks;
+        AGNES_CHECK_HIP(hipHostMalloc(&s->host_feat, fbytes, hipHostMallocMapped));
+        memcpy(s->host_feat, feat->data, fdata);
+        if (fbytes > fdata) memset((char*)s->host_feat + fdata, 0, fbytes - fdata);
+        AGNES_CHECK_HIP(hipHostGetDevicePointer(&s->host_feat_dev, s->host_feat, 0));
+        s->pool.reserve((size_t)pool_blocks * (size_t)s->rpb * (size_t)row_bytes);
+        s->tbuf.reserve((size_t)s->nfblk * 4);
+        fill_u32(s->tbuf.ptr, 0xFFFFFFFFu, s->nfblk, st);
+        s->slot_block.assign((size_t)pool_blocks, -1);
+        s->slot_stamp.assign((size_t)pool_blocks, -1);
+        s->block_slot.assign((size_t)s->nfblk, -1);
+        AGNES_CHECK_HIP(hipEventCreateWithFlags(&s->pool_free, hipEventDisableTiming));
+        AGNES_CHECK_HIP(hipEventRecord(s->pool_free, st));
+    } else {
+        s->features.reserve(fbytes);
+        AGNES_CHECK_HIP(hipMemcpyAsync(s->features.ptr, feat->data, fdata, hipMemcpyHostToDevice, st));
+        if (fbytes > fdata)
+            AGNES_CHECK_HIP(hipMemsetAsync((char*)s->features.ptr + fdata, 0, fbytes - fdata, st));
+    }
     fill_u32(s->first_node.ptr, 0xFFFFFFFFu, s->nblk, st);
     fill_u32(s->last_node.ptr, 0xFFFFFFFFu, s->nblk, st);
     if (o64)
