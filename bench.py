@@ -193,6 +193,56 @@ def staged_tier(ag, w, cfg, dev_targets, H, pool_blocks, warmup, steps, ob, rb, 
     return out
 
 
+def sage_bench(store, cfg, targets_dev, H, steps, torch, hidden):
+    """GraphSAGE forward (agnes_sage_forward) over one prepared hyperbatch:
+    random bf16 weights, dims [feature dim, hidden, ..., hidden]; the forward is
+    timed alone (HIP events on the current stream), its GEMM flops and the
+    aggregation's algorithmic bytes are reported."""
+    L = len(cfg.fanouts)
+    dims = [cfg.dim] + [hidden] * L
+    rng = np.random.default_rng(0)
+    def bits(x):
+        u = np.asarray(x, np.float32).view(np.uint32).astype(np.uint64)
+        return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16).view(np.int16)
+    Ws = [torch.from_numpy(bits(rng.standard_normal((dims[i + 1], 2 * dims[i])) / np.sqrt(dims[i]))).cuda()
+          for i in range(L)]
+    bs = [torch.from_numpy((rng.standard_normal(dims[i + 1]) * 0.1).astype(np.float32)).cuda() for i in range(L)]
+    b = store.prepare(targets_dev, cfg.fanouts, seed=cfg.seed, mb_base=0)
+    out = b.sage_forward(Ws, bs)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        b.sage_forward(Ws, bs, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    st = b.stats()
+    v = b.view()
+    lsz = np.ctypeslib.as_array(v.layer_sizes, shape=(H * (L + 1),)).reshape(H, L + 1)
+    esz0 = 4 if cfg.feat_dtype == "float32" else 2
+    flops = agg_bytes = 0
+    layers = []
+    for i in range(L):
+        l = L - 1 - i
+        M = int(lsz[:, l].sum())
+        din, dout = dims[i], dims[i + 1]
+        esz = esz0 if i == 0 else 2
+        f = 2 * M * 2 * din * dout
+        a = (st["sampled"][l] + M) * din * esz + M * 2 * din * 2
+        flops += f
+        agg_bytes += a
+        layers.append({"hop": l, "rows": M, "edges": st["sampled"][l], "gemm_flop": f, "aggregation_bytes": a})
+    res = {"mode": "GraphSAGE forward over one prepared hyperbatch (bf16 MFMA GEMMs, float32 mean aggregation)",
+           "config": {"workload": cfg.describe(), "hyperbatch": H, "dims": dims},
+           "steps": steps, "forward_ms": round(ms, 4), "gemm_GFLOP": round(flops / 1e9, 3),
+           "TFLOPs_over_forward": round(flops / (ms * 1e-3) / 1e12, 2),
+           "aggregation_algorithmic_GB": round(agg_bytes / 1e9, 4),
+           "aggregation_GBps_over_forward": round(agg_bytes / (ms * 1e-3) / 1e9, 1), "layers": layers}
+    b.close()
+    return res
+
+
 def cpu_baseline(w, cfg, steps_targets, budget_s=20.0):
     """The plain oracle on the host: whole minibatches (sampling + gather) of the
     benchmark's hyperbatches, in order, until about budget_s seconds of work."""
@@ -282,6 +332,9 @@ def main():
     ap.add_argument("--staged", type=int, default=None, metavar="POOL_BLOCKS",
                     help="instead of the benchmark line, run the staged feature tier (features in pinned "
                          "host memory) with a pool of POOL_BLOCKS feature blocks in HBM")
+    ap.add_argument("--sage", type=int, default=None, metavar="HIDDEN",
+                    help="instead of the benchmark line, time the GraphSAGE forward over one prepared "
+                         "hyperbatch with hidden width HIDDEN")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
     args = ap.parse_args()
@@ -320,6 +373,10 @@ def main():
                                      8 if w["offsets"].dtype == np.int64 else 4, cfg.row_bytes, torch)), flush=True)
         return
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
+    if args.sage is not None:
+        print(json.dumps(sage_bench(store, cfg, dev_targets[0], H, max(1, args.steps), torch, args.sage)), flush=True)
+        store.close()
+        return
     if args.ablation:
         tg = torch.from_numpy(np.ascontiguousarray(step_targets[0])).cuda()
         ob_ = 8 if w["offsets"].dtype == np.int64 else 4

@@ -262,6 +262,40 @@ typedef struct {
 
 agnes_status agnes_batch_tier_stats(const agnes_batch* batch, agnes_tier_stats* out);  /* waits for the batch */
 
+/* GraphSAGE forward pass over a prepared hyperbatch (the step after data
+ * preparation; Eq. (1), Sec. 3.1): L layers, layer i on hop l = L-1-i, from the
+ * outermost hop to the targets.  For every destination node v of hop l in
+ * minibatch j (local ids 0 .. layer_sizes[j][l]-1):
+ *   m_v = mean of h_u over the sampled neighbours u of v (zero vector when v
+ *         has none), with h the layer's input embeddings (layer 0: the
+ *         gathered feature rows, converted to float);
+ *   z_v = W_i [h_v ; m_v] + b_i,   h'_v = max(z_v, 0) for i < L-1, z_v for the last layer.
+ * Node v's own input row is the same local id of the previous node set (the
+ * destination nodes of a hop are a prefix of its source nodes).
+ *   dims[0] = feature dim; dims[i+1] = output dim of layer i; every dims[i]
+ *     must be a positive multiple of 32, at most 4096.
+ *   weight[i]: device bf16 (raw uint16 bits), [dims[i+1]][2*dims[i]] row-major:
+ *     columns 0 .. dims[i]-1 multiply h_v, the others m_v (the layout of a
+ *     linear layer's weight, output-major).
+ *   bias[i]: device float32 [dims[i+1]].
+ *   out: device float32 [H*B][dims[L]]: the targets' embeddings, minibatch-major
+ *     in the order the targets were given.
+ * Arithmetic: m_v is accumulated in float32; [h_v ; m_v] is rounded to bf16
+ * and multiplied with bf16 MFMA, accumulating in float32; hidden embeddings
+ * are stored as bf16.  The call enqueues on hip_stream after the batch's
+ * gather and returns; the batch owns the intermediate buffers.
+ * Errors: a batch without a finished hyperbatch, L != the batch's hop count,
+ * dims out of range or dims[0] != the feature dim -> AGNES_ERR_INVALID. */
+typedef struct {
+    int32_t L;
+    int32_t dims[AGNES_MAX_LAYERS + 1];
+    const uint16_t* weight[AGNES_MAX_LAYERS];
+    const float* bias[AGNES_MAX_LAYERS];
+} agnes_sage_model;
+
+agnes_status agnes_sage_forward(agnes_batch* batch, const agnes_sage_model* model, float* out,
+                                void* hip_stream);
+
 /* Store facts: out[0] num_nodes, out[1] num_edges, out[2] topology blocks,
  * out[3] edges per topology block, out[4] feature blocks, out[5] rows per
  * feature block, out[6] row_bytes, out[7] device bytes held by the store. */

@@ -20,7 +20,7 @@ from ._binding import AgnesError, agnes_batch_stats, agnes_batch_view_get, agnes
 from ._binding import agnes_batch_finish, agnes_batch_wait, agnes_hyperbatch_begin  # noqa: F401
 from ._binding import agnes_free, agnes_hyperbatch_prepare, agnes_last_error  # noqa: F401
 from ._binding import agnes_store_info, agnes_store_object_table, agnes_store_set_option  # noqa: F401
-from ._binding import agnes_batch_tier_stats, agnes_build_blocks_staged  # noqa: F401
+from ._binding import agnes_batch_tier_stats, agnes_build_blocks_staged, agnes_sage_forward  # noqa: F401
 
 _FEAT_DTYPES = {np.dtype(np.float32): B.AGNES_FLOAT32, np.dtype(np.float16): B.AGNES_FLOAT16}
 
@@ -176,6 +176,39 @@ class Batch:
                     new_nodes=list(s.new_nodes[:L]), topo_blocks=list(s.topo_blocks[:L]),
                     rows=s.rows, distinct_rows=s.distinct_rows, feat_blocks=s.feat_blocks,
                     sample_ms=s.sample_ms, gather_ms=s.gather_ms, copy_ms=s.copy_ms)
+
+    def sage_forward(self, weights, biases, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """GraphSAGE forward over this batch (agnes_sage_forward).  weights[i]:
+        CUDA bf16 (or int16/uint16 bits) [dims[i+1], 2 dims[i]]; biases[i]: CUDA
+        float32 [dims[i+1]]; returns float32 [H*B, dims[L]] (enqueued on `stream`)."""
+        L = len(weights)
+        if L != len(biases) or L < 1 or L > B.AGNES_MAX_LAYERS:
+            raise ValueError("one weight and one bias per layer")
+        m = B.agnes_sage_model()
+        m.L = L
+        for i, (w, b) in enumerate(zip(weights, biases)):
+            if not (w.is_cuda and w.dim() == 2 and w.element_size() == 2 and w.is_contiguous()):
+                raise TypeError("weights must be contiguous 2-D CUDA bf16 tensors")
+            if not (b.is_cuda and b.dtype == torch.float32 and b.is_contiguous()):
+                raise TypeError("biases must be contiguous CUDA float32 tensors")
+            if b.numel() != w.shape[0] or w.shape[1] % 2:
+                raise ValueError("weight %d is [dims[i+1], 2 dims[i]] and bias %d [dims[i+1]]" % (i, i))
+            if i > 0 and w.shape[1] // 2 != weights[i - 1].shape[0]:
+                raise ValueError("layer %d's input dim is layer %d's output dim" % (i, i - 1))
+            m.dims[i] = w.shape[1] // 2
+            m.weight[i] = w.data_ptr()
+            m.bias[i] = b.data_ptr()
+        m.dims[L] = weights[-1].shape[0]
+        v = self.view()
+        rows = v.H * int(np.ctypeslib.as_array(v.layer_sizes, shape=(v.H * (v.L + 1),))[0])
+        if out is None:
+            out = torch.empty((rows, m.dims[L]), dtype=torch.float32, device="cuda")
+        if not (out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and
+                tuple(out.shape) == (rows, m.dims[L])):
+            raise ValueError("out must be a contiguous CUDA float32 tensor [H*B, dims[L]]")
+        agnes_sage_forward(self.handle, m, out.data_ptr(), _stream_handle(stream))
+        self._sage_keep = (weights, biases, out)
+        return out
 
     def tier_stats(self) -> dict:
         """Staged-tier counters (all zero for HBM-resident features)."""

@@ -25,7 +25,7 @@ AGNES_OPT_GATHER_CHUNKS = 5
 EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_hyperbatch_prepare",
             "agnes_hyperbatch_begin", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
             "agnes_batch_stats", "agnes_batch_tier_stats", "agnes_store_set_option", "agnes_store_info",
-            "agnes_store_object_table", "agnes_free", "agnes_last_error"]
+            "agnes_store_object_table", "agnes_sage_forward", "agnes_free", "agnes_last_error"]
 
 
 class agnes_csr(ctypes.Structure):
@@ -68,6 +68,11 @@ class agnes_tier_stats(ctypes.Structure):
                 ("staged_bytes", ctypes.c_int64), ("gather_ms", ctypes.c_float)]
 
 
+class agnes_sage_model(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("dims", ctypes.c_int32 * (AGNES_MAX_LAYERS + 1)),
+                ("weight", ctypes.c_void_p * AGNES_MAX_LAYERS), ("bias", ctypes.c_void_p * AGNES_MAX_LAYERS)]
+
+
 class AgnesError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), msg))
@@ -96,6 +101,8 @@ def lib():
                                             vp, ctypes.POINTER(vp)]
     L.agnes_batch_tier_stats.restype = st
     L.agnes_batch_tier_stats.argtypes = [vp, ctypes.POINTER(agnes_tier_stats)]
+    L.agnes_sage_forward.restype = st
+    L.agnes_sage_forward.argtypes = [vp, ctypes.POINTER(agnes_sage_model), vp, vp]
     L.agnes_hyperbatch_prepare.restype = st
     L.agnes_hyperbatch_prepare.argtypes = [vp, vp, i32, i32, vp, i32, u64, i64, vp, ctypes.POINTER(vp)]
     L.agnes_hyperbatch_begin.restype = st
@@ -148,6 +155,11 @@ def agnes_batch_tier_stats(batch: int) -> agnes_tier_stats:
     s = agnes_tier_stats()
     check(lib().agnes_batch_tier_stats(ctypes.c_void_p(batch), ctypes.byref(s)))
     return s
+
+
+def agnes_sage_forward(batch: int, model: agnes_sage_model, out_ptr: int, stream: int = 0) -> None:
+    check(lib().agnes_sage_forward(ctypes.c_void_p(batch), ctypes.byref(model), ctypes.c_void_p(out_ptr),
+                                   ctypes.c_void_p(stream)))
 
 
 def agnes_hyperbatch_prepare(store: int, targets_ptr: int, H: int, B: int, fanouts_arr, L: int,

@@ -139,6 +139,7 @@ struct Store {
     int e_blk_log2 = 0;
     int64_t nblk = 0;                 // topology blocks
     int64_t row_bytes = 0;
+    int feat_dtype = AGNES_FLOAT32;   // element type of the feature rows
     int64_t rpb = 0;                  // feature rows per block
     int64_t nfblk = 0;                // feature blocks
     int64_t block_bytes = 0;
@@ -200,10 +201,15 @@ struct Batch {
     Workspace ws;
     agnes_stats stats{};
     agnes_tier_stats tier{};
+    // GraphSAGE forward (sage.hip): per-layer offsets, the [h ; mean] rows, hidden embeddings
+    PinnedBuf sage_host;
+    DevBuf sage_off, sage_a, sage_h[2];
+    hipEvent_t sage_ev = nullptr;     // the offsets upload has left sage_host
     ~Batch() {
         if (sampled) (void)hipEventDestroy(sampled);
         if (gathered) (void)hipEventDestroy(gathered);
         if (needed) (void)hipEventDestroy(needed);
+        if (sage_ev) (void)hipEventDestroy(sage_ev);
         for (auto& e : ws.ev)
             if (e) (void)hipEventDestroy(e);
     }
@@ -218,6 +224,8 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
                       hipStream_t stream);
 void finish_hyperbatch(Batch& b, hipStream_t stream);
 void wait_batch(Batch& b);
+// GraphSAGE forward over a prepared batch (sage.hip); enqueues on `stream`.
+void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t stream);
 // Store construction (store.hip).
 // pool_blocks == 0: features in HBM; > 0: staged feature tier with that many slots.
 Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t block_bytes,

@@ -1,0 +1,263 @@
+// GraphSAGE forward over a prepared hyperbatch (Eq. (1), Sec. 3.1): the
+// computation step that consumes the per-hop CSR blocks and gathered rows.
+//
+// Layer i runs on hop l = L-1-i.  Per layer two kernels:
+//   k_sage_agg   one wave per destination node: its own input row and the
+//                float32 mean of its sampled neighbours' rows, both rounded to
+//                bf16, as one row [h_v ; m_v] of A (M x 2d, row-major);
+//   k_sage_gemm  Z = A W^T + b with bf16 MFMA (32x32x8, float32 accumulate),
+//                ReLU on hidden layers; hidden outputs stored as bf16, the last
+//                layer's as float32.
+// Destination rows of all minibatches are stacked minibatch-major, so a layer
+// is one GEMM over the whole hyperbatch.
+#include <algorithm>
+#include <cstring>
+
+#include "device.hpp"
+#include "runtime.hpp"
+
+namespace agnes {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4s __attribute__((ext_vector_type(4)));
+
+// float -> bf16 bits, round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ uint16_t to_bf16(float x) {
+    uint32_t u = __float_as_uint(x);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf16_to_float(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// Four consecutive input elements as float.
+template <typename InT> struct In4;
+template <> struct In4<float> {
+    static __device__ __forceinline__ f32x4 load(const float* p) { return *(const f32x4*)p; }
+};
+template <> struct In4<_Float16> {
+    static __device__ __forceinline__ f32x4 load(const _Float16* p) {
+        typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+        const h4 v = *(const h4*)p;
+        return f32x4{(float)v.x, (float)v.y, (float)v.z, (float)v.w};
+    }
+};
+template <> struct In4<uint16_t> {   // bf16 bits
+    static __device__ __forceinline__ f32x4 load(const uint16_t* p) {
+        const u16x4 v = *(const u16x4*)p;
+        return f32x4{bf16_to_float(v.x), bf16_to_float(v.y), bf16_to_float(v.z), bf16_to_float(v.w)};
+    }
+};
+
+// Offsets of one layer, all [H+1] int64: destination rows of minibatch j are
+// [d_off[j], d_off[j+1]); its input rows start at in_off[j]; its hop-l row
+// pointers at rp_off[j] and columns at col_off[j].
+struct LayerOffsets {
+    const int64_t* d_off;
+    const int64_t* in_off;
+    const int64_t* rp_off;
+    const int64_t* col_off;
+};
+
+template <typename InT>
+__global__ __launch_bounds__(kBlock) void k_sage_agg(const InT* __restrict__ hin, LayerOffsets o,
+                                                     const int32_t* __restrict__ row_ptr,
+                                                     const int32_t* __restrict__ col, int H, int64_t M, int din,
+                                                     uint16_t* __restrict__ A) {
+    const int lane = lane_id();
+    const int64_t nw = (int64_t)gridDim.x * kWavesPerBlock;
+    for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave_id(); row < M; row += nw) {
+        const int j = upper_segment(o.d_off, H, row);
+        const int64_t v = row - o.d_off[j];
+        const int32_t* rp = row_ptr + o.rp_off[j] + v;
+        const int32_t beg = rp[0], end = rp[1];
+        const int32_t* cb = col + o.col_off[j];
+        const InT* base = hin + o.in_off[j] * (int64_t)din;
+        uint16_t* arow = A + row * 2 * (int64_t)din;
+        for (int c = lane * 4; c < din; c += kWave * 4) {
+            const f32x4 self = In4<InT>::load(base + v * din + c);
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            int32_t t = beg;
+            for (; t + 4 <= end; t += 4) {
+                const int32_t u0 = cb[t], u1 = cb[t + 1], u2 = cb[t + 2], u3 = cb[t + 3];
+                const f32x4 x0 = In4<InT>::load(base + (int64_t)u0 * din + c);
+                const f32x4 x1 = In4<InT>::load(base + (int64_t)u1 * din + c);
+                const f32x4 x2 = In4<InT>::load(base + (int64_t)u2 * din + c);
+                const f32x4 x3 = In4<InT>::load(base + (int64_t)u3 * din + c);
+                acc += x0;
+                acc += x1;
+                acc += x2;
+                acc += x3;
+            }
+            for (; t < end; t++) acc += In4<InT>::load(base + (int64_t)cb[t] * din + c);
+            const int deg = end - beg;
+            f32x4 mean = {0.f, 0.f, 0.f, 0.f};
+            if (deg > 0) {
+                const float d = (float)deg;
+                mean = f32x4{acc.x / d, acc.y / d, acc.z / d, acc.w / d};
+            }
+            *(u16x4*)(arow + c) = u16x4{to_bf16(self.x), to_bf16(self.y), to_bf16(self.z), to_bf16(self.w)};
+            *(u16x4*)(arow + din + c) = u16x4{to_bf16(mean.x), to_bf16(mean.y), to_bf16(mean.z), to_bf16(mean.w)};
+        }
+    }
+}
+
+// Z[M][N] = A[M][K] W[N][K]^T + b.  Workgroup tile 128 x 128, K step 32; wave
+// w owns the 64 x 64 quarter (w / 2, w % 2) as 2 x 2 MFMA 32x32 blocks.
+// Operand layout of v_mfma_f32_32x32x8_bf16_1k: lane l holds A[l % 32][4 (l / 32) + q]
+// and B[4 (l / 32) + q][l % 32] for q = 0..3, and D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32]
+// for r = 0..15.  W is stored output-major, so both tiles sit in LDS with k
+// innermost and every operand is one 8-byte LDS read.
+constexpr int kGM = 128, kGN = 128, kGK = 32, kGKP = kGK + 8;   // padded LDS row (uint16)
+
+template <bool RELU, bool OUT_F32>
+__global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+                                                      const float* __restrict__ bias, int64_t M, int N, int K,
+                                                      void* __restrict__ Z) {
+    __shared__ uint16_t As[kGM][kGKP];
+    __shared__ uint16_t Bs[kGN][kGKP];
+    const int lane = lane_id(), w = wave_id(), t = threadIdx.x;
+    const int64_t m0 = (int64_t)blockIdx.x * kGM;
+    const int n0 = blockIdx.y * kGN;
+    const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; a++)
+#pragma unroll
+        for (int b = 0; b < 2; b++)
+#pragma unroll
+            for (int r = 0; r < 16; r++) acc[a][b][r] = 0.f;
+    // each thread moves 16 bytes of A and of W per half tile: row t / 2, k (t % 2) * 16
+    const int lr = t >> 1, lk = (t & 1) * 16;
+    for (int k0 = 0; k0 < K; k0 += kGK) {
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+            const int kk = lk + h * 8;
+            const int64_t gm = m0 + lr;
+            u32x4s va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
+            if (gm < M) va = *(const u32x4s*)(A + gm * K + k0 + kk);
+            if (n0 + lr < N) vb = *(const u32x4s*)(W + (int64_t)(n0 + lr) * K + k0 + kk);
+            *(u32x4s*)&As[lr][kk] = va;
+            *(u32x4s*)&Bs[lr][kk] = vb;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < kGK; ks += 8) {
+            const int kq = ks + (lane >> 5) * 4;
+            s16x4 a[2], b[2];
+#pragma unroll
+            for (int i = 0; i < 2; i++) a[i] = *(const s16x4*)&As[wm + i * 32 + (lane & 31)][kq];
+#pragma unroll
+            for (int i = 0; i < 2; i++) b[i] = *(const s16x4*)&Bs[wn + i * 32 + (lane & 31)][kq];
+#pragma unroll
+            for (int i = 0; i < 2; i++)
+#pragma unroll
+                for (int jj = 0; jj < 2; jj++)
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a[i], b[jj], acc[i][jj], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int jj = 0; jj < 2; jj++) {
+            const int gn = n0 + wn + jj * 32 + (lane & 31);
+            if (gn >= N) continue;
+            const float bv = bias[gn];
+#pragma unroll
+            for (int r = 0; r < 16; r++) {
+                const int64_t gm = m0 + wm + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                if (gm >= M) continue;
+                float z = acc[i][jj][r] + bv;
+                if (RELU) z = z > 0.f ? z : 0.f;
+                if (OUT_F32) ((float*)Z)[gm * N + gn] = z;
+                else ((uint16_t*)Z)[gm * N + gn] = to_bf16(z);
+            }
+        }
+}
+
+template <typename InT>
+static void launch_agg(const void* hin, const LayerOffsets& o, const int32_t* row_ptr, const int32_t* col, int H,
+                       int64_t M, int din, uint16_t* A, hipStream_t st) {
+    const int G = (int)std::max<int64_t>(1, std::min<int64_t>((M + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 20));
+    hipLaunchKernelGGL(k_sage_agg<InT>, dim3(G), dim3(kBlock), 0, st, (const InT*)hin, o, row_ptr, col, H, M, din, A);
+}
+
+void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t st) {
+    const Store& s = *b.store;
+    AGNES_REQUIRE(b.state == kGathering || b.state == kDone, AGNES_ERR_INVALID, "the batch holds no finished hyperbatch");
+    AGNES_REQUIRE(m.L == b.L, AGNES_ERR_INVALID, "the model needs one layer per hop of the batch");
+    AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+    for (int i = 0; i <= m.L; i++)
+        AGNES_REQUIRE(m.dims[i] >= 32 && m.dims[i] <= 4096 && m.dims[i] % 32 == 0, AGNES_ERR_INVALID,
+                      "dims must be positive multiples of 32, at most 4096");
+    const int esz = s.feat_dtype == AGNES_FLOAT32 ? 4 : 2;
+    AGNES_REQUIRE((int64_t)m.dims[0] * esz == s.row_bytes, AGNES_ERR_INVALID, "dims[0] must be the feature dim");
+    for (int i = 0; i < m.L; i++)
+        AGNES_REQUIRE(m.weight[i] && m.bias[i], AGNES_ERR_INVALID, "weights and biases must not be NULL");
+    const int H = b.H, L = b.L;
+    // host offsets of every layer: d_off, in_off, rp_off, col_off ([H+1] each)
+    std::vector<int64_t> offs((size_t)L * 4 * (H + 1));
+    int64_t Mmax = 0, Amax = 0, Hmax = 1;
+    std::vector<int64_t> Ms(L);
+    for (int i = 0; i < L; i++) {
+        const int l = L - 1 - i;
+        int64_t* d_off = &offs[((size_t)i * 4 + 0) * (H + 1)];
+        int64_t* in_off = &offs[((size_t)i * 4 + 1) * (H + 1)];
+        int64_t* rp = &offs[((size_t)i * 4 + 2) * (H + 1)];
+        int64_t* co = &offs[((size_t)i * 4 + 3) * (H + 1)];
+        d_off[0] = 0;
+        for (int j = 0; j < H; j++) d_off[j + 1] = d_off[j] + b.layer_sizes[(size_t)j * (L + 1) + l];
+        for (int j = 0; j <= H; j++) {
+            in_off[j] = i == 0 ? b.node_off[j] : offs[((size_t)(i - 1) * 4 + 0) * (H + 1) + j];
+            rp[j] = b.rp_off[l][j];
+            co[j] = b.col_off[l][j];
+        }
+        Ms[i] = d_off[H];
+        Mmax = std::max(Mmax, Ms[i]);
+        Amax = std::max(Amax, Ms[i] * 2 * m.dims[i]);
+        if (i + 1 < L) Hmax = std::max(Hmax, Ms[i] * m.dims[i + 1]);
+    }
+    if (b.sage_ev) AGNES_CHECK_HIP(hipEventSynchronize(b.sage_ev));   // the previous upload has left the pinned buffer
+    else AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.sage_ev, hipEventDisableTiming));
+    b.sage_host.reserve(offs.size() * 8);
+    memcpy(b.sage_host.ptr, offs.data(), offs.size() * 8);
+    b.sage_off.reserve(offs.size() * 8);
+    b.sage_a.reserve((size_t)std::max<int64_t>(Amax, 1) * 2);
+    for (int k = 0; k < 2; k++) b.sage_h[k].reserve((size_t)Hmax * 2);
+    if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.gathered, 0));
+    AGNES_CHECK_HIP(hipMemcpyAsync(b.sage_off.ptr, b.sage_host.ptr, offs.size() * 8, hipMemcpyHostToDevice, st));
+    AGNES_CHECK_HIP(hipEventRecord(b.sage_ev, st));
+    const int64_t* doffs = b.sage_off.as<int64_t>();
+    const void* hin = b.features.ptr;
+    for (int i = 0; i < L; i++) {
+        const int l = L - 1 - i;
+        LayerOffsets o{doffs + ((size_t)i * 4 + 0) * (H + 1), doffs + ((size_t)i * 4 + 1) * (H + 1),
+                       doffs + ((size_t)i * 4 + 2) * (H + 1), doffs + ((size_t)i * 4 + 3) * (H + 1)};
+        const int din = m.dims[i], dout = m.dims[i + 1];
+        const int64_t M = Ms[i];
+        if (M == 0) continue;
+        uint16_t* A = b.sage_a.as<uint16_t>();
+        if (i == 0 && s.feat_dtype == AGNES_FLOAT32)
+            launch_agg<float>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
+        else if (i == 0 && s.feat_dtype == AGNES_FLOAT16)
+            launch_agg<_Float16>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
+        else
+            launch_agg<uint16_t>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
+        const dim3 grid((unsigned)((M + kGM - 1) / kGM), (unsigned)((dout + kGN - 1) / kGN));
+        if (i + 1 < L) {
+            void* z = b.sage_h[i & 1].ptr;
+            hipLaunchKernelGGL((k_sage_gemm<true, false>), grid, dim3(kBlock), 0, st, A,
+                               (const uint16_t*)m.weight[i], m.bias[i], M, dout, 2 * din, z);
+            hin = z;
+        } else {
+            hipLaunchKernelGGL((k_sage_gemm<false, true>), grid, dim3(kBlock), 0, st, A,
+                               (const uint16_t*)m.weight[i], m.bias[i], M, dout, 2 * din, (void*)out);
+        }
+        AGNES_CHECK_HIP(hipGetLastError());
+    }
+}
+
+}  // namespace agnes

@@ -97,6 +97,7 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
     while (((int64_t)1 << s->e_blk_log2) < s->e_blk) s->e_blk_log2++;
     s->nblk = e > 0 ? (e + s->e_blk - 1) / s->e_blk : 1;
     s->row_bytes = row_bytes;
+    s->feat_dtype = feat->dtype;
     s->rpb = (int64_t)block_bytes / row_bytes;
     s->nfblk = (n + s->rpb - 1) / s->rpb;
     s->max_degree = maxdeg;
