@@ -104,13 +104,15 @@ __global__ __launch_bounds__(kBlock) void k_sage_agg(const InT* __restrict__ hin
     }
 }
 
-// Z[M][N] = A[M][K] W[N][K]^T + b.  Workgroup tile 128 x 128, K step 32; wave
+// Z[M][N] = A[M][K] W[N][K]^T + b.  Workgroup tile 128 x 128, K step 64; wave
 // w owns the 64 x 64 quarter (w / 2, w % 2) as 2 x 2 MFMA 32x32 blocks.
 // Operand layout of v_mfma_f32_32x32x8_bf16_1k: lane l holds A[l % 32][4 (l / 32) + q]
 // and B[4 (l / 32) + q][l % 32] for q = 0..3, and D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32]
 // for r = 0..15.  W is stored output-major, so both tiles sit in LDS with k
-// innermost and every operand is one 8-byte LDS read.
-constexpr int kGM = 128, kGN = 128, kGK = 32, kGKP = kGK + 8;   // padded LDS row (uint16)
+// innermost and every operand is one 8-byte LDS read.  The next K step's tiles
+// are loaded into registers while the MFMAs consume the current ones.
+constexpr int kGM = 128, kGN = 128, kGK = 64, kGKP = kGK + 8;   // padded LDS row (uint16)
+constexpr int kGLoads = kGM * kGK / 8 / kBlock;                 // 16-byte pieces per thread per tile (4)
 
 template <bool RELU, bool OUT_F32>
 __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
@@ -129,20 +131,30 @@ __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict
         for (int b = 0; b < 2; b++)
 #pragma unroll
             for (int r = 0; r < 16; r++) acc[a][b][r] = 0.f;
-    // each thread moves 16 bytes of A and of W per half tile: row t / 2, k (t % 2) * 16
-    const int lr = t >> 1, lk = (t & 1) * 16;
-    for (int k0 = 0; k0 < K; k0 += kGK) {
+    // piece p of thread t: row (t + p * 256) / 8, k offset ((t + p * 256) % 8) * 8
+    u32x4s ra[kGLoads], rb[kGLoads];
+    auto fetch = [&](int k0) {
 #pragma unroll
-        for (int h = 0; h < 2; h++) {
-            const int kk = lk + h * 8;
-            const int64_t gm = m0 + lr;
-            u32x4s va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
-            if (gm < M) va = *(const u32x4s*)(A + gm * K + k0 + kk);
-            if (n0 + lr < N) vb = *(const u32x4s*)(W + (int64_t)(n0 + lr) * K + k0 + kk);
-            *(u32x4s*)&As[lr][kk] = va;
-            *(u32x4s*)&Bs[lr][kk] = vb;
+        for (int p = 0; p < kGLoads; p++) {
+            const int idx = t + p * kBlock;
+            const int r = idx >> 3, kk = (idx & 7) * 8;
+            const int64_t gm = m0 + r;
+            ra[p] = gm < M ? *(const u32x4s*)(A + gm * K + k0 + kk) : u32x4s{0u, 0u, 0u, 0u};
+            rb[p] = n0 + r < N ? *(const u32x4s*)(W + (int64_t)(n0 + r) * K + k0 + kk) : u32x4s{0u, 0u, 0u, 0u};
+        }
+    };
+    fetch(0);
+    for (int k0 = 0; k0 < K; k0 += kGK) {
+        __syncthreads();                      // the previous step's operands are consumed
+#pragma unroll
+        for (int p = 0; p < kGLoads; p++) {
+            const int idx = t + p * kBlock;
+            const int r = idx >> 3, kk = (idx & 7) * 8;
+            *(u32x4s*)&As[r][kk] = ra[p];
+            *(u32x4s*)&Bs[r][kk] = rb[p];
         }
         __syncthreads();
+        if (k0 + kGK < K) fetch(k0 + kGK);
 #pragma unroll
         for (int ks = 0; ks < kGK; ks += 8) {
             const int kq = ks + (lane >> 5) * 4;
@@ -157,7 +169,6 @@ __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict
                 for (int jj = 0; jj < 2; jj++)
                     acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a[i], b[jj], acc[i][jj], 0, 0, 0);
         }
-        __syncthreads();
     }
 #pragma unroll
     for (int i = 0; i < 2; i++)
