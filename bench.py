@@ -146,12 +146,13 @@ def ablation(store, cfg, targets_dev, H, reps, ob, rb, torch):
     return out
 
 
-def staged_tier(ag, w, cfg, dev_targets, H, pool_blocks, warmup, steps, ob, rb, torch):
+def staged_tier(ag, w, cfg, dev_targets, H, pool_blocks, warmup, steps, ob, rb, torch, cache_rows=None,
+                cache_threshold=2):
     """Hyperbatches on a store whose features sit in pinned host memory, with a
     pool of pool_blocks feature blocks in HBM: consecutive fresh hyperbatches
     (synchronous prepare calls), so later ones hit blocks staged earlier."""
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype,
-                     pool_blocks=pool_blocks)
+                     pool_blocks=pool_blocks, cache_rows=cache_rows, cache_threshold=cache_threshold)
     store.set_profiling(True)
     info = store.info()
     b = None
@@ -159,7 +160,7 @@ def staged_tier(ag, w, cfg, dev_targets, H, pool_blocks, warmup, steps, ob, rb, 
         b = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=b)
     torch.cuda.synchronize()
     acc = dict(ms=0.0, gather_ms=0.0, bytes=0, staged_blocks=0, hit_blocks=0, needed_blocks=0, rounds=0,
-               staged_bytes=0, rows_bytes=0)
+               staged_bytes=0, rows_bytes=0, cache_hit_rows=0, admitted_rows=0, distinct_rows=0)
     for s in range(warmup, warmup + steps):
         t0 = time.perf_counter()
         b = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=b)
@@ -170,13 +171,17 @@ def staged_tier(ag, w, cfg, dev_targets, H, pool_blocks, warmup, steps, ob, rb, 
         acc["bytes"] += bs + bg
         acc["gather_ms"] += ts["gather_ms"]
         acc["rows_bytes"] += st["rows"] * rb
-        for k in ("staged_blocks", "hit_blocks", "needed_blocks", "rounds", "staged_bytes"):
+        acc["distinct_rows"] += st["distinct_rows"]
+        for k in ("staged_blocks", "hit_blocks", "needed_blocks", "rounds", "staged_bytes", "cache_hit_rows",
+                  "admitted_rows"):
             acc[k] += ts[k]
+        cached = ts["cached_rows"]
     K = steps
     out = {"mode": "staged feature tier: features in pinned host memory, HBM pool of feature blocks "
                    "(synchronous prepare calls on fresh hyperbatches)",
            "config": {"workload": cfg.describe(), "hyperbatch": H, "minibatch": cfg.B,
                       "pool_blocks": pool_blocks, "pool_bytes": pool_blocks * info["rows_per_block"] * rb,
+                      "cache_rows": cache_rows or 0, "cache_threshold": cache_threshold if cache_rows else None,
                       "feature_blocks": info["feat_blocks"], "rows_per_block": info["rows_per_block"]},
            "steps": K, "warmup": warmup,
            "ms_per_step": round(acc["ms"] / K, 3),
@@ -187,7 +192,10 @@ def staged_tier(ag, w, cfg, dev_targets, H, pool_blocks, warmup, steps, ob, rb, 
            "hit_rate": round(acc["hit_blocks"] / max(1, acc["needed_blocks"]), 4),
            "staged_GB": round(acc["staged_bytes"] / K / 1e9, 4),
            "staged_GBps_over_gather": round(acc["staged_bytes"] / max(1e-9, acc["gather_ms"] * 1e-3) / 1e9, 2),
-           "gathered_rows_GB": round(acc["rows_bytes"] / K / 1e9, 4)}
+           "gathered_rows_GB": round(acc["rows_bytes"] / K / 1e9, 4),
+           "distinct_rows": acc["distinct_rows"] // K, "cache_hit_rows": acc["cache_hit_rows"] // K,
+           "cache_row_hit_rate": round(acc["cache_hit_rows"] / max(1, acc["distinct_rows"]), 4),
+           "admitted_rows": acc["admitted_rows"] // K, "cached_rows_at_end": cached}
     b.close()
     store.close()
     return out
@@ -335,6 +343,10 @@ def main():
     ap.add_argument("--sage", type=int, default=None, metavar="HIDDEN",
                     help="instead of the benchmark line, time the GraphSAGE forward over one prepared "
                          "hyperbatch with hidden width HIDDEN")
+    ap.add_argument("--cache-rows", type=int, default=None,
+                    help="with --staged: a feature cache of this many rows in HBM")
+    ap.add_argument("--cache-threshold", type=int, default=2,
+                    help="with --cache-rows: access count at which a row enters the cache")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
     args = ap.parse_args()
@@ -370,7 +382,8 @@ def main():
 
     if args.staged is not None:
         print(json.dumps(staged_tier(ag, w, cfg, dev_targets, H, args.staged, args.warmup, args.steps,
-                                     8 if w["offsets"].dtype == np.int64 else 4, cfg.row_bytes, torch)), flush=True)
+                                     8 if w["offsets"].dtype == np.int64 else 4, cfg.row_bytes, torch,
+                                     args.cache_rows, args.cache_threshold)), flush=True)
         return
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
     if args.sage is not None:

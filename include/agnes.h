@@ -246,17 +246,42 @@ agnes_status agnes_build_blocks_staged(const agnes_csr* csr, const agnes_feature
                                        uint64_t block_bytes, int64_t pool_blocks, void* hip_stream,
                                        agnes_store** out);
 
+/* Staged tier with a feature cache (Sec. 3.4(2): the number of accesses to
+ * every feature vector is counted, and vectors whose count reaches a
+ * threshold are kept in a feature cache; the others are loaded with their
+ * blocks when needed).  As agnes_build_blocks_staged, plus an HBM cache of
+ * `cache_rows` feature rows (the cache index table maps a node to its cache
+ * row):
+ *   - a hyperbatch's rows found in the cache are copied from it; the needed
+ *     feature blocks are the blocks of its other rows (staged and pooled as
+ *     above);
+ *   - after its gather, every row the hyperbatch gathered adds the number of
+ *     its minibatches to its access count; rows not in the cache whose count
+ *     is now >= `threshold` enter it, ascending by node id, while it has room
+ *     (copied from host memory); rows never leave it.
+ * cache_rows = 0 gives agnes_build_blocks_staged.  Errors: pool_blocks < 1,
+ * cache_rows < 0 or threshold < 1 -> AGNES_ERR_INVALID. */
+agnes_status agnes_build_blocks_cached(const agnes_csr* csr, const agnes_features* feat,
+                                       uint64_t block_bytes, int64_t pool_blocks, int64_t cache_rows,
+                                       int64_t threshold, void* hip_stream, agnes_store** out);
+
 /* Feature-tier counters of a prepared hyperbatch (all zero for a store with
- * HBM-resident features): needed feature blocks (= agnes_stats.feat_blocks),
- * blocks copied from host memory, blocks found in the pool, rounds, bytes
- * copied from host memory, and the device time of the gather including the
- * staging copies when profiling is on (else -1). */
+ * HBM-resident features): needed feature blocks (the blocks of its rows not in
+ * the feature cache; = agnes_stats.feat_blocks without a cache), blocks copied
+ * from host memory, blocks found in the pool, rounds, bytes copied from host
+ * memory for blocks, distinct rows served by the feature cache, rows that
+ * entered the cache after this hyperbatch, rows in the cache after it, and the
+ * device time of the gather including staging and admission when profiling is
+ * on (else -1). */
 typedef struct {
     int64_t needed_blocks;
     int64_t staged_blocks;
     int64_t hit_blocks;
     int64_t rounds;
     int64_t staged_bytes;
+    int64_t cache_hit_rows;
+    int64_t admitted_rows;
+    int64_t cached_rows;
     float gather_ms;
 } agnes_tier_stats;
 

@@ -78,3 +78,46 @@ def needed_blocks(minibatches, rows_per_block: int) -> np.ndarray:
         return np.zeros(0, np.int64)
     nodes = np.concatenate([np.asarray(m.nodes, dtype=np.int64) for m in minibatches])
     return np.unique(nodes // rows_per_block)
+
+
+class CachedPoolModel:
+    """The staged tier with a feature cache (Sec. 3.4(2): access counts per
+    feature vector; vectors whose count reaches a threshold are kept in a
+    feature cache; the others are loaded with their blocks when needed).
+
+    Per hyperbatch:
+    - its rows are the distinct nodes of its minibatches; a row's multiplicity
+      is the number of minibatches holding it;
+    - rows in the cache are served from it; the needed blocks are the blocks
+      of the other rows, and go through the block pool (PoolModel);
+    - then every row's access count grows by its multiplicity, and rows not
+      in the cache whose count reaches the threshold enter it, ascending by
+      node id, while it has fewer than `cache_rows` rows; rows never leave it.
+    """
+
+    def __init__(self, pool_blocks: int, cache_rows: int, threshold: int, rows_per_block: int):
+        self.pool = PoolModel(pool_blocks)
+        self.C = cache_rows
+        self.T = threshold
+        self.rpb = rows_per_block
+        self.cache: dict[int, int] = {}
+        self.count: dict[int, int] = {}
+
+    def hyperbatch(self, minibatches) -> dict:
+        mult: dict[int, int] = {}
+        for m in minibatches:
+            for u in set(int(x) for x in np.asarray(m.nodes)):
+                mult[u] = mult.get(u, 0) + 1
+        rows = sorted(mult)
+        hits = [u for u in rows if u in self.cache]
+        unc = [u for u in rows if u not in self.cache]
+        out = self.pool.hyperbatch(sorted(set(u // self.rpb for u in unc)))
+        for u in rows:
+            self.count[u] = min(0xFFFFFFFF, self.count.get(u, 0) + mult[u])
+        admitted = 0
+        for u in unc:
+            if self.count[u] >= self.T and len(self.cache) < self.C:
+                self.cache[u] = len(self.cache)
+                admitted += 1
+        out.update(cache_hit_rows=len(hits), admitted_rows=admitted, cached_rows=len(self.cache))
+        return out

@@ -21,6 +21,7 @@ from ._binding import agnes_batch_finish, agnes_batch_wait, agnes_hyperbatch_beg
 from ._binding import agnes_free, agnes_hyperbatch_prepare, agnes_last_error  # noqa: F401
 from ._binding import agnes_store_info, agnes_store_object_table, agnes_store_set_option  # noqa: F401
 from ._binding import agnes_batch_tier_stats, agnes_build_blocks_staged, agnes_sage_forward  # noqa: F401
+from ._binding import agnes_build_blocks_cached  # noqa: F401
 
 _FEAT_DTYPES = {np.dtype(np.float32): B.AGNES_FLOAT32, np.dtype(np.float16): B.AGNES_FLOAT16}
 
@@ -56,10 +57,13 @@ class Store:
     """HBM-resident topology and feature blocks (agnes_build_blocks), or with
     pool_blocks set, HBM-resident topology and a staged feature tier: features
     in pinned host memory, a pool of pool_blocks feature blocks in HBM
-    (agnes_build_blocks_staged)."""
+    (agnes_build_blocks_staged), and with cache_rows set also a feature cache
+    of that many rows, admitting rows at cache_threshold accesses
+    (agnes_build_blocks_cached)."""
 
     def __init__(self, offsets, indices, features, block_bytes: int, feat_dtype: str | None = None,
-                 stream=None, pool_blocks: int | None = None):
+                 stream=None, pool_blocks: int | None = None, cache_rows: int | None = None,
+                 cache_threshold: int = 2):
         off = np.ascontiguousarray(offsets)
         if off.dtype not in (np.int32, np.int64):
             raise TypeError("offsets must be int32 or int64")
@@ -77,9 +81,14 @@ class Store:
                           off.ctypes.data, idx.ctypes.data if len(idx) else None)
         fs = B.agnes_features(feat.ctypes.data, feat.shape[1], fdt)
         if pool_blocks is None:
+            if cache_rows is not None:
+                raise ValueError("a feature cache needs the staged tier (pool_blocks)")
             self.handle = agnes_build_blocks(csr, fs, block_bytes, _stream_handle(stream))
-        else:
+        elif cache_rows is None:
             self.handle = agnes_build_blocks_staged(csr, fs, block_bytes, int(pool_blocks), _stream_handle(stream))
+        else:
+            self.handle = agnes_build_blocks_cached(csr, fs, block_bytes, int(pool_blocks), int(cache_rows),
+                                                    int(cache_threshold), _stream_handle(stream))
         self.pool_blocks = pool_blocks
         self.num_nodes = len(off) - 1
         self.row_bytes = feat.shape[1] * feat.itemsize
@@ -214,7 +223,8 @@ class Batch:
         """Staged-tier counters (all zero for HBM-resident features)."""
         t = agnes_batch_tier_stats(self.handle)
         return dict(needed_blocks=t.needed_blocks, staged_blocks=t.staged_blocks, hit_blocks=t.hit_blocks,
-                    rounds=t.rounds, staged_bytes=t.staged_bytes, gather_ms=t.gather_ms)
+                    rounds=t.rounds, staged_bytes=t.staged_bytes, cache_hit_rows=t.cache_hit_rows,
+                    admitted_rows=t.admitted_rows, cached_rows=t.cached_rows, gather_ms=t.gather_ms)
 
     def view(self) -> B.agnes_batch_view:
         return agnes_batch_view_get(self.handle)

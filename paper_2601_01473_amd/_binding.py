@@ -22,7 +22,7 @@ AGNES_OPT_GATHER_UNROLL = 3
 AGNES_OPT_GATHER_NONTEMPORAL = 4
 AGNES_OPT_GATHER_CHUNKS = 5
 
-EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_hyperbatch_prepare",
+EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_build_blocks_cached", "agnes_hyperbatch_prepare",
             "agnes_hyperbatch_begin", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
             "agnes_batch_stats", "agnes_batch_tier_stats", "agnes_store_set_option", "agnes_store_info",
             "agnes_store_object_table", "agnes_sage_forward", "agnes_free", "agnes_last_error"]
@@ -65,7 +65,8 @@ class agnes_stats(ctypes.Structure):
 class agnes_tier_stats(ctypes.Structure):
     _fields_ = [("needed_blocks", ctypes.c_int64), ("staged_blocks", ctypes.c_int64),
                 ("hit_blocks", ctypes.c_int64), ("rounds", ctypes.c_int64),
-                ("staged_bytes", ctypes.c_int64), ("gather_ms", ctypes.c_float)]
+                ("staged_bytes", ctypes.c_int64), ("cache_hit_rows", ctypes.c_int64),
+                ("admitted_rows", ctypes.c_int64), ("cached_rows", ctypes.c_int64), ("gather_ms", ctypes.c_float)]
 
 
 class agnes_sage_model(ctypes.Structure):
@@ -99,6 +100,9 @@ def lib():
     L.agnes_build_blocks_staged.restype = st
     L.agnes_build_blocks_staged.argtypes = [ctypes.POINTER(agnes_csr), ctypes.POINTER(agnes_features), u64, i64,
                                             vp, ctypes.POINTER(vp)]
+    L.agnes_build_blocks_cached.restype = st
+    L.agnes_build_blocks_cached.argtypes = [ctypes.POINTER(agnes_csr), ctypes.POINTER(agnes_features), u64, i64,
+                                            i64, i64, vp, ctypes.POINTER(vp)]
     L.agnes_batch_tier_stats.restype = st
     L.agnes_batch_tier_stats.argtypes = [vp, ctypes.POINTER(agnes_tier_stats)]
     L.agnes_sage_forward.restype = st
@@ -148,6 +152,14 @@ def agnes_build_blocks_staged(csr: agnes_csr, feat: agnes_features, block_bytes:
     out = ctypes.c_void_p()
     check(lib().agnes_build_blocks_staged(ctypes.byref(csr), ctypes.byref(feat), block_bytes, pool_blocks,
                                           ctypes.c_void_p(stream), ctypes.byref(out)))
+    return out.value
+
+
+def agnes_build_blocks_cached(csr: agnes_csr, feat: agnes_features, block_bytes: int, pool_blocks: int,
+                              cache_rows: int, threshold: int, stream: int = 0) -> int:
+    out = ctypes.c_void_p()
+    check(lib().agnes_build_blocks_cached(ctypes.byref(csr), ctypes.byref(feat), block_bytes, pool_blocks,
+                                          cache_rows, threshold, ctypes.c_void_p(stream), ctypes.byref(out)))
     return out.value
 
 

@@ -51,7 +51,7 @@ agnes_status agnes_build_blocks(const agnes_csr* csr, const agnes_features* feat
     if (out) *out = nullptr;
     return guarded([&] {
         AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
-        Store* s = build_store(csr, feat, block_bytes, 0, (hipStream_t)hip_stream);
+        Store* s = build_store(csr, feat, block_bytes, 0, 0, 1, (hipStream_t)hip_stream);
         *out = reinterpret_cast<agnes_store*>(s);
     });
 }
@@ -63,7 +63,22 @@ agnes_status agnes_build_blocks_staged(const agnes_csr* csr, const agnes_feature
     return guarded([&] {
         AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
         AGNES_REQUIRE(pool_blocks >= 1, AGNES_ERR_INVALID, "pool_blocks must be >= 1");
-        Store* s = build_store(csr, feat, block_bytes, pool_blocks, (hipStream_t)hip_stream);
+        Store* s = build_store(csr, feat, block_bytes, pool_blocks, 0, 1, (hipStream_t)hip_stream);
+        *out = reinterpret_cast<agnes_store*>(s);
+    });
+}
+
+agnes_status agnes_build_blocks_cached(const agnes_csr* csr, const agnes_features* feat,
+                                       uint64_t block_bytes, int64_t pool_blocks, int64_t cache_rows,
+                                       int64_t threshold, void* hip_stream, agnes_store** out) {
+    if (out) *out = nullptr;
+    return guarded([&] {
+        AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
+        AGNES_REQUIRE(pool_blocks >= 1, AGNES_ERR_INVALID, "pool_blocks must be >= 1");
+        AGNES_REQUIRE(cache_rows >= 0, AGNES_ERR_INVALID, "cache_rows must not be negative");
+        AGNES_REQUIRE(threshold >= 1, AGNES_ERR_INVALID, "threshold must be >= 1");
+        AGNES_REQUIRE(cache_rows < 0x7FFFFFFFll, AGNES_ERR_INVALID, "cache_rows must be < 2^31");
+        Store* s = build_store(csr, feat, block_bytes, pool_blocks, cache_rows, threshold, (hipStream_t)hip_stream);
         *out = reinterpret_cast<agnes_store*>(s);
     });
 }
@@ -252,7 +267,8 @@ agnes_status agnes_store_info(const agnes_store* store, int64_t out[8]) {
         out[5] = s->rpb;
         out[6] = s->row_bytes;
         out[7] = (int64_t)(s->offsets.bytes + s->indices.bytes + s->features.bytes +
-                           s->first_node.bytes + s->last_node.bytes + s->pool.bytes + s->tbuf.bytes);
+                           s->first_node.bytes + s->last_node.bytes + s->pool.bytes + s->tbuf.bytes +
+                           s->tch.bytes + s->acc_count.bytes + s->cache_used.bytes);
     });
 }
 

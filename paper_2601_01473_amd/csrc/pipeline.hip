@@ -673,9 +673,15 @@ __global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, u
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Source row of node u: u itself when the features are in HBM; in the staged
-// tier, row (u mod rpb) of the pool slot that holds u's feature block.
-__device__ __forceinline__ uint32_t source_row(const int32_t* tbuf, uint32_t rpb, uint32_t u) {
+// Source row of node u in the staged tier: its feature-cache row when it has
+// one (the cache rows follow the pool's), else row (u mod rpb) of the pool
+// slot that holds u's feature block.
+__device__ __forceinline__ uint32_t source_row(const int32_t* tbuf, uint32_t rpb, const int32_t* tch,
+                                               uint32_t pool_rows, uint32_t u) {
+    if (tch) {
+        const int32_t c = tch[u];
+        if (c >= 0) return pool_rows + (uint32_t)c;
+    }
     const uint32_t b = u / rpb;
     return (uint32_t)tbuf[b] * rpb + (u - b * rpb);
 }
@@ -700,7 +706,8 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
                                                    const uint64_t* __restrict__ rl_key,
                                                    const int32_t* __restrict__ rl_val, const int64_t* node_off_g,
                                                    int H, int64_t base, int64_t rows, int64_t row_units,
-                                                   const int32_t* __restrict__ tbuf, uint32_t rpb) {
+                                                   const int32_t* __restrict__ tbuf, uint32_t rpb,
+                                                   const int32_t* __restrict__ tch, uint32_t pool_rows) {
     constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
     constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
     // Hold at least 88 VGPRs, i.e. at most 5 of the 8 wave slots of a SIMD (512
@@ -734,7 +741,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             const uint32_t pu = k > 0 ? (uint32_t)(key[k - 1] >> 32) : prev_u;
             const uint32_t d = (uint32_t)(node_off[(uint32_t)key[k]] + val[k]);
             fresh[k] = ok[k] && (k == 0 || u != pu);
-            src[k] = (TIER && ok[k]) ? source_row(tbuf, rpb, u) : u;
+            src[k] = (TIER && ok[k]) ? source_row(tbuf, rpb, tch, pool_rows, u) : u;
             dst[k] = d;
             if (ok[k] && li == 0) nodes_out[d] = (int32_t)u;
         }
@@ -774,7 +781,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict_
                                                         const int32_t* __restrict__ rl_val,
                                                         const int64_t* node_off_g, int H, int64_t base,
                                                         int64_t rows, int64_t row_units,
-                                                        const int32_t* __restrict__ tbuf, uint32_t rpb) {
+                                                        const int32_t* __restrict__ tbuf, uint32_t rpb,
+                                                        const int32_t* __restrict__ tch, uint32_t pool_rows) {
     static_assert(U <= kWave, "one lane per entry");
     extern __shared__ int64_t node_off[];
     load_offsets(node_off, node_off_g, H);
@@ -789,7 +797,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict_
             const uint64_t key = rl_key[e];
             u = (uint32_t)(key >> 32);
             d = (uint32_t)(node_off[(uint32_t)key] + rl_val[e]);
-            row = TIER ? source_row(tbuf, rpb, u) : u;
+            row = TIER ? source_row(tbuf, rpb, tch, pool_rows, u) : u;
             nodes_out[d] = (int32_t)u;
         }
         const uint32_t pu = (uint32_t)__shfl_up((int)u, 1, kWave);
@@ -842,6 +850,8 @@ struct GatherArgs {
     int64_t base, rows, row_units;   // entries [base, base + rows) of the list
     const int32_t* tbuf;             // staged tier: block -> pool slot (feat is then the pool); else null
     uint32_t rpb;
+    const int32_t* tch;              // staged tier with a feature cache: node -> cache row; else null
+    uint32_t pool_rows;              // the cache's rows follow this many pool rows
 };
 
 template <typename Unit, int LPR, int U, bool NT, bool ONE, bool TIER>
@@ -849,7 +859,7 @@ static void launch_gather_k2(const GatherArgs& a, int G, hipStream_t st) {
     const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
     hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, ONE, TIER>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
                        (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
-                       a.row_units, a.tbuf, a.rpb);
+                       a.row_units, a.tbuf, a.rpb, a.tch, a.pool_rows);
 }
 
 template <typename Unit, int LPR, int U, bool NT>
@@ -888,11 +898,11 @@ static void launch_gather_rows_k(const GatherArgs& a, int groups, hipStream_t st
     if (a.tbuf)
         hipLaunchKernelGGL((k_gather_rows<U, UPR, NT, true>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
                            (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
-                           a.row_units, a.tbuf, a.rpb);
+                           a.row_units, a.tbuf, a.rpb, a.tch, a.pool_rows);
     else
         hipLaunchKernelGGL((k_gather_rows<U, UPR, NT, false>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
                            (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
-                           a.row_units, a.tbuf, a.rpb);
+                           a.row_units, a.tbuf, a.rpb, a.tch, a.pool_rows);
 }
 
 template <int UPR>
@@ -939,25 +949,104 @@ static void launch_gather(const GatherArgs& all, int groups, int unroll, bool nt
 // Per round the GPU updates the block -> slot table, copies the missing blocks
 // from pinned host memory into their slots, and copies the round's rows.
 
-__global__ __launch_bounds__(kBlock) void k_block_flags(const uint64_t* rl_key, uint32_t rpb, int32_t* flag,
+// Step 1: flag the list entries whose rows are not in the feature cache (all
+// of them without a cache).
+__global__ __launch_bounds__(kBlock) void k_unc_flags(const uint64_t* rl_key, const int32_t* tch, int32_t* flag,
+                                                      const Ctl* ctl) {
+    const int64_t n = ctl->rows;
+    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < n; p += (int64_t)gridDim.x * kBlock)
+        flag[p] = (!tch || tch[(uint32_t)(rl_key[p] >> 32)] < 0) ? 1 : 0;
+}
+
+__global__ __launch_bounds__(kBlock) void k_unc_compact(const int32_t* flag, const int64_t* off, int32_t* unc,
                                                         const Ctl* ctl) {
     const int64_t n = ctl->rows;
-    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < n; p += (int64_t)gridDim.x * kBlock) {
-        const uint32_t b = (uint32_t)(rl_key[p] >> 32) / rpb;
-        flag[p] = (p == 0 || (uint32_t)(rl_key[p - 1] >> 32) / rpb != b) ? 1 : 0;
+    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < n; p += (int64_t)gridDim.x * kBlock)
+        if (flag[p]) unc[off[p]] = (int32_t)p;
+}
+
+// Step 2: among those entries, the first of every feature block.
+__global__ __launch_bounds__(kBlock) void k_block_flags(const uint64_t* rl_key, const int32_t* unc, uint32_t rpb,
+                                                        int32_t* flag, const Ctl* ctl) {
+    const int64_t n = ctl->tier_unc;
+    for (int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x; k < n; k += (int64_t)gridDim.x * kBlock) {
+        const uint32_t b = (uint32_t)(rl_key[unc[k]] >> 32) / rpb;
+        flag[k] = (k == 0 || (uint32_t)(rl_key[unc[k - 1]] >> 32) / rpb != b) ? 1 : 0;
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_block_compact(const uint64_t* rl_key, uint32_t rpb, const int32_t* flag,
-                                                          const int64_t* off, int64_t* need_entry,
-                                                          int32_t* need_block, const Ctl* ctl) {
-    const int64_t n = ctl->rows;
-    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < n; p += (int64_t)gridDim.x * kBlock) {
-        if (flag[p]) {
-            const int64_t k = off[p];
-            need_entry[k] = p;
-            need_block[k] = (int32_t)((uint32_t)(rl_key[p] >> 32) / rpb);
+__global__ __launch_bounds__(kBlock) void k_block_compact(const uint64_t* rl_key, const int32_t* unc, uint32_t rpb,
+                                                          const int32_t* flag, const int64_t* off,
+                                                          int64_t* need_entry, int32_t* need_block, const Ctl* ctl) {
+    const int64_t n = ctl->tier_unc;
+    for (int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x; k < n; k += (int64_t)gridDim.x * kBlock) {
+        if (flag[k]) {
+            const int64_t i = off[k];
+            need_entry[i] = unc[k];
+            need_block[i] = (int32_t)((uint32_t)(rl_key[unc[k]] >> 32) / rpb);
         }
+    }
+}
+
+// After the gather: every row's access count grows by its number of list
+// entries (the minibatches that gathered it; a node's entries are one run,
+// counted by the run's first entry); rows served by the cache are counted; a
+// row not in the cache whose count reaches the threshold is flagged for
+// admission.
+__global__ __launch_bounds__(kBlock) void k_access_count(const uint64_t* rl_key, const int32_t* tch, uint32_t* count,
+                                                         uint32_t threshold, int32_t* flag, Ctl* ctl) {
+    __shared__ unsigned long long hits;
+    if (threadIdx.x == 0) hits = 0;
+    __syncthreads();
+    const int64_t n = ctl->rows;
+    unsigned long long h = 0;
+    for (int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x; p < n; p += (int64_t)gridDim.x * kBlock) {
+        const uint32_t u = (uint32_t)(rl_key[p] >> 32);
+        int32_t f = 0;
+        if (p == 0 || (uint32_t)(rl_key[p - 1] >> 32) != u) {
+            uint32_t len = 1;
+            while (p + len < n && (uint32_t)(rl_key[p + len] >> 32) == u) len++;
+            const uint32_t c0 = count[u];
+            const uint32_t c = c0 > 0xFFFFFFFFu - len ? 0xFFFFFFFFu : c0 + len;
+            count[u] = c;
+            if (tch[u] >= 0) h++;
+            else if (c >= threshold) f = 1;
+        }
+        flag[p] = f;
+    }
+    if (h) atomicAdd(&hits, h);
+    __syncthreads();
+    if (threadIdx.x == 0 && hits) atomicAdd((unsigned long long*)&ctl->tier_hits, hits);
+}
+
+// Flagged rows enter the cache in list (ascending node) order while it has
+// room: one wave per entry copies the row from pinned host memory.
+template <typename Unit>
+__global__ __launch_bounds__(kBlock) void k_admit(const uint64_t* rl_key, const int32_t* flag, const int64_t* off,
+                                                  const Unit* __restrict__ host, Unit* __restrict__ rows_buf,
+                                                  int64_t pool_rows, int64_t row_units, int32_t* tch,
+                                                  const int64_t* used, int64_t capacity, const Ctl* ctl) {
+    const int64_t n = ctl->rows;
+    const int64_t nw = (int64_t)gridDim.x * kWavesPerBlock;
+    for (int64_t p = (int64_t)blockIdx.x * kWavesPerBlock + wave_id(); p < n; p += nw) {
+        if (!flag[p]) continue;
+        const int64_t slot = *used + off[p];
+        if (slot >= capacity) continue;
+        const uint32_t u = (uint32_t)(rl_key[p] >> 32);
+        const Unit* src = host + (int64_t)u * row_units;
+        Unit* dst = rows_buf + (pool_rows + slot) * row_units;
+        for (int64_t c = lane_id(); c < row_units; c += kWave) dst[c] = src[c];
+        if (lane_id() == 0) tch[u] = (int32_t)slot;
+    }
+}
+
+__global__ void k_admit_close(int64_t* used, int64_t capacity, Ctl* ctl) {
+    if (threadIdx.x == 0) {
+        const int64_t u0 = *used;
+        const int64_t u1 = std::min<int64_t>(capacity, u0 + ctl->tier_cand);
+        *used = u1;
+        ctl->tier_admitted = u1 - u0;
+        ctl->tier_cached = u1;
     }
 }
 
@@ -1101,20 +1190,28 @@ struct TierRound {
 // the slots not used in this round.  Every hit and every staging is one use.
 // The plan is written to the batch's pinned plan buffer; the store's pool view
 // is advanced as if the rounds had run (they are enqueued in the same order).
-static std::vector<TierRound> plan_staging(const Store& s, Batch& b, hipStream_t) {
+static std::vector<TierRound> plan_staging(const Store& s, Batch& b, hipStream_t st) {
     Workspace& w = b.ws;
-    const int64_t nb = b.stats.feat_blocks;
     const int64_t rows = b.node_off[b.H];
-    AGNES_REQUIRE(nb >= 1 && nb <= b.need_cap, AGNES_ERR_INTERNAL, "needed feature blocks out of range");
-    w.need_host.reserve_slack((size_t)nb * 12);
     if (!b.needed) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.needed, hipEventDisableTiming));
+    // the number of needed blocks, then the lists
+    AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, w.sync.ptr, sizeof(Ctl), hipMemcpyDeviceToHost, st));
+    AGNES_CHECK_HIP(hipEventRecord(b.needed, st));
+    AGNES_CHECK_HIP(hipEventSynchronize(b.needed));
+    Ctl hc;
+    memcpy(&hc, w.sync_host.ptr, sizeof(Ctl));
+    const int64_t nb = hc.tier_nb;
+    AGNES_REQUIRE(nb >= 0 && nb <= b.need_cap, AGNES_ERR_INTERNAL, "needed feature blocks out of range");
+    w.need_host.reserve_slack((size_t)std::max<int64_t>(nb, 1) * 12);
     int64_t* need_entry = (int64_t*)w.need_host.ptr;
     int32_t* need_block = (int32_t*)((char*)w.need_host.ptr + (size_t)nb * 8);
-    AGNES_CHECK_HIP(hipMemcpyAsync(need_entry, w.need.ptr, (size_t)nb * 8, hipMemcpyDeviceToHost, b.stream));
-    AGNES_CHECK_HIP(hipMemcpyAsync(need_block, (char*)w.need.ptr + (size_t)b.need_cap * 8, (size_t)nb * 4,
-                                   hipMemcpyDeviceToHost, b.stream));
-    AGNES_CHECK_HIP(hipEventRecord(b.needed, b.stream));
-    AGNES_CHECK_HIP(hipEventSynchronize(b.needed));
+    if (nb > 0) {
+        AGNES_CHECK_HIP(hipMemcpyAsync(need_entry, w.need.ptr, (size_t)nb * 8, hipMemcpyDeviceToHost, st));
+        AGNES_CHECK_HIP(hipMemcpyAsync(need_block, (char*)w.need.ptr + (size_t)b.need_cap * 8, (size_t)nb * 4,
+                                       hipMemcpyDeviceToHost, st));
+        AGNES_CHECK_HIP(hipEventRecord(b.needed, st));
+        AGNES_CHECK_HIP(hipEventSynchronize(b.needed));
+    }
 
     const int64_t P = s.pool_blocks;
     std::vector<TierRound> rounds;
@@ -1173,7 +1270,7 @@ static std::vector<TierRound> plan_staging(const Store& s, Batch& b, hipStream_t
             staged++;
         }
         TierRound r;
-        r.e0 = need_entry[i0];
+        r.e0 = i0 == 0 ? 0 : need_entry[i0];
         r.e1 = i1 < nb ? need_entry[i1] : rows;
         r.n_upd = (int)(upd.size() / 2);
         r.n_miss = (int)(miss.size() / 2);
@@ -1183,6 +1280,8 @@ static std::vector<TierRound> plan_staging(const Store& s, Batch& b, hipStream_t
         plan.insert(plan.end(), miss.begin(), miss.end());
         rounds.push_back(r);
     }
+    const int64_t staging_rounds = (int64_t)rounds.size();
+    if (nb == 0) rounds.push_back(TierRound{0, rows, 0, 0, 0, 0});   // every row is in the feature cache: copies only
     // keep the queue near the pool size: rebuild it from the live stamps
     if ((int64_t)s.lru.size() > 4 * P + 1024) {
         std::vector<std::pair<int64_t, int32_t>> all;
@@ -1199,7 +1298,7 @@ static std::vector<TierRound> plan_staging(const Store& s, Batch& b, hipStream_t
     b.tier.needed_blocks = nb;
     b.tier.staged_blocks = staged;
     b.tier.hit_blocks = hits;
-    b.tier.rounds = (int64_t)rounds.size();
+    b.tier.rounds = staging_rounds;
     b.tier.staged_bytes = staged * s.rpb * s.row_bytes;
     return rounds;
 }
@@ -1258,21 +1357,6 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
                        w.mb_off.as<int64_t>());
     hipLaunchKernelGGL(k_list_stats, dim3(grid_for(g.rows_max / kStatItems + 1, 512)), dim3(kBlock), 0, st,
                        w.rl_key[cur].as<uint64_t>(), (uint32_t)s.rpb, ctl);
-    if (s.tiered) {
-        // staged tier: the needed feature blocks (block starts of the final list)
-        w.blk_flag.reserve((size_t)g.rows_max * 4);
-        w.blk_off.reserve((size_t)(g.rows_max + 1) * 8);
-        w.need.reserve((size_t)g.rows_max * 12 + 256);
-        const int gl = grid_for(g.rows_max, 4096);
-        hipLaunchKernelGGL(k_block_flags, dim3(gl), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
-                           (uint32_t)s.rpb, w.blk_flag.as<int32_t>(), ctl);
-        scan_counts(w.blk_flag.as<int32_t>(), w.blk_off.as<int64_t>(), &ctl->rows, g.rows_max, nullptr,
-                    w.scan_part.as<int64_t>(), st);
-        hipLaunchKernelGGL(k_block_compact, dim3(gl), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
-                           (uint32_t)s.rpb, w.blk_flag.as<int32_t>(), w.blk_off.as<int64_t>(), w.need.as<int64_t>(),
-                           (int32_t*)((char*)w.need.ptr + (size_t)g.rows_max * 8), ctl);
-        b.need_cap = g.rows_max;
-    }
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
     // sizes of the outputs travel to pinned host memory; finish reads them
@@ -1343,8 +1427,31 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     };
     memset(&b.tier, 0, sizeof(b.tier));
     if (s.tiered && rows > 0) {
+        // the previous tiered gather, and its feature-cache admissions, are done
+        AGNES_CHECK_HIP(hipStreamWaitEvent(st, s.pool_free, 0));
+        Ctl* ctl = w.sync.as<Ctl>();
+        const bool cache = s.cache_rows > 0;
+        const int32_t* tch = cache ? s.tch.as<int32_t>() : nullptr;
+        int64_t* part = w.scan_part.as<int64_t>();
+        // needed feature blocks: the blocks of the entries whose rows are not cached
+        w.blk_flag.reserve((size_t)rows * 4);
+        w.blk_off.reserve((size_t)(rows + 1) * 8);
+        w.unc.reserve((size_t)rows * 4);
+        w.need.reserve((size_t)rows * 12 + 256);
+        b.need_cap = rows;
+        const int gl = grid_for(rows, 4096);
+        int32_t* flag = w.blk_flag.as<int32_t>();
+        int64_t* off = w.blk_off.as<int64_t>();
+        hipLaunchKernelGGL(k_unc_flags, dim3(gl), dim3(kBlock), 0, st, rlk, tch, flag, ctl);
+        scan_counts(flag, off, &ctl->rows, rows, &ctl->tier_unc, part, st);
+        hipLaunchKernelGGL(k_unc_compact, dim3(gl), dim3(kBlock), 0, st, flag, off, w.unc.as<int32_t>(), ctl);
+        hipLaunchKernelGGL(k_block_flags, dim3(gl), dim3(kBlock), 0, st, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
+                           flag, ctl);
+        scan_counts(flag, off, &ctl->tier_unc, rows, &ctl->tier_nb, part, st);
+        hipLaunchKernelGGL(k_block_compact, dim3(gl), dim3(kBlock), 0, st, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
+                           flag, off, w.need.as<int64_t>(), (int32_t*)((char*)w.need.ptr + (size_t)rows * 8), ctl);
+        AGNES_CHECK_HIP(hipGetLastError());
         std::vector<TierRound> rounds = plan_staging(s, b, st);
-        AGNES_CHECK_HIP(hipStreamWaitEvent(st, s.pool_free, 0));   // the previous tiered gather is done
         if (s.profile) {
             AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
             AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
@@ -1354,6 +1461,8 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
         const int64_t blk_bytes = s.rpb * s.row_bytes;
         ga.feat = s.pool.ptr;
         ga.tbuf = s.tbuf.as<int32_t>();
+        ga.tch = tch;
+        ga.pool_rows = (uint32_t)s.pool_rows;
         for (const TierRound& r : rounds) {
             if (r.n_upd)
                 hipLaunchKernelGGL(k_tbuf_update, dim3(grid_for(r.n_upd, 256)), dim3(kBlock), 0, st, plan + r.upd_at,
@@ -1371,10 +1480,30 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
             GatherArgs a = ga;
             a.base = r.e0;
             a.rows = r.e1 - r.e0;
-            copy_rows(a);
+            if (a.rows > 0) copy_rows(a);
+        }
+        if (cache) {
+            // access counts, then admissions in ascending node order while the cache has room
+            hipLaunchKernelGGL(k_access_count, dim3(gl), dim3(kBlock), 0, st, rlk, tch, s.acc_count.as<uint32_t>(),
+                               (uint32_t)std::min<int64_t>(s.cache_threshold, 0xFFFFFFFFll), flag, ctl);
+            scan_counts(flag, off, &ctl->rows, rows, &ctl->tier_cand, part, st);
+            const int ga2 = (int)std::max<int64_t>(1, std::min<int64_t>((rows + 3) / 4, 1 << 20));
+            if (s.row_bytes % 16 == 0)
+                hipLaunchKernelGGL(k_admit<u32x4>, dim3(ga2), dim3(kBlock), 0, st, rlk, flag, off,
+                                   (const u32x4*)s.host_feat_dev, s.pool.as<u32x4>(), s.pool_rows, s.row_bytes / 16,
+                                   s.tch.as<int32_t>(), s.cache_used.as<int64_t>(), s.cache_rows, ctl);
+            else
+                hipLaunchKernelGGL(k_admit<uint32_t>, dim3(ga2), dim3(kBlock), 0, st, rlk, flag, off,
+                                   (const uint32_t*)s.host_feat_dev, s.pool.as<uint32_t>(), s.pool_rows,
+                                   s.row_bytes / 4, s.tch.as<int32_t>(), s.cache_used.as<int64_t>(), s.cache_rows,
+                                   ctl);
+            hipLaunchKernelGGL(k_admit_close, dim3(1), dim3(kWave), 0, st, s.cache_used.as<int64_t>(), s.cache_rows,
+                               ctl);
         }
         AGNES_CHECK_HIP(hipGetLastError());
         if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));
+        // tier counters for wait
+        AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st));
         AGNES_CHECK_HIP(hipEventRecord(s.pool_free, st));
     } else {
         if (s.profile) {
@@ -1401,7 +1530,16 @@ void wait_batch(Batch& b) {
         AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.gather_ms, w.ev[2], w.ev[4]));
         AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.copy_ms, w.ev[3], w.ev[4]));
     }
-    if (b.store->tiered) b.tier.gather_ms = b.stats.gather_ms;
+    if (b.store->tiered) {
+        b.tier.gather_ms = b.stats.gather_ms;
+        if (b.node_off[b.H] > 0) {
+            Ctl hc;
+            memcpy(&hc, b.ws.sync_host.ptr, sizeof(Ctl));
+            b.tier.cache_hit_rows = hc.tier_hits;
+            b.tier.admitted_rows = hc.tier_admitted;
+            b.tier.cached_rows = hc.tier_cached;
+        }
+    }
     b.state = kDone;
 }
 

@@ -101,6 +101,11 @@ struct Ctl {
     int64_t distinct;   // distinct gathered rows
     int64_t fblocks;    // non-empty feature-block rows
     int64_t targets;    // H * B
+    int64_t tier_unc;   // staged tier: list entries whose rows are not in the feature cache
+    int64_t tier_nb;    // staged tier: needed feature blocks
+    int64_t tier_hits;  // staged tier: distinct rows served by the feature cache
+    int64_t tier_cand;  // staged tier: rows that reached the threshold this hyperbatch
+    int64_t tier_admitted, tier_cached;
     int64_t requests[AGNES_MAX_LAYERS];
     int64_t sampled[AGNES_MAX_LAYERS];
     int64_t new_nodes[AGNES_MAX_LAYERS];
@@ -121,7 +126,8 @@ struct Workspace {
     DevBuf ghist, gemit;              // join: per group new nodes per minibatch, merged entries
     DevBuf rs_hist, rs_dtot;          // radix-sort histograms
     DevBuf scan_part;                 // scan partial sums
-    DevBuf blk_flag, blk_off;         // staged tier: block starts of the final list, their offsets
+    DevBuf blk_flag, blk_off;         // staged tier: flags over the final list and their offsets
+    DevBuf unc;                       // staged tier: list entries whose rows are not in the feature cache
     DevBuf need;                      // staged tier: [needed blocks] first list entry, then block ids
     DevBuf plan;                      // staged tier: the rounds' (block, slot) updates and misses
     PinnedBuf need_host, plan_host;
@@ -153,7 +159,13 @@ struct Store {
     void* host_feat = nullptr;        // pinned host copy of the padded feature matrix
     void* host_feat_dev = nullptr;    // its device-visible address
     int64_t pool_blocks = 0;          // slots of the pool (rpb rows each)
-    DevBuf pool;                      // [pool_blocks][rpb][row_bytes]
+    int64_t pool_rows = 0;            // pool_blocks * rpb: the feature cache's rows follow them in `pool`
+    int64_t cache_rows = 0;           // rows of the feature cache (0: none)
+    int64_t cache_threshold = 1;      // access count at which a row enters the cache
+    DevBuf pool;                      // [pool_blocks * rpb + cache_rows][row_bytes]
+    DevBuf tch;                       // [num_nodes] int32: cache row of node u, or -1
+    DevBuf acc_count;                 // [num_nodes] uint32: accesses of node u's feature row so far
+    DevBuf cache_used;                // int64: rows in the cache
     DevBuf tbuf;                      // [nfblk] int32: slot holding feature block b, or -1
     mutable std::vector<int32_t> slot_block;  // host view of the pool: block in slot s, or -1
     mutable std::vector<int64_t> slot_stamp;  // access number of slot s's last use (-1: never)
@@ -227,9 +239,10 @@ void wait_batch(Batch& b);
 // GraphSAGE forward over a prepared batch (sage.hip); enqueues on `stream`.
 void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t stream);
 // Store construction (store.hip).
-// pool_blocks == 0: features in HBM; > 0: staged feature tier with that many slots.
+// pool_blocks == 0: features in HBM; > 0: staged feature tier with that many
+// slots and a feature cache of cache_rows rows (0: none).
 Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t block_bytes,
-                   int64_t pool_blocks, hipStream_t stream);
+                   int64_t pool_blocks, int64_t cache_rows, int64_t cache_threshold, hipStream_t stream);
 
 // ----------------------------------------------------------------- primitives (prims.hip)
 

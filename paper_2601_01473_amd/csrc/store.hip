@@ -55,8 +55,10 @@ static int64_t validate_offsets(const OffT* off, int64_t n, int64_t e) {
 }
 
 Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t block_bytes,
-                   int64_t pool_blocks, hipStream_t st) {
+                   int64_t pool_blocks, int64_t cache_rows, int64_t cache_threshold, hipStream_t st) {
     AGNES_REQUIRE(pool_blocks >= 0, AGNES_ERR_INVALID, "pool_blocks must not be negative");
+    AGNES_REQUIRE(cache_rows >= 0, AGNES_ERR_INVALID, "cache_rows must not be negative");
+    AGNES_REQUIRE(cache_threshold >= 1, AGNES_ERR_INVALID, "the cache threshold must be >= 1");
     AGNES_REQUIRE(csr && feat, AGNES_ERR_INVALID, "csr and features must not be NULL");
     const int64_t n = csr->num_nodes, e = csr->num_edges;
     AGNES_REQUIRE(n >= 1 && n < 0x7FFFFFFFll, AGNES_ERR_INVALID, "num_nodes must be in [1, 2^31-1)");
@@ -126,9 +128,20 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
         memcpy(s->host_feat, feat->data, fdata);
         if (fbytes > fdata) memset((char*)s->host_feat + fdata, 0, fbytes - fdata);
         AGNES_CHECK_HIP(hipHostGetDevicePointer(&s->host_feat_dev, s->host_feat, 0));
-        s->pool.reserve((size_t)pool_blocks * (size_t)s->rpb * (size_t)row_bytes);
+        s->pool_rows = pool_blocks * s->rpb;
+        s->cache_rows = cache_rows;
+        s->cache_threshold = cache_threshold;
+        s->pool.reserve((size_t)(s->pool_rows + cache_rows) * (size_t)row_bytes);
         s->tbuf.reserve((size_t)s->nfblk * 4);
         fill_u32(s->tbuf.ptr, 0xFFFFFFFFu, s->nfblk, st);
+        if (cache_rows > 0) {
+            s->tch.reserve((size_t)n * 4);
+            s->acc_count.reserve((size_t)n * 4);
+            s->cache_used.reserve(8);
+            fill_u32(s->tch.ptr, 0xFFFFFFFFu, n, st);
+            fill_u32(s->acc_count.ptr, 0u, n, st);
+            fill_u32(s->cache_used.ptr, 0u, 2, st);
+        }
         s->slot_block.assign((size_t)pool_blocks, -1);
         s->slot_stamp.assign((size_t)pool_blocks, -1);
         s->block_slot.assign((size_t)s->nfblk, -1);

@@ -96,3 +96,42 @@ def test_staged_store_rejects_empty_pool(agnes):
     feat = features(100, 8, 1)
     with pytest.raises(agnes.AgnesError):
         agnes.Store(off, idx, feat, 256, pool_blocks=0)
+
+
+@pytest.mark.parametrize("cache_rows,threshold", [(0, 1), (7, 2), (300, 1), (100000, 3)])
+@pytest.mark.parametrize("dim,dtype,block_bytes", [(256, np.float32, 4096), (3, np.float32, 64),
+                                                   (20, np.float32, 256)])
+def test_feature_cache_matches_oracle_and_model(agnes, cache_rows, threshold, dim, dtype, block_bytes):
+    """Hyperbatches that repeat earlier targets make rows hot: rows reaching the
+    threshold enter the cache and are served from it, their blocks are no
+    longer staged, and every counter equals the model's."""
+    from oracle.staging import CachedPoolModel
+    off, idx = random_graph(2200, 9, 4, hubs=2, hub_deg=500)
+    feat = features(2200, dim, 6, dtype)
+    fan = [5, 3]
+    base = [distinct_targets(2200, 4, 30, 20 + s) for s in range(3)]
+    hbs = [(base[0], 0), (base[1], 4), (base[0], 0), (base[2], 8), (base[0], 0), (base[1], 4)]
+    pool = 20
+    store = agnes.Store(off, idx, feat, block_bytes, pool_blocks=pool, cache_rows=cache_rows,
+                        cache_threshold=threshold)
+    o = oracle.Oracle(off, idx)
+    fb = feature_bytes(feat)
+    rpb = block_bytes // fb.shape[1]
+    model = CachedPoolModel(pool, cache_rows, threshold, rpb)
+    b = None
+    for s, (tg, mb_base) in enumerate(hbs):
+        t = torch.from_numpy(np.ascontiguousarray(tg)).cuda()
+        b = store.prepare(t, fan, seed=7, mb_base=mb_base, batch=b)
+        ref = o.hyperbatch(tg, fan, 7, mb_base)
+        got = b.to_host()
+        for j in range(tg.shape[0]):
+            compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=("cache", s, j))
+        ts = b.tier_stats()
+        want = model.hyperbatch(ref)
+        log("cache", cache_rows, threshold, s, ts)
+        for k, v in want.items():
+            assert ts[k] == v, (s, k, ts[k], v)
+    if cache_rows:
+        assert ts["cached_rows"] > 0
+    b.close()
+    store.close()

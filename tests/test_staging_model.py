@@ -76,3 +76,51 @@ def test_needed_blocks_are_the_distinct_blocks_of_all_node_lists():
             self.nodes = np.asarray(nodes)
     got = needed_blocks([M([9, 3, 4]), M([4, 15, 0])], 4)
     assert got.tolist() == [0, 1, 2, 3]
+
+
+class _MB:
+    def __init__(self, nodes):
+        self.nodes = np.asarray(nodes)
+
+
+def test_cache_hand_example():
+    # rows_per_block 2, pool 4 blocks, cache 1 row, threshold 2.
+    # hb1: minibatches [0, 5] and [0]: rows 0 (x2), 5; blocks 0, 2 staged; counts
+    #      0:2, 5:1; row 0 reaches 2 and enters the cache.
+    # hb2: [0, 1]: row 0 from the cache; row 1's block 0 is still pooled (hit);
+    #      counts 0:3, 1:1; nothing new reaches 2.
+    # hb3: [1] and [1, 5]: rows 1 (x2), 5 not cached; blocks 0, 2 pooled; counts
+    #      1:3, 5:2 reach 2 but the cache is full.
+    from oracle.staging import CachedPoolModel
+    m = CachedPoolModel(4, 1, 2, 2)
+    assert m.hyperbatch([_MB([0, 5]), _MB([0])]) == dict(
+        needed_blocks=2, staged_blocks=2, hit_blocks=0, rounds=1, cache_hit_rows=0, admitted_rows=1, cached_rows=1)
+    assert m.hyperbatch([_MB([0, 1])]) == dict(
+        needed_blocks=1, staged_blocks=0, hit_blocks=1, rounds=1, cache_hit_rows=1, admitted_rows=0, cached_rows=1)
+    assert m.hyperbatch([_MB([1]), _MB([1, 5])]) == dict(
+        needed_blocks=2, staged_blocks=0, hit_blocks=2, rounds=1, cache_hit_rows=0, admitted_rows=0, cached_rows=1)
+
+
+def test_cache_threshold_one_serves_a_repeated_hyperbatch_entirely():
+    from oracle.staging import CachedPoolModel
+    rng = np.random.default_rng(3)
+    mbs = [_MB(rng.choice(500, size=40, replace=False)) for _ in range(3)]
+    m = CachedPoolModel(8, 10 ** 6, 1, 4)
+    first = m.hyperbatch(mbs)
+    distinct = len(set(np.concatenate([x.nodes for x in mbs]).tolist()))
+    assert first["admitted_rows"] == distinct and first["cache_hit_rows"] == 0
+    again = m.hyperbatch(mbs)
+    assert again == dict(needed_blocks=0, staged_blocks=0, hit_blocks=0, rounds=0, cache_hit_rows=distinct,
+                         admitted_rows=0, cached_rows=distinct)
+
+
+def test_no_cache_reduces_to_the_pool_model():
+    from oracle.staging import CachedPoolModel
+    rng = np.random.default_rng(5)
+    a, b = CachedPoolModel(5, 0, 1, 3), PoolModel(5)
+    for _ in range(6):
+        mbs = [_MB(rng.choice(100, size=12, replace=False)) for _ in range(2)]
+        got = a.hyperbatch(mbs)
+        want = b.hyperbatch(needed_blocks(mbs, 3))
+        assert {k: got[k] for k in want} == want
+        assert got["cache_hit_rows"] == got["admitted_rows"] == got["cached_rows"] == 0
