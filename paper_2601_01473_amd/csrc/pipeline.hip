@@ -125,9 +125,16 @@ __global__ __launch_bounds__(kBlock) void k_list0(const uint32_t* sk, const uint
 // the output row offsets.
 __global__ __launch_bounds__(kBlock) void k_begin(int l, int L, int H, Ctl* ctl, int32_t* size,
                                                   int64_t* newcnt, int32_t* lsz, int64_t* ecount,
-                                                  int64_t* req_off, const int64_t* e_off, int64_t* node_off) {
+                                                  int64_t* req_off, const int64_t* e_off, int64_t* node_off,
+                                                  const uint32_t* topo_part, int n_part) {
     __shared__ int64_t lds[kWavesPerBlock];
     if (l > 0) {
+        // the previous hop's non-empty Bck rows: the sampler's per-workgroup counts
+        int64_t t = 0;
+        for (int i = threadIdx.x; i < n_part; i += kBlock) t += topo_part[i];
+        int64_t tot;
+        (void)block_exclusive_scan(t, lds, tot);
+        if (threadIdx.x == 0) ctl->topo_blocks[l - 1] = tot;
         for (int j = threadIdx.x; j < H; j += kBlock) {
             ecount[(int64_t)j * L + (l - 1)] = e_off[req_off[j + 1]] - e_off[req_off[j]];
             size[j] += (int32_t)newcnt[j];
@@ -189,8 +196,10 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, uint
                                                    const OffT* off, const int32_t* adj, int e_blk_log2,
                                                    int64_t nblk, const uint64_t* rl_key, const int32_t* rl_val,
                                                    const int64_t* req_off_g, const int64_t* e_off,
-                                                   int32_t* cg, Ctl* ctl) {
+                                                   int32_t* cg, uint32_t* topo_part, const Ctl* ctl) {
     extern __shared__ int64_t req_off[];      // [H+1] request offsets
+    __shared__ uint32_t opened;
+    if (threadIdx.x == 0) opened = 0;
     load_offsets(req_off, req_off_g, H);
     const int64_t R = ctl->R;
     for (int64_t base = (int64_t)blockIdx.x * kBlock; base < R; base += (int64_t)gridDim.x * kBlock) {
@@ -238,8 +247,12 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, uint
         }
         bool opens = active && (p == 0 || prev != blk);
         uint64_t m = __ballot(opens);
-        if (lane_id() == 0 && m) atomicAdd((unsigned long long*)&ctl->topo_blocks[l], (unsigned long long)__popcll(m));
+        if (lane_id() == 0 && m) atomicAdd(&opened, (uint32_t)__popcll(m));
     }
+    // one count per workgroup (summed by the next k_begin): a device-wide
+    // atomic per wave on one address would serialize
+    __syncthreads();
+    if (threadIdx.x == 0) topo_part[blockIdx.x] = opened;
 }
 
 // ----------------------------------------------------------------- join
@@ -630,11 +643,13 @@ static size_t join_write_lds(int H) {
 }
 
 // Statistics of the final list (the feature bucket): distinct rows (runs of one
-// node) and non-empty feature-block rows (runs of one feature block).  Runs on
-// the sampling stream so that the row copy does nothing but copy.
+// node) and non-empty feature-block rows (runs of one feature block), one
+// partial pair per workgroup for the host to add up.  Runs on the sampling
+// stream so that the row copy does nothing but copy.
 constexpr int kStatItems = 8;   // entries per thread per round (independent loads in flight)
 
-__global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, uint32_t rpb, Ctl* ctl) {
+__global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, uint32_t rpb, uint64_t* part,
+                                                       const Ctl* ctl) {
     __shared__ unsigned long long cnt[2];
     if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
     __syncthreads();
@@ -663,9 +678,10 @@ __global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, u
         if (nf) atomicAdd(&cnt[1], nf);
     }
     __syncthreads();
+    // one pair per workgroup, summed on the host (no device-wide atomics)
     if (threadIdx.x == 0) {
-        if (cnt[0]) atomicAdd((unsigned long long*)&ctl->distinct, cnt[0]);
-        if (cnt[1]) atomicAdd((unsigned long long*)&ctl->fblocks, cnt[1]);
+        part[2 * blockIdx.x] = cnt[0];
+        part[2 * blockIdx.x + 1] = cnt[1];
     }
 }
 
@@ -699,7 +715,7 @@ __device__ __forceinline__ uint32_t source_row(const int32_t* tbuf, uint32_t rpb
 // the row already in registers; the others load theirs (U rows in flight).
 // A launch covers list entries [base, base + rows); the host may split the list
 // into several launches so that other streams' kernels are dispatched between
-// them.  Also counts the distinct rows and the non-empty feature-block rows.
+// them.
 template <typename Unit, int LPR, int U, bool NT, bool ONE, bool TIER>
 __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat, Unit* __restrict__ out,
                                                    int32_t* __restrict__ nodes_out,
@@ -1073,14 +1089,19 @@ __global__ __launch_bounds__(kBlock) void k_stage(const Unit* __restrict__ host,
 // Layout of the block that the host reads at the synchronisation point:
 // [Ctl][layer sizes H x (L+1) int32][edge counts H x L int64].
 struct SyncLayout {
-    size_t lsz, ecount, bytes;
+    size_t lsz, ecount, lstat, bytes;
+    int n_lstat;                      // workgroups of k_list_stats (one partial pair each)
 };
 
-static SyncLayout sync_layout(int H, int L) {
+static int list_stats_groups(int64_t rows_max) { return grid_for(rows_max / kStatItems + 1, 512); }
+
+static SyncLayout sync_layout(int H, int L, int64_t rows_max) {
     SyncLayout y;
     y.lsz = (sizeof(Ctl) + 255) / 256 * 256;
     y.ecount = (y.lsz + (size_t)H * (L + 1) * 4 + 255) / 256 * 256;
-    y.bytes = y.ecount + (size_t)H * L * 8;
+    y.lstat = (y.ecount + (size_t)H * L * 8 + 255) / 256 * 256;
+    y.n_lstat = list_stats_groups(rows_max);
+    y.bytes = y.lstat + (size_t)y.n_lstat * 16;
     return y;
 }
 
@@ -1109,6 +1130,7 @@ static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout&
     w.rs_hist.reserve((size_t)radix_hist_entries(g.sort_max) * 4);
     w.rs_dtot.reserve((size_t)radix_dtot_entries() * 4);
     w.scan_part.reserve((size_t)scan_partials_needed() * 8);
+    w.topo_part.reserve((size_t)grid_for(g.Rmax, 2048) * 4);
     if (!w.ev[0])
         for (auto& e : w.ev) AGNES_CHECK_HIP(hipEventCreate(&e));
 }
@@ -1128,7 +1150,7 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
 
     hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, l, g.L, g.H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ecount, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
-                       (int64_t*)nullptr);
+                       (int64_t*)nullptr, w.topo_part.as<uint32_t>(), gR);
     hipLaunchKernelGGL(k_count<OffT>, dim3(gR), dim3(kBlock), lds_h, st, g.H, g.capN, f, off,
                        w.nodes.as<int32_t>(), w.req_off.as<int64_t>(), w.cnt.as<int32_t>(), ctl);
     scan_counts(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, g.Rmax, &ctl->S, part, st);
@@ -1137,7 +1159,7 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
 #define AGNES_SAMPLE(MK)                                                                               \
     hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, seed,     \
                        mb_base, off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),      \
-                       w.e_off.as<int64_t>(), cg, ctl)
+                       w.e_off.as<int64_t>(), cg, w.topo_part.as<uint32_t>(), ctl)
     // the register sampler's work grows with MAXK^2 (ranks) and MAXK/4 (Philox
     // calls), so common fanouts get a bound of their own
     if (f <= 4) AGNES_SAMPLE(4);
@@ -1314,9 +1336,10 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
     Geometry g = plan(s, H, B, fanouts, L);
     AGNES_REQUIRE(join_write_lds(H) <= (size_t)s.max_lds && (size_t)(H + 1) * 16 <= (size_t)s.max_lds,
                   AGNES_ERR_RANGE, "H is too large for the device's workgroup memory");
-    SyncLayout y = sync_layout(H, L);
+    SyncLayout y = sync_layout(H, L, g.rows_max);
     Workspace& w = b.ws;
     reserve_workspace(w, g, y);
+    b.rows_max = g.rows_max;
     if (!b.sampled) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.sampled, hipEventDisableTiming));
     if (!b.gathered) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.gathered, hipEventDisableTiming));
     b.store = &s;
@@ -1354,9 +1377,9 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
     // close the last hop: edge counts, final node counts, output row offsets
     hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
-                       w.mb_off.as<int64_t>());
-    hipLaunchKernelGGL(k_list_stats, dim3(grid_for(g.rows_max / kStatItems + 1, 512)), dim3(kBlock), 0, st,
-                       w.rl_key[cur].as<uint64_t>(), (uint32_t)s.rpb, ctl);
+                       w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), grid_for(g.Rmax, 2048));
+    hipLaunchKernelGGL(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
+                       (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl);
     AGNES_CHECK_HIP(hipGetLastError());
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
     // sizes of the outputs travel to pinned host memory; finish reads them
@@ -1370,7 +1393,7 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     const Store& s = *b.store;
     Workspace& w = b.ws;
     const int H = b.H, L = b.L;
-    SyncLayout y = sync_layout(H, L);
+    SyncLayout y = sync_layout(H, L, b.rows_max);
     AGNES_CHECK_HIP(hipEventSynchronize(b.sampled));
     b.state = kIdle;   // until the gather is enqueued
     Ctl hc;
@@ -1390,8 +1413,16 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
         b.stats.new_nodes[l] = hc.new_nodes[l];
         b.stats.topo_blocks[l] = hc.topo_blocks[l];
     }
-    b.stats.distinct_rows = hc.distinct;
-    b.stats.feat_blocks = hc.fblocks;
+    {
+        const uint64_t* lp = (const uint64_t*)((const char*)w.sync_host.ptr + y.lstat);
+        int64_t nd = 0, nf = 0;
+        for (int i = 0; i < y.n_lstat; i++) {
+            nd += (int64_t)lp[2 * i];
+            nf += (int64_t)lp[2 * i + 1];
+        }
+        b.stats.distinct_rows = nd;
+        b.stats.feat_blocks = nf;
+    }
 
     // host view offsets
     b.node_off.assign((size_t)H + 1, 0);

@@ -98,8 +98,6 @@ struct Ctl {
     int64_t n_new;      // new nodes of the current hop (all minibatches)
     int64_t rows;       // gathered rows (sum of |N_j|)
     int64_t err;        // bit 0: target out of range, bit 1: duplicate target, bit 2: capacity
-    int64_t distinct;   // distinct gathered rows
-    int64_t fblocks;    // non-empty feature-block rows
     int64_t targets;    // H * B
     int64_t tier_unc;   // staged tier: list entries whose rows are not in the feature cache
     int64_t tier_nb;    // staged tier: needed feature blocks
@@ -126,6 +124,7 @@ struct Workspace {
     DevBuf ghist, gemit;              // join: per group new nodes per minibatch, merged entries
     DevBuf rs_hist, rs_dtot;          // radix-sort histograms
     DevBuf scan_part;                 // scan partial sums
+    DevBuf topo_part;                 // per sampler workgroup: Bck rows it opened
     DevBuf blk_flag, blk_off;         // staged tier: flags over the final list and their offsets
     DevBuf unc;                       // staged tier: list entries whose rows are not in the feature cache
     DevBuf need;                      // staged tier: [needed blocks] first list entry, then block ids
@@ -202,6 +201,7 @@ struct Batch {
     hipEvent_t gathered = nullptr;    // outputs and statistics are complete
     hipEvent_t needed = nullptr;      // staged tier: the needed feature blocks are in ws.need_host
     int64_t capN = 0;
+    int64_t rows_max = 0;             // node-list capacity of the hyperbatch (sizes the sync block)
     int cur = 0;                      // which list buffer holds the final list
     int64_t need_cap = 0;             // staged tier: entries of each array in ws.need
     std::vector<int64_t> node_off;
