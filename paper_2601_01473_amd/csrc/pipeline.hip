@@ -726,11 +726,6 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
                                                    const int32_t* __restrict__ tch, uint32_t pool_rows) {
     constexpr int RPW = kWave / LPR;             // lane groups (rows) per wave
     constexpr int GPB = kWavesPerBlock * RPW;    // lane groups per workgroup
-    // Hold at least 88 VGPRs, i.e. at most 5 of the 8 wave slots of a SIMD (512
-    // VGPRs each).  The copy alone runs as fast this way, and kernels of other
-    // streams (the sampling of the next hyperbatches) always find free slots
-    // instead of waiting for the copy's backlog of workgroups to drain.
-    asm volatile("" ::: "v87");
     extern __shared__ int64_t node_off[];
     load_offsets(node_off, node_off_g, H);
     const int G = gridDim.x;
