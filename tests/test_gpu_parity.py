@@ -54,6 +54,36 @@ def test_hand_example_on_gpu(agnes):
     assert first.tolist() == [0, 3] and last.tolist() == [2, 5]
 
 
+def test_stored_fixture_on_gpu(agnes):
+    """The HIP path against values stored under tests/golden/ (written by the
+    oracle's fixture script), not against a fresh oracle run."""
+    import json
+    import os
+    with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "oracle_small.json")) as fh:
+        fx = json.load(fh)
+    off = np.array(fx["offsets"], np.int64)
+    idx = np.array(fx["indices"], np.int32)
+    feat = np.array(fx["features"], np.float32)
+    tg = np.array(fx["targets"], np.int32)
+    log("golden oracle_small", tg.shape, fx["fanouts"])
+    store = agnes.Store(off, idx, feat, fx["block_bytes"])
+    b = store.prepare(torch.from_numpy(tg).cuda(), fx["fanouts"], seed=fx["seed"], mb_base=fx["mb_base"])
+    got = b.to_host()
+    fb = feature_bytes(feat)
+    for j, want in enumerate(fx["expected"]["minibatches"]):
+        g = got[j]
+        assert g["nodes"].tolist() == want["nodes"], j
+        assert g["layer_sizes"].tolist() == want["layer_sizes"], j
+        assert [r.tolist() for r in g["row_ptr"]] == want["row_ptr"], j
+        assert [c.tolist() for c in g["col"]] == want["col"], j
+        assert np.array_equal(g["features"], fb[np.array(want["nodes"], np.int64)]), j
+    st = b.stats()
+    for k, v in fx["expected"]["stats"].items():
+        assert st[k] == v, (k, st[k], v)
+    b.close()
+    store.close()
+
+
 @pytest.mark.parametrize("seed", range(4))
 def test_random_graphs_int64(agnes, seed):
     off, idx = random_graph(3000, 14, seed, hubs=4, hub_deg=900)
