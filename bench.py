@@ -334,6 +334,8 @@ def main():
     ap.add_argument("--gather-unroll", type=int, default=None, help="rows in flight per lane group")
     ap.add_argument("--gather-nt", type=int, default=None, help="1 = non-temporal row stores, 0 = ordinary")
     ap.add_argument("--gather-chunks", type=int, default=None, help="launches the row copy is split into")
+    ap.add_argument("--sampling-graph", type=int, choices=[0, 1], default=0,
+                    help="1: replay the sampling kernels from a captured HIP graph; 0: launch them one by one")
     ap.add_argument("--ablation", action="store_true",
                     help="instead of the benchmark line, compare the hyperbatch with its minibatches "
                          "prepared one at a time (time, bytes, block reads)")
@@ -400,6 +402,7 @@ def main():
     store.set_profiling(True)
     store.set_gather_shape(args.gather_groups, args.gather_unroll,
                            None if args.gather_nt is None else bool(args.gather_nt), args.gather_chunks)
+    store.set_sampling_graph(bool(args.sampling_graph))
     stream = torch.cuda.current_stream()
     ob = 8 if w["offsets"].dtype == np.int64 else 4
     rb = cfg.row_bytes
@@ -525,7 +528,8 @@ def main():
                      "copy_kernel": round(copy_avg_ms, 4)},
         "mode": f"pipelined ({args.schedule}): {NSLOT} batch slots; "
                 f"hyperbatches t+1..t+{D} sample while t gathers"
-                f"; {len(s_streams)} sampling stream(s); gather on the {args.gather_stream} stream",
+                f"; {len(s_streams)} sampling stream(s); gather on the {args.gather_stream} stream"
+                f"; sampling kernels {'replayed from a HIP graph' if args.sampling_graph else 'launched one by one'}",
         "serial_ms_per_step": round(serial_ms, 4),
         "per_step": {"algorithmic_bytes": tot_bytes // K, "sample_bytes": tot_sample // K,
                      "gather_bytes": tot_gather // K, "rows": rows // K,

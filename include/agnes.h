@@ -211,13 +211,22 @@ agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);   /*
  *   AGNES_OPT_GATHER_CHUNKS: the row copy runs as this many consecutive
  *     launches over consecutive parts of the bucket, in [1, 64] (default 1);
  *     kernels of other streams are dispatched between them.
+ *   AGNES_OPT_SAMPLING_GRAPH: 0 = (default) every hyperbatch launches its
+ *     sampling kernels one by one.  1 = a batch that begins two hyperbatches
+ *     of the same shape in a row (same H, B, fanouts and store, and the same
+ *     scratch buffers) captures the sampling kernels as a HIP graph and from
+ *     then on replays it with one graph launch per hyperbatch; a batch holds
+ *     one such graph and captures again when the shape changes.  Replay
+ *     shortens one hyperbatch's latency on small shapes but slows hyperbatches
+ *     that sample concurrently on several streams.
  * Options change launch shapes and store kinds only, never results. */
 typedef enum {
     AGNES_OPT_PROFILE = 1,
     AGNES_OPT_GATHER_GROUPS = 2,
     AGNES_OPT_GATHER_UNROLL = 3,
     AGNES_OPT_GATHER_NONTEMPORAL = 4,
-    AGNES_OPT_GATHER_CHUNKS = 5
+    AGNES_OPT_GATHER_CHUNKS = 5,
+    AGNES_OPT_SAMPLING_GRAPH = 6
 } agnes_option;
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value);
 

@@ -110,6 +110,11 @@ class Store:
     def set_profiling(self, on: bool) -> None:
         agnes_store_set_option(self.handle, B.AGNES_OPT_PROFILE, 1 if on else 0)
 
+    def set_sampling_graph(self, on: bool) -> None:
+        """Replay the sampling kernels of a repeated hyperbatch shape from a
+        captured HIP graph, or launch them one by one (the default)."""
+        agnes_store_set_option(self.handle, B.AGNES_OPT_SAMPLING_GRAPH, 1 if on else 0)
+
     def set_gather_shape(self, groups: int | None = None, unroll: int | None = None,
                          nontemporal: bool | None = None, chunks: int | None = None) -> None:
         """Launch shape and store kind of the row-copy kernel (never change results)."""

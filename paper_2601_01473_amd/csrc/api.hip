@@ -249,6 +249,8 @@ agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_
         } else if (opt == AGNES_OPT_GATHER_CHUNKS) {
             AGNES_REQUIRE(value >= 1 && value <= 64, AGNES_ERR_INVALID, "gather chunks must be in [1, 64]");
             s->gather_chunks = (int)value;
+        } else if (opt == AGNES_OPT_SAMPLING_GRAPH) {
+            s->sampling_graph = value ? 1 : 0;
         } else {
             throw Error{AGNES_ERR_INVALID, "unknown option"};
         }

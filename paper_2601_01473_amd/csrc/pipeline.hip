@@ -73,6 +73,23 @@ __device__ __forceinline__ void load_mb_edges(int64_t* mb_e, const int64_t* req_
     __syncthreads();
 }
 
+// Values that change from call to call.  The host hands them to k_params by
+// value; every later kernel of the sampling phase reads them from device
+// memory, so the same launches (or a graph captured from them) serve any call.
+struct ChainParams {
+    const int32_t* targets;   // [H][B] device
+    uint64_t seed;
+    int64_t mb_base;          // global index of minibatch 0
+};
+
+__global__ void k_params(ChainParams* p, const int32_t* targets, uint64_t seed, int64_t mb_base) {
+    if (threadIdx.x == 0) {
+        p->targets = targets;
+        p->seed = seed;
+        p->mb_base = mb_base;
+    }
+}
+
 __global__ void k_ctl_init(Ctl* ctl, int64_t targets) {
     int64_t* p = (int64_t*)ctl;
     for (int i = threadIdx.x; i < (int)(sizeof(Ctl) / 8); i += kBlock) p[i] = 0;
@@ -83,9 +100,10 @@ __global__ void k_ctl_init(Ctl* ctl, int64_t targets) {
 // Targets become the first B nodes of every minibatch.  An out-of-range target
 // is recorded as an error and replaced by node 0 so that later kernels stay in
 // bounds.  tkey receives the node ids for the sort that builds the list.
-__global__ __launch_bounds__(kBlock) void k_init(const int32_t* targets, int H, int B, int64_t num_nodes,
+__global__ __launch_bounds__(kBlock) void k_init(const ChainParams* prm, int H, int B, int64_t num_nodes,
                                                  int64_t capN, int32_t* nodes, int32_t* size,
                                                  int64_t* newcnt, uint32_t* tkey, Ctl* ctl) {
+    const int32_t* targets = prm->targets;
     int64_t n = (int64_t)H * B;
     for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) {
         int64_t j = i / B, r = i - j * B;
@@ -192,13 +210,15 @@ __global__ __launch_bounds__(kBlock) void k_count(int H, int64_t capN, int32_t f
 // minibatch, and the requests of one node are neighbours.  Also counts the
 // topology blocks the hop touches (non-empty rows of Bck).
 template <typename OffT, int MAXK>
-__global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, uint64_t seed, int64_t mb_base,
+__global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, const ChainParams* prm,
                                                    const OffT* off, const int32_t* adj, int e_blk_log2,
                                                    int64_t nblk, const uint64_t* rl_key, const int32_t* rl_val,
                                                    const int64_t* req_off_g, const int64_t* e_off,
                                                    int32_t* cg, uint32_t* topo_part, const Ctl* ctl) {
     extern __shared__ int64_t req_off[];      // [H+1] request offsets
     __shared__ uint32_t opened;
+    const uint64_t seed = prm->seed;
+    const int64_t mb_base = prm->mb_base;
     if (threadIdx.x == 0) opened = 0;
     load_offsets(req_off, req_off_g, H);
     const int64_t R = ctl->R;
@@ -1126,13 +1146,15 @@ static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout&
     w.rs_dtot.reserve((size_t)radix_dtot_entries() * 4);
     w.scan_part.reserve((size_t)scan_partials_needed() * 8);
     w.topo_part.reserve((size_t)grid_for(g.Rmax, 2048) * 4);
+    w.params.reserve(sizeof(ChainParams));
     if (!w.ev[0])
         for (auto& e : w.ev) AGNES_CHECK_HIP(hipEventCreate(&e));
 }
 
 template <typename OffT>
-static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l, int32_t f, uint64_t seed,
-                         int64_t mb_base, Batch& b, const SyncLayout& y, int cur, hipStream_t st) {
+static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l, int32_t f, Batch& b,
+                         const SyncLayout& y, int cur, hipStream_t st) {
+    const ChainParams* prm = w.params.as<ChainParams>();
     Ctl* ctl = w.sync.as<Ctl>();
     int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
     int64_t* ecount = (int64_t*)((char*)w.sync.ptr + y.ecount);
@@ -1152,8 +1174,8 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     const int32_t* adj = s.indices.as<int32_t>();
     int32_t* cg = w.skey.as<int32_t>();
 #define AGNES_SAMPLE(MK)                                                                               \
-    hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, seed,     \
-                       mb_base, off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),      \
+    hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, prm,      \
+                       off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),      \
                        w.e_off.as<int64_t>(), cg, w.topo_part.as<uint32_t>(), ctl)
     // the register sampler's work grows with MAXK^2 (ranks) and MAXK/4 (Philox
     // calls), so common fanouts get a bound of their own
@@ -1321,6 +1343,93 @@ static std::vector<TierRound> plan_staging(const Store& s, Batch& b, hipStream_t
 }
 
 
+// The sampling phase's kernels: counters cleared, targets sorted into the list
+// of hop 0, the hops, the close of the last hop and the statistics of the final
+// list.  Every size they need is read from device memory and every per-call
+// value from the params block, so the sequence depends only on the shape, the
+// store and the buffer addresses (the key of a captured graph).
+static void launch_chain(const Store& s, Batch& b, const Geometry& g, const SyncLayout& y,
+                         const int32_t* fanouts, hipStream_t st) {
+    Workspace& w = b.ws;
+    const int32_t H = g.H, B = g.B, L = g.L;
+    Ctl* ctl = w.sync.as<Ctl>();
+    int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
+    int64_t* ec = (int64_t*)((char*)w.sync.ptr + y.ecount);
+    hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(kBlock), 0, st, ctl, (int64_t)H * B);
+    hipLaunchKernelGGL(k_init, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
+                       w.params.as<ChainParams>(), H, B, s.num_nodes, g.capN, w.nodes.as<int32_t>(),
+                       w.size.as<int32_t>(), w.newcnt.as<int64_t>(), w.skey.as<uint32_t>(), ctl);
+    int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
+                                    w.sval2.as<uint32_t>(), &ctl->targets, (int64_t)H * B, s.node_bits,
+                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
+    hipLaunchKernelGGL(k_list0, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
+                       in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>(),
+                       in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>(), B, w.rl_key[0].as<uint64_t>(),
+                       w.rl_val[0].as<int32_t>(), ctl);
+    AGNES_CHECK_HIP(hipGetLastError());
+    int cur = 0;
+    for (int l = 0; l < L; l++) {
+        if (s.offsets64) launch_layer<int64_t>(s, w, g, l, fanouts[l], b, y, cur, st);
+        else launch_layer<int32_t>(s, w, g, l, fanouts[l], b, y, cur, st);
+        cur ^= 1;
+    }
+    // close the last hop: edge counts, final node counts, output row offsets
+    hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
+                       w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
+                       w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), grid_for(g.Rmax, 2048));
+    hipLaunchKernelGGL(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
+                       (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl);
+    AGNES_CHECK_HIP(hipGetLastError());
+}
+
+// Everything launch_chain's launches depend on apart from the params block.
+static std::vector<uint64_t> chain_key(const Store& s, const Batch& b, const Geometry& g, const int32_t* fanouts) {
+    const Workspace& w = b.ws;
+    auto a = [](const void* p) { return (uint64_t)(uintptr_t)p; };
+    std::vector<uint64_t> k = {a(&s), (uint64_t)s.num_nodes, (uint64_t)s.nblk, (uint64_t)s.offsets64,
+                               (uint64_t)s.node_bits, (uint64_t)s.e_blk_log2, (uint64_t)s.rpb,
+                               a(s.offsets.ptr), a(s.indices.ptr), (uint64_t)g.H, (uint64_t)g.B, (uint64_t)g.L};
+    for (int l = 0; l < g.L; l++) k.push_back((uint64_t)fanouts[l]);
+    for (const DevBuf* d : {&w.nodes, &w.size, &w.newcnt, &w.req_off, &w.mb_off, &w.sync, &w.cnt, &w.e_off,
+                            &w.rl_key[0], &w.rl_key[1], &w.rl_val[0], &w.rl_val[1], &w.skey, &w.sval, &w.skey2,
+                            &w.sval2, &w.split, &w.ghist, &w.gemit, &w.rs_hist, &w.rs_dtot, &w.scan_part,
+                            &w.topo_part, &w.params})
+        k.push_back(a(d->ptr));
+    for (int l = 0; l < g.L; l++) {
+        k.push_back(a(b.row_ptr[l].ptr));
+        k.push_back(a(b.col[l].ptr));
+    }
+    return k;
+}
+
+// Captures launch_chain as a HIP graph on the batch's private stream (nothing
+// runs during a capture) and keeps its executable instance.
+static void capture_chain(const Store& s, Batch& b, const Geometry& g, const SyncLayout& y,
+                          const int32_t* fanouts, const std::vector<uint64_t>& key) {
+    if (b.chain) {
+        (void)hipGraphExecDestroy(b.chain);
+        b.chain = nullptr;
+        b.chain_key.clear();
+    }
+    if (!b.cap_stream) AGNES_CHECK_HIP(hipStreamCreateWithFlags(&b.cap_stream, hipStreamNonBlocking));
+    AGNES_CHECK_HIP(hipStreamBeginCapture(b.cap_stream, hipStreamCaptureModeThreadLocal));
+    hipGraph_t graph = nullptr;
+    try {
+        launch_chain(s, b, g, y, fanouts, b.cap_stream);
+    } catch (...) {
+        (void)hipStreamEndCapture(b.cap_stream, &graph);
+        if (graph) (void)hipGraphDestroy(graph);
+        throw;
+    }
+    AGNES_CHECK_HIP(hipStreamEndCapture(b.cap_stream, &graph));
+    hipGraphExec_t exec = nullptr;
+    const hipError_t e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    AGNES_CHECK_HIP(e);
+    b.chain = exec;
+    b.chain_key = key;
+}
+
 void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
                       const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
                       hipStream_t st) {
@@ -1345,37 +1454,19 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
         b.row_ptr[l].reserve((size_t)(H * g.cap[l] + H) * 4);
         b.col[l].reserve((size_t)std::max<int64_t>(1, H * g.cap[l] * fanouts[l]) * 4);
     }
-    Ctl* ctl = w.sync.as<Ctl>();
-    int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
-    int64_t* ec = (int64_t*)((char*)w.sync.ptr + y.ecount);
 
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[0], st));
-    hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(kBlock), 0, st, ctl, (int64_t)H * B);
-    hipLaunchKernelGGL(k_init, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st, targets, H, B,
-                       s.num_nodes, g.capN, w.nodes.as<int32_t>(), w.size.as<int32_t>(), w.newcnt.as<int64_t>(),
-                       w.skey.as<uint32_t>(), ctl);
-    int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
-                                    w.sval2.as<uint32_t>(), &ctl->targets, (int64_t)H * B, s.node_bits,
-                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
-    hipLaunchKernelGGL(k_list0, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
-                       in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>(),
-                       in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>(), B, w.rl_key[0].as<uint64_t>(),
-                       w.rl_val[0].as<int32_t>(), ctl);
+    hipLaunchKernelGGL(k_params, dim3(1), dim3(kWave), 0, st, w.params.as<ChainParams>(), targets, seed, mb_base);
     AGNES_CHECK_HIP(hipGetLastError());
-    int cur = 0;
-    for (int l = 0; l < L; l++) {
-        if (s.offsets64) launch_layer<int64_t>(s, w, g, l, fanouts[l], seed, mb_base, b, y, cur, st);
-        else launch_layer<int32_t>(s, w, g, l, fanouts[l], seed, mb_base, b, y, cur, st);
-        cur ^= 1;
-    }
-    b.cur = cur;
-    // close the last hop: edge counts, final node counts, output row offsets
-    hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
-                       w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
-                       w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), grid_for(g.Rmax, 2048));
-    hipLaunchKernelGGL(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
-                       (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl);
-    AGNES_CHECK_HIP(hipGetLastError());
+    // With the graph option, a shape seen twice in a row is captured once and
+    // then replayed: one graph launch instead of about 25 launches per hop.
+    std::vector<uint64_t> key = chain_key(s, b, g, fanouts);
+    if (s.sampling_graph && !(b.chain && key == b.chain_key) && key == b.last_key)
+        capture_chain(s, b, g, y, fanouts, key);
+    if (s.sampling_graph && b.chain && key == b.chain_key) AGNES_CHECK_HIP(hipGraphLaunch(b.chain, st));
+    else launch_chain(s, b, g, y, fanouts, st);
+    b.last_key = std::move(key);
+    b.cur = L & 1;                    // the list buffers alternate hop by hop
     if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
     // sizes of the outputs travel to pinned host memory; finish reads them
     AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, w.sync.ptr, y.bytes, hipMemcpyDeviceToHost, st));

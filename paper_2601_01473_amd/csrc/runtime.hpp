@@ -125,6 +125,7 @@ struct Workspace {
     DevBuf rs_hist, rs_dtot;          // radix-sort histograms
     DevBuf scan_part;                 // scan partial sums
     DevBuf topo_part;                 // per sampler workgroup: Bck rows it opened
+    DevBuf params;                    // per-call values the sampling kernels read (targets, seed, minibatch base)
     DevBuf blk_flag, blk_off;         // staged tier: flags over the final list and their offsets
     DevBuf unc;                       // staged tier: list entries whose rows are not in the feature cache
     DevBuf need;                      // staged tier: [needed blocks] first list entry, then block ids
@@ -181,6 +182,7 @@ struct Store {
         if (pool_free) (void)hipEventDestroy(pool_free);
     }
     int profile = 0;
+    int sampling_graph = 0;           // 1 = replay the sampling kernels from a captured HIP graph
     int gather_groups = 1 << 22;      // workgroups of the row-copy kernel (upper bound)
     int gather_unroll = 4;            // rows in flight per lane group (4, 8 or 16)
     int gather_nt = 1;                // 1 = non-temporal stores of the gathered rows
@@ -217,7 +219,16 @@ struct Batch {
     PinnedBuf sage_host;
     DevBuf sage_off, sage_a, sage_h[2];
     hipEvent_t sage_ev = nullptr;     // the offsets upload has left sage_host
+    // The sampling kernels of one hyperbatch shape, captured as a HIP graph.
+    // chain_key lists everything the captured launches depend on (shape, store,
+    // buffer addresses); a call with another key runs kernel by kernel and is
+    // captured when the next call repeats its key.
+    hipGraphExec_t chain = nullptr;
+    hipStream_t cap_stream = nullptr; // private stream the chain is captured on (never runs work)
+    std::vector<uint64_t> chain_key, last_key;
     ~Batch() {
+        if (chain) (void)hipGraphExecDestroy(chain);
+        if (cap_stream) (void)hipStreamDestroy(cap_stream);
         if (sampled) (void)hipEventDestroy(sampled);
         if (gathered) (void)hipEventDestroy(gathered);
         if (needed) (void)hipEventDestroy(needed);

@@ -389,3 +389,52 @@ def test_single_minibatch_many_targets(agnes):
     tg = distinct_targets(30000, 1, 7001, 11)
     feat = features(30000, 8, 10)
     run_case(agnes, off, idx, feat, tg, [6, 4], 7, 2, 1024, tag="H1")
+
+
+def _same_outputs(a, b, tag):
+    for key in ("nodes", "layer_sizes", "features"):
+        assert np.array_equal(a[key], b[key]), (tag, key)
+    for key in ("row_ptr", "col"):
+        assert len(a[key]) == len(b[key]), (tag, key)
+        for l, (x, y) in enumerate(zip(a[key], b[key])):
+            assert np.array_equal(x, y), (tag, key, l)
+
+
+def test_sampling_graph_replays_equal_launches(agnes):
+    """The sampling kernels replayed from a captured HIP graph give what they
+    give launched one by one, on every replay: new targets, seeds and minibatch
+    bases each call, torch work and synchronizations between replays, shape
+    changes (a new capture) and growing buffers.  The last replay is also
+    checked against the oracle."""
+    n = 3000
+    off, idx = random_graph(n, 12, seed=21)
+    feat = features(n, 16, 5)
+    one_by_one = agnes.Store(off, idx, feat, 256)
+    one_by_one.set_sampling_graph(False)
+    replayed = agnes.Store(off, idx, feat, 256)
+    replayed.set_sampling_graph(True)
+    shapes = [(4, 64, [5, 3])] * 4 + [(2, 32, [7])] * 3 + [(4, 64, [5, 3])] * 2 + [(8, 128, [5, 3])] * 3
+    b1 = b2 = None
+    side = torch.cuda.Stream()
+    for i, (H, B, fan) in enumerate(shapes):
+        tg = distinct_targets(n, H, B, 100 + i)
+        log("graph replay", i, H, B, fan)
+        t = torch.from_numpy(tg).cuda()
+        b1 = one_by_one.prepare(t, fan, seed=9 + i, mb_base=10 * i, batch=b1)
+        b2 = replayed.prepare(t, fan, seed=9 + i, mb_base=10 * i, batch=b2, stream=side if i % 2 else None)
+        got1, got2 = b1.to_host(), b2.to_host()
+        for j in range(H):
+            _same_outputs(got1[j], got2[j], (i, j))
+        assert b1.stats()["rows"] == b2.stats()["rows"]
+        # unrelated eager work and a synchronization before the next replay
+        x = torch.randn(4096, device="cuda")
+        assert torch.isfinite((x * 2).sum()).item()
+        torch.cuda.synchronize()
+    ref = oracle.Oracle(off, idx).hyperbatch(tg, fan, 9 + i, 10 * i)
+    fb = feature_bytes(feat)
+    for j in range(H):
+        compare_minibatch(got2[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=("graph", j))
+    for b in (b1, b2):
+        b.close()
+    one_by_one.close()
+    replayed.close()
