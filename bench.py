@@ -314,7 +314,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5,
+                    help="untimed steps before the timed ones; raised to depth + 2 so that every batch slot "
+                         "is allocated before timing (the JSON line reports the number run)")
     ap.add_argument("--config", default="c3")
     ap.add_argument("--H", type=int, default=None, help="minibatches per hyperbatch (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
