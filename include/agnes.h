@@ -198,6 +198,29 @@ typedef struct {
 
 agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);   /* waits for the batch */
 
+/* Device memory allocator.  By default the library allocates its device
+ * memory (stores, batches, their scratch space and outputs) with hipMalloc and
+ * frees it with hipFree.  A caller that wants its own allocator to own that
+ * memory (e.g. a framework's caching allocator) installs two callbacks:
+ *   alloc(bytes, user) returns device memory of the current device, aligned
+ *     to 256 bytes, or NULL on failure (the library call then fails with
+ *     AGNES_ERR_NOMEM; a misaligned block is released and AGNES_ERR_INVALID
+ *     returned);
+ *   release(ptr, bytes, user) takes back a block that alloc returned.  The
+ *     library calls it only after every piece of work it enqueued on that
+ *     block's device has completed (it synchronises the device first, as
+ *     hipFree does), so the block may be reused at once.
+ * Both callbacks non-NULL installs them, both NULL restores hipMalloc / hipFree,
+ * anything else is AGNES_ERR_INVALID.  The setting is process-wide and applies
+ * to allocations made after the call; each block is released through the
+ * callback that pairs with the allocator it came from, whatever is installed
+ * by then.  Install it before the library's other calls, not concurrently with
+ * them.  Allocations happen when a store is built and when a batch's buffers
+ * grow (the first hyperbatches of a shape); pinned host memory is not affected. */
+typedef void* (*agnes_device_alloc_fn)(uint64_t bytes, void* user);
+typedef void (*agnes_device_free_fn)(void* ptr, uint64_t bytes, void* user);
+agnes_status agnes_set_device_allocator(agnes_device_alloc_fn alloc, agnes_device_free_fn release, void* user);
+
 /* Store options.
  *   AGNES_OPT_PROFILE: 1 = record HIP events around the phases of every
  *     hyperbatch (reported by agnes_batch_stats), 0 = off (default).

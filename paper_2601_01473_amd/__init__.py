@@ -21,11 +21,43 @@ from ._binding import agnes_batch_finish, agnes_batch_wait, agnes_hyperbatch_beg
 from ._binding import agnes_free, agnes_hyperbatch_prepare, agnes_last_error  # noqa: F401
 from ._binding import agnes_store_info, agnes_store_object_table, agnes_store_set_option  # noqa: F401
 from ._binding import agnes_batch_tier_stats, agnes_build_blocks_staged, agnes_sage_forward  # noqa: F401
-from ._binding import agnes_build_blocks_cached  # noqa: F401
+from ._binding import agnes_build_blocks_cached, agnes_set_device_allocator  # noqa: F401
 
 _FEAT_DTYPES = {np.dtype(np.float32): B.AGNES_FLOAT32, np.dtype(np.float16): B.AGNES_FLOAT16}
 
 _hip = None
+
+# Every callback pair ever installed: a block keeps the release callback of the
+# allocator it came from, so the ctypes objects must outlive every block.
+_installed_callbacks = []
+
+
+def use_torch_allocator(on: bool = True) -> None:
+    """Let torch's caching allocator own the library's device memory (stores,
+    batches, scratch space), or go back to hipMalloc / hipFree.  Blocks are
+    allocated on the current device and stream; the stream is synchronised
+    before a block is used, since the allocator may hand out memory whose last
+    user's work is still pending on it.  Affects allocations made afterwards."""
+    if not on:
+        agnes_set_device_allocator(None, None)
+        return
+
+    def alloc(nbytes, user):
+        try:
+            dev = torch.cuda.current_device()
+            stream = torch.cuda.current_stream(dev)
+            ptr = torch.cuda.caching_allocator_alloc(int(nbytes), dev, stream)
+            stream.synchronize()
+            return ptr
+        except Exception:          # the library reports AGNES_ERR_NOMEM
+            return None
+
+    def release(ptr, nbytes, user):
+        torch.cuda.caching_allocator_delete(ptr)
+
+    cbs = (B.DEVICE_ALLOC_FN(alloc), B.DEVICE_FREE_FN(release))
+    _installed_callbacks.append(cbs)
+    agnes_set_device_allocator(*cbs)
 
 
 def _hiprt():

@@ -26,7 +26,12 @@ AGNES_OPT_SAMPLING_GRAPH = 6
 EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_build_blocks_cached", "agnes_hyperbatch_prepare",
             "agnes_hyperbatch_begin", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
             "agnes_batch_stats", "agnes_batch_tier_stats", "agnes_store_set_option", "agnes_store_info",
-            "agnes_store_object_table", "agnes_sage_forward", "agnes_free", "agnes_last_error"]
+            "agnes_store_object_table", "agnes_sage_forward", "agnes_set_device_allocator", "agnes_free",
+            "agnes_last_error"]
+
+# void* alloc(uint64_t bytes, void* user); void release(void* ptr, uint64_t bytes, void* user)
+DEVICE_ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p)
+DEVICE_FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p)
 
 
 class agnes_csr(ctypes.Structure):
@@ -126,6 +131,8 @@ def lib():
     L.agnes_store_info.argtypes = [vp, ctypes.POINTER(i64)]
     L.agnes_store_object_table.restype = st
     L.agnes_store_object_table.argtypes = [vp, vp, vp]
+    L.agnes_set_device_allocator.restype = st
+    L.agnes_set_device_allocator.argtypes = [DEVICE_ALLOC_FN, DEVICE_FREE_FN, vp]
     L.agnes_free.restype = None
     L.agnes_free.argtypes = [vp]
     L.agnes_last_error.restype = ctypes.c_char_p
@@ -191,6 +198,14 @@ def agnes_hyperbatch_begin(store: int, targets_ptr: int, H: int, B: int, fanouts
                                        fanouts_arr, L, seed, mb_base, ctypes.c_void_p(stream),
                                        ctypes.byref(out)))
     return out.value
+
+
+def agnes_set_device_allocator(alloc, release, user: int | None = None) -> None:
+    """alloc / release: DEVICE_ALLOC_FN / DEVICE_FREE_FN callbacks, or both None
+    (hipMalloc / hipFree).  The caller keeps the callback objects alive."""
+    a = alloc if alloc is not None else DEVICE_ALLOC_FN()
+    r = release if release is not None else DEVICE_FREE_FN()
+    check(lib().agnes_set_device_allocator(a, r, ctypes.c_void_p(user)))
 
 
 def agnes_batch_finish(batch: int, stream: int = 0) -> None:

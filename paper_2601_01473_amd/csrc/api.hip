@@ -10,6 +10,11 @@ namespace agnes {
 
 static thread_local std::string g_last_error;
 
+DeviceAllocator& device_allocator() {
+    static DeviceAllocator a;
+    return a;
+}
+
 void set_last_error(const std::string& msg) { g_last_error = msg; }
 void clear_last_error() { g_last_error.clear(); }
 
@@ -281,6 +286,17 @@ agnes_status agnes_store_object_table(const agnes_store* store, int32_t* first_n
         AGNES_REQUIRE(first_node && last_node, AGNES_ERR_INVALID, "outputs must not be NULL");
         AGNES_CHECK_HIP(hipMemcpy(first_node, s->first_node.ptr, (size_t)s->nblk * 4, hipMemcpyDeviceToHost));
         AGNES_CHECK_HIP(hipMemcpy(last_node, s->last_node.ptr, (size_t)s->nblk * 4, hipMemcpyDeviceToHost));
+    });
+}
+
+agnes_status agnes_set_device_allocator(agnes_device_alloc_fn alloc, agnes_device_free_fn release, void* user) {
+    return guarded([&] {
+        AGNES_REQUIRE((alloc == nullptr) == (release == nullptr), AGNES_ERR_INVALID,
+                      "install both allocator callbacks or neither");
+        DeviceAllocator& a = device_allocator();
+        a.alloc = alloc;
+        a.release = release;
+        a.user = alloc ? user : nullptr;
     });
 }
 

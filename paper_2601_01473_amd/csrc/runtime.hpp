@@ -39,22 +39,64 @@ void clear_last_error();
 
 // ----------------------------------------------------------------- device buffer
 
+// The process-wide device allocator: hipMalloc / hipFree unless the caller
+// installed callbacks (agnes_set_device_allocator).
+struct DeviceAllocator {
+    agnes_device_alloc_fn alloc = nullptr;
+    agnes_device_free_fn release = nullptr;
+    void* user = nullptr;
+};
+DeviceAllocator& device_allocator();
+
 // An owned device allocation that only grows (contents are not preserved).
+// A buffer from the caller's allocator remembers the free callback that pairs
+// with it and its device; before handing the memory back it waits for that
+// device's enqueued work, as hipFree does, since a caching allocator may give
+// the block to its next user at once.
 struct DevBuf {
     void* ptr = nullptr;
     size_t bytes = 0;
+    agnes_device_free_fn free_fn = nullptr;   // null: the memory came from hipMalloc
+    void* free_user = nullptr;
+    int device = 0;
     ~DevBuf() { release(); }
     void release() {
-        if (ptr) (void)hipFree(ptr);
+        if (ptr) {
+            if (free_fn) {
+                int cur = 0;
+                if (hipGetDevice(&cur) == hipSuccess && cur != device) (void)hipSetDevice(device);
+                (void)hipDeviceSynchronize();
+                free_fn(ptr, (uint64_t)bytes, free_user);
+                if (cur != device) (void)hipSetDevice(cur);
+            } else {
+                (void)hipFree(ptr);
+            }
+        }
         ptr = nullptr;
         bytes = 0;
+        free_fn = nullptr;
+        free_user = nullptr;
     }
     // Make room for `need` bytes; returns true when a new allocation was made.
     bool reserve(size_t need) {
         if (need <= bytes && ptr) return false;
         release();
         size_t b = need ? need : 256;
-        AGNES_CHECK_HIP(hipMalloc(&ptr, b));
+        const DeviceAllocator& a = device_allocator();
+        if (a.alloc) {
+            void* p = a.alloc((uint64_t)b, a.user);
+            if (!p) throw Error{AGNES_ERR_NOMEM, "the device allocator returned no memory for " + std::to_string(b) + " bytes"};
+            if ((uintptr_t)p & 255u) {
+                a.release(p, (uint64_t)b, a.user);
+                throw Error{AGNES_ERR_INVALID, "the device allocator must return 256-byte aligned memory"};
+            }
+            AGNES_CHECK_HIP(hipGetDevice(&device));
+            ptr = p;
+            free_fn = a.release;
+            free_user = a.user;
+        } else {
+            AGNES_CHECK_HIP(hipMalloc(&ptr, b));
+        }
         bytes = b;
         return true;
     }

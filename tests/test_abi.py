@@ -128,3 +128,17 @@ def test_view_and_stats_reject_bad_handles(ag):
     assert lib.agnes_store_set_option(None, 1, 1) == 1
     info = (ctypes.c_int64 * 8)()
     assert lib.agnes_store_info(None, info) == 1
+
+
+def test_device_allocator_needs_both_callbacks(ag):
+    """Host-only: the setter checks its arguments and touches no device."""
+    from paper_2601_01473_amd import _binding as B
+    alloc = B.DEVICE_ALLOC_FN(lambda nbytes, user: None)
+    release = B.DEVICE_FREE_FN(lambda ptr, nbytes, user: None)
+    with pytest.raises(B.AgnesError) as e:
+        ag.agnes_set_device_allocator(alloc, None)
+    assert e.value.status == B.AGNES_ERR_INVALID and "both" in str(e.value)
+    with pytest.raises(B.AgnesError):
+        ag.agnes_set_device_allocator(None, release)
+    ag.agnes_set_device_allocator(alloc, release)       # installed ...
+    ag.agnes_set_device_allocator(None, None)           # ... and hipMalloc / hipFree restored

@@ -438,3 +438,44 @@ def test_sampling_graph_replays_equal_launches(agnes):
         b.close()
     one_by_one.close()
     replayed.close()
+
+
+def test_torch_allocator_owns_device_memory(agnes):
+    """With torch's caching allocator installed, the library's device memory
+    is torch's (memory_allocated grows), results stay bit-exact, and every
+    block goes back when the store and batch close.  A store built before the
+    switch keeps freeing through hipFree."""
+    off, idx = random_graph(2000, 10, seed=31)
+    feat = features(2000, 32, 6)
+    tg = distinct_targets(2000, 6, 48, 44)
+    old_store = agnes.Store(off, idx, feat, 512)       # hipMalloc
+    t_dev = torch.from_numpy(tg).cuda()
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    agnes.use_torch_allocator(True)
+    try:
+        store = agnes.Store(off, idx, feat, 512)
+        assert torch.cuda.memory_allocated() > base
+        b = None
+        for rep in range(3):
+            log("torch allocator", rep)
+            b = store.prepare(t_dev, [6, 4], seed=3 + rep, mb_base=rep, batch=b)
+            got = b.to_host()
+            ref = oracle.Oracle(off, idx).hyperbatch(tg, [6, 4], 3 + rep, rep)
+            fb = feature_bytes(feat)
+            for j in range(tg.shape[0]):
+                compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=("torch-alloc", rep, j))
+        # a batch of the hipMalloc store, allocated while torch's allocator is installed
+        b2 = old_store.prepare(t_dev, [6, 4], seed=3, mb_base=0)
+        ref0 = oracle.Oracle(off, idx).hyperbatch(tg, [6, 4], 3, 0)
+        assert b2.to_host()[0]["nodes"].tolist() == ref0[0].nodes.tolist()
+        b.close()
+        b2.close()
+        store.close()
+    finally:
+        agnes.use_torch_allocator(False)
+    import gc
+    gc.collect()
+    torch.cuda.synchronize()
+    assert torch.cuda.memory_allocated() <= base
+    old_store.close()
