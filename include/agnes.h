@@ -198,6 +198,16 @@ typedef struct {
 
 agnes_status agnes_batch_stats(const agnes_batch* batch, agnes_stats* out);   /* waits for the batch */
 
+/* The sampler's random-number generator, Philox4x64-10 (Sec. 3.4(3): every
+ * request's draws come from a counter-based generator keyed by the request),
+ * evaluated by the device code the sampler uses, for checking it against the
+ * generator's published definition.  counters: host [n][4], keys: host [n][2],
+ * out: host [n][4] (the four output words of each pair); n >= 0.  Runs on the
+ * current device and waits for the result.  The sampler's draw i of request
+ * (node v, minibatch m, hop l) is word i % 4 of counter (i / 4, v, m, l) and
+ * key (seed, 0). */
+agnes_status agnes_philox4x64_10(const uint64_t* counters, const uint64_t* keys, int64_t n, uint64_t* out);
+
 /* Device memory allocator.  By default the library allocates its device
  * memory (stores, batches, their scratch space and outputs) with hipMalloc and
  * frees it with hipFree.  A caller that wants its own allocator to own that

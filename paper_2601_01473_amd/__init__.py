@@ -21,7 +21,7 @@ from ._binding import agnes_batch_finish, agnes_batch_wait, agnes_hyperbatch_beg
 from ._binding import agnes_free, agnes_hyperbatch_prepare, agnes_last_error  # noqa: F401
 from ._binding import agnes_store_info, agnes_store_object_table, agnes_store_set_option  # noqa: F401
 from ._binding import agnes_batch_tier_stats, agnes_build_blocks_staged, agnes_sage_forward  # noqa: F401
-from ._binding import agnes_build_blocks_cached, agnes_set_device_allocator  # noqa: F401
+from ._binding import agnes_build_blocks_cached, agnes_philox4x64_10, agnes_set_device_allocator  # noqa: F401
 
 _FEAT_DTYPES = {np.dtype(np.float32): B.AGNES_FLOAT32, np.dtype(np.float16): B.AGNES_FLOAT16}
 

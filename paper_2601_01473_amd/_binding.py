@@ -26,7 +26,7 @@ AGNES_OPT_SAMPLING_GRAPH = 6
 EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_build_blocks_cached", "agnes_hyperbatch_prepare",
             "agnes_hyperbatch_begin", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
             "agnes_batch_stats", "agnes_batch_tier_stats", "agnes_store_set_option", "agnes_store_info",
-            "agnes_store_object_table", "agnes_sage_forward", "agnes_set_device_allocator", "agnes_free",
+            "agnes_store_object_table", "agnes_sage_forward", "agnes_philox4x64_10", "agnes_set_device_allocator", "agnes_free",
             "agnes_last_error"]
 
 # void* alloc(uint64_t bytes, void* user); void release(void* ptr, uint64_t bytes, void* user)
@@ -131,6 +131,8 @@ def lib():
     L.agnes_store_info.argtypes = [vp, ctypes.POINTER(i64)]
     L.agnes_store_object_table.restype = st
     L.agnes_store_object_table.argtypes = [vp, vp, vp]
+    L.agnes_philox4x64_10.restype = st
+    L.agnes_philox4x64_10.argtypes = [vp, vp, i64, vp]
     L.agnes_set_device_allocator.restype = st
     L.agnes_set_device_allocator.argtypes = [DEVICE_ALLOC_FN, DEVICE_FREE_FN, vp]
     L.agnes_free.restype = None
@@ -198,6 +200,18 @@ def agnes_hyperbatch_begin(store: int, targets_ptr: int, H: int, B: int, fanouts
                                        fanouts_arr, L, seed, mb_base, ctypes.c_void_p(stream),
                                        ctypes.byref(out)))
     return out.value
+
+
+def agnes_philox4x64_10(counters, keys):
+    """Device Philox4x64-10 words: counters uint64 [n, 4], keys uint64 [n, 2] -> uint64 [n, 4]."""
+    import numpy as np
+    c = np.ascontiguousarray(counters, dtype=np.uint64).reshape(-1, 4)
+    k = np.ascontiguousarray(keys, dtype=np.uint64).reshape(-1, 2)
+    if len(c) != len(k):
+        raise ValueError("one key pair per counter")
+    out = np.empty_like(c)
+    check(lib().agnes_philox4x64_10(c.ctypes.data, k.ctypes.data, len(c), out.ctypes.data))
+    return out
 
 
 def agnes_set_device_allocator(alloc, release, user: int | None = None) -> None:

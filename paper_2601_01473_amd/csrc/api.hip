@@ -289,6 +289,22 @@ agnes_status agnes_store_object_table(const agnes_store* store, int32_t* first_n
     });
 }
 
+agnes_status agnes_philox4x64_10(const uint64_t* counters, const uint64_t* keys, int64_t n, uint64_t* out) {
+    return guarded([&] {
+        AGNES_REQUIRE(n >= 0 && n <= ((int64_t)1 << 26), AGNES_ERR_INVALID, "n must be in [0, 2^26]");
+        if (n == 0) return;
+        AGNES_REQUIRE(counters && keys && out, AGNES_ERR_INVALID, "counters, keys and out must not be NULL");
+        DevBuf c, k, o;
+        c.reserve((size_t)n * 32);
+        k.reserve((size_t)n * 16);
+        o.reserve((size_t)n * 32);
+        AGNES_CHECK_HIP(hipMemcpy(c.ptr, counters, (size_t)n * 32, hipMemcpyHostToDevice));
+        AGNES_CHECK_HIP(hipMemcpy(k.ptr, keys, (size_t)n * 16, hipMemcpyHostToDevice));
+        philox_words(c.as<uint64_t>(), k.as<uint64_t>(), n, o.as<uint64_t>(), nullptr);
+        AGNES_CHECK_HIP(hipMemcpy(out, o.ptr, (size_t)n * 32, hipMemcpyDeviceToHost));
+    });
+}
+
 agnes_status agnes_set_device_allocator(agnes_device_alloc_fn alloc, agnes_device_free_fn release, void* user) {
     return guarded([&] {
         AGNES_REQUIRE((alloc == nullptr) == (release == nullptr), AGNES_ERR_INVALID,

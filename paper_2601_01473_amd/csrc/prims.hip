@@ -20,6 +20,23 @@ void fill_u32(void* p, uint32_t value, int64_t n, hipStream_t st) {
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
+// ----------------------------------------------------------------- Philox words
+
+// The sampler's generator on given counters and keys ([n][4] and [n][2]), for
+// checking it against the published definition.
+__global__ void k_philox_words(const uint64_t* c, const uint64_t* k, int64_t n, uint64_t* out) {
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) {
+        const Words4 w = philox4x64_10(c[4 * i], c[4 * i + 1], c[4 * i + 2], c[4 * i + 3], k[2 * i], k[2 * i + 1]);
+        for (int q = 0; q < 4; q++) out[4 * i + q] = w.w[q];
+    }
+}
+
+void philox_words(const uint64_t* c, const uint64_t* k, int64_t n, uint64_t* out, hipStream_t st) {
+    if (n <= 0) return;
+    hipLaunchKernelGGL(k_philox_words, dim3(grid_for(n, 1024)), dim3(kBlock), 0, st, c, k, n, out);
+    AGNES_CHECK_HIP(hipGetLastError());
+}
+
 // ----------------------------------------------------------------- scan
 
 constexpr int kScanGroups = 1024;   // partial sums per scan

@@ -321,6 +321,9 @@ int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint3
 int64_t radix_hist_entries(int64_t n_max);
 int64_t radix_dtot_entries();
 
+// Philox4x64-10 words of n (counter [4], key [2]) pairs, device arrays (prims.hip).
+void philox_words(const uint64_t* counters, const uint64_t* keys, int64_t n, uint64_t* out, hipStream_t st);
+
 // Fill n 32-bit words with a value (a kernel, so that it can be captured in a graph).
 void fill_u32(void* p, uint32_t value, int64_t n, hipStream_t st);
 
