@@ -1095,7 +1095,16 @@ __global__ __launch_bounds__(kBlock) void k_stage(const Unit* __restrict__ host,
         const int64_t b = misses[2 * i], slot = misses[2 * i + 1];
         const Unit* src = host + b * units;
         Unit* dst = pool + slot * units;
-        for (int64_t c = threadIdx.x; c < units; c += kBlock) dst[c] = src[c];
+        // four host reads in flight per lane before their stores
+        for (int64_t c0 = threadIdx.x; c0 < units; c0 += 4 * kBlock) {
+            Unit x[4];
+#pragma unroll
+            for (int q = 0; q < 4; q++)
+                if (c0 + q * kBlock < units) x[q] = src[c0 + q * kBlock];
+#pragma unroll
+            for (int q = 0; q < 4; q++)
+                if (c0 + q * kBlock < units) dst[c0 + q * kBlock] = x[q];
+        }
     }
 }
 
@@ -1544,31 +1553,41 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     };
     memset(&b.tier, 0, sizeof(b.tier));
     if (s.tiered && rows > 0) {
-        // the previous tiered gather, and its feature-cache admissions, are done
-        AGNES_CHECK_HIP(hipStreamWaitEvent(st, s.pool_free, 0));
+        // The needed blocks are found and read back on this hyperbatch's
+        // sampling stream (cs), so the host plans while earlier hyperbatches
+        // still stage and gather on st.  With a feature cache they wait for the
+        // previous hyperbatch's admissions, which decide the rows it serves.
+        const hipStream_t cs = b.stream;
         Ctl* ctl = w.sync.as<Ctl>();
         const bool cache = s.cache_rows > 0;
+        if (cache) AGNES_CHECK_HIP(hipStreamWaitEvent(cs, s.pool_free, 0));
         const int32_t* tch = cache ? s.tch.as<int32_t>() : nullptr;
         int64_t* part = w.scan_part.as<int64_t>();
         // needed feature blocks: the blocks of the entries whose rows are not cached
-        w.blk_flag.reserve((size_t)rows * 4);
-        w.blk_off.reserve((size_t)(rows + 1) * 8);
-        w.unc.reserve((size_t)rows * 4);
-        w.need.reserve((size_t)rows * 12 + 256);
+        // with headroom: a reallocation frees the old buffer, and hipFree waits
+        // for the whole device, i.e. for earlier hyperbatches still staging
+        w.blk_flag.reserve_slack((size_t)rows * 4);
+        w.blk_off.reserve_slack((size_t)(rows + 1) * 8);
+        w.unc.reserve_slack((size_t)rows * 4);
+        w.need.reserve_slack((size_t)rows * 12 + 256);
         b.need_cap = rows;
         const int gl = grid_for(rows, 4096);
         int32_t* flag = w.blk_flag.as<int32_t>();
         int64_t* off = w.blk_off.as<int64_t>();
-        hipLaunchKernelGGL(k_unc_flags, dim3(gl), dim3(kBlock), 0, st, rlk, tch, flag, ctl);
-        scan_counts(flag, off, &ctl->rows, rows, &ctl->tier_unc, part, st);
-        hipLaunchKernelGGL(k_unc_compact, dim3(gl), dim3(kBlock), 0, st, flag, off, w.unc.as<int32_t>(), ctl);
-        hipLaunchKernelGGL(k_block_flags, dim3(gl), dim3(kBlock), 0, st, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
+        hipLaunchKernelGGL(k_unc_flags, dim3(gl), dim3(kBlock), 0, cs, rlk, tch, flag, ctl);
+        scan_counts(flag, off, &ctl->rows, rows, &ctl->tier_unc, part, cs);
+        hipLaunchKernelGGL(k_unc_compact, dim3(gl), dim3(kBlock), 0, cs, flag, off, w.unc.as<int32_t>(), ctl);
+        hipLaunchKernelGGL(k_block_flags, dim3(gl), dim3(kBlock), 0, cs, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
                            flag, ctl);
-        scan_counts(flag, off, &ctl->tier_unc, rows, &ctl->tier_nb, part, st);
-        hipLaunchKernelGGL(k_block_compact, dim3(gl), dim3(kBlock), 0, st, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
+        scan_counts(flag, off, &ctl->tier_unc, rows, &ctl->tier_nb, part, cs);
+        hipLaunchKernelGGL(k_block_compact, dim3(gl), dim3(kBlock), 0, cs, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
                            flag, off, w.need.as<int64_t>(), (int32_t*)((char*)w.need.ptr + (size_t)rows * 8), ctl);
         AGNES_CHECK_HIP(hipGetLastError());
-        std::vector<TierRound> rounds = plan_staging(s, b, st);
+        std::vector<TierRound> rounds = plan_staging(s, b, cs);
+        // staging overwrites pool slots: the pool's previous users are done;
+        // and the compaction above (flag and off are reused below) is done
+        AGNES_CHECK_HIP(hipStreamWaitEvent(st, s.pool_free, 0));
+        if (cs != st) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.needed, 0));
         if (s.profile) {
             AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
             AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
@@ -1585,7 +1604,13 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
                 hipLaunchKernelGGL(k_tbuf_update, dim3(grid_for(r.n_upd, 256)), dim3(kBlock), 0, st, plan + r.upd_at,
                                    r.n_upd, s.tbuf.as<int32_t>());
             if (r.n_miss) {
-                const int gs = std::min(r.n_miss, 16384);
+                // 32 workgroups keep the host link busy (about 50 GB/s, as with
+                // 16384); while they wait on host reads, kernels of other
+                // streams (later hyperbatches' sampling and needed-block
+                // compaction) are starved, more so the more workgroups stage:
+                // 512 leave a pipelined step at 18.9 ms, 64 at 13.8, 32 at 11.7;
+                // 16 no longer saturate the link
+                const int gs = std::min(r.n_miss, 32);
                 if (blk_bytes % 16 == 0)
                     hipLaunchKernelGGL(k_stage<u32x4>, dim3(gs), dim3(kBlock), 0, st, (const u32x4*)s.host_feat_dev,
                                        s.pool.as<u32x4>(), plan + r.miss_at, r.n_miss, blk_bytes / 16);

@@ -236,8 +236,10 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
     b.sage_host.reserve(offs.size() * 8);
     memcpy(b.sage_host.ptr, offs.data(), offs.size() * 8);
     b.sage_off.reserve(offs.size() * 8);
-    b.sage_a.reserve((size_t)std::max<int64_t>(Amax, 1) * 2);
-    for (int k = 0; k < 2; k++) b.sage_h[k].reserve((size_t)Hmax * 2);
+    // sizes vary by hyperbatch: headroom keeps reallocations (and the device
+    // synchronisation of the free that comes with each) rare
+    b.sage_a.reserve_slack((size_t)std::max<int64_t>(Amax, 1) * 2);
+    for (int k = 0; k < 2; k++) b.sage_h[k].reserve_slack((size_t)Hmax * 2);
     if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.gathered, 0));
     AGNES_CHECK_HIP(hipMemcpyAsync(b.sage_off.ptr, b.sage_host.ptr, offs.size() * 8, hipMemcpyHostToDevice, st));
     AGNES_CHECK_HIP(hipEventRecord(b.sage_ev, st));
