@@ -2,6 +2,8 @@
 // (key, value) pairs.  Element counts are read from device memory, so a launch
 // sequence never waits for the host to learn a size; the host only supplies an
 // upper bound for the buffers.
+#include <algorithm>
+
 #include "device.hpp"
 #include "runtime.hpp"
 
@@ -161,34 +163,36 @@ void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_
 
 // ----------------------------------------------------------------- radix sort
 
-// LSD radix sort of 32-bit keys with 32-bit values, 8-bit digits, tiles of
-// 256 x ITEMS keys (2048 for sorts of at most 2M keys, where more and shorter
-// workgroups hide latency better; 4096 above, for longer runs per digit).
-// Per pass: (1) digit histogram of every tile, stored tile-major
-// (each tile writes its 256 counts contiguously), (2) per digit, an exclusive
-// scan over the tiles (the table is small and stays in L2), (3) each tile ranks
-// its keys stably, reorders them by digit in LDS and writes every digit's run
-// contiguously.
+// LSD radix sort of 32-bit keys with 32-bit values, tiles of 256 x ITEMS keys
+// (2048 for sorts of at most 2M keys, where more and shorter workgroups hide
+// latency better; 4096 above, for longer runs per digit).  Digits are RB = 8,
+// 9 or 10 bits, the fewest passes that cover the key bits with digits of at
+// most 10 bits: 20-bit keys take two passes of 10, 26-bit keys three of 9,
+// 23-bit keys three of 8.  Per pass: (1) digit histogram of every tile, stored
+// tile-major (each tile writes its counts contiguously), (2) per digit, an
+// exclusive scan over the tiles (the table is small and stays in L2), (3) each
+// tile ranks its keys stably, reorders them by digit in LDS and writes every
+// digit's run contiguously.
 constexpr int64_t kSmallSort = 1 << 21;
 static int sort_items(int64_t n_max) { return n_max <= kSmallSort ? 8 : 16; }
-constexpr int kRadixBits = 8;
-constexpr int kRadixBins = 1 << kRadixBits;
+constexpr int kMaxRadixBits = 10;
 
 int64_t radix_tiles(int64_t n_max) {
     const int64_t tile = (int64_t)kBlock * sort_items(n_max);
     return (n_max + tile - 1) / tile + 1;
 }
-int64_t radix_hist_entries(int64_t n_max) { return (int64_t)kRadixBins * radix_tiles(n_max); }
-int64_t radix_dtot_entries() { return kRadixBins; }
+int64_t radix_hist_entries(int64_t n_max) { return ((int64_t)1 << kMaxRadixBits) * radix_tiles(n_max); }
+int64_t radix_dtot_entries() { return (int64_t)1 << kMaxRadixBits; }
 
-template <int ITEMS>
+template <int ITEMS, int RB>
 __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const int64_t* n_dev, int shift,
                                                     uint32_t* hist) {
-    __shared__ uint32_t h[kRadixBins];
+    constexpr int BINS = 1 << RB;
+    __shared__ uint32_t h[BINS];
     const int64_t n = *n_dev;
     const int64_t t0 = (int64_t)blockIdx.x * (kBlock * ITEMS);
     if (t0 >= n) return;                        // tiles past the end are not scanned
-    h[threadIdx.x] = 0;
+    for (int d = threadIdx.x; d < BINS; d += kBlock) h[d] = 0;
     uint32_t k[ITEMS];
 #pragma unroll
     for (int q = 0; q < ITEMS; q++) {
@@ -198,15 +202,16 @@ __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const 
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < ITEMS; q++)
-        if (t0 + q * kBlock + threadIdx.x < n) atomicAdd(&h[(k[q] >> shift) & (kRadixBins - 1)], 1u);
+        if (t0 + q * kBlock + threadIdx.x < n) atomicAdd(&h[(k[q] >> shift) & (BINS - 1)], 1u);
     __syncthreads();
-    hist[(int64_t)blockIdx.x * kRadixBins + threadIdx.x] = h[threadIdx.x];
+    for (int d = threadIdx.x; d < BINS; d += kBlock) hist[(int64_t)blockIdx.x * BINS + d] = h[d];
 }
 
 // One workgroup per digit: exclusive scan over the tiles that hold keys of
 // column d of the tile-major table (in place), digit total.
-template <int ITEMS>
+template <int ITEMS, int RB>
 __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_t* n_dev, uint32_t* dtot) {
+    constexpr int BINS = 1 << RB;
     __shared__ uint32_t lds[kWavesPerBlock];
     const int d = blockIdx.x;
     const int tiles = (int)((*n_dev + (kBlock * ITEMS) - 1) / (kBlock * ITEMS));
@@ -217,7 +222,7 @@ __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_
 #pragma unroll
         for (int k = 0; k < 4; k++) {
             const int i = b0 + threadIdx.x * 4 + k;
-            v[k] = i < tiles ? hist[(int64_t)i * kRadixBins + d] : 0u;
+            v[k] = i < tiles ? hist[(int64_t)i * BINS + d] : 0u;
             local += v[k];
         }
         uint32_t total;
@@ -225,7 +230,7 @@ __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_
 #pragma unroll
         for (int k = 0; k < 4; k++) {
             const int i = b0 + threadIdx.x * 4 + k;
-            if (i < tiles) hist[(int64_t)i * kRadixBins + d] = ex;
+            if (i < tiles) hist[(int64_t)i * BINS + d] = ex;
             ex += v[k];
         }
         carry += total;
@@ -235,14 +240,18 @@ __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_
 
 // Wave w ranks a quarter of the tile's keys in ITEMS rounds of 64; ranks
 // inside a round follow lane order (ballot match), rounds follow each other, and
-// waves follow each other, so equal digits keep their input order.
-template <int ITEMS>
+// waves follow each other, so equal digits keep their input order.  Thread t
+// owns digits [t Q, (t + 1) Q), Q = BINS / 256, in the per-digit scans.
+template <int ITEMS, int RB>
 __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, const uint32_t* vin,
                                                        uint32_t* kout, uint32_t* vout, const int64_t* n_dev,
                                                        int shift, const uint32_t* hist, const uint32_t* dtot) {
-    __shared__ uint32_t wcnt[kWavesPerBlock][kRadixBins];
-    __shared__ uint32_t lbase[kRadixBins];
-    __shared__ uint32_t gbase[kRadixBins];
+    constexpr int BINS = 1 << RB;
+    constexpr int Q = BINS / kBlock;
+    static_assert(Q >= 1 && Q * kBlock == BINS, "at least one digit per thread");
+    __shared__ uint32_t wcnt[kWavesPerBlock][BINS];
+    __shared__ uint32_t lbase[BINS];
+    __shared__ uint32_t gbase[BINS];
     __shared__ uint32_t lds[kWavesPerBlock];
     __shared__ uint32_t sk[kBlock * ITEMS];
     __shared__ uint32_t sv[kBlock * ITEMS];
@@ -250,11 +259,22 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     const int64_t t0 = (int64_t)blockIdx.x * (kBlock * ITEMS);
     if (t0 >= n) return;
     const int t = threadIdx.x, w = wave_id(), lane = lane_id();
-    for (int x = t; x < kWavesPerBlock * kRadixBins; x += kBlock) (&wcnt[0][0])[x] = 0;
+    for (int x = t; x < kWavesPerBlock * BINS; x += kBlock) (&wcnt[0][0])[x] = 0;
     {
+        uint32_t dt[Q], sum = 0;
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+            dt[q] = dtot[t * Q + q];
+            sum += dt[q];
+        }
         uint32_t tot;
-        uint32_t ex = block_exclusive_scan(dtot[t], lds, tot);
-        gbase[t] = ex + hist[(int64_t)blockIdx.x * kRadixBins + t];
+        uint32_t ex = block_exclusive_scan(sum, lds, tot);
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+            const int d = t * Q + q;
+            gbase[d] = ex + hist[(int64_t)blockIdx.x * BINS + d];
+            ex += dt[q];
+        }
     }
     __syncthreads();
     uint32_t key[ITEMS], val[ITEMS], rnk[ITEMS];
@@ -268,10 +288,10 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     for (int r = 0; r < ITEMS; r++) {
         int64_t i = t0 + w * (ITEMS * kWave) + r * kWave + lane;
         bool valid = i < n;
-        int d = valid ? (int)((key[r] >> shift) & (kRadixBins - 1)) : -1;
+        int d = valid ? (int)((key[r] >> shift) & (BINS - 1)) : -1;
         uint64_t peers = __ballot(valid);
 #pragma unroll
-        for (int b = 0; b < kRadixBits; b++) {
+        for (int b = 0; b < RB; b++) {
             uint64_t m = __ballot((d >> b) & 1);
             peers &= ((d >> b) & 1) ? m : ~m;
         }
@@ -286,22 +306,34 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
         rnk[r] = old + rank;
     }
     __syncthreads();
-    // per digit (thread t = digit t): wave prefixes and the tile's digit offsets
+    // per digit: wave prefixes and the tile's digit offsets
     {
-        uint32_t c0 = wcnt[0][t], c1 = wcnt[1][t], c2 = wcnt[2][t], c3 = wcnt[3][t];
+        uint32_t c[Q][kWavesPerBlock], sum = 0;
+#pragma unroll
+        for (int q = 0; q < Q; q++)
+#pragma unroll
+            for (int x = 0; x < kWavesPerBlock; x++) {
+                c[q][x] = wcnt[x][t * Q + q];
+                sum += c[q][x];
+            }
         uint32_t tot;
-        uint32_t ex = block_exclusive_scan(c0 + c1 + c2 + c3, lds, tot);
-        lbase[t] = ex;
-        wcnt[0][t] = ex;
-        wcnt[1][t] = ex + c0;
-        wcnt[2][t] = ex + c0 + c1;
-        wcnt[3][t] = ex + c0 + c1 + c2;
+        uint32_t ex = block_exclusive_scan(sum, lds, tot);
+#pragma unroll
+        for (int q = 0; q < Q; q++) {
+            const int d = t * Q + q;
+            lbase[d] = ex;
+#pragma unroll
+            for (int x = 0; x < kWavesPerBlock; x++) {
+                wcnt[x][d] = ex;
+                ex += c[q][x];
+            }
+        }
     }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < ITEMS; r++) {
         if (t0 + w * (ITEMS * kWave) + r * kWave + lane < n) {
-            uint32_t pos = wcnt[w][(key[r] >> shift) & (kRadixBins - 1)] + rnk[r];
+            uint32_t pos = wcnt[w][(key[r] >> shift) & (BINS - 1)] + rnk[r];
             sk[pos] = key[r];
             sv[pos] = val[r];
         }
@@ -310,41 +342,56 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     const int cnt = (int)((n - t0) < (kBlock * ITEMS) ? (n - t0) : (kBlock * ITEMS));
     for (int i = t; i < cnt; i += kBlock) {
         uint32_t k = sk[i];
-        int d = (int)((k >> shift) & (kRadixBins - 1));
+        int d = (int)((k >> shift) & (BINS - 1));
         uint32_t dst = gbase[d] + (uint32_t)i - lbase[d];
         kout[dst] = k;
         vout[dst] = sv[i];
     }
 }
 
-template <int ITEMS>
+template <int ITEMS, int RB>
 static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                          const int64_t* n_dev, int tiles, int passes, uint32_t* hist, uint32_t* dtot,
                          hipStream_t st, bool vals_iota) {
     uint32_t *ka = keys, *kb = keys_tmp;
     uint32_t *va = vals, *vb = vals_tmp;
     for (int p = 0; p < passes; p++) {
-        int shift = p * kRadixBits;
+        int shift = p * RB;
         const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
-        hipLaunchKernelGGL(k_rs_hist<ITEMS>, dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, hist);
-        hipLaunchKernelGGL(k_rs_scan<ITEMS>, dim3(kRadixBins), dim3(kBlock), 0, st, hist, n_dev, dtot);
-        hipLaunchKernelGGL(k_rs_scatter<ITEMS>, dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev, shift,
-                           hist, dtot);
+        hipLaunchKernelGGL((k_rs_hist<ITEMS, RB>), dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, hist);
+        hipLaunchKernelGGL((k_rs_scan<ITEMS, RB>), dim3(1 << RB), dim3(kBlock), 0, st, hist, n_dev, dtot);
+        hipLaunchKernelGGL((k_rs_scatter<ITEMS, RB>), dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev,
+                           shift, hist, dtot);
         uint32_t* tk = ka; ka = kb; kb = tk;
         uint32_t* tv = va; va = vb; vb = tv;
     }
+}
+
+template <int ITEMS>
+static void radix_passes_rb(int rb, uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
+                            const int64_t* n_dev, int tiles, int passes, uint32_t* hist, uint32_t* dtot,
+                            hipStream_t st, bool vals_iota) {
+    if (rb == 8)
+        radix_passes<ITEMS, 8>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+    else if (rb == 9)
+        radix_passes<ITEMS, 9>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+    else
+        radix_passes<ITEMS, 10>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
 }
 
 int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                        const int64_t* n_dev, int64_t n_max, int bits, uint32_t* hist,
                        uint32_t* dtot, hipStream_t st, bool vals_iota) {
     if (bits < 1) bits = 1;
-    const int passes = (bits + kRadixBits - 1) / kRadixBits;
+    // the fewest passes with digits of at most 10 bits, then the narrowest
+    // digit (at least 8 bits) that covers the key in that many passes
+    const int passes = (bits + kMaxRadixBits - 1) / kMaxRadixBits;
+    const int rb = std::max(8, (bits + passes - 1) / passes);
     const int tiles = (int)radix_tiles(n_max);
     if (sort_items(n_max) == 8)
-        radix_passes<8>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+        radix_passes_rb<8>(rb, keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
     else
-        radix_passes<16>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+        radix_passes_rb<16>(rb, keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
     AGNES_CHECK_HIP(hipGetLastError());
     return passes & 1;   // 1: the sorted pairs are in keys_tmp / vals_tmp
 }

@@ -310,7 +310,8 @@ void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_
 int64_t scan_partials_needed();
 
 // Stable LSD radix sort of 32-bit keys with 32-bit values on key bits
-// [0, bits), 8 bits per pass; n read from *n_dev (at most n_max).  With
+// [0, bits), in the fewest passes of 8-10-bit digits; n read from *n_dev (at
+// most n_max).  With
 // vals_iota the input values are 0, 1, 2, ... (vals is then only an output
 // buffer).  hist needs radix_hist_entries(n_max) entries, dtot
 // radix_dtot_entries().  Returns 0 when the result is in keys/vals and 1 when it
