@@ -283,6 +283,10 @@ agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_
  * identical to a store with HBM-resident features.
  * Hyperbatches of one store are gathered one at a time in the order their
  * finish calls are made (each waits for the previous gather on any stream).
+ * agnes_batch_finish finds the needed blocks on the batch's begin stream and
+ * waits on the host only for them, so the host plans a hyperbatch's rounds
+ * while earlier hyperbatches still stage and gather (with a feature cache, the
+ * search also waits for the previous hyperbatch's admissions).
  * Errors: as agnes_build_blocks; pool_blocks < 1 -> AGNES_ERR_INVALID. */
 agnes_status agnes_build_blocks_staged(const agnes_csr* csr, const agnes_features* feat,
                                        uint64_t block_bytes, int64_t pool_blocks, void* hip_stream,
