@@ -479,3 +479,68 @@ def test_torch_allocator_owns_device_memory(agnes):
     torch.cuda.synchronize()
     assert torch.cuda.memory_allocated() <= base
     old_store.close()
+
+
+def test_argument_limits_are_rejected_and_store_stays_usable(agnes):
+    from paper_2601_01473_amd import _binding as B
+    off, idx = random_graph(300, 6, seed=61)
+    feat = features(300, 8, 2)
+    store = agnes.Store(off, idx, feat, 256)
+    good = distinct_targets(300, 2, 8, 3)
+    cases = [
+        (np.zeros((0, 8), np.int32), [3]),            # H = 0
+        (np.zeros((2, 0), np.int32), [3]),            # B = 0
+        (good, []),                                   # L = 0
+        (good, [1] * 9),                              # L = 9
+        (good, [-1]),                                 # negative fanout
+        (good, [1025]),                               # fanout above 1024
+    ]
+    for tg, fan in cases:
+        log("limit", tg.shape, fan)
+        t = torch.from_numpy(np.ascontiguousarray(tg)).cuda() if tg.size else torch.zeros(tg.shape, dtype=torch.int32, device="cuda")
+        with pytest.raises((B.AgnesError, ValueError)) as e:
+            store.prepare(t, fan, seed=0)
+        if isinstance(e.value, B.AgnesError):
+            assert e.value.status == B.AGNES_ERR_INVALID, (tg.shape, fan, str(e.value))
+    with pytest.raises(B.AgnesError) as e:
+        store.prepare(torch.from_numpy(good).cuda(), [3], seed=0, mb_base=-1)
+    assert e.value.status == B.AGNES_ERR_INVALID
+    # H above 4096
+    big = np.arange(300, dtype=np.int32)[np.arange(4097) % 300].reshape(4097, 1)
+    with pytest.raises(B.AgnesError) as e:
+        store.prepare(torch.from_numpy(big).cuda(), [1], seed=0)
+    assert e.value.status == B.AGNES_ERR_INVALID
+    b = store.prepare(torch.from_numpy(good).cuda(), [3, 2], seed=4)
+    ref = oracle.Oracle(off, idx).hyperbatch(good, [3, 2], 4, 0)
+    got = b.to_host()
+    for j in range(good.shape[0]):
+        compare_minibatch(got[j], ref[j], oracle.gather(feature_bytes(feat), ref[j].nodes), tag=("after limits", j))
+    b.close()
+    store.close()
+
+
+def test_largest_fanout_against_a_hub(agnes):
+    """Fanout 1024 (the largest accepted) where a hub has 3000 neighbours, so
+    Floyd draws 1024 of 3000 positions in the sampler's staged-position path."""
+    n = 4000
+    rng = np.random.default_rng(71)
+    rows = [np.sort(rng.choice(np.arange(1, n), size=3000, replace=False)).astype(np.int32)]
+    for v in range(1, n):
+        k = int(rng.integers(0, 12))
+        cand = np.delete(np.arange(n), v)
+        rows.append(np.sort(rng.choice(cand, size=k, replace=False)).astype(np.int32))
+    off = np.zeros(n + 1, np.int64)
+    off[1:] = np.cumsum([len(r) for r in rows])
+    idx = np.concatenate(rows).astype(np.int32)
+    feat = features(n, 8, 3)
+    tg = np.array([[0, 5, 17, 900], [0, 2, 3, 4]], np.int32)
+    run_case(agnes, off, idx, feat, tg, [1024], 9, 2, 4096, tag="fanout 1024")
+
+
+def test_eight_hops(agnes):
+    """The largest hop count: eight hops of small fanouts, frontiers capped by
+    the graph's size."""
+    off, idx = random_graph(600, 5, seed=81)
+    feat = features(600, 4, 5)
+    tg = distinct_targets(600, 3, 4, 8)
+    run_case(agnes, off, idx, feat, tg, [2, 2, 1, 2, 1, 1, 2, 1], 13, 3, 256, tag="eight hops")
