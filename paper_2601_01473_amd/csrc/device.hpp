@@ -11,6 +11,7 @@ namespace agnes {
 constexpr int kWave = 64;
 constexpr int kBlock = 256;                 // threads per workgroup
 constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kXcds = 8;                    // accelerator dies of the chip; workgroups are dealt to them in turn
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 __device__ __forceinline__ int wave_id() { return threadIdx.x / kWave; }

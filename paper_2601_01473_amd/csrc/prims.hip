@@ -208,12 +208,16 @@ __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const 
 }
 
 // One workgroup per digit: exclusive scan over the tiles that hold keys of
-// column d of the tile-major table (in place), digit total.
+// column d of the tile-major table (in place), digit total.  Neighbouring
+// digits share cache lines of the table, and workgroups are dealt to the 8
+// XCDs (each with its own L2) in turn, so XCD x is given the contiguous digits
+// [x BINS / 8, (x + 1) BINS / 8): a line is then read into one L2, not eight.
 template <int ITEMS, int RB>
 __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_t* n_dev, uint32_t* dtot) {
     constexpr int BINS = 1 << RB;
+    static_assert(BINS % kXcds == 0, "digits split evenly over the XCDs");
     __shared__ uint32_t lds[kWavesPerBlock];
-    const int d = blockIdx.x;
+    const int d = (int)(blockIdx.x % kXcds) * (BINS / kXcds) + (int)(blockIdx.x / kXcds);
     const int tiles = (int)((*n_dev + (kBlock * ITEMS) - 1) / (kBlock * ITEMS));
     uint32_t carry = 0;
     for (int b0 = 0; b0 < tiles; b0 += kBlock * 4) {
