@@ -246,6 +246,11 @@ __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_
 // inside a round follow lane order (ballot match), rounds follow each other, and
 // waves follow each other, so equal digits keep their input order.  Thread t
 // owns digits [t Q, (t + 1) Q), Q = BINS / 256, in the per-digit scans.
+// Consecutive tiles write consecutive pieces of every digit's run, so their
+// partial cache lines are shared; workgroups are dealt to the XCDs in turn, so
+// XCD x takes the contiguous tiles [x per, (x + 1) per), per = ceil(tiles / 8),
+// and those lines fill up in one L2.  The grid is a multiple of 8 workgroups
+// covering 8 ceil(max tiles / 8) (scatter_grid).
 template <int ITEMS, int RB>
 __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, const uint32_t* vin,
                                                        uint32_t* kout, uint32_t* vout, const int64_t* n_dev,
@@ -260,8 +265,12 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     __shared__ uint32_t sk[kBlock * ITEMS];
     __shared__ uint32_t sv[kBlock * ITEMS];
     const int64_t n = *n_dev;
-    const int64_t t0 = (int64_t)blockIdx.x * (kBlock * ITEMS);
-    if (t0 >= n) return;
+    const int64_t tiles = (n + kBlock * ITEMS - 1) / (kBlock * ITEMS);
+    const int64_t per = (tiles + kXcds - 1) / kXcds;
+    const int64_t local = blockIdx.x / kXcds;
+    const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per + local;
+    if (local >= per || tile >= tiles) return;
+    const int64_t t0 = tile * (kBlock * ITEMS);
     const int t = threadIdx.x, w = wave_id(), lane = lane_id();
     for (int x = t; x < kWavesPerBlock * BINS; x += kBlock) (&wcnt[0][0])[x] = 0;
     {
@@ -276,7 +285,7 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
 #pragma unroll
         for (int q = 0; q < Q; q++) {
             const int d = t * Q + q;
-            gbase[d] = ex + hist[(int64_t)blockIdx.x * BINS + d];
+            gbase[d] = ex + hist[tile * BINS + d];
             ex += dt[q];
         }
     }
@@ -353,6 +362,10 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     }
 }
 
+// Workgroups of k_rs_scatter for at most `tiles` tiles: 8 ceil(tiles / 8), so
+// that every XCD's contiguous range of tiles has a workgroup for each tile.
+static int scatter_grid(int tiles) { return (tiles + kXcds - 1) / kXcds * kXcds; }
+
 template <int ITEMS, int RB>
 static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                          const int64_t* n_dev, int tiles, int passes, uint32_t* hist, uint32_t* dtot,
@@ -364,8 +377,8 @@ static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uin
         const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
         hipLaunchKernelGGL((k_rs_hist<ITEMS, RB>), dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, hist);
         hipLaunchKernelGGL((k_rs_scan<ITEMS, RB>), dim3(1 << RB), dim3(kBlock), 0, st, hist, n_dev, dtot);
-        hipLaunchKernelGGL((k_rs_scatter<ITEMS, RB>), dim3(tiles), dim3(kBlock), 0, st, ka, vin, kb, vb, n_dev,
-                           shift, hist, dtot);
+        hipLaunchKernelGGL((k_rs_scatter<ITEMS, RB>), dim3(scatter_grid(tiles)), dim3(kBlock), 0, st, ka, vin, kb,
+                           vb, n_dev, shift, hist, dtot);
         uint32_t* tk = ka; ka = kb; kb = tk;
         uint32_t* tv = va; va = vb; vb = tv;
     }
