@@ -1197,9 +1197,12 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     else if (f <= 32) AGNES_SAMPLE(32);
     else AGNES_SAMPLE(0);
 #undef AGNES_SAMPLE
-    // sampled neighbours sorted by node id; values = edge numbers (stable: minibatch order kept)
+    // sampled neighbours sorted by node id; values = edge numbers (stable: minibatch order kept).
+    // This hop's own bound sizes the sort's tiles and grid (hop 0 samples far
+    // fewer edges than the last hop).
+    const int64_t s_max = std::max<int64_t>(1, std::min<int64_t>(g.Smax, (int64_t)g.H * g.cap[l] * f));
     int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
-                                    w.sval2.as<uint32_t>(), &ctl->S, g.Smax, s.node_bits,
+                                    w.sval2.as<uint32_t>(), &ctl->S, s_max, s.node_bits,
                                     w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
     const uint32_t* su = in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>();
     const uint32_t* se = in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>();

@@ -177,11 +177,19 @@ constexpr int64_t kSmallSort = 1 << 21;
 static int sort_items(int64_t n_max) { return n_max <= kSmallSort ? 8 : 16; }
 constexpr int kMaxRadixBits = 10;
 
+// Tiles rounded up to a multiple of the XCD count (the scatter's grid).
+static int64_t scatter_grid_tiles(int64_t tiles) { return (tiles + kXcds - 1) / kXcds * kXcds; }
+
 int64_t radix_tiles(int64_t n_max) {
     const int64_t tile = (int64_t)kBlock * sort_items(n_max);
     return (n_max + tile - 1) / tile + 1;
 }
-int64_t radix_hist_entries(int64_t n_max) { return ((int64_t)1 << kMaxRadixBits) * radix_tiles(n_max); }
+// Histogram entries for any sort of at most n_max keys: tiles are shorter up
+// to kSmallSort keys, so a smaller sort can need more tiles than a larger one.
+int64_t radix_hist_entries(int64_t n_max) {
+    const int64_t tiles = std::max(radix_tiles(std::min(n_max, kSmallSort)), radix_tiles(n_max));
+    return ((int64_t)1 << kMaxRadixBits) * scatter_grid_tiles(tiles);
+}
 int64_t radix_dtot_entries() { return (int64_t)1 << kMaxRadixBits; }
 
 template <int ITEMS, int RB>
