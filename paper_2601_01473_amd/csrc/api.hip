@@ -118,8 +118,8 @@ static void release_batch(Batch* b) {
     if (b && b->magic == kBatchMagic) {
         if (b->state == kSampled || b->state == kGathering) {
             // let enqueued work finish before the memory goes away
-            if (b->state == kSampled && b->sampled) (void)hipEventSynchronize(b->sampled);
-            if (b->state == kGathering && b->gathered) (void)hipEventSynchronize(b->gathered);
+            if (b->state == kSampled && b->sampled_at) (void)hipEventSynchronize(b->sampled_at);
+            if (b->state == kGathering && b->gathered_at) (void)hipEventSynchronize(b->gathered_at);
         }
         b->magic = 0;
         delete b;

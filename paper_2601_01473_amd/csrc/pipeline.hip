@@ -1467,7 +1467,8 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
         b.col[l].reserve((size_t)std::max<int64_t>(1, H * g.cap[l] * fanouts[l]) * 4);
     }
 
-    if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[0], st));
+    b.prof = s.profile;
+    if (b.prof) AGNES_CHECK_HIP(hipEventRecord(w.ev[0], st));
     hipLaunchKernelGGL(k_params, dim3(1), dim3(kWave), 0, st, w.params.as<ChainParams>(), targets, seed, mb_base);
     AGNES_CHECK_HIP(hipGetLastError());
     // With the graph option, a shape seen twice in a row is captured once and
@@ -1479,10 +1480,10 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
     else launch_chain(s, b, g, y, fanouts, st);
     b.last_key = std::move(key);
     b.cur = L & 1;                    // the list buffers alternate hop by hop
-    if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[1], st));
     // sizes of the outputs travel to pinned host memory; finish reads them
     AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, w.sync.ptr, y.bytes, hipMemcpyDeviceToHost, st));
-    AGNES_CHECK_HIP(hipEventRecord(b.sampled, st));
+    b.sampled_at = b.prof ? w.ev[1] : b.sampled;
+    AGNES_CHECK_HIP(hipEventRecord(b.sampled_at, st));
     b.state = kSampled;
 }
 
@@ -1492,7 +1493,7 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     Workspace& w = b.ws;
     const int H = b.H, L = b.L;
     SyncLayout y = sync_layout(H, L, b.rows_max);
-    AGNES_CHECK_HIP(hipEventSynchronize(b.sampled));
+    AGNES_CHECK_HIP(hipEventSynchronize(b.sampled_at));
     b.state = kIdle;   // until the gather is enqueued
     Ctl hc;
     memcpy(&hc, w.sync_host.ptr, sizeof(Ctl));
@@ -1543,7 +1544,7 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     b.features.reserve_slack((size_t)std::max<int64_t>(rows, 1) * (size_t)s.row_bytes);
 
     // gather over the final list, ordered after the sampling phase
-    if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.sampled, 0));
+    if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.sampled_at, 0));
     const uint64_t* rlk = w.rl_key[b.cur].as<uint64_t>();
     const int32_t* rlv = w.rl_val[b.cur].as<int32_t>();
     GatherArgs ga{s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv, w.mb_off.as<int64_t>(),
@@ -1591,10 +1592,7 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
         // and the compaction above (flag and off are reused below) is done
         AGNES_CHECK_HIP(hipStreamWaitEvent(st, s.pool_free, 0));
         if (cs != st) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.needed, 0));
-        if (s.profile) {
-            AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
-            AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
-        }
+        if (b.prof) AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
         AGNES_CHECK_HIP(hipMemcpyAsync(w.plan.ptr, w.plan_host.ptr, w.plan_used, hipMemcpyHostToDevice, st));
         const int32_t* plan = w.plan.as<int32_t>();
         const int64_t blk_bytes = s.rpb * s.row_bytes;
@@ -1646,20 +1644,17 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
                                ctl);
         }
         AGNES_CHECK_HIP(hipGetLastError());
-        if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));
         // tier counters for wait
         AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, ctl, sizeof(Ctl), hipMemcpyDeviceToHost, st));
         AGNES_CHECK_HIP(hipEventRecord(s.pool_free, st));
     } else {
-        if (s.profile) {
-            AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
-            AGNES_CHECK_HIP(hipEventRecord(w.ev[3], st));
-        }
+        if (b.prof) AGNES_CHECK_HIP(hipEventRecord(w.ev[2], st));
         if (rows > 0) copy_rows(ga);
         AGNES_CHECK_HIP(hipGetLastError());
-        if (s.profile) AGNES_CHECK_HIP(hipEventRecord(w.ev[4], st));
     }
-    AGNES_CHECK_HIP(hipEventRecord(b.gathered, st));
+    // the end of the gather (after the tier counters' copy): what wait waits for
+    b.gathered_at = b.prof ? w.ev[4] : b.gathered;
+    AGNES_CHECK_HIP(hipEventRecord(b.gathered_at, st));
     b.stream = st;
     b.state = kGathering;
 }
@@ -1667,13 +1662,13 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
 void wait_batch(Batch& b) {
     if (b.state == kDone) return;
     AGNES_REQUIRE(b.state == kGathering, AGNES_ERR_INVALID, "the batch holds no finished hyperbatch");
-    AGNES_CHECK_HIP(hipEventSynchronize(b.gathered));
+    AGNES_CHECK_HIP(hipEventSynchronize(b.gathered_at));
     b.stats.sample_ms = b.stats.gather_ms = b.stats.copy_ms = -1.0f;
-    if (b.store->profile) {
+    if (b.prof) {
         Workspace& w = b.ws;
         AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.sample_ms, w.ev[0], w.ev[1]));
         AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.gather_ms, w.ev[2], w.ev[4]));
-        AGNES_CHECK_HIP(hipEventElapsedTime(&b.stats.copy_ms, w.ev[3], w.ev[4]));
+        b.stats.copy_ms = b.stats.gather_ms;
     }
     if (b.store->tiered) {
         b.tier.gather_ms = b.stats.gather_ms;

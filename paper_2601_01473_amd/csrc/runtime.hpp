@@ -243,6 +243,11 @@ struct Batch {
     hipStream_t stream = nullptr;     // stream of the sampling phase
     hipEvent_t sampled = nullptr;     // sizes of the outputs are in ws.sync_host
     hipEvent_t gathered = nullptr;    // outputs and statistics are complete
+    // The events that mark those points for the current hyperbatch: `sampled`
+    // and `gathered`, or, when it is profiled, the timing events recorded at
+    // the same points (one marker fewer per phase on the stream).
+    int prof = 0;
+    hipEvent_t sampled_at = nullptr, gathered_at = nullptr;
     hipEvent_t needed = nullptr;      // staged tier: the needed feature blocks are in ws.need_host
     int64_t capN = 0;
     int64_t rows_max = 0;             // node-list capacity of the hyperbatch (sizes the sync block)

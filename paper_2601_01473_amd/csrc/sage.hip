@@ -240,7 +240,7 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
     // synchronisation of the free that comes with each) rare
     b.sage_a.reserve_slack((size_t)std::max<int64_t>(Amax, 1) * 2);
     for (int k = 0; k < 2; k++) b.sage_h[k].reserve_slack((size_t)Hmax * 2);
-    if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.gathered, 0));
+    if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.gathered_at, 0));
     AGNES_CHECK_HIP(hipMemcpyAsync(b.sage_off.ptr, b.sage_host.ptr, offs.size() * 8, hipMemcpyHostToDevice, st));
     AGNES_CHECK_HIP(hipEventRecord(b.sage_ev, st));
     const int64_t* doffs = b.sage_off.as<int64_t>();
