@@ -198,21 +198,24 @@ __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const 
     constexpr int BINS = 1 << RB;
     __shared__ uint32_t h[BINS];
     const int64_t n = *n_dev;
-    const int64_t t0 = (int64_t)blockIdx.x * (kBlock * ITEMS);
-    if (t0 >= n) return;                        // tiles past the end are not scanned
-    for (int d = threadIdx.x; d < BINS; d += kBlock) h[d] = 0;
-    uint32_t k[ITEMS];
+    const int64_t tiles = (n + kBlock * ITEMS - 1) / (kBlock * ITEMS);
+    for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+        const int64_t t0 = tile * (kBlock * ITEMS);
+        __syncthreads();                        // the previous tile's counts are written out
+        for (int d = threadIdx.x; d < BINS; d += kBlock) h[d] = 0;
+        uint32_t k[ITEMS];
 #pragma unroll
-    for (int q = 0; q < ITEMS; q++) {
-        const int64_t i = t0 + q * kBlock + threadIdx.x;
-        k[q] = i < n ? keys[i] : 0u;
+        for (int q = 0; q < ITEMS; q++) {
+            const int64_t i = t0 + q * kBlock + threadIdx.x;
+            k[q] = i < n ? keys[i] : 0u;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < ITEMS; q++)
+            if (t0 + q * kBlock + threadIdx.x < n) atomicAdd(&h[(k[q] >> shift) & (BINS - 1)], 1u);
+        __syncthreads();
+        for (int d = threadIdx.x; d < BINS; d += kBlock) hist[tile * BINS + d] = h[d];
     }
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < ITEMS; q++)
-        if (t0 + q * kBlock + threadIdx.x < n) atomicAdd(&h[(k[q] >> shift) & (BINS - 1)], 1u);
-    __syncthreads();
-    for (int d = threadIdx.x; d < BINS; d += kBlock) hist[(int64_t)blockIdx.x * BINS + d] = h[d];
 }
 
 // One workgroup per digit: exclusive scan over the tiles that hold keys of
@@ -257,8 +260,8 @@ __global__ __launch_bounds__(kBlock) void k_rs_scan(uint32_t* hist, const int64_
 // Consecutive tiles write consecutive pieces of every digit's run, so their
 // partial cache lines are shared; workgroups are dealt to the XCDs in turn, so
 // XCD x takes the contiguous tiles [x per, (x + 1) per), per = ceil(tiles / 8),
-// and those lines fill up in one L2.  The grid is a multiple of 8 workgroups
-// covering 8 ceil(max tiles / 8) (scatter_grid).
+// and those lines fill up in one L2.  The grid is a multiple of 8 workgroups;
+// the workgroups of one XCD take its tiles in turn.
 template <int ITEMS, int RB>
 __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, const uint32_t* vin,
                                                        uint32_t* kout, uint32_t* vout, const int64_t* n_dev,
@@ -275,11 +278,13 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     const int64_t n = *n_dev;
     const int64_t tiles = (n + kBlock * ITEMS - 1) / (kBlock * ITEMS);
     const int64_t per = (tiles + kXcds - 1) / kXcds;
-    const int64_t local = blockIdx.x / kXcds;
-    const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per + local;
-    if (local >= per || tile >= tiles) return;
-    const int64_t t0 = tile * (kBlock * ITEMS);
+    const int64_t wx = gridDim.x / kXcds;          // workgroups of one XCD
     const int t = threadIdx.x, w = wave_id(), lane = lane_id();
+    for (int64_t local = blockIdx.x / kXcds; local < per; local += wx) {
+    const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per + local;
+    if (tile >= tiles) break;
+    const int64_t t0 = tile * (kBlock * ITEMS);
+    __syncthreads();                               // the previous tile's LDS is consumed
     for (int x = t; x < kWavesPerBlock * BINS; x += kBlock) (&wcnt[0][0])[x] = 0;
     {
         uint32_t dt[Q], sum = 0;
@@ -368,11 +373,17 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
         kout[dst] = k;
         vout[dst] = sv[i];
     }
+    }
 }
 
-// Workgroups of k_rs_scatter for at most `tiles` tiles: 8 ceil(tiles / 8), so
-// that every XCD's contiguous range of tiles has a workgroup for each tile.
-static int scatter_grid(int tiles) { return (tiles + kXcds - 1) / kXcds * kXcds; }
+// Workgroups of the histogram and scatter kernels for at most `tiles` tiles:
+// at most kRadixGroups, which loop over the tiles.  The grid is sized from the
+// hop's upper bound while the keys actually sorted are often far fewer, and
+// beside a long kernel of another stream every workgroup, even one that finds
+// no tile, waits for a slot: a capped grid keeps such kernels short.  A
+// multiple of 8 (the scatter splits its workgroups evenly over the XCDs).
+constexpr int kRadixGroups = 2048;
+static int radix_grid(int tiles) { return std::min(kRadixGroups, (tiles + kXcds - 1) / kXcds * kXcds); }
 
 template <int ITEMS, int RB>
 static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
@@ -383,9 +394,10 @@ static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uin
     for (int p = 0; p < passes; p++) {
         int shift = p * RB;
         const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
-        hipLaunchKernelGGL((k_rs_hist<ITEMS, RB>), dim3(tiles), dim3(kBlock), 0, st, ka, n_dev, shift, hist);
+        hipLaunchKernelGGL((k_rs_hist<ITEMS, RB>), dim3(radix_grid(tiles)), dim3(kBlock), 0, st, ka, n_dev, shift,
+                           hist);
         hipLaunchKernelGGL((k_rs_scan<ITEMS, RB>), dim3(1 << RB), dim3(kBlock), 0, st, hist, n_dev, dtot);
-        hipLaunchKernelGGL((k_rs_scatter<ITEMS, RB>), dim3(scatter_grid(tiles)), dim3(kBlock), 0, st, ka, vin, kb,
+        hipLaunchKernelGGL((k_rs_scatter<ITEMS, RB>), dim3(radix_grid(tiles)), dim3(kBlock), 0, st, ka, vin, kb,
                            vb, n_dev, shift, hist, dtot);
         uint32_t* tk = ka; ka = kb; kb = tk;
         uint32_t* tv = va; va = vb; vb = tv;
