@@ -60,6 +60,9 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
     return g;
 }
 
+// Workgroups of the per-request kernels (k_count, k_sample) of hop l.
+static int hop_grid(const Geometry& g, int l) { return grid_for((int64_t)g.H * g.cap[l], 2048); }
+
 // ----------------------------------------------------------------- small kernels
 
 __device__ __forceinline__ void load_offsets(int64_t* dst, const int64_t* src, int n) {
@@ -1169,17 +1172,22 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     int64_t* ecount = (int64_t*)((char*)w.sync.ptr + y.ecount);
     const OffT* off = s.offsets.as<OffT>();
     const size_t lds_h = (size_t)(g.H + 1) * sizeof(int64_t);
-    const int gR = grid_for(g.Rmax, 2048);
+    // this hop's requests are at most H cap[l]: its own bound sizes the grids
+    // (beside a long kernel of another stream even an idle workgroup waits for
+    // a slot); k_begin sums the previous hop's per-workgroup counts
+    const int gR = hop_grid(g, l);
+    const int gPrev = l > 0 ? hop_grid(g, l - 1) : 0;
     int64_t* part = w.scan_part.as<int64_t>();
     const uint64_t* rlk = w.rl_key[cur].as<uint64_t>();
     const int32_t* rlv = w.rl_val[cur].as<int32_t>();
 
     hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, l, g.L, g.H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ecount, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
-                       (int64_t*)nullptr, w.topo_part.as<uint32_t>(), gR);
+                       (int64_t*)nullptr, w.topo_part.as<uint32_t>(), gPrev);
     hipLaunchKernelGGL(k_count<OffT>, dim3(gR), dim3(kBlock), lds_h, st, g.H, g.capN, f, off,
                        w.nodes.as<int32_t>(), w.req_off.as<int64_t>(), w.cnt.as<int32_t>(), ctl);
-    scan_counts(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, g.Rmax, &ctl->S, part, st);
+    scan_counts(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, std::max<int64_t>(1, (int64_t)g.H * g.cap[l]),
+                &ctl->S, part, st);
     const int32_t* adj = s.indices.as<int32_t>();
     int32_t* cg = w.skey.as<int32_t>();
 #define AGNES_SAMPLE(MK)                                                                               \
@@ -1388,7 +1396,7 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     // close the last hop: edge counts, final node counts, output row offsets
     hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
-                       w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), grid_for(g.Rmax, 2048));
+                       w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), hop_grid(g, L - 1));
     hipLaunchKernelGGL(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
                        (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl);
     AGNES_CHECK_HIP(hipGetLastError());
