@@ -121,8 +121,17 @@ __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict
     __shared__ uint16_t As[kGM][kGKP];
     __shared__ uint16_t Bs[kGN][kGKP];
     const int lane = lane_id(), w = wave_id(), t = threadIdx.x;
-    const int64_t m0 = (int64_t)blockIdx.x * kGM;
-    const int n0 = blockIdx.y * kGN;
+    // Tile of workgroup i (1-D grid): runs of 8 NB workgroups cover 8 row
+    // blocks x NB column blocks.  Workgroups i and i + 8 share an XCD (they are
+    // dealt to the 8 XCDs in turn) and follow each other there, so the column
+    // blocks of one row block run back to back on one XCD and all but the
+    // first read its A tile from that XCD's L2.
+    const int NB = (N + kGN - 1) / kGN;
+    const int64_t i = blockIdx.x;
+    const int64_t mb = (i / (8 * (int64_t)NB)) * 8 + (i % 8);
+    const int64_t m0 = mb * kGM;
+    const int n0 = (int)((i / 8) % NB) * kGN;
+    if (m0 >= M) return;
     const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
     f32x16 acc[2][2];
 #pragma unroll
@@ -259,7 +268,8 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
             launch_agg<_Float16>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
         else
             launch_agg<uint16_t>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
-        const dim3 grid((unsigned)((M + kGM - 1) / kGM), (unsigned)((dout + kGN - 1) / kGN));
+        const int64_t mbs = (M + kGM - 1) / kGM, nbs = (dout + kGN - 1) / kGN;
+        const dim3 grid((unsigned)((mbs + 7) / 8 * 8 * nbs));
         if (i + 1 < L) {
             void* z = b.sage_h[i & 1].ptr;
             hipLaunchKernelGGL((k_sage_gemm<true, false>), grid, dim3(kBlock), 0, st, A,
