@@ -5,7 +5,7 @@
 //   k_sage_agg   one wave per destination node: its own input row and the
 //                float32 mean of its sampled neighbours' rows, both rounded to
 //                bf16, as one row [h_v ; m_v] of A (M x 2d, row-major);
-//   k_sage_gemm  Z = A W^T + b with bf16 MFMA (32x32x8, float32 accumulate),
+//   k_sage_gemm  Z = A W^T + b with bf16 MFMA (32x32x16, float32 accumulate),
 //                ReLU on hidden layers; hidden outputs stored as bf16, the last
 //                layer's as float32.
 // Destination rows of all minibatches are stacked minibatch-major, so a layer
@@ -20,7 +20,7 @@ namespace agnes {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4s __attribute__((ext_vector_type(4)));
 
@@ -106,10 +106,12 @@ __global__ __launch_bounds__(kBlock) void k_sage_agg(const InT* __restrict__ hin
 
 // Z[M][N] = A[M][K] W[N][K]^T + b.  Workgroup tile 128 x 128, K step 64; wave
 // w owns the 64 x 64 quarter (w / 2, w % 2) as 2 x 2 MFMA 32x32 blocks.
-// Operand layout of v_mfma_f32_32x32x8_bf16_1k: lane l holds A[l % 32][4 (l / 32) + q]
-// and B[4 (l / 32) + q][l % 32] for q = 0..3, and D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32]
-// for r = 0..15.  W is stored output-major, so both tiles sit in LDS with k
-// innermost and every operand is one 8-byte LDS read.  The next K step's tiles
+// Operand layout of v_mfma_f32_32x32x16_bf16 (the CDNA4 instruction with twice
+// the K depth of the 32x32x8 one at the same cycle count): lane l holds
+// A[l % 32][8 (l / 32) + q] and B[8 (l / 32) + q][l % 32] for q = 0..7, and
+// D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32] for r = 0..15.  W is stored
+// output-major, so both tiles sit in LDS with k innermost and every operand is
+// one 16-byte LDS read.  The next K step's tiles
 // are loaded into registers while the MFMAs consume the current ones.
 constexpr int kGM = 128, kGN = 128, kGK = 64, kGKP = kGK + 8;   // padded LDS row (uint16)
 constexpr int kGLoads = kGM * kGK / 8 / kBlock;                 // 16-byte pieces per thread per tile (4)
@@ -165,18 +167,18 @@ __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict
         __syncthreads();
         if (k0 + kGK < K) fetch(k0 + kGK);
 #pragma unroll
-        for (int ks = 0; ks < kGK; ks += 8) {
-            const int kq = ks + (lane >> 5) * 4;
-            s16x4 a[2], b[2];
+        for (int ks = 0; ks < kGK; ks += 16) {
+            const int kq = ks + (lane >> 5) * 8;
+            bf16x8 a[2], b[2];
 #pragma unroll
-            for (int i = 0; i < 2; i++) a[i] = *(const s16x4*)&As[wm + i * 32 + (lane & 31)][kq];
+            for (int i = 0; i < 2; i++) a[i] = *(const bf16x8*)&As[wm + i * 32 + (lane & 31)][kq];
 #pragma unroll
-            for (int i = 0; i < 2; i++) b[i] = *(const s16x4*)&Bs[wn + i * 32 + (lane & 31)][kq];
+            for (int i = 0; i < 2; i++) b[i] = *(const bf16x8*)&Bs[wn + i * 32 + (lane & 31)][kq];
 #pragma unroll
             for (int i = 0; i < 2; i++)
 #pragma unroll
                 for (int jj = 0; jj < 2; jj++)
-                    acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a[i], b[jj], acc[i][jj], 0, 0, 0);
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[jj], acc[i][jj], 0, 0, 0);
         }
     }
 #pragma unroll
