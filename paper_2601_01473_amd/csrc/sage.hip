@@ -2,9 +2,9 @@
 // computation step that consumes the per-hop CSR blocks and gathered rows.
 //
 // Layer i runs on hop l = L-1-i.  Per layer two kernels:
-//   k_sage_agg   one wave per destination node: its own input row and the
-//                float32 mean of its sampled neighbours' rows, both rounded to
-//                bf16, as one row [h_v ; m_v] of A (M x 2d, row-major);
+//   k_sage_agg   one lane group per destination node: its own input row and
+//                the float32 mean of its sampled neighbours' rows, both rounded
+//                to bf16, as one row [h_v ; m_v] of A (M x 2d, row-major);
 //   k_sage_gemm  Z = A W^T + b with bf16 MFMA (32x32x16, float32 accumulate),
 //                ReLU on hidden layers; hidden outputs stored as bf16, the last
 //                layer's as float32.
@@ -22,6 +22,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4s __attribute__((ext_vector_type(4)));
 
 // float -> bf16 bits, round to nearest, ties to even (finite inputs).
@@ -32,24 +33,44 @@ __device__ __forceinline__ uint16_t to_bf16(float x) {
 }
 __device__ __forceinline__ float bf16_to_float(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// Four consecutive input elements as float.
-template <typename InT> struct In4;
-template <> struct In4<float> {
-    static __device__ __forceinline__ f32x4 load(const float* p) { return *(const f32x4*)p; }
-};
-template <> struct In4<_Float16> {
-    static __device__ __forceinline__ f32x4 load(const _Float16* p) {
-        typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-        const h4 v = *(const h4*)p;
-        return f32x4{(float)v.x, (float)v.y, (float)v.z, (float)v.w};
+// Sixteen bytes of consecutive input elements (4 float or 8 half / bf16) as float.
+template <typename InT> struct In16;
+template <> struct In16<float> {
+    static constexpr int E = 4;
+    static __device__ __forceinline__ void load(const float* p, float (&x)[E]) {
+        const f32x4 v = *(const f32x4*)p;
+        x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
     }
 };
-template <> struct In4<uint16_t> {   // bf16 bits
-    static __device__ __forceinline__ f32x4 load(const uint16_t* p) {
-        const u16x4 v = *(const u16x4*)p;
-        return f32x4{bf16_to_float(v.x), bf16_to_float(v.y), bf16_to_float(v.z), bf16_to_float(v.w)};
+template <> struct In16<_Float16> {
+    static constexpr int E = 8;
+    static __device__ __forceinline__ void load(const _Float16* p, float (&x)[E]) {
+        typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+        const h8 v = *(const h8*)p;
+#pragma unroll
+        for (int q = 0; q < E; q++) x[q] = (float)v[q];
     }
 };
+template <> struct In16<uint16_t> {   // bf16 bits
+    static constexpr int E = 8;
+    static __device__ __forceinline__ void load(const uint16_t* p, float (&x)[E]) {
+        const u16x8 v = *(const u16x8*)p;
+#pragma unroll
+        for (int q = 0; q < E; q++) x[q] = bf16_to_float(v[q]);
+    }
+};
+
+// E bf16 values (E = 4 or 8) as one 8- or 16-byte store.
+template <int E> __device__ __forceinline__ void store_bf16(uint16_t* p, const float (&x)[E]);
+template <> __device__ __forceinline__ void store_bf16<4>(uint16_t* p, const float (&x)[4]) {
+    *(u16x4*)p = u16x4{to_bf16(x[0]), to_bf16(x[1]), to_bf16(x[2]), to_bf16(x[3])};
+}
+template <> __device__ __forceinline__ void store_bf16<8>(uint16_t* p, const float (&x)[8]) {
+    u16x8 v;
+#pragma unroll
+    for (int q = 0; q < 8; q++) v[q] = to_bf16(x[q]);
+    *(u16x8*)p = v;
+}
 
 // Offsets of one layer, all [H+1] int64: destination rows of minibatch j are
 // [d_off[j], d_off[j+1]); its input rows start at in_off[j]; its hop-l row
@@ -61,14 +82,22 @@ struct LayerOffsets {
     const int64_t* col_off;
 };
 
-template <typename InT>
+// One group of LPR lanes per destination row (64 / LPR rows per wave), each
+// lane holding 16 bytes of the row per chunk: LPR = 64 for rows of 1 KiB and
+// up, fewer lanes for narrower rows so that no lane idles.
+template <typename InT, int LPR>
 __global__ __launch_bounds__(kBlock) void k_sage_agg(const InT* __restrict__ hin, LayerOffsets o,
                                                      const int32_t* __restrict__ row_ptr,
                                                      const int32_t* __restrict__ col, int H, int64_t M, int din,
                                                      uint16_t* __restrict__ A) {
+    constexpr int E = In16<InT>::E, RPW = kWave / LPR;
     const int lane = lane_id();
+    const int g = RPW == 1 ? 0 : lane / LPR;        // a whole wave per row keeps the row's indices uniform
+    const int gl = RPW == 1 ? lane : lane % LPR;
     const int64_t nw = (int64_t)gridDim.x * kWavesPerBlock;
-    for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave_id(); row < M; row += nw) {
+    for (int64_t r0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave_id()) * RPW; r0 < M; r0 += nw * RPW) {
+        const int64_t row = r0 + g;
+        if (row >= M) break;
         const int j = upper_segment(o.d_off, H, row);
         const int64_t v = row - o.d_off[j];
         const int32_t* rp = row_ptr + o.rp_off[j] + v;
@@ -76,30 +105,36 @@ __global__ __launch_bounds__(kBlock) void k_sage_agg(const InT* __restrict__ hin
         const int32_t* cb = col + o.col_off[j];
         const InT* base = hin + o.in_off[j] * (int64_t)din;
         uint16_t* arow = A + row * 2 * (int64_t)din;
-        for (int c = lane * 4; c < din; c += kWave * 4) {
-            const f32x4 self = In4<InT>::load(base + v * din + c);
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int c = gl * E; c < din; c += LPR * E) {
+            float self[E], acc[E];
+            In16<InT>::load(base + v * din + c, self);
+#pragma unroll
+            for (int q = 0; q < E; q++) acc[q] = 0.f;
             int32_t t = beg;
             for (; t + 4 <= end; t += 4) {
                 const int32_t u0 = cb[t], u1 = cb[t + 1], u2 = cb[t + 2], u3 = cb[t + 3];
-                const f32x4 x0 = In4<InT>::load(base + (int64_t)u0 * din + c);
-                const f32x4 x1 = In4<InT>::load(base + (int64_t)u1 * din + c);
-                const f32x4 x2 = In4<InT>::load(base + (int64_t)u2 * din + c);
-                const f32x4 x3 = In4<InT>::load(base + (int64_t)u3 * din + c);
-                acc += x0;
-                acc += x1;
-                acc += x2;
-                acc += x3;
+                float x0[E], x1[E], x2[E], x3[E];
+                In16<InT>::load(base + (int64_t)u0 * din + c, x0);
+                In16<InT>::load(base + (int64_t)u1 * din + c, x1);
+                In16<InT>::load(base + (int64_t)u2 * din + c, x2);
+                In16<InT>::load(base + (int64_t)u3 * din + c, x3);
+#pragma unroll
+                for (int q = 0; q < E; q++) acc[q] = (((acc[q] + x0[q]) + x1[q]) + x2[q]) + x3[q];
             }
-            for (; t < end; t++) acc += In4<InT>::load(base + (int64_t)cb[t] * din + c);
+            for (; t < end; t++) {
+                float x[E];
+                In16<InT>::load(base + (int64_t)cb[t] * din + c, x);
+#pragma unroll
+                for (int q = 0; q < E; q++) acc[q] += x[q];
+            }
             const int deg = end - beg;
-            f32x4 mean = {0.f, 0.f, 0.f, 0.f};
             if (deg > 0) {
                 const float d = (float)deg;
-                mean = f32x4{acc.x / d, acc.y / d, acc.z / d, acc.w / d};
+#pragma unroll
+                for (int q = 0; q < E; q++) acc[q] = acc[q] / d;
             }
-            *(u16x4*)(arow + c) = u16x4{to_bf16(self.x), to_bf16(self.y), to_bf16(self.z), to_bf16(self.w)};
-            *(u16x4*)(arow + din + c) = u16x4{to_bf16(mean.x), to_bf16(mean.y), to_bf16(mean.z), to_bf16(mean.w)};
+            store_bf16<E>(arow + c, self);
+            store_bf16<E>(arow + din + c, acc);
         }
     }
 }
@@ -200,11 +235,26 @@ __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict
         }
 }
 
+template <typename InT, int LPR>
+static void launch_agg_k(const void* hin, const LayerOffsets& o, const int32_t* row_ptr, const int32_t* col, int H,
+                         int64_t M, int din, uint16_t* A, hipStream_t st) {
+    constexpr int64_t per_wg = (int64_t)kWavesPerBlock * (kWave / LPR);
+    const int G = (int)std::max<int64_t>(1, std::min<int64_t>((M + per_wg - 1) / per_wg, 1 << 20));
+    hipLaunchKernelGGL((k_sage_agg<InT, LPR>), dim3(G), dim3(kBlock), 0, st, (const InT*)hin, o, row_ptr, col, H, M,
+                       din, A);
+}
+
+// Lanes per row: the largest power of two up to 64 that the row's 16-byte
+// pieces fill (din is a multiple of 32, so there are at least 4 pieces).
 template <typename InT>
 static void launch_agg(const void* hin, const LayerOffsets& o, const int32_t* row_ptr, const int32_t* col, int H,
                        int64_t M, int din, uint16_t* A, hipStream_t st) {
-    const int G = (int)std::max<int64_t>(1, std::min<int64_t>((M + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 20));
-    hipLaunchKernelGGL(k_sage_agg<InT>, dim3(G), dim3(kBlock), 0, st, (const InT*)hin, o, row_ptr, col, H, M, din, A);
+    const int pieces = din / In16<InT>::E;
+    if (pieces >= 64) launch_agg_k<InT, 64>(hin, o, row_ptr, col, H, M, din, A, st);
+    else if (pieces >= 32) launch_agg_k<InT, 32>(hin, o, row_ptr, col, H, M, din, A, st);
+    else if (pieces >= 16) launch_agg_k<InT, 16>(hin, o, row_ptr, col, H, M, din, A, st);
+    else if (pieces >= 8) launch_agg_k<InT, 8>(hin, o, row_ptr, col, H, M, din, A, st);
+    else launch_agg_k<InT, 4>(hin, o, row_ptr, col, H, M, din, A, st);
 }
 
 void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t st) {

@@ -3,7 +3,9 @@
 bf16 operands, float32 sums and bf16 hidden storage.
 
 Cases: fp32 / fp16 / bf16 feature rows; one to three layers; output dims that
-are and are not multiples of the 128-wide tile; zero fanout (empty rows) and
+are and are not multiples of the 128-wide tile; row widths that give the
+aggregation every lane-group size (4 to 64 lanes of 16 bytes per row, with a
+partial last chunk, and rows of more than 64 pieces); zero fanout (empty rows) and
 fanouts above every degree; a batch with many minibatches; and the 2^14-node
 workload at full size.
 """
@@ -63,7 +65,7 @@ def run(ag, off, idx, feat, feat_dtype, X64, tg, fan, dims, seed, block_bytes=25
 
 
 @pytest.mark.parametrize("dims,fan", [([32, 64, 32], [5, 3]), ([64, 96], [7]), ([32, 32, 160, 32], [4, 3, 2]),
-                                      ([128, 256, 64], [6, 4])])
+                                      ([128, 256, 64], [6, 4]), ([256, 64], [5]), ([512, 1024, 32], [4, 3])])
 def test_fp32_features(agnes, dims, fan):
     off, idx = random_graph(2000, 9, 3, hubs=2, hub_deg=400)
     tg = distinct_targets(2000, 3, 40, 5)
@@ -72,11 +74,12 @@ def test_fp32_features(agnes, dims, fan):
         block_bytes=max(256, 1 << int(np.ceil(np.log2(dims[0] * 4)))))
 
 
-def test_fp16_features(agnes):
+@pytest.mark.parametrize("dims", [[64, 64, 32], [128, 256, 96]])
+def test_fp16_features(agnes, dims):
     off, idx = random_graph(1500, 8, 6, hubs=2, hub_deg=300)
     tg = distinct_targets(1500, 4, 25, 2)
-    feat = features(1500, 64, 3, np.float16)
-    run(agnes, off, idx, feat, None, feat.astype(np.float64), tg, [5, 5], [64, 64, 32], seed=2)
+    feat = features(1500, dims[0], 3, np.float16)
+    run(agnes, off, idx, feat, None, feat.astype(np.float64), tg, [5, 5], dims, seed=2)
 
 
 def test_bf16_features(agnes):
