@@ -347,16 +347,17 @@ agnes_status agnes_batch_tier_stats(const agnes_batch* batch, agnes_tier_stats* 
  *     must be a positive multiple of 32, at most 4096.
  *   weight[i]: device bf16 (raw uint16 bits), [dims[i+1]][2*dims[i]] row-major:
  *     columns 0 .. dims[i]-1 multiply h_v, the others m_v (the layout of a
- *     linear layer's weight, output-major).
+ *     linear layer's weight, output-major); 16-byte aligned.
  *   bias[i]: device float32 [dims[i+1]].
  *   out: device float32 [H*B][dims[L]]: the targets' embeddings, minibatch-major
- *     in the order the targets were given.
+ *     in the order the targets were given; 16-byte aligned.
  * Arithmetic: m_v is accumulated in float32; [h_v ; m_v] is rounded to bf16
  * and multiplied with bf16 MFMA, accumulating in float32; hidden embeddings
  * are stored as bf16.  The call enqueues on hip_stream after the batch's
  * gather and returns; the batch owns the intermediate buffers.
  * Errors: a batch without a finished hyperbatch, L != the batch's hop count,
- * dims out of range or dims[0] != the feature dim -> AGNES_ERR_INVALID. */
+ * dims out of range, dims[0] != the feature dim, a NULL or misaligned pointer
+ * -> AGNES_ERR_INVALID. */
 typedef struct {
     int32_t L;
     int32_t dims[AGNES_MAX_LAYERS + 1];

@@ -143,10 +143,13 @@ __global__ __launch_bounds__(kBlock) void k_sage_agg(const InT* __restrict__ hin
 // w owns the 64 x 64 quarter (w / 2, w % 2) as 2 x 2 MFMA 32x32 blocks.
 // Operand layout of v_mfma_f32_32x32x16_bf16 (the CDNA4 instruction with twice
 // the K depth of the 32x32x8 one at the same cycle count): lane l holds
-// A[l % 32][8 (l / 32) + q] and B[8 (l / 32) + q][l % 32] for q = 0..7, and
-// D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32] for r = 0..15.  W is stored
-// output-major, so both tiles sit in LDS with k innermost and every operand is
-// one 16-byte LDS read.  The next K step's tiles
+// X[l % 32][8 (l / 32) + q] of the first operand and Y[8 (l / 32) + q][l % 32]
+// of the second for q = 0..7, and D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32] for
+// r = 0..15.  W is stored output-major, so both tiles sit in LDS with k
+// innermost and every operand is one 16-byte LDS read.  W's rows go in as the
+// first operand and A's as the second, so D is a block of Z^T: lane l holds
+// row l % 32 of Z and four adjacent columns per group of four registers,
+// written with one 8-byte (bf16) or 16-byte (float) store.  The next K step's tiles
 // are loaded into registers while the MFMAs consume the current ones.
 constexpr int kGM = 128, kGN = 128, kGK = 64, kGKP = kGK + 8;   // padded LDS row (uint16)
 constexpr int kGLoads = kGM * kGK / 8 / kBlock;                 // 16-byte pieces per thread per tile (4)
@@ -213,24 +216,29 @@ __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict
             for (int i = 0; i < 2; i++)
 #pragma unroll
                 for (int jj = 0; jj < 2; jj++)
-                    acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[jj], acc[i][jj], 0, 0, 0);
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[jj], a[i], acc[i][jj], 0, 0, 0);
         }
     }
+    // N is a multiple of 32 (checked on the host), so a group of four columns
+    // that starts inside Z ends inside it.
 #pragma unroll
     for (int i = 0; i < 2; i++)
 #pragma unroll
         for (int jj = 0; jj < 2; jj++) {
-            const int gn = n0 + wn + jj * 32 + (lane & 31);
-            if (gn >= N) continue;
-            const float bv = bias[gn];
+            const int64_t gm = m0 + wm + i * 32 + (lane & 31);
+            if (gm >= M) continue;
 #pragma unroll
-            for (int r = 0; r < 16; r++) {
-                const int64_t gm = m0 + wm + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-                if (gm >= M) continue;
-                float z = acc[i][jj][r] + bv;
-                if (RELU) z = z > 0.f ? z : 0.f;
-                if (OUT_F32) ((float*)Z)[gm * N + gn] = z;
-                else ((uint16_t*)Z)[gm * N + gn] = to_bf16(z);
+            for (int g = 0; g < 4; g++) {
+                const int gn = n0 + wn + jj * 32 + g * 8 + (lane >> 5) * 4;
+                if (gn >= N) continue;
+                float z[4];
+#pragma unroll
+                for (int c = 0; c < 4; c++) {
+                    z[c] = acc[i][jj][g * 4 + c] + bias[gn + c];
+                    if (RELU) z[c] = z[c] > 0.f ? z[c] : 0.f;
+                }
+                if (OUT_F32) *(f32x4*)((float*)Z + gm * N + gn) = f32x4{z[0], z[1], z[2], z[3]};
+                else *(u16x4*)((uint16_t*)Z + gm * N + gn) = u16x4{to_bf16(z[0]), to_bf16(z[1]), to_bf16(z[2]), to_bf16(z[3])};
             }
         }
 }
@@ -267,8 +275,11 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
                       "dims must be positive multiples of 32, at most 4096");
     const int esz = s.feat_dtype == AGNES_FLOAT32 ? 4 : 2;
     AGNES_REQUIRE((int64_t)m.dims[0] * esz == s.row_bytes, AGNES_ERR_INVALID, "dims[0] must be the feature dim");
-    for (int i = 0; i < m.L; i++)
+    for (int i = 0; i < m.L; i++) {
         AGNES_REQUIRE(m.weight[i] && m.bias[i], AGNES_ERR_INVALID, "weights and biases must not be NULL");
+        AGNES_REQUIRE(((uintptr_t)m.weight[i] & 15) == 0, AGNES_ERR_INVALID, "weights must be 16-byte aligned");
+    }
+    AGNES_REQUIRE(((uintptr_t)out & 15) == 0, AGNES_ERR_INVALID, "out must be 16-byte aligned");
     const int H = b.H, L = b.L;
     // host offsets of every layer: d_off, in_off, rp_off, col_off ([H+1] each)
     std::vector<int64_t> offs((size_t)L * 4 * (H + 1));

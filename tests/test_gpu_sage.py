@@ -128,5 +128,17 @@ def test_rejects_wrong_dims(agnes):
     with pytest.raises(agnes.AgnesError):
         b.sage_forward([torch.from_numpy(w.view(np.int16)).cuda() for w in Ws2],
                        [torch.from_numpy(x).cuda() for x in bs2])
+    # misaligned weight and output pointers are refused before any launch
+    rows = 8
+    big = torch.empty(rows * 32 + 1, dtype=torch.float32, device="cuda")
+    with pytest.raises(agnes.AgnesError):
+        b.sage_forward(tw, tb, out=big[1:].view(rows, 32))
+    wbig = torch.empty(tw[0].numel() + 1, dtype=torch.int16, device="cuda")
+    wbig[1:].copy_(tw[0].view(-1))
+    with pytest.raises(agnes.AgnesError):
+        b.sage_forward([wbig[1:].view(tw[0].shape), tw[1]], tb)
+    out = b.sage_forward(tw, tb)                     # the batch is still usable
+    torch.cuda.synchronize()
+    assert out.shape == (rows, 32) and bool(torch.isfinite(out).all())
     b.close()
     store.close()
