@@ -12,6 +12,7 @@
 // is one GEMM over the whole hyperbatch.
 #include <algorithm>
 #include <cstring>
+#include <type_traits>
 
 #include "device.hpp"
 #include "runtime.hpp"
@@ -148,9 +149,9 @@ __global__ __launch_bounds__(kBlock) void k_sage_agg(const InT* __restrict__ hin
 // r = 0..15.  W is stored output-major, so both tiles sit in LDS with k
 // innermost and every operand is one 16-byte LDS read.  W's rows go in as the
 // first operand and A's as the second, so D is a block of Z^T: lane l holds
-// row l % 32 of Z and four adjacent columns per group of four registers,
-// written with one 8-byte (bf16) or 16-byte (float) store.  The next K step's tiles
-// are loaded into registers while the MFMAs consume the current ones.
+// row l % 32 of Z and four adjacent columns per group of four registers.  The
+// next K step's tiles are loaded into registers while the MFMAs consume the
+// current ones.
 constexpr int kGM = 128, kGN = 128, kGK = 64, kGKP = kGK + 8;   // padded LDS row (uint16)
 constexpr int kGLoads = kGM * kGK / 8 / kBlock;                 // 16-byte pieces per thread per tile (4)
 
@@ -158,8 +159,10 @@ template <bool RELU, bool OUT_F32>
 __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
                                                       const float* __restrict__ bias, int64_t M, int N, int K,
                                                       void* __restrict__ Z) {
-    __shared__ uint16_t As[kGM][kGKP];
-    __shared__ uint16_t Bs[kGN][kGKP];
+    // one LDS block: the operand tiles during the K loop, the output tile after it
+    __shared__ __attribute__((aligned(16))) uint16_t smem[(kGM + kGN) * kGKP];
+    uint16_t (*As)[kGKP] = reinterpret_cast<uint16_t (*)[kGKP]>(smem);
+    uint16_t (*Bs)[kGKP] = reinterpret_cast<uint16_t (*)[kGKP]>(smem + kGM * kGKP);
     const int lane = lane_id(), w = wave_id(), t = threadIdx.x;
     // Tile of workgroup i (1-D grid): runs of 8 NB workgroups cover 8 row
     // blocks x NB column blocks.  Workgroups i and i + 8 share an XCD (they are
@@ -219,28 +222,54 @@ __global__ __launch_bounds__(kBlock) void k_sage_gemm(const uint16_t* __restrict
                     acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[jj], a[i], acc[i][jj], 0, 0, 0);
         }
     }
-    // N is a multiple of 32 (checked on the host), so a group of four columns
-    // that starts inside Z ends inside it.
+    // Epilogue through LDS: the tile (bias added, ReLU, converted) is written
+    // there in the MFMA's layout and leaves as whole rows of 16-byte pieces, so
+    // every line of Z is written by one store instruction (stored straight from
+    // the MFMA layout, the partial lines doubled Z's HBM write traffic).  A
+    // float tile is larger than the operand tiles, so it leaves in two passes of
+    // 64 rows: rows i = 0 of every wave's quarter, then rows i = 1.  N is a
+    // multiple of 32 (checked on the host), so a piece or a group of four
+    // columns that starts inside Z ends inside it.
+    typedef typename std::conditional<OUT_F32, float, uint16_t>::type OutT;
+    constexpr int PASSES = OUT_F32 ? 2 : 1;
+    constexpr int RP = kGM / PASSES;                    // tile rows per pass
+    constexpr int CE = 16 / (int)sizeof(OutT);          // elements per 16-byte piece
+    constexpr int CP = kGN + CE;                        // padded LDS row (elements)
+    static_assert(RP * CP * sizeof(OutT) <= sizeof(smem), "the output tile fits the operand tiles' LDS");
+    OutT (*Cs)[CP] = reinterpret_cast<OutT (*)[CP]>(smem);
 #pragma unroll
-    for (int i = 0; i < 2; i++)
+    for (int pass = 0; pass < PASSES; pass++) {
+        __syncthreads();                                // LDS is free: operands consumed, previous pass written out
 #pragma unroll
-        for (int jj = 0; jj < 2; jj++) {
-            const int64_t gm = m0 + wm + i * 32 + (lane & 31);
-            if (gm >= M) continue;
+        for (int i = 0; i < 2; i++) {
+            if (PASSES == 2 && i != pass) continue;
+            const int lrow = PASSES == 1 ? wm + i * 32 + (lane & 31) : (wm >> 1) + (lane & 31);
 #pragma unroll
-            for (int g = 0; g < 4; g++) {
-                const int gn = n0 + wn + jj * 32 + g * 8 + (lane >> 5) * 4;
-                if (gn >= N) continue;
-                float z[4];
+            for (int jj = 0; jj < 2; jj++)
 #pragma unroll
-                for (int c = 0; c < 4; c++) {
-                    z[c] = acc[i][jj][g * 4 + c] + bias[gn + c];
-                    if (RELU) z[c] = z[c] > 0.f ? z[c] : 0.f;
+                for (int g = 0; g < 4; g++) {
+                    const int c = wn + jj * 32 + g * 8 + (lane >> 5) * 4;
+                    if (n0 + c >= N) continue;
+                    float z[4];
+#pragma unroll
+                    for (int e = 0; e < 4; e++) {
+                        z[e] = acc[i][jj][g * 4 + e] + bias[n0 + c + e];
+                        if (RELU) z[e] = z[e] > 0.f ? z[e] : 0.f;
+                    }
+                    if (OUT_F32) *(f32x4*)&Cs[lrow][c] = f32x4{z[0], z[1], z[2], z[3]};
+                    else *(u16x4*)&Cs[lrow][c] = u16x4{to_bf16(z[0]), to_bf16(z[1]), to_bf16(z[2]), to_bf16(z[3])};
                 }
-                if (OUT_F32) *(f32x4*)((float*)Z + gm * N + gn) = f32x4{z[0], z[1], z[2], z[3]};
-                else *(u16x4*)((uint16_t*)Z + gm * N + gn) = u16x4{to_bf16(z[0]), to_bf16(z[1]), to_bf16(z[2]), to_bf16(z[3])};
-            }
         }
+        __syncthreads();
+        constexpr int PPR = kGN / CE;                   // pieces per tile row
+#pragma unroll
+        for (int q = 0; q < RP * PPR / kBlock; q++) {
+            const int idx = t + q * kBlock, lrow = idx / PPR, c = (idx % PPR) * CE;
+            const int r = PASSES == 1 ? lrow : (lrow / 32) * 64 + pass * 32 + lrow % 32;
+            const int64_t gm = m0 + r;
+            if (gm < M && n0 + c < N) *(u32x4s*)((OutT*)Z + gm * N + n0 + c) = *(const u32x4s*)&Cs[lrow][c];
+        }
+    }
 }
 
 template <typename InT, int LPR>
