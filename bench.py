@@ -34,16 +34,17 @@ GATHER_TRAFFIC_FILE = os.path.join("profiles", "k_gather_rows.rmat-2^23.hbm-traf
 
 
 def gather_fingerprint(root: str) -> str:
-    """sha256 of the row-copy kernel's source and its default launch shape: the
-    measured HBM traffic stays valid only while these are unchanged."""
+    """sha256 of the row-copy kernels' source, their launch code and the default
+    launch shape: the measured HBM traffic stays valid only while these are
+    unchanged."""
     import hashlib
     import re
     src = open(os.path.join(root, "paper_2601_01473_amd", "csrc", "pipeline.hip")).read()
     m = re.search(r"template <[^>]*>\n__global__ __launch_bounds__\(kBlock\) void k_gather_rows\(", src)
-    if m is None or "struct GatherArgs {" not in src[m.start():]:
+    if m is None or "// ----------------------------------------------------------------- staged feature tier" not in src[m.start():]:
         return ""
     a = m.start()
-    b = src.index("struct GatherArgs {", a)
+    b = src.index("// ----------------------------------------------------------------- staged feature tier", a)
     rt = open(os.path.join(root, "paper_2601_01473_amd", "csrc", "runtime.hpp")).read()
     shape = [ln.strip() for ln in rt.splitlines() if ln.strip().startswith(("int gather_groups", "int gather_unroll",
                                                                              "int gather_nt"))]
@@ -389,7 +390,8 @@ def main():
                          "sample-first: the next sampling is enqueued before each gather; gather-first: each "
                          "gather is queued before the previous one is waited for")
     ap.add_argument("--gather-groups", type=int, default=None, help="row-copy kernel workgroups")
-    ap.add_argument("--gather-unroll", type=int, default=None, help="rows in flight per lane group")
+    ap.add_argument("--gather-unroll", type=int, default=None,
+                    help="rows in flight per lane group, 4, 8 or 16 (default: 16 for rows of 1-2 KiB, else 4)")
     ap.add_argument("--gather-nt", type=int, default=None, help="1 = non-temporal row stores, 0 = ordinary")
     ap.add_argument("--gather-chunks", type=int, default=None, help="launches the row copy is split into")
     ap.add_argument("--sampling-graph", type=int, choices=[0, 1], default=0,

@@ -238,7 +238,8 @@ agnes_status agnes_set_device_allocator(agnes_device_alloc_fn alloc, agnes_devic
  *     [8, 2^22] (default 2^22); a launch never takes more workgroups than it
  *     has blocks of rows.  Fewer leave room for another stream's work.
  *   AGNES_OPT_GATHER_UNROLL: rows each lane group keeps in flight, 4, 8 or
- *     16 (default 4).
+ *     16; 0 (default) picks by row width: 16 for rows of 1 KiB up to 2 KiB
+ *     (one 16-byte piece per lane), 4 for all others.
  *   AGNES_OPT_GATHER_NONTEMPORAL: 1 = write gathered rows with non-temporal
  *     stores (default), 0 = ordinary stores.
  *   AGNES_OPT_GATHER_CHUNKS: the row copy runs as this many consecutive

@@ -246,8 +246,8 @@ agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_
             AGNES_REQUIRE(value >= 8 && value <= (1 << 22), AGNES_ERR_INVALID, "gather groups must be in [8, 2^22]");
             s->gather_groups = (int)value;
         } else if (opt == AGNES_OPT_GATHER_UNROLL) {
-            AGNES_REQUIRE(value == 4 || value == 8 || value == 16, AGNES_ERR_INVALID,
-                          "gather unroll must be 4, 8 or 16");
+            AGNES_REQUIRE(value == 0 || value == 4 || value == 8 || value == 16, AGNES_ERR_INVALID,
+                          "gather unroll must be 0, 4, 8 or 16");
             s->gather_unroll = (int)value;
         } else if (opt == AGNES_OPT_GATHER_NONTEMPORAL) {
             s->gather_nt = value ? 1 : 0;

@@ -955,6 +955,12 @@ static void launch_gather_rows_upr(const GatherArgs& a, int groups, int unroll, 
 // list is copied in `chunks` consecutive launches of groups/chunks workgroups.
 template <typename Unit>
 static void launch_gather(const GatherArgs& all, int groups, int unroll, bool nt, int chunks, hipStream_t st) {
+    // Rows in flight per lane group when the store leaves it open: 16 for rows
+    // of one 16-byte piece per lane (1 KiB up to 2 KiB), where a wave's 16
+    // entries also let more repeats of a node reuse its row; 4 elsewhere, where
+    // more rows in flight cost occupancy (2 KiB rows hold two pieces per lane)
+    // or lane groups already keep enough bytes moving.
+    if (unroll == 0) unroll = (sizeof(Unit) == 16 && all.row_units >= 64 && all.row_units < 128) ? 16 : 4;
     chunks = (int)std::max<int64_t>(1, std::min<int64_t>(chunks, all.rows));
     for (int c = 0; c < chunks; c++) {
         GatherArgs a = all;

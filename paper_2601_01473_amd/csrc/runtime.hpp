@@ -226,7 +226,7 @@ struct Store {
     int profile = 0;
     int sampling_graph = 0;           // 1 = replay the sampling kernels from a captured HIP graph
     int gather_groups = 1 << 22;      // workgroups of the row-copy kernel (upper bound)
-    int gather_unroll = 4;            // rows in flight per lane group (4, 8 or 16)
+    int gather_unroll = 0;            // rows in flight per lane group (4, 8 or 16; 0 = by row width)
     int gather_nt = 1;                // 1 = non-temporal stores of the gathered rows
     int gather_chunks = 1;            // consecutive launches the row copy is split into
 };

@@ -345,7 +345,8 @@ def test_gather_launch_shapes_do_not_change_results(agnes, rows_dim, dtype):
     want = oracle.hyperbatch_stats(off, block, fb.shape[1], ref, len(fan))
     for groups, unroll, nt, chunks in [(8, 4, True, 1), (8, 16, False, 3), (24, 8, True, 1),
                                        (2048, 4, False, 7), (65536, 8, True, 64), (1000, 16, True, 2),
-                                       (1 << 22, 4, True, 1), (1 << 22, 16, False, 5)]:
+                                       (1 << 22, 4, True, 1), (1 << 22, 16, False, 5), (1 << 22, 0, True, 1),
+                                       (64, 0, False, 3)]:
         log("gather shape", rows_dim, groups, unroll, nt, chunks)
         store.set_gather_shape(groups, unroll, nt, chunks)
         b = store.prepare(t, fan, seed=9, mb_base=0)
