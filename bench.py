@@ -370,7 +370,9 @@ def copy_calibration(torch, nbytes=4 << 30, reps=5):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=100,
+                    help="timed steps; the pipeline fills and drains inside the timed region (about 0.6 ms at "
+                         "the 2^23-node workload), so more steps come closer to a long run's steady state")
     ap.add_argument("--warmup", type=int, default=5,
                     help="untimed steps before the timed ones; raised to depth + 2 so that every batch slot "
                          "is allocated before timing (the JSON line reports the number run)")
