@@ -87,37 +87,32 @@ __global__ void k_scan_reduce(const T* in, const int64_t* n_dev, int G, int64_t*
     }
 }
 
-__global__ void k_scan_top(int64_t* partials, int G, const int64_t* n_dev, int64_t* out,
-                           int64_t* total_dev) {
-    __shared__ int64_t lds[kWavesPerBlock];
-    // G <= kScanGroups = 4 * kBlock: four consecutive partials per thread
-    int64_t v[4];
-    int64_t local = 0;
-    for (int k = 0; k < 4; k++) {
-        int i = threadIdx.x * 4 + k;
-        v[k] = (i < G) ? partials[i] : 0;
-        local += v[k];
-    }
-    int64_t total;
-    int64_t ex = block_exclusive_scan(local, lds, total);
-    for (int k = 0; k < 4; k++) {
-        int i = threadIdx.x * 4 + k;
-        if (i < G) partials[i] = ex;
-        ex += v[k];
-    }
-    if (threadIdx.x == 0) {
-        out[*n_dev] = total;
-        if (total_dev) *total_dev = total;
-    }
-}
-
+// Each block adds the partial sums of the blocks before it itself (G <=
+// kScanGroups = 4 * kBlock: four per thread), so no separate launch scans
+// them; block 0 also writes the total after the last element and to
+// total_dev.
 template <typename T>
 __global__ void k_scan_final(const T* in, int64_t* out, const int64_t* n_dev, int G,
-                             const int64_t* partials) {
+                             const int64_t* partials, int64_t* total_dev) {
     __shared__ int64_t lds[kWavesPerBlock];
+    const int64_t n = *n_dev;
     int64_t lo, hi;
-    scan_range(*n_dev, G, blockIdx.x, lo, hi);
-    int64_t carry = partials[blockIdx.x];
+    scan_range(n, G, blockIdx.x, lo, hi);
+    int64_t before = 0, all = 0;
+    for (int k = 0; k < 4; k++) {
+        const int i = threadIdx.x * 4 + k;
+        const int64_t v = (i < G) ? partials[i] : 0;
+        all += v;
+        if (i < (int)blockIdx.x) before += v;
+    }
+    int64_t carry, total;
+    (void)block_exclusive_scan(before, lds, carry);
+    __syncthreads();                                  // lds is reused
+    (void)block_exclusive_scan(all, lds, total);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        out[n] = total;
+        if (total_dev) *total_dev = total;
+    }
     for (int64_t base = lo; base < hi; base += kScanTile) {
         int64_t v[kScanItems];
         int64_t local = 0;
@@ -146,8 +141,7 @@ static void scan_impl(const T* in, int64_t* out, const int64_t* n_dev, int64_t n
     int64_t g = (n_max + kScanTile - 1) / kScanTile;
     int G = (int)(g < 1 ? 1 : (g > kScanGroups ? kScanGroups : g));
     hipLaunchKernelGGL(k_scan_reduce<T>, dim3(G), dim3(kBlock), 0, st, in, n_dev, G, partials, nonzero);
-    hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, st, partials, G, n_dev, out, total_dev);
-    hipLaunchKernelGGL(k_scan_final<T>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials);
+    hipLaunchKernelGGL(k_scan_final<T>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials, total_dev);
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
