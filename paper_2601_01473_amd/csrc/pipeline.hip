@@ -85,19 +85,19 @@ struct ChainParams {
     int64_t mb_base;          // global index of minibatch 0
 };
 
-__global__ void k_params(ChainParams* p, const int32_t* targets, uint64_t seed, int64_t mb_base) {
+// Also clears the hyperbatch's counters (one launch instead of two at the head
+// of every chain).
+__global__ void k_params(ChainParams* p, const int32_t* targets, uint64_t seed, int64_t mb_base, Ctl* ctl,
+                         int64_t ntargets) {
+    int64_t* c = (int64_t*)ctl;
+    for (int i = threadIdx.x; i < (int)(sizeof(Ctl) / 8); i += kBlock) c[i] = 0;
+    __syncthreads();
     if (threadIdx.x == 0) {
         p->targets = targets;
         p->seed = seed;
         p->mb_base = mb_base;
+        ctl->targets = ntargets;
     }
-}
-
-__global__ void k_ctl_init(Ctl* ctl, int64_t targets) {
-    int64_t* p = (int64_t*)ctl;
-    for (int i = threadIdx.x; i < (int)(sizeof(Ctl) / 8); i += kBlock) p[i] = 0;
-    __syncthreads();
-    if (threadIdx.x == 0) ctl->targets = targets;
 }
 
 // Targets become the first B nodes of every minibatch.  An out-of-range target
@@ -1381,7 +1381,6 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     Ctl* ctl = w.sync.as<Ctl>();
     int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
     int64_t* ec = (int64_t*)((char*)w.sync.ptr + y.ecount);
-    hipLaunchKernelGGL(k_ctl_init, dim3(1), dim3(kBlock), 0, st, ctl, (int64_t)H * B);
     hipLaunchKernelGGL(k_init, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
                        w.params.as<ChainParams>(), H, B, s.num_nodes, g.capN, w.nodes.as<int32_t>(),
                        w.size.as<int32_t>(), w.newcnt.as<int64_t>(), w.skey.as<uint32_t>(), ctl);
@@ -1483,7 +1482,8 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
 
     b.prof = s.profile;
     if (b.prof) AGNES_CHECK_HIP(hipEventRecord(w.ev[0], st));
-    hipLaunchKernelGGL(k_params, dim3(1), dim3(kWave), 0, st, w.params.as<ChainParams>(), targets, seed, mb_base);
+    hipLaunchKernelGGL(k_params, dim3(1), dim3(kBlock), 0, st, w.params.as<ChainParams>(), targets, seed, mb_base,
+                       w.sync.as<Ctl>(), (int64_t)H * B);
     AGNES_CHECK_HIP(hipGetLastError());
     // With the graph option, a shape seen twice in a row is captured once and
     // then replayed: one graph launch instead of about 25 launches per hop.
