@@ -108,9 +108,16 @@ agnes_status agnes_build_blocks(const agnes_csr* csr, const agnes_features* feat
  * (store, targets, fanouts, seed, mb_base), not on the bucketing, the launch
  * geometry or how minibatches are grouped into hyperbatches.
  *
- * targets: DEVICE int32 [H][B]; distinct within each row, each in [0, N).
+ * targets: HOST int32 [H][B] (Alg. 1's input N, row j = minibatch j); distinct
+ * within each row, each in [0, N).  The call copies them (through a pinned
+ * staging buffer owned by the batch) to the device on hip_stream, so the
+ * caller may reuse the array as soon as the call returns.
  * H in [1, 4096], B >= 1, L in [1, AGNES_MAX_LAYERS], fanouts: host int32 [L],
  * each in [0, 1024].  seed: any 64-bit value.  mb_base >= 0.
+ * Every hop's requests plus sampled edges must stay below 2^32 in the worst
+ * case: H * cap_l * (1 + f_l) < 2^32, where cap_0 = B and cap_{l+1} =
+ * min(cap_l * (1 + f_l), max(num_nodes, B)); otherwise AGNES_ERR_RANGE is
+ * returned before anything is allocated or enqueued.
  * out: if *out is NULL a new batch is created; if it holds a batch previously
  *      returned for the same store, that batch's device buffers are reused (and
  *      grown when needed) and its previous contents are overwritten.
@@ -118,7 +125,8 @@ agnes_status agnes_build_blocks(const agnes_csr* csr, const agnes_features* feat
  * Each batch owns the scratch memory of its hyperbatch, so several batches can
  * be in flight on one store.
  * Errors: INVALID (bad sizes, target out of range or duplicated within a
- * minibatch), RANGE (a minibatch with >= 2^31 nodes or edges), NOMEM, DEVICE.
+ * minibatch), RANGE (a minibatch with >= 2^31 nodes or edges, or the 2^32
+ * bound above), NOMEM, DEVICE.
  * On error *out is NULL and a batch passed in is released.
  */
 agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets, int32_t H,
@@ -126,14 +134,22 @@ agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets
                                       uint64_t seed, int64_t mb_base, void* hip_stream,
                                       agnes_batch** out);
 
+/* The same with the targets already in DEVICE memory (int32 [H][B] on the
+ * store's device; read by kernels on hip_stream, so they must stay valid until
+ * the call returns).  No host copy or upload is made. */
+agnes_status agnes_hyperbatch_prepare_device(agnes_store* store, const int32_t* targets, int32_t H,
+                                             int32_t B, const int32_t* fanouts, int32_t L,
+                                             uint64_t seed, int64_t mb_base, void* hip_stream,
+                                             agnes_batch** out);
+
 /*
  * The same hyperbatch in two steps, so that the sampling of one hyperbatch can
  * run while the gather of another streams rows (Sec. 3.4(4): work continues
  * while data moves).  agnes_hyperbatch_prepare = begin + finish + wait.
  *
- * agnes_hyperbatch_begin: same arguments and checks as prepare; enqueues the L
- *   sampling hops on hip_stream and returns without waiting.  `targets` must
- *   stay valid until the hyperbatch is finished.  A batch that is still
+ * agnes_hyperbatch_begin: same arguments and checks as prepare (HOST targets,
+ *   copied by the call); enqueues their upload and the L sampling hops on
+ *   hip_stream and returns without waiting.  A batch that is still
  *   gathering from an earlier hyperbatch may be passed in: the call first waits
  *   for that gather; the batch's previous views become invalid.
  * agnes_batch_finish: waits on the host for the output sizes of the begun
@@ -147,13 +163,23 @@ agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets
 agnes_status agnes_hyperbatch_begin(agnes_store* store, const int32_t* targets, int32_t H,
                                     int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed,
                                     int64_t mb_base, void* hip_stream, agnes_batch** out);
+/* agnes_hyperbatch_begin_device: the same with DEVICE targets, which must stay
+ *   valid until the hyperbatch is finished. */
+agnes_status agnes_hyperbatch_begin_device(agnes_store* store, const int32_t* targets, int32_t H,
+                                           int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed,
+                                           int64_t mb_base, void* hip_stream, agnes_batch** out);
 agnes_status agnes_batch_finish(agnes_batch* batch, void* hip_stream);
 agnes_status agnes_batch_wait(agnes_batch* batch);
 
 #define AGNES_MAX_LAYERS 8
 
-/* Read-only view of a batch.  Host arrays stay valid until the batch is freed
- * or reused; device arrays likewise.
+/* Read-only view of a batch: Alg. 1's outputs, the sampled node set N_s of
+ * every minibatch (nodes, with the per-hop CSR blocks that the sampling loop
+ * builds) and the gathered feature rows F_g (features, the gathering loop's
+ * output), together with the offsets that locate each minibatch in them.
+ * Host arrays stay valid until the batch is freed or reused; device arrays
+ * likewise.  Fails with AGNES_ERR_INVALID for a batch whose hyperbatch has not
+ * been finished (agnes_batch_finish or prepare); ownership stays with the batch.
  *   node_off[H+1]: minibatch j owns nodes[node_off[j] .. node_off[j+1]) and the
  *                  same rows of features.
  *   layer_sizes[H*(L+1)]: |D_0| = B, then the node count after each hop.
@@ -178,10 +204,15 @@ typedef struct {
 
 agnes_status agnes_batch_view_get(const agnes_batch* batch, agnes_batch_view* out);
 
-/* Exact integer statistics of a prepared hyperbatch (per hop l: requests R_l,
- * sampled edges S_l, new nodes U_l, non-empty topology-block rows of Bck T_l;
- * gathered rows sum |N_j|, distinct rows, non-empty feature-block rows) and the
- * device time of each phase when profiling is on (else -1). */
+/* Exact integer statistics of a prepared hyperbatch and the device time of
+ * each phase when profiling is on (else -1).  Per hop l: requests R_l (the
+ * nodes of every minibatch that the hop samples from), sampled edges S_l, new
+ * nodes U_l, and T_l, the non-empty rows of the bucket matrix Bck (Sec. 3.4(3):
+ * one row per topology block, the topology blocks the hop loads in Alg. 1's
+ * sampling loop); then the gathered rows sum_j |N_j|, the distinct rows among
+ * them, and the non-empty feature-block rows (the feature blocks Alg. 1's
+ * gathering loop loads).  Waits for the batch; out is caller-owned.  Fails
+ * with AGNES_ERR_INVALID for a batch with no finished hyperbatch. */
 typedef struct {
     int32_t L;
     int64_t requests[AGNES_MAX_LAYERS];

@@ -24,7 +24,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-o", tmp, _SRC])
+        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -54,6 +54,9 @@ def lib():
                                        i64, vp, i64, vp, vp, vp]
         L.oracle_gather.restype = None
         L.oracle_gather.argtypes = [vp, i64, vp, i64, vp]
+        L.oracle_hyperbatch_threads.restype = ctypes.c_int
+        L.oracle_hyperbatch_threads.argtypes = [i64, vp, vp, vp, i64, vp, i32, i32, vp, i32, u64, i64, i32,
+                                                vp, vp, vp, ctypes.c_uint32, vp, vp]
         L.oracle_hyperbatch_blocked.restype = ctypes.c_int
         L.oracle_hyperbatch_blocked.argtypes = [i64, vp, vp, i64, vp, i64, vp, i32, i32, vp, i32,
                                                 u64, i64, i64, vp, vp, vp, i64, vp, i64, vp, vp, vp]
@@ -176,6 +179,38 @@ class Oracle:
         for j in rows:
             out[j] = self.minibatch(targets[j], fanouts, seed, mb_base + j)
         return out
+
+
+class ThreadedRunner:
+    """The plain order over whole hyperbatches on several threads
+    (oracle_hyperbatch_threads): every minibatch runs oracle_minibatch and
+    oracle_gather unchanged; used to time the CPU baseline on all cores."""
+
+    def __init__(self, offsets, indices, features):
+        self.offsets = _as_i64_offsets(offsets)
+        self.indices = np.ascontiguousarray(indices, dtype=np.int32)
+        self.num_nodes = len(self.offsets) - 1
+        f = np.ascontiguousarray(features)
+        self.feat = f.view(np.uint8).reshape(self.num_nodes, -1)
+        self.seen = np.zeros(max(self.num_nodes, 1), np.uint32)
+        self.stamp = 0
+
+    def run(self, targets, fanouts, seed: int, mb_base: int, threads: int = 0) -> dict:
+        t = np.ascontiguousarray(targets, dtype=np.int32)
+        H, B = t.shape
+        fan = np.ascontiguousarray(fanouts, dtype=np.int32)
+        L = len(fan)
+        ls = np.empty((H, L + 1), np.int32)
+        ec = np.empty((H, max(L, 1)), np.int64)
+        self.stamp += 1
+        d = np.zeros(1, np.int64)
+        used = np.zeros(1, np.int32)
+        rc = lib().oracle_hyperbatch_threads(self.num_nodes, _p(self.offsets), _p(self.indices), _p(self.feat),
+                                             self.feat.shape[1], _p(t), H, B, _p(fan), L, seed, mb_base, threads,
+                                             _p(ls), _p(ec), _p(self.seen), self.stamp, _p(d), _p(used))
+        if rc != 0:
+            raise RuntimeError("oracle_hyperbatch_threads failed with code %d" % rc)
+        return dict(layer_sizes=ls, edge_counts=ec[:, :L], distinct=int(d[0]), threads=int(used[0]))
 
 
 def gather(features: np.ndarray, nodes) -> np.ndarray:

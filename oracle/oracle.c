@@ -33,6 +33,7 @@
  * (oracle_minibatch) and the block-bucketed hyperbatch order of Alg. 1
  * (oracle_hyperbatch_blocked).  They must produce identical results.
  */
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -432,4 +433,76 @@ done:
     free(cell_cnt); free(cell_ptr); free(cell_fill); free(cell_items);
     free(samp); free(samp_k); free(pos); free(seen_any);
     return rc;
+}
+
+/* ------------------------------------------------------ all cores (CPU baseline) */
+
+/*
+ * The plain order on every core: the minibatches of a hyperbatch are
+ * independent (each has its own random stream, keyed by its global index), so
+ * threads take whole minibatches, each running oracle_minibatch and
+ * oracle_gather unchanged on buffers of its own.  Used only to time the CPU
+ * baseline; nothing here computes anything the plain functions do not.
+ *
+ * Per minibatch j the outputs are its layer sizes (layer_sizes[j][L+1]) and
+ * edge counts (edge_counts[j][L]); *distinct receives the number of distinct
+ * nodes over the hyperbatch (the rows read once by a block-bucketed gather),
+ * counted through seen[num_nodes], whose entries must differ from `stamp` on
+ * entry.  threads <= 0 leaves the count to the OpenMP runtime; the number used
+ * is returned in *used.  Returns ORACLE_OK or the first failing code.
+ */
+int oracle_hyperbatch_threads(int64_t num_nodes, const int64_t* offsets, const int32_t* indices,
+                              const uint8_t* feat, int64_t row_bytes, const int32_t* targets, int32_t H,
+                              int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
+                              int32_t threads, int32_t* layer_sizes, int64_t* edge_counts, uint32_t* seen,
+                              uint32_t stamp, int64_t* distinct, int32_t* used) {
+    /* per-minibatch capacities, as for one call of oracle_minibatch */
+    int64_t cap_n = B, cap_rp = 0, cap_e = 0;
+    for (int32_t l = 0; l < L; l++) {
+        cap_rp += cap_n + 1;
+        cap_e += cap_n * (int64_t)fanouts[l];
+        cap_n = cap_n * (1 + (int64_t)fanouts[l]);
+        if (cap_n > num_nodes) cap_n = num_nodes;
+    }
+    if (cap_n < B) cap_n = B;
+    int rc_all = ORACLE_OK;
+    int64_t nd_all = 0;
+    int nthr = 1;
+#pragma omp parallel num_threads(threads > 0 ? threads : omp_get_max_threads()) reduction(+ : nd_all)
+    {
+#pragma omp single
+        nthr = omp_get_num_threads();
+        int32_t* id = (int32_t*)malloc((size_t)(num_nodes > 0 ? num_nodes : 1) * sizeof(int32_t));
+        int32_t* nodes = (int32_t*)malloc((size_t)cap_n * sizeof(int32_t));
+        int32_t* rp = (int32_t*)malloc((size_t)(cap_rp > 0 ? cap_rp : 1) * sizeof(int32_t));
+        int32_t* col = (int32_t*)malloc((size_t)(cap_e > 0 ? cap_e : 1) * sizeof(int32_t));
+        uint8_t* rows = (uint8_t*)malloc((size_t)cap_n * (size_t)row_bytes);
+        int ok = id && nodes && rp && col && rows;
+        if (ok)
+            for (int64_t i = 0; i < num_nodes; i++) id[i] = -1;
+#pragma omp for schedule(dynamic, 1)
+        for (int32_t j = 0; j < H; j++) {
+            if (!ok) {
+#pragma omp critical
+                rc_all = ORACLE_NOMEM;
+                continue;
+            }
+            int32_t* ls = layer_sizes + (int64_t)j * (L + 1);
+            int rc = oracle_minibatch(num_nodes, offsets, indices, targets + (int64_t)j * B, B, fanouts, L, seed,
+                                      mb_base + j, cap_n, nodes, ls, edge_counts + (int64_t)j * L, cap_rp, rp,
+                                      cap_e, col, NULL, id);
+            if (rc != ORACLE_OK) {
+#pragma omp critical
+                if (rc_all == ORACLE_OK) rc_all = rc;
+                continue;
+            }
+            oracle_gather(feat, row_bytes, nodes, ls[L], rows);
+            for (int64_t i = 0; i < ls[L]; i++)
+                if (__atomic_exchange_n(&seen[nodes[i]], stamp, __ATOMIC_RELAXED) != stamp) nd_all++;
+        }
+        free(id); free(nodes); free(rp); free(col); free(rows);
+    }
+    *distinct = nd_all;
+    *used = nthr;
+    return rc_all;
 }

@@ -1,11 +1,12 @@
 """MI355X (gfx950) hyperbatch GNN data preparation (AGNES, arXiv 2601.01473).
 
 The work runs in libagnes.so (HIP kernels behind the C ABI of include/agnes.h).
-This package marshals arguments: numpy arrays in, torch CUDA tensors (device
-memory, streams) for the targets, and copies of the outputs back to numpy.
+This package marshals arguments: numpy arrays in, targets as a host numpy
+array (uploaded by the library) or a torch CUDA tensor (already on the device),
+torch streams, and copies of the outputs back to numpy.
 
     store = Store(offsets, indices, features, block_bytes=65536)
-    batch = store.prepare(targets_cuda_int32_HxB, fanouts=[25, 10], seed=0)
+    batch = store.prepare(targets_int32_HxB, fanouts=[25, 10], seed=0)
     out = batch.to_host()          # per-minibatch nodes, per-hop CSR, features
 """
 from __future__ import annotations
@@ -19,6 +20,7 @@ from . import _binding as B
 from ._binding import AgnesError, agnes_batch_stats, agnes_batch_view_get, agnes_build_blocks  # noqa: F401
 from ._binding import agnes_batch_finish, agnes_batch_wait, agnes_hyperbatch_begin  # noqa: F401
 from ._binding import agnes_free, agnes_hyperbatch_prepare, agnes_last_error  # noqa: F401
+from ._binding import agnes_hyperbatch_begin_device, agnes_hyperbatch_prepare_device  # noqa: F401
 from ._binding import agnes_store_info, agnes_store_object_table, agnes_store_set_option  # noqa: F401
 from ._binding import agnes_batch_tier_stats, agnes_build_blocks_staged, agnes_sage_forward  # noqa: F401
 from ._binding import agnes_build_blocks_cached, agnes_philox4x64_10, agnes_set_device_allocator  # noqa: F401
@@ -159,32 +161,44 @@ class Store:
         if nontemporal is not None:
             agnes_store_set_option(self.handle, B.AGNES_OPT_GATHER_NONTEMPORAL, 1 if nontemporal else 0)
 
-    def prepare(self, targets: torch.Tensor, fanouts, seed: int = 0, mb_base: int = 0,
+    def prepare(self, targets, fanouts, seed: int = 0, mb_base: int = 0,
                 batch: "Batch | None" = None, stream=None) -> "Batch":
-        """One hyperbatch, synchronously: targets is a CUDA int32 tensor [H, B]."""
-        return self._start(agnes_hyperbatch_prepare, targets, fanouts, seed, mb_base, batch, stream)
+        """One hyperbatch, synchronously.  targets: int32 [H, B], a host numpy
+        array (uploaded by the call) or a CUDA tensor (read in place)."""
+        return self._start(agnes_hyperbatch_prepare, agnes_hyperbatch_prepare_device, targets, fanouts, seed,
+                           mb_base, batch, stream)
 
-    def begin(self, targets: torch.Tensor, fanouts, seed: int = 0, mb_base: int = 0,
+    def begin(self, targets, fanouts, seed: int = 0, mb_base: int = 0,
               batch: "Batch | None" = None, stream=None) -> "Batch":
         """Enqueue the sampling hops of one hyperbatch and return (see Batch.finish)."""
-        return self._start(agnes_hyperbatch_begin, targets, fanouts, seed, mb_base, batch, stream)
+        return self._start(agnes_hyperbatch_begin, agnes_hyperbatch_begin_device, targets, fanouts, seed,
+                           mb_base, batch, stream)
 
-    def _start(self, fn, targets, fanouts, seed, mb_base, batch, stream):
-        if not (isinstance(targets, torch.Tensor) and targets.is_cuda and targets.dtype == torch.int32):
-            raise TypeError("targets must be a CUDA int32 tensor [H, B]")
-        if targets.dim() != 2:
+    def _start(self, fn_host, fn_dev, targets, fanouts, seed, mb_base, batch, stream):
+        if isinstance(targets, torch.Tensor):
+            if not (targets.is_cuda and targets.dtype == torch.int32):
+                raise TypeError("a targets tensor must be a CUDA int32 tensor [H, B]")
+            t = targets.contiguous()
+            fn, ptr = fn_dev, t.data_ptr()
+        elif isinstance(targets, np.ndarray):
+            if targets.dtype != np.int32:
+                raise TypeError("a targets array must be int32 [H, B]")
+            t = np.ascontiguousarray(targets)
+            fn, ptr = fn_host, t.ctypes.data
+        else:
+            raise TypeError("targets must be an int32 numpy array or CUDA tensor [H, B]")
+        if t.ndim != 2:
             raise ValueError("targets must be [H, B]")
-        t = targets.contiguous()
         H, Bsz = t.shape
         fan = (ctypes.c_int32 * len(fanouts))(*[int(f) for f in fanouts])
         prev = batch.handle if batch is not None else None
         if batch is not None:
             batch.handle = None          # ownership passes to the call (released on error)
-        h = fn(self.handle, t.data_ptr(), H, Bsz, fan, len(fanouts), seed, mb_base, _stream_handle(stream), prev)
+        h = fn(self.handle, ptr, H, Bsz, fan, len(fanouts), seed, mb_base, _stream_handle(stream), prev)
         if batch is None:
             batch = Batch(self)
         batch.handle = h
-        batch._targets = t               # kept alive until the hyperbatch is finished
+        batch._targets = t               # a device tensor is read until the hyperbatch is finished
         return batch
 
     def close(self) -> None:

@@ -24,7 +24,7 @@ AGNES_OPT_GATHER_CHUNKS = 5
 AGNES_OPT_SAMPLING_GRAPH = 6
 
 EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_build_blocks_cached", "agnes_hyperbatch_prepare",
-            "agnes_hyperbatch_begin", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
+            "agnes_hyperbatch_prepare_device", "agnes_hyperbatch_begin", "agnes_hyperbatch_begin_device", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
             "agnes_batch_stats", "agnes_batch_tier_stats", "agnes_store_set_option", "agnes_store_info",
             "agnes_store_object_table", "agnes_sage_forward", "agnes_philox4x64_10", "agnes_set_device_allocator", "agnes_free",
             "agnes_last_error"]
@@ -117,6 +117,9 @@ def lib():
     L.agnes_hyperbatch_prepare.argtypes = [vp, vp, i32, i32, vp, i32, u64, i64, vp, ctypes.POINTER(vp)]
     L.agnes_hyperbatch_begin.restype = st
     L.agnes_hyperbatch_begin.argtypes = [vp, vp, i32, i32, vp, i32, u64, i64, vp, ctypes.POINTER(vp)]
+    for name in ("agnes_hyperbatch_prepare_device", "agnes_hyperbatch_begin_device"):
+        getattr(L, name).restype = st
+        getattr(L, name).argtypes = [vp, vp, i32, i32, vp, i32, u64, i64, vp, ctypes.POINTER(vp)]
     L.agnes_batch_finish.restype = st
     L.agnes_batch_finish.argtypes = [vp, vp]
     L.agnes_batch_wait.restype = st
@@ -184,22 +187,39 @@ def agnes_sage_forward(batch: int, model: agnes_sage_model, out_ptr: int, stream
                                    ctypes.c_void_p(stream)))
 
 
+def _start_call(fn, store, targets_ptr, H, B, fanouts_arr, L, seed, mb_base, stream, batch):
+    out = ctypes.c_void_p(batch)
+    check(fn(ctypes.c_void_p(store), ctypes.c_void_p(targets_ptr), H, B, fanouts_arr, L, seed, mb_base,
+             ctypes.c_void_p(stream), ctypes.byref(out)))
+    return out.value
+
+
 def agnes_hyperbatch_prepare(store: int, targets_ptr: int, H: int, B: int, fanouts_arr, L: int,
                              seed: int, mb_base: int, stream: int = 0, batch: int | None = None) -> int:
-    out = ctypes.c_void_p(batch)
-    check(lib().agnes_hyperbatch_prepare(ctypes.c_void_p(store), ctypes.c_void_p(targets_ptr), H, B,
-                                         fanouts_arr, L, seed, mb_base, ctypes.c_void_p(stream),
-                                         ctypes.byref(out)))
-    return out.value
+    """targets_ptr: host int32 [H*B]."""
+    return _start_call(lib().agnes_hyperbatch_prepare, store, targets_ptr, H, B, fanouts_arr, L, seed, mb_base,
+                       stream, batch)
+
+
+def agnes_hyperbatch_prepare_device(store: int, targets_ptr: int, H: int, B: int, fanouts_arr, L: int,
+                                    seed: int, mb_base: int, stream: int = 0, batch: int | None = None) -> int:
+    """targets_ptr: device int32 [H*B]."""
+    return _start_call(lib().agnes_hyperbatch_prepare_device, store, targets_ptr, H, B, fanouts_arr, L, seed,
+                       mb_base, stream, batch)
 
 
 def agnes_hyperbatch_begin(store: int, targets_ptr: int, H: int, B: int, fanouts_arr, L: int,
                            seed: int, mb_base: int, stream: int = 0, batch: int | None = None) -> int:
-    out = ctypes.c_void_p(batch)
-    check(lib().agnes_hyperbatch_begin(ctypes.c_void_p(store), ctypes.c_void_p(targets_ptr), H, B,
-                                       fanouts_arr, L, seed, mb_base, ctypes.c_void_p(stream),
-                                       ctypes.byref(out)))
-    return out.value
+    """targets_ptr: host int32 [H*B]."""
+    return _start_call(lib().agnes_hyperbatch_begin, store, targets_ptr, H, B, fanouts_arr, L, seed, mb_base,
+                       stream, batch)
+
+
+def agnes_hyperbatch_begin_device(store: int, targets_ptr: int, H: int, B: int, fanouts_arr, L: int,
+                                  seed: int, mb_base: int, stream: int = 0, batch: int | None = None) -> int:
+    """targets_ptr: device int32 [H*B]."""
+    return _start_call(lib().agnes_hyperbatch_begin_device, store, targets_ptr, H, B, fanouts_arr, L, seed,
+                       mb_base, stream, batch)
 
 
 def agnes_philox4x64_10(counters, keys):

@@ -1,8 +1,11 @@
 // The C ABI (include/agnes.h): argument checks, error mapping and handle
 // management around the store (store.hip) and the pipeline (pipeline.hip).
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
+
+#include <rocprofiler-sdk-roctx/roctx.h>
 
 #include "runtime.hpp"
 
@@ -17,6 +20,31 @@ DeviceAllocator& device_allocator() {
 
 void set_last_error(const std::string& msg) { g_last_error = msg; }
 void clear_last_error() { g_last_error.clear(); }
+
+bool debug_sync() {
+    static const bool on = [] {
+        const char* v = std::getenv("AGNES_DEBUG_SYNC");
+        return v && v[0] && std::strcmp(v, "0") != 0;
+    }();
+    return on;
+}
+
+void check_launch(hipStream_t st, const char* what) {
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && debug_sync()) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(st, &cs) == hipSuccess && cs == hipStreamCaptureStatusNone) {
+            e = hipStreamSynchronize(st);
+            if (e == hipSuccess) e = hipGetLastError();
+        }
+    }
+    if (e != hipSuccess)
+        throw Error{e == hipErrorOutOfMemory ? AGNES_ERR_NOMEM : AGNES_ERR_DEVICE,
+                    std::string("kernel ") + what + ": " + hipGetErrorString(e)};
+}
+
+Range::Range(const char* name) { (void)roctxRangePushA(name); }
+Range::~Range() { (void)roctxRangePop(); }
 
 template <typename F>
 static agnes_status guarded(F&& f) {
@@ -121,6 +149,7 @@ static void release_batch(Batch* b) {
             if (b->state == kSampled && b->sampled_at) (void)hipEventSynchronize(b->sampled_at);
             if (b->state == kGathering && b->gathered_at) (void)hipEventSynchronize(b->gathered_at);
         }
+        if (b->sage_pending && b->sage_done) (void)hipEventSynchronize(b->sage_done);
         b->magic = 0;
         delete b;
     }
@@ -136,10 +165,9 @@ static Batch* as_batch(void* p) {
 
 extern "C" {
 
-agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets, int32_t H,
-                                      int32_t B, const int32_t* fanouts, int32_t L,
-                                      uint64_t seed, int64_t mb_base, void* hip_stream,
-                                      agnes_batch** out) {
+static agnes_status prepare_impl(agnes_store* store, const int32_t* targets, bool on_host, int32_t H, int32_t B,
+                                 const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
+                                 void* hip_stream, agnes_batch** out) {
     Batch* reuse = (out && *out) ? reinterpret_cast<Batch*>(*out) : nullptr;
     if (out) *out = nullptr;
     Batch* b = nullptr;
@@ -148,7 +176,7 @@ agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets
         Store* s = nullptr;
         b = check_begin(store, targets, H, B, fanouts, L, mb_base, reuse, s);
         hipStream_t st = (hipStream_t)hip_stream;
-        begin_hyperbatch(*s, *b, targets, H, B, fanouts, L, seed, mb_base, st);
+        begin_hyperbatch(*s, *b, targets, on_host, H, B, fanouts, L, seed, mb_base, st);
         finish_hyperbatch(*b, st);
         wait_batch(*b);
         *out = reinterpret_cast<agnes_batch*>(b);
@@ -157,9 +185,9 @@ agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets
     return rc;
 }
 
-agnes_status agnes_hyperbatch_begin(agnes_store* store, const int32_t* targets, int32_t H,
-                                    int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed,
-                                    int64_t mb_base, void* hip_stream, agnes_batch** out) {
+static agnes_status begin_impl(agnes_store* store, const int32_t* targets, bool on_host, int32_t H, int32_t B,
+                               const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
+                               void* hip_stream, agnes_batch** out) {
     Batch* reuse = (out && *out) ? reinterpret_cast<Batch*>(*out) : nullptr;
     if (out) *out = nullptr;
     Batch* b = nullptr;
@@ -167,11 +195,37 @@ agnes_status agnes_hyperbatch_begin(agnes_store* store, const int32_t* targets, 
         AGNES_REQUIRE(out, AGNES_ERR_INVALID, "out must not be NULL");
         Store* s = nullptr;
         b = check_begin(store, targets, H, B, fanouts, L, mb_base, reuse, s);
-        begin_hyperbatch(*s, *b, targets, H, B, fanouts, L, seed, mb_base, (hipStream_t)hip_stream);
+        begin_hyperbatch(*s, *b, targets, on_host, H, B, fanouts, L, seed, mb_base, (hipStream_t)hip_stream);
         *out = reinterpret_cast<agnes_batch*>(b);
     });
     if (rc != AGNES_OK) release_batch(b ? b : reuse);
     return rc;
+}
+
+agnes_status agnes_hyperbatch_prepare(agnes_store* store, const int32_t* targets, int32_t H,
+                                      int32_t B, const int32_t* fanouts, int32_t L,
+                                      uint64_t seed, int64_t mb_base, void* hip_stream,
+                                      agnes_batch** out) {
+    return prepare_impl(store, targets, true, H, B, fanouts, L, seed, mb_base, hip_stream, out);
+}
+
+agnes_status agnes_hyperbatch_prepare_device(agnes_store* store, const int32_t* targets, int32_t H,
+                                             int32_t B, const int32_t* fanouts, int32_t L,
+                                             uint64_t seed, int64_t mb_base, void* hip_stream,
+                                             agnes_batch** out) {
+    return prepare_impl(store, targets, false, H, B, fanouts, L, seed, mb_base, hip_stream, out);
+}
+
+agnes_status agnes_hyperbatch_begin(agnes_store* store, const int32_t* targets, int32_t H,
+                                    int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed,
+                                    int64_t mb_base, void* hip_stream, agnes_batch** out) {
+    return begin_impl(store, targets, true, H, B, fanouts, L, seed, mb_base, hip_stream, out);
+}
+
+agnes_status agnes_hyperbatch_begin_device(agnes_store* store, const int32_t* targets, int32_t H,
+                                           int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed,
+                                           int64_t mb_base, void* hip_stream, agnes_batch** out) {
+    return begin_impl(store, targets, false, H, B, fanouts, L, seed, mb_base, hip_stream, out);
 }
 
 agnes_status agnes_batch_finish(agnes_batch* batch, void* hip_stream) {

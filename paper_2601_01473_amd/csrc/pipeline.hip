@@ -40,6 +40,9 @@ struct Geometry {
     int jbits;
 };
 
+// Edge numbers, sort positions and positions in the join of one hop are
+// 32-bit: a hop whose requests plus sampled edges can reach 2^32 (bound
+// H cap_l (1 + f_l)) is refused here, before anything is allocated or launched.
 static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanouts, int32_t L) {
     Geometry g{};
     g.H = H; g.B = B; g.L = L;
@@ -47,6 +50,9 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
     g.Rmax = 0; g.Smax = 0;
     const int64_t nmax = std::max<int64_t>(s.num_nodes, B);
     for (int l = 0; l < L; l++) {
+        const unsigned __int128 bound = (unsigned __int128)H * (uint64_t)g.cap[l] * (uint64_t)(1 + fanouts[l]);
+        AGNES_REQUIRE(bound < ((unsigned __int128)1 << 32), AGNES_ERR_RANGE,
+                      "a hop's requests and sampled edges can reach 2^32 (H * frontier capacity * (1 + fanout))");
         g.Rmax = std::max<int64_t>(g.Rmax, (int64_t)H * g.cap[l]);
         g.Smax = std::max<int64_t>(g.Smax, (int64_t)H * g.cap[l] * fanouts[l]);
         g.cap[l + 1] = std::min<int64_t>(g.cap[l] * (1 + (int64_t)fanouts[l]), nmax);
@@ -891,7 +897,7 @@ struct GatherArgs {
 template <typename Unit, int LPR, int U, bool NT, bool ONE, bool TIER>
 static void launch_gather_k2(const GatherArgs& a, int G, hipStream_t st) {
     const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
-    hipLaunchKernelGGL((k_gather<Unit, LPR, U, NT, ONE, TIER>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
+    AGNES_LAUNCH((k_gather<Unit, LPR, U, NT, ONE, TIER>), dim3(G), dim3(kBlock), lds, st, (const Unit*)a.feat,
                        (Unit*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
                        a.row_units, a.tbuf, a.rpb, a.tch, a.pool_rows);
 }
@@ -930,11 +936,11 @@ static void launch_gather_rows_k(const GatherArgs& a, int groups, hipStream_t st
     constexpr int64_t per_wg = (int64_t)kWavesPerBlock * U;
     const int G = (int)std::max<int64_t>(1, std::min<int64_t>(groups, (a.rows + per_wg - 1) / per_wg));
     if (a.tbuf)
-        hipLaunchKernelGGL((k_gather_rows<U, UPR, NT, true>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
+        AGNES_LAUNCH((k_gather_rows<U, UPR, NT, true>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
                            (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
                            a.row_units, a.tbuf, a.rpb, a.tch, a.pool_rows);
     else
-        hipLaunchKernelGGL((k_gather_rows<U, UPR, NT, false>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
+        AGNES_LAUNCH((k_gather_rows<U, UPR, NT, false>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
                            (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
                            a.row_units, a.tbuf, a.rpb, a.tch, a.pool_rows);
 }
@@ -1187,17 +1193,17 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     const uint64_t* rlk = w.rl_key[cur].as<uint64_t>();
     const int32_t* rlv = w.rl_val[cur].as<int32_t>();
 
-    hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, l, g.L, g.H, ctl, w.size.as<int32_t>(),
+    AGNES_LAUNCH(k_begin, dim3(1), dim3(kBlock), 0, st, l, g.L, g.H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ecount, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
                        (int64_t*)nullptr, w.topo_part.as<uint32_t>(), gPrev);
-    hipLaunchKernelGGL(k_count<OffT>, dim3(gR), dim3(kBlock), lds_h, st, g.H, g.capN, f, off,
+    AGNES_LAUNCH(k_count<OffT>, dim3(gR), dim3(kBlock), lds_h, st, g.H, g.capN, f, off,
                        w.nodes.as<int32_t>(), w.req_off.as<int64_t>(), w.cnt.as<int32_t>(), ctl);
     scan_counts(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, std::max<int64_t>(1, (int64_t)g.H * g.cap[l]),
                 &ctl->S, part, st);
     const int32_t* adj = s.indices.as<int32_t>();
     int32_t* cg = w.skey.as<int32_t>();
 #define AGNES_SAMPLE(MK)                                                                               \
-    hipLaunchKernelGGL((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, prm,      \
+    AGNES_LAUNCH((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, prm,      \
                        off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),      \
                        w.e_off.as<int64_t>(), cg, w.topo_part.as<uint32_t>(), ctl)
     // the register sampler's work grows with MAXK^2 (ranks) and MAXK/4 (Philox
@@ -1224,15 +1230,15 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     const int64_t tiles_l = ((int64_t)g.H * g.cap[l] * (1 + (int64_t)f)) / kJoinTile + 1;
     const int gJ = (int)std::min<int64_t>(2048, (tiles_l + 1) * kSplitLanes / kBlock + 1);
     int64_t* split = w.split.as<int64_t>();
-    hipLaunchKernelGGL(k_join_split, dim3(gJ), dim3(kBlock), lds_h, st, g.H, w.req_off.as<int64_t>(),
+    AGNES_LAUNCH(k_join_split, dim3(gJ), dim3(kBlock), lds_h, st, g.H, w.req_off.as<int64_t>(),
                        w.e_off.as<int64_t>(), rlk, su, se, split, ctl);
     const int G = join_groups(g.H, tiles_l);
-    hipLaunchKernelGGL(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H), st, g.H,
+    AGNES_LAUNCH(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H), st, g.H,
                        w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se, split, G,
                        w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), b.row_ptr[l].as<int32_t>(), ctl);
-    hipLaunchKernelGGL(k_join_scan, dim3(g.H + 1), dim3(kBlock), 0, st, g.H, G, w.ghist.as<int64_t>(),
+    AGNES_LAUNCH(k_join_scan, dim3(g.H + 1), dim3(kBlock), 0, st, g.H, G, w.ghist.as<int64_t>(),
                        w.gemit.as<int64_t>(), w.newcnt.as<int64_t>(), ctl);
-    hipLaunchKernelGGL(k_join_write, dim3(G), dim3(kBlock), join_write_lds(g.H), st, g.H, g.jbits,
+    AGNES_LAUNCH(k_join_write, dim3(G), dim3(kBlock), join_write_lds(g.H), st, g.H, g.jbits,
                        g.capN, g.rows_max, (int)(l + 1 < g.L), w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se,
                        split, G, w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), w.size.as<int32_t>(),
                        w.nodes.as<int32_t>(), w.rl_key[cur ^ 1].as<uint64_t>(), w.rl_val[cur ^ 1].as<int32_t>(),
@@ -1381,13 +1387,13 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     Ctl* ctl = w.sync.as<Ctl>();
     int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
     int64_t* ec = (int64_t*)((char*)w.sync.ptr + y.ecount);
-    hipLaunchKernelGGL(k_init, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
+    AGNES_LAUNCH(k_init, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
                        w.params.as<ChainParams>(), H, B, s.num_nodes, g.capN, w.nodes.as<int32_t>(),
                        w.size.as<int32_t>(), w.newcnt.as<int64_t>(), w.skey.as<uint32_t>(), ctl);
     int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
                                     w.sval2.as<uint32_t>(), &ctl->targets, (int64_t)H * B, s.node_bits,
                                     w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
-    hipLaunchKernelGGL(k_list0, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
+    AGNES_LAUNCH(k_list0, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
                        in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>(),
                        in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>(), B, w.rl_key[0].as<uint64_t>(),
                        w.rl_val[0].as<int32_t>(), ctl);
@@ -1399,10 +1405,10 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
         cur ^= 1;
     }
     // close the last hop: edge counts, final node counts, output row offsets
-    hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
+    AGNES_LAUNCH(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
                        w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), hop_grid(g, L - 1));
-    hipLaunchKernelGGL(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
+    AGNES_LAUNCH(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
                        (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl);
     AGNES_CHECK_HIP(hipGetLastError());
 }
@@ -1455,14 +1461,18 @@ static void capture_chain(const Store& s, Batch& b, const Geometry& g, const Syn
     b.chain_key = key;
 }
 
-void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
-                      const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
+void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, bool targets_on_host, int32_t H,
+                      int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
                       hipStream_t st) {
+    Range range("agnes_hyperbatch_begin");
     AGNES_REQUIRE(b.state != kSampled, AGNES_ERR_INVALID, "the batch has a hyperbatch begun but not finished");
+    Geometry g = plan(s, H, B, fanouts, L);
     // a batch still gathering: its buffers are in use until the gather ends
     if (b.state == kGathering) wait_batch(b);
     b.state = kIdle;
-    Geometry g = plan(s, H, B, fanouts, L);
+    // a forward still reading the batch's CSR and rows: this hyperbatch's
+    // kernels overwrite them, so they queue behind it
+    if (b.sage_pending) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.sage_done, 0));
     AGNES_REQUIRE(join_write_lds(H) <= (size_t)s.max_lds && (size_t)(H + 1) * 16 <= (size_t)s.max_lds,
                   AGNES_ERR_RANGE, "H is too large for the device's workgroup memory");
     SyncLayout y = sync_layout(H, L, g.rows_max);
@@ -1482,7 +1492,18 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
 
     b.prof = s.profile;
     if (b.prof) AGNES_CHECK_HIP(hipEventRecord(w.ev[0], st));
-    hipLaunchKernelGGL(k_params, dim3(1), dim3(kBlock), 0, st, w.params.as<ChainParams>(), targets, seed, mb_base,
+    if (targets_on_host) {
+        // Alg. 1's input N arrives in host memory: staged through the batch's
+        // pinned copy (its previous upload finished with the previous
+        // hyperbatch's sampling) and uploaded on the sampling stream
+        const size_t tb = (size_t)H * B * sizeof(int32_t);
+        w.targets_host.reserve_slack(tb);
+        memcpy(w.targets_host.ptr, targets, tb);
+        w.targets.reserve_slack(tb);
+        AGNES_CHECK_HIP(hipMemcpyAsync(w.targets.ptr, w.targets_host.ptr, tb, hipMemcpyHostToDevice, st));
+        targets = w.targets.as<int32_t>();
+    }
+    AGNES_LAUNCH(k_params, dim3(1), dim3(kBlock), 0, st, w.params.as<ChainParams>(), targets, seed, mb_base,
                        w.sync.as<Ctl>(), (int64_t)H * B);
     AGNES_CHECK_HIP(hipGetLastError());
     // With the graph option, a shape seen twice in a row is captured once and
@@ -1502,6 +1523,7 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t 
 }
 
 void finish_hyperbatch(Batch& b, hipStream_t st) {
+    Range range("agnes_batch_finish");
     AGNES_REQUIRE(b.state == kSampled, AGNES_ERR_INVALID, "finish needs a begun hyperbatch");
     const Store& s = *b.store;
     Workspace& w = b.ws;
@@ -1592,13 +1614,13 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
         const int gl = grid_for(rows, 4096);
         int32_t* flag = w.blk_flag.as<int32_t>();
         int64_t* off = w.blk_off.as<int64_t>();
-        hipLaunchKernelGGL(k_unc_flags, dim3(gl), dim3(kBlock), 0, cs, rlk, tch, flag, ctl);
+        AGNES_LAUNCH(k_unc_flags, dim3(gl), dim3(kBlock), 0, cs, rlk, tch, flag, ctl);
         scan_counts(flag, off, &ctl->rows, rows, &ctl->tier_unc, part, cs);
-        hipLaunchKernelGGL(k_unc_compact, dim3(gl), dim3(kBlock), 0, cs, flag, off, w.unc.as<int32_t>(), ctl);
-        hipLaunchKernelGGL(k_block_flags, dim3(gl), dim3(kBlock), 0, cs, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
+        AGNES_LAUNCH(k_unc_compact, dim3(gl), dim3(kBlock), 0, cs, flag, off, w.unc.as<int32_t>(), ctl);
+        AGNES_LAUNCH(k_block_flags, dim3(gl), dim3(kBlock), 0, cs, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
                            flag, ctl);
         scan_counts(flag, off, &ctl->tier_unc, rows, &ctl->tier_nb, part, cs);
-        hipLaunchKernelGGL(k_block_compact, dim3(gl), dim3(kBlock), 0, cs, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
+        AGNES_LAUNCH(k_block_compact, dim3(gl), dim3(kBlock), 0, cs, rlk, w.unc.as<int32_t>(), (uint32_t)s.rpb,
                            flag, off, w.need.as<int64_t>(), (int32_t*)((char*)w.need.ptr + (size_t)rows * 8), ctl);
         AGNES_CHECK_HIP(hipGetLastError());
         std::vector<TierRound> rounds = plan_staging(s, b, cs);
@@ -1616,7 +1638,7 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
         ga.pool_rows = (uint32_t)s.pool_rows;
         for (const TierRound& r : rounds) {
             if (r.n_upd)
-                hipLaunchKernelGGL(k_tbuf_update, dim3(grid_for(r.n_upd, 256)), dim3(kBlock), 0, st, plan + r.upd_at,
+                AGNES_LAUNCH(k_tbuf_update, dim3(grid_for(r.n_upd, 256)), dim3(kBlock), 0, st, plan + r.upd_at,
                                    r.n_upd, s.tbuf.as<int32_t>());
             if (r.n_miss) {
                 // 32 workgroups keep the host link busy (about 50 GB/s, as with
@@ -1627,10 +1649,10 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
                 // 16 no longer saturate the link
                 const int gs = std::min(r.n_miss, 32);
                 if (blk_bytes % 16 == 0)
-                    hipLaunchKernelGGL(k_stage<u32x4>, dim3(gs), dim3(kBlock), 0, st, (const u32x4*)s.host_feat_dev,
+                    AGNES_LAUNCH(k_stage<u32x4>, dim3(gs), dim3(kBlock), 0, st, (const u32x4*)s.host_feat_dev,
                                        s.pool.as<u32x4>(), plan + r.miss_at, r.n_miss, blk_bytes / 16);
                 else
-                    hipLaunchKernelGGL(k_stage<uint32_t>, dim3(gs), dim3(kBlock), 0, st,
+                    AGNES_LAUNCH(k_stage<uint32_t>, dim3(gs), dim3(kBlock), 0, st,
                                        (const uint32_t*)s.host_feat_dev, s.pool.as<uint32_t>(), plan + r.miss_at,
                                        r.n_miss, blk_bytes / 4);
             }
@@ -1641,20 +1663,20 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
         }
         if (cache) {
             // access counts, then admissions in ascending node order while the cache has room
-            hipLaunchKernelGGL(k_access_count, dim3(gl), dim3(kBlock), 0, st, rlk, tch, s.acc_count.as<uint32_t>(),
+            AGNES_LAUNCH(k_access_count, dim3(gl), dim3(kBlock), 0, st, rlk, tch, s.acc_count.as<uint32_t>(),
                                (uint32_t)std::min<int64_t>(s.cache_threshold, 0xFFFFFFFFll), flag, ctl);
             scan_counts(flag, off, &ctl->rows, rows, &ctl->tier_cand, part, st);
             const int ga2 = (int)std::max<int64_t>(1, std::min<int64_t>((rows + 3) / 4, 1 << 20));
             if (s.row_bytes % 16 == 0)
-                hipLaunchKernelGGL(k_admit<u32x4>, dim3(ga2), dim3(kBlock), 0, st, rlk, flag, off,
+                AGNES_LAUNCH(k_admit<u32x4>, dim3(ga2), dim3(kBlock), 0, st, rlk, flag, off,
                                    (const u32x4*)s.host_feat_dev, s.pool.as<u32x4>(), s.pool_rows, s.row_bytes / 16,
                                    s.tch.as<int32_t>(), s.cache_used.as<int64_t>(), s.cache_rows, ctl);
             else
-                hipLaunchKernelGGL(k_admit<uint32_t>, dim3(ga2), dim3(kBlock), 0, st, rlk, flag, off,
+                AGNES_LAUNCH(k_admit<uint32_t>, dim3(ga2), dim3(kBlock), 0, st, rlk, flag, off,
                                    (const uint32_t*)s.host_feat_dev, s.pool.as<uint32_t>(), s.pool_rows,
                                    s.row_bytes / 4, s.tch.as<int32_t>(), s.cache_used.as<int64_t>(), s.cache_rows,
                                    ctl);
-            hipLaunchKernelGGL(k_admit_close, dim3(1), dim3(kWave), 0, st, s.cache_used.as<int64_t>(), s.cache_rows,
+            AGNES_LAUNCH(k_admit_close, dim3(1), dim3(kWave), 0, st, s.cache_used.as<int64_t>(), s.cache_rows,
                                ctl);
         }
         AGNES_CHECK_HIP(hipGetLastError());
@@ -1675,6 +1697,7 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
 
 void wait_batch(Batch& b) {
     if (b.state == kDone) return;
+    Range range("agnes_batch_wait");
     AGNES_REQUIRE(b.state == kGathering, AGNES_ERR_INVALID, "the batch holds no finished hyperbatch");
     AGNES_CHECK_HIP(hipEventSynchronize(b.gathered_at));
     b.stats.sample_ms = b.stats.gather_ms = b.stats.copy_ms = -1.0f;

@@ -18,7 +18,7 @@ __global__ void k_fill_u32(uint32_t* p, uint32_t value, int64_t n) {
 
 void fill_u32(void* p, uint32_t value, int64_t n, hipStream_t st) {
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_fill_u32, dim3(grid_for(n, 2048)), dim3(kBlock), 0, st, (uint32_t*)p, value, n);
+    AGNES_LAUNCH(k_fill_u32, dim3(grid_for(n, 2048)), dim3(kBlock), 0, st, (uint32_t*)p, value, n);
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
@@ -35,7 +35,7 @@ __global__ void k_philox_words(const uint64_t* c, const uint64_t* k, int64_t n, 
 
 void philox_words(const uint64_t* c, const uint64_t* k, int64_t n, uint64_t* out, hipStream_t st) {
     if (n <= 0) return;
-    hipLaunchKernelGGL(k_philox_words, dim3(grid_for(n, 1024)), dim3(kBlock), 0, st, c, k, n, out);
+    AGNES_LAUNCH(k_philox_words, dim3(grid_for(n, 1024)), dim3(kBlock), 0, st, c, k, n, out);
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
@@ -140,8 +140,8 @@ static void scan_impl(const T* in, int64_t* out, const int64_t* n_dev, int64_t n
                       int64_t* total_dev, int64_t* partials, int64_t* nonzero, hipStream_t st) {
     int64_t g = (n_max + kScanTile - 1) / kScanTile;
     int G = (int)(g < 1 ? 1 : (g > kScanGroups ? kScanGroups : g));
-    hipLaunchKernelGGL(k_scan_reduce<T>, dim3(G), dim3(kBlock), 0, st, in, n_dev, G, partials, nonzero);
-    hipLaunchKernelGGL(k_scan_final<T>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials, total_dev);
+    AGNES_LAUNCH(k_scan_reduce<T>, dim3(G), dim3(kBlock), 0, st, in, n_dev, G, partials, nonzero);
+    AGNES_LAUNCH(k_scan_final<T>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials, total_dev);
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
@@ -388,10 +388,10 @@ static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uin
     for (int p = 0; p < passes; p++) {
         int shift = p * RB;
         const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
-        hipLaunchKernelGGL((k_rs_hist<ITEMS, RB>), dim3(radix_grid(tiles)), dim3(kBlock), 0, st, ka, n_dev, shift,
+        AGNES_LAUNCH((k_rs_hist<ITEMS, RB>), dim3(radix_grid(tiles)), dim3(kBlock), 0, st, ka, n_dev, shift,
                            hist);
-        hipLaunchKernelGGL((k_rs_scan<ITEMS, RB>), dim3(1 << RB), dim3(kBlock), 0, st, hist, n_dev, dtot);
-        hipLaunchKernelGGL((k_rs_scatter<ITEMS, RB>), dim3(radix_grid(tiles)), dim3(kBlock), 0, st, ka, vin, kb,
+        AGNES_LAUNCH((k_rs_scan<ITEMS, RB>), dim3(1 << RB), dim3(kBlock), 0, st, hist, n_dev, dtot);
+        AGNES_LAUNCH((k_rs_scatter<ITEMS, RB>), dim3(radix_grid(tiles)), dim3(kBlock), 0, st, ka, vin, kb,
                            vb, n_dev, shift, hist, dtot);
         uint32_t* tk = ka; ka = kb; kb = tk;
         uint32_t* tv = va; va = vb; vb = tv;

@@ -37,6 +37,28 @@ void clear_last_error();
         if (!(cond)) throw ::agnes::Error{(code), (msg)};                                   \
     } while (0)
 
+// Debug mode: with AGNES_DEBUG_SYNC=1 in the environment when the library is
+// loaded, every kernel launch is followed by a synchronisation of its stream
+// (skipped while the stream is being captured into a graph) and an error check,
+// so a failing kernel is reported under the name of the launch that enqueued it.
+bool debug_sync();
+void check_launch(hipStream_t st, const char* what);
+
+#define AGNES_LAUNCH(kernel, grid, block, lds, st, ...)                                    \
+    do {                                                                                    \
+        hipLaunchKernelGGL(kernel, grid, block, lds, st, __VA_ARGS__);                      \
+        ::agnes::check_launch((st), #kernel);                                               \
+    } while (0)
+
+// Host-side ranges around the library's phases (roctx; seen by rocprofv3
+// --marker-trace, free when no profiler is attached).
+struct Range {
+    explicit Range(const char* name);
+    ~Range();
+    Range(const Range&) = delete;
+    Range& operator=(const Range&) = delete;
+};
+
 // ----------------------------------------------------------------- device buffer
 
 // The process-wide device allocator: hipMalloc / hipFree unless the caller
@@ -168,6 +190,8 @@ struct Workspace {
     DevBuf scan_part;                 // scan partial sums
     DevBuf topo_part;                 // per sampler workgroup: Bck rows it opened
     DevBuf params;                    // per-call values the sampling kernels read (targets, seed, minibatch base)
+    DevBuf targets;                   // targets uploaded from host memory by the call
+    PinnedBuf targets_host;           // their pinned staging copy
     DevBuf blk_flag, blk_off;         // staged tier: flags over the final list and their offsets
     DevBuf unc;                       // staged tier: list entries whose rows are not in the feature cache
     DevBuf need;                      // staged tier: [needed blocks] first list entry, then block ids
@@ -266,6 +290,10 @@ struct Batch {
     PinnedBuf sage_host;
     DevBuf sage_off, sage_a, sage_h[2];
     hipEvent_t sage_ev = nullptr;     // the offsets upload has left sage_host
+    // The end of the last forward enqueued on this batch: the next hyperbatch
+    // and the next forward wait for it before they overwrite what it reads.
+    hipEvent_t sage_done = nullptr;
+    bool sage_pending = false;
     // The sampling kernels of one hyperbatch shape, captured as a HIP graph.
     // chain_key lists everything the captured launches depend on (shape, store,
     // buffer addresses); a call with another key runs kernel by kernel and is
@@ -280,6 +308,7 @@ struct Batch {
         if (gathered) (void)hipEventDestroy(gathered);
         if (needed) (void)hipEventDestroy(needed);
         if (sage_ev) (void)hipEventDestroy(sage_ev);
+        if (sage_done) (void)hipEventDestroy(sage_done);
         for (auto& e : ws.ev)
             if (e) (void)hipEventDestroy(e);
     }
@@ -289,8 +318,10 @@ struct Batch {
 // `stream` and returns; finish waits for the output sizes, makes room for the
 // outputs and enqueues the gather on `stream`; wait blocks until the batch is
 // complete and fills its statistics.
-void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, int32_t H, int32_t B,
-                      const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
+// targets_on_host: targets is host memory, copied by the call (through pinned
+// memory) to the device on `stream`; otherwise it is device memory.
+void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, bool targets_on_host, int32_t H,
+                      int32_t B, const int32_t* fanouts, int32_t L, uint64_t seed, int64_t mb_base,
                       hipStream_t stream);
 void finish_hyperbatch(Batch& b, hipStream_t stream);
 void wait_batch(Batch& b);

@@ -277,7 +277,7 @@ static void launch_agg_k(const void* hin, const LayerOffsets& o, const int32_t* 
                          int64_t M, int din, uint16_t* A, hipStream_t st) {
     constexpr int64_t per_wg = (int64_t)kWavesPerBlock * (kWave / LPR);
     const int G = (int)std::max<int64_t>(1, std::min<int64_t>((M + per_wg - 1) / per_wg, 1 << 20));
-    hipLaunchKernelGGL((k_sage_agg<InT, LPR>), dim3(G), dim3(kBlock), 0, st, (const InT*)hin, o, row_ptr, col, H, M,
+    AGNES_LAUNCH((k_sage_agg<InT, LPR>), dim3(G), dim3(kBlock), 0, st, (const InT*)hin, o, row_ptr, col, H, M,
                        din, A);
 }
 
@@ -334,6 +334,10 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
     }
     if (b.sage_ev) AGNES_CHECK_HIP(hipEventSynchronize(b.sage_ev));   // the previous upload has left the pinned buffer
     else AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.sage_ev, hipEventDisableTiming));
+    if (!b.sage_done) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.sage_done, hipEventDisableTiming));
+    // a previous forward on another stream still reads the scratch rows this
+    // one overwrites
+    if (b.sage_pending) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.sage_done, 0));
     b.sage_host.reserve(offs.size() * 8);
     memcpy(b.sage_host.ptr, offs.data(), offs.size() * 8);
     b.sage_off.reserve(offs.size() * 8);
@@ -364,15 +368,18 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
         const dim3 grid((unsigned)((mbs + 7) / 8 * 8 * nbs));
         if (i + 1 < L) {
             void* z = b.sage_h[i & 1].ptr;
-            hipLaunchKernelGGL((k_sage_gemm<true, false>), grid, dim3(kBlock), 0, st, A,
+            AGNES_LAUNCH((k_sage_gemm<true, false>), grid, dim3(kBlock), 0, st, A,
                                (const uint16_t*)m.weight[i], m.bias[i], M, dout, 2 * din, z);
             hin = z;
         } else {
-            hipLaunchKernelGGL((k_sage_gemm<false, true>), grid, dim3(kBlock), 0, st, A,
+            AGNES_LAUNCH((k_sage_gemm<false, true>), grid, dim3(kBlock), 0, st, A,
                                (const uint16_t*)m.weight[i], m.bias[i], M, dout, 2 * din, (void*)out);
         }
         AGNES_CHECK_HIP(hipGetLastError());
     }
+    // what the next hyperbatch or forward on this batch waits for
+    AGNES_CHECK_HIP(hipEventRecord(b.sage_done, st));
+    b.sage_pending = true;
 }
 
 }  // namespace agnes

@@ -156,11 +156,11 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
     fill_u32(s->first_node.ptr, 0xFFFFFFFFu, s->nblk, st);
     fill_u32(s->last_node.ptr, 0xFFFFFFFFu, s->nblk, st);
     if (o64)
-        hipLaunchKernelGGL(k_object_table<int64_t>, dim3(grid_for(n, 4096)), dim3(kBlock), 0, st,
+        AGNES_LAUNCH(k_object_table<int64_t>, dim3(grid_for(n, 4096)), dim3(kBlock), 0, st,
                            s->offsets.as<int64_t>(), n, s->e_blk_log2, s->nblk,
                            s->first_node.as<int32_t>(), s->last_node.as<int32_t>());
     else
-        hipLaunchKernelGGL(k_object_table<int32_t>, dim3(grid_for(n, 4096)), dim3(kBlock), 0, st,
+        AGNES_LAUNCH(k_object_table<int32_t>, dim3(grid_for(n, 4096)), dim3(kBlock), 0, st,
                            s->offsets.as<int32_t>(), n, s->e_blk_log2, s->nblk,
                            s->first_node.as<int32_t>(), s->last_node.as<int32_t>());
     AGNES_CHECK_HIP(hipGetLastError());
