@@ -400,6 +400,25 @@ typedef struct {
 agnes_status agnes_sage_forward(agnes_batch* batch, const agnes_sage_model* model, float* out,
                                 void* hip_stream);
 
+/* The same forward for callers that cannot allocate memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): it
+ * calls no hipMalloc, hipFree or other allocating routine.  Same arguments,
+ * checks, kernels and results as agnes_sage_forward.  Its intermediate rows
+ * (the per-layer offsets, the [h_v ; m_v] rows and the hidden embeddings) live
+ * in one static device array of AGNES_NOALLOC_SCRATCH_BYTES per GPU, held
+ * from the first call on that GPU until the process ends; a forward needing
+ * more (bytes: 8 * 4 * L * (H+1) + 2 * max_i(M_i * 2 * dims[i]) + 4 *
+ * max_{i<L-1}(M_i * dims[i+1]), each rounded up to 256, with M_i the
+ * destination rows of layer i over the hyperbatch) fails with
+ * AGNES_ERR_RANGE before anything is enqueued.  Every call on one GPU uses
+ * that GPU's single array: calls whose work overlaps on one GPU (several
+ * streams, or several host threads) race and must be serialised by the
+ * caller, e.g. by enqueueing them on one stream.  The next hyperbatch begun on
+ * the batch waits for the forward, as with agnes_sage_forward. */
+#define AGNES_NOALLOC_SCRATCH_BYTES (64ull << 20)
+agnes_status agnes_sage_forward_noalloc(agnes_batch* batch, const agnes_sage_model* model, float* out,
+                                        void* hip_stream);
+
 /* Store facts: out[0] num_nodes, out[1] num_edges, out[2] topology blocks,
  * out[3] edges per topology block, out[4] feature blocks, out[5] rows per
  * feature block, out[6] row_bytes, out[7] device bytes held by the store. */

@@ -237,10 +237,12 @@ class Batch:
                     rows=s.rows, distinct_rows=s.distinct_rows, feat_blocks=s.feat_blocks,
                     sample_ms=s.sample_ms, gather_ms=s.gather_ms, copy_ms=s.copy_ms)
 
-    def sage_forward(self, weights, biases, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
-        """GraphSAGE forward over this batch (agnes_sage_forward).  weights[i]:
-        CUDA bf16 (or int16/uint16 bits) [dims[i+1], 2 dims[i]]; biases[i]: CUDA
-        float32 [dims[i+1]]; returns float32 [H*B, dims[L]] (enqueued on `stream`)."""
+    def sage_forward(self, weights, biases, out: torch.Tensor | None = None, stream=None,
+                     noalloc: bool = False) -> torch.Tensor:
+        """GraphSAGE forward over this batch (agnes_sage_forward, or with
+        noalloc agnes_sage_forward_noalloc).  weights[i]: CUDA bf16 (or
+        int16/uint16 bits) [dims[i+1], 2 dims[i]]; biases[i]: CUDA float32
+        [dims[i+1]]; returns float32 [H*B, dims[L]] (enqueued on `stream`)."""
         L = len(weights)
         if L != len(biases) or L < 1 or L > B.AGNES_MAX_LAYERS:
             raise ValueError("one weight and one bias per layer")
@@ -266,7 +268,8 @@ class Batch:
         if not (out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and
                 tuple(out.shape) == (rows, m.dims[L])):
             raise ValueError("out must be a contiguous CUDA float32 tensor [H*B, dims[L]]")
-        agnes_sage_forward(self.handle, m, out.data_ptr(), _stream_handle(stream))
+        fn = B.agnes_sage_forward_noalloc if noalloc else agnes_sage_forward
+        fn(self.handle, m, out.data_ptr(), _stream_handle(stream))
         self._sage_keep = (weights, biases, out)
         return out
 

@@ -26,7 +26,7 @@ AGNES_OPT_SAMPLING_GRAPH = 6
 EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_build_blocks_cached", "agnes_hyperbatch_prepare",
             "agnes_hyperbatch_prepare_device", "agnes_hyperbatch_begin", "agnes_hyperbatch_begin_device", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",
             "agnes_batch_stats", "agnes_batch_tier_stats", "agnes_store_set_option", "agnes_store_info",
-            "agnes_store_object_table", "agnes_sage_forward", "agnes_philox4x64_10", "agnes_set_device_allocator", "agnes_free",
+            "agnes_store_object_table", "agnes_sage_forward", "agnes_sage_forward_noalloc", "agnes_philox4x64_10", "agnes_set_device_allocator", "agnes_free",
             "agnes_last_error"]
 
 # void* alloc(uint64_t bytes, void* user); void release(void* ptr, uint64_t bytes, void* user)
@@ -113,6 +113,8 @@ def lib():
     L.agnes_batch_tier_stats.argtypes = [vp, ctypes.POINTER(agnes_tier_stats)]
     L.agnes_sage_forward.restype = st
     L.agnes_sage_forward.argtypes = [vp, ctypes.POINTER(agnes_sage_model), vp, vp]
+    L.agnes_sage_forward_noalloc.restype = st
+    L.agnes_sage_forward_noalloc.argtypes = [vp, ctypes.POINTER(agnes_sage_model), vp, vp]
     L.agnes_hyperbatch_prepare.restype = st
     L.agnes_hyperbatch_prepare.argtypes = [vp, vp, i32, i32, vp, i32, u64, i64, vp, ctypes.POINTER(vp)]
     L.agnes_hyperbatch_begin.restype = st
@@ -192,6 +194,11 @@ def _start_call(fn, store, targets_ptr, H, B, fanouts_arr, L, seed, mb_base, str
     check(fn(ctypes.c_void_p(store), ctypes.c_void_p(targets_ptr), H, B, fanouts_arr, L, seed, mb_base,
              ctypes.c_void_p(stream), ctypes.byref(out)))
     return out.value
+
+
+def agnes_sage_forward_noalloc(batch: int, model: agnes_sage_model, out_ptr: int, stream: int = 0) -> None:
+    check(lib().agnes_sage_forward_noalloc(ctypes.c_void_p(batch), ctypes.byref(model), ctypes.c_void_p(out_ptr),
+                                           ctypes.c_void_p(stream)))
 
 
 def agnes_hyperbatch_prepare(store: int, targets_ptr: int, H: int, B: int, fanouts_arr, L: int,

@@ -282,6 +282,15 @@ agnes_status agnes_sage_forward(agnes_batch* batch, const agnes_sage_model* mode
     });
 }
 
+agnes_status agnes_sage_forward_noalloc(agnes_batch* batch, const agnes_sage_model* model, float* out,
+                                        void* hip_stream) {
+    return guarded([&] {
+        Batch* b = as_batch(batch);
+        AGNES_REQUIRE(model, AGNES_ERR_INVALID, "model must not be NULL");
+        sage_forward_noalloc(*b, *model, out, (hipStream_t)hip_stream);
+    });
+}
+
 agnes_status agnes_batch_tier_stats(const agnes_batch* batch, agnes_tier_stats* out) {
     return guarded([&] {
         Batch* b = as_batch((void*)batch);

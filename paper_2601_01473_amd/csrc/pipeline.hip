@@ -1481,6 +1481,9 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, bool tar
     b.rows_max = g.rows_max;
     if (!b.sampled) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.sampled, hipEventDisableTiming));
     if (!b.gathered) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.gathered, hipEventDisableTiming));
+    if (!b.sage_done) AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.sage_done, hipEventDisableTiming));
+    b.d_lsz = (const int32_t*)((const char*)w.sync.ptr + y.lsz);
+    b.d_ecount = (const int64_t*)((const char*)w.sync.ptr + y.ecount);
     b.store = &s;
     b.H = H; b.B = B; b.L = L;
     b.capN = g.capN;

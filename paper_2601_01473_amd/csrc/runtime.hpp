@@ -294,6 +294,10 @@ struct Batch {
     // and the next forward wait for it before they overwrite what it reads.
     hipEvent_t sage_done = nullptr;
     bool sage_pending = false;
+    // Device copies of the layer sizes [H][L+1] and per-hop edge counts [H][L]
+    // (inside ws.sync), valid once the hyperbatch's sampling has finished.
+    const int32_t* d_lsz = nullptr;
+    const int64_t* d_ecount = nullptr;
     // The sampling kernels of one hyperbatch shape, captured as a HIP graph.
     // chain_key lists everything the captured launches depend on (shape, store,
     // buffer addresses); a call with another key runs kernel by kernel and is
@@ -327,6 +331,10 @@ void finish_hyperbatch(Batch& b, hipStream_t stream);
 void wait_batch(Batch& b);
 // GraphSAGE forward over a prepared batch (sage.hip); enqueues on `stream`.
 void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t stream);
+// The same without any allocation: scratch space from a static device array
+// of kNoAllocScratchBytes per GPU (sage.hip).
+constexpr size_t kNoAllocScratchBytes = AGNES_NOALLOC_SCRATCH_BYTES;
+void sage_forward_noalloc(Batch& b, const agnes_sage_model& m, float* out, hipStream_t stream);
 // Store construction (store.hip).
 // pool_blocks == 0: features in HBM; > 0: staged feature tier with that many
 // slots and a feature cache of cache_rows rows (0: none).

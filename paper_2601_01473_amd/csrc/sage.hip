@@ -12,7 +12,10 @@
 // is one GEMM over the whole hyperbatch.
 #include <algorithm>
 #include <cstring>
+#include <mutex>
+#include <string>
 #include <type_traits>
+#include <vector>
 
 #include "device.hpp"
 #include "runtime.hpp"
@@ -294,7 +297,7 @@ static void launch_agg(const void* hin, const LayerOffsets& o, const int32_t* ro
     else launch_agg_k<InT, 4>(hin, o, row_ptr, col, H, M, din, A, st);
 }
 
-void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t st) {
+static void check_forward(const Batch& b, const agnes_sage_model& m, const float* out) {
     const Store& s = *b.store;
     AGNES_REQUIRE(b.state == kGathering || b.state == kDone, AGNES_ERR_INVALID, "the batch holds no finished hyperbatch");
     AGNES_REQUIRE(m.L == b.L, AGNES_ERR_INVALID, "the model needs one layer per hop of the batch");
@@ -309,11 +312,71 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
         AGNES_REQUIRE(((uintptr_t)m.weight[i] & 15) == 0, AGNES_ERR_INVALID, "weights must be 16-byte aligned");
     }
     AGNES_REQUIRE(((uintptr_t)out & 15) == 0, AGNES_ERR_INVALID, "out must be 16-byte aligned");
+}
+
+// Destination rows of layer i (hop L-1-i) over the hyperbatch, and the largest
+// [h ; mean] matrix and hidden output (elements) of the forward.
+struct ForwardSizes {
+    int64_t M[AGNES_MAX_LAYERS];
+    int64_t Amax, Hmax;
+};
+
+static ForwardSizes forward_sizes(const Batch& b, const agnes_sage_model& m) {
+    ForwardSizes z{};
+    z.Hmax = 1;
     const int H = b.H, L = b.L;
+    for (int i = 0; i < L; i++) {
+        const int l = L - 1 - i;
+        int64_t M = 0;
+        for (int j = 0; j < H; j++) M += b.layer_sizes[(size_t)j * (L + 1) + l];
+        z.M[i] = M;
+        z.Amax = std::max(z.Amax, M * 2 * m.dims[i]);
+        if (i + 1 < L) z.Hmax = std::max(z.Hmax, M * m.dims[i + 1]);
+    }
+    return z;
+}
+
+// The forward's kernels on st: per layer the aggregation into A, then the GEMM
+// (into hidden[i & 1], or into out for the last layer).  doffs holds the
+// layers' offsets, [L][4][H+1] int64 (d_off, in_off, rp_off, col_off).
+static void enqueue_forward(const Batch& b, const agnes_sage_model& m, const ForwardSizes& z, const int64_t* doffs,
+                            uint16_t* A, void* const hidden[2], float* out, hipStream_t st) {
+    const Store& s = *b.store;
+    const int H = b.H, L = b.L;
+    const void* hin = b.features.ptr;
+    for (int i = 0; i < L; i++) {
+        const int l = L - 1 - i;
+        LayerOffsets o{doffs + ((size_t)i * 4 + 0) * (H + 1), doffs + ((size_t)i * 4 + 1) * (H + 1),
+                       doffs + ((size_t)i * 4 + 2) * (H + 1), doffs + ((size_t)i * 4 + 3) * (H + 1)};
+        const int din = m.dims[i], dout = m.dims[i + 1];
+        const int64_t M = z.M[i];
+        if (M == 0) continue;
+        if (i == 0 && s.feat_dtype == AGNES_FLOAT32)
+            launch_agg<float>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
+        else if (i == 0 && s.feat_dtype == AGNES_FLOAT16)
+            launch_agg<_Float16>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
+        else
+            launch_agg<uint16_t>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
+        const int64_t mbs = (M + kGM - 1) / kGM, nbs = (dout + kGN - 1) / kGN;
+        const dim3 grid((unsigned)((mbs + 7) / 8 * 8 * nbs));
+        if (i + 1 < L) {
+            void* zout = hidden[i & 1];
+            AGNES_LAUNCH((k_sage_gemm<true, false>), grid, dim3(kBlock), 0, st, A,
+                         (const uint16_t*)m.weight[i], m.bias[i], M, dout, 2 * din, zout);
+            hin = zout;
+        } else {
+            AGNES_LAUNCH((k_sage_gemm<false, true>), grid, dim3(kBlock), 0, st, A,
+                         (const uint16_t*)m.weight[i], m.bias[i], M, dout, 2 * din, (void*)out);
+        }
+    }
+}
+
+void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t st) {
+    check_forward(b, m, out);
+    const int H = b.H, L = b.L;
+    const ForwardSizes z = forward_sizes(b, m);
     // host offsets of every layer: d_off, in_off, rp_off, col_off ([H+1] each)
     std::vector<int64_t> offs((size_t)L * 4 * (H + 1));
-    int64_t Mmax = 0, Amax = 0, Hmax = 1;
-    std::vector<int64_t> Ms(L);
     for (int i = 0; i < L; i++) {
         const int l = L - 1 - i;
         int64_t* d_off = &offs[((size_t)i * 4 + 0) * (H + 1)];
@@ -327,10 +390,6 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
             rp[j] = b.rp_off[l][j];
             co[j] = b.col_off[l][j];
         }
-        Ms[i] = d_off[H];
-        Mmax = std::max(Mmax, Ms[i]);
-        Amax = std::max(Amax, Ms[i] * 2 * m.dims[i]);
-        if (i + 1 < L) Hmax = std::max(Hmax, Ms[i] * m.dims[i + 1]);
     }
     if (b.sage_ev) AGNES_CHECK_HIP(hipEventSynchronize(b.sage_ev));   // the previous upload has left the pinned buffer
     else AGNES_CHECK_HIP(hipEventCreateWithFlags(&b.sage_ev, hipEventDisableTiming));
@@ -343,41 +402,107 @@ void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t s
     b.sage_off.reserve(offs.size() * 8);
     // sizes vary by hyperbatch: headroom keeps reallocations (and the device
     // synchronisation of the free that comes with each) rare
-    b.sage_a.reserve_slack((size_t)std::max<int64_t>(Amax, 1) * 2);
-    for (int k = 0; k < 2; k++) b.sage_h[k].reserve_slack((size_t)Hmax * 2);
+    b.sage_a.reserve_slack((size_t)std::max<int64_t>(z.Amax, 1) * 2);
+    for (int k = 0; k < 2; k++) b.sage_h[k].reserve_slack((size_t)z.Hmax * 2);
     if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.gathered_at, 0));
     AGNES_CHECK_HIP(hipMemcpyAsync(b.sage_off.ptr, b.sage_host.ptr, offs.size() * 8, hipMemcpyHostToDevice, st));
     AGNES_CHECK_HIP(hipEventRecord(b.sage_ev, st));
-    const int64_t* doffs = b.sage_off.as<int64_t>();
-    const void* hin = b.features.ptr;
+    void* const hidden[2] = {b.sage_h[0].ptr, b.sage_h[1].ptr};
+    enqueue_forward(b, m, z, b.sage_off.as<int64_t>(), b.sage_a.as<uint16_t>(), hidden, out, st);
+    // what the next hyperbatch or forward on this batch waits for
+    AGNES_CHECK_HIP(hipEventRecord(b.sage_done, st));
+    b.sage_pending = true;
+}
+
+// ----------------------------------------------------------------- no allocation
+
+// Scratch space of agnes_sage_forward_noalloc: one array per GPU, held by the
+// loaded code object until the process ends.  Host code never uses this name
+// as an address; it uses the device address that hipGetSymbolAddress returns
+// for the current device (scratch_on_device).
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+static void* scratch_on_device(int dev) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    AGNES_REQUIRE(dev >= 0 && dev < kMaxDevices, AGNES_ERR_INVALID, "device index out of range");
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        AGNES_CHECK_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        AGNES_REQUIRE(p, AGNES_ERR_DEVICE, "no device address for the scratch array");
+        addr[dev] = p;
+    }
+    return addr[dev];
+}
+
+// The layers' offsets ([L][4][H+1], as enqueue_forward reads them) from the
+// batch's device-side layer sizes [H][L+1], edge counts [H][L] and output row
+// offsets node_off [H+1]: one workgroup, per layer and array an exclusive
+// scan over the minibatches.
+__global__ __launch_bounds__(kBlock) void k_sage_offsets(const int32_t* lsz, const int64_t* ecount,
+                                                         const int64_t* node_off, int H, int L, int64_t* offs) {
+    __shared__ int64_t lds[kWavesPerBlock];
     for (int i = 0; i < L; i++) {
         const int l = L - 1 - i;
-        LayerOffsets o{doffs + ((size_t)i * 4 + 0) * (H + 1), doffs + ((size_t)i * 4 + 1) * (H + 1),
-                       doffs + ((size_t)i * 4 + 2) * (H + 1), doffs + ((size_t)i * 4 + 3) * (H + 1)};
-        const int din = m.dims[i], dout = m.dims[i + 1];
-        const int64_t M = Ms[i];
-        if (M == 0) continue;
-        uint16_t* A = b.sage_a.as<uint16_t>();
-        if (i == 0 && s.feat_dtype == AGNES_FLOAT32)
-            launch_agg<float>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
-        else if (i == 0 && s.feat_dtype == AGNES_FLOAT16)
-            launch_agg<_Float16>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
-        else
-            launch_agg<uint16_t>(hin, o, b.row_ptr[l].as<int32_t>(), b.col[l].as<int32_t>(), H, M, din, A, st);
-        const int64_t mbs = (M + kGM - 1) / kGM, nbs = (dout + kGN - 1) / kGN;
-        const dim3 grid((unsigned)((mbs + 7) / 8 * 8 * nbs));
-        if (i + 1 < L) {
-            void* z = b.sage_h[i & 1].ptr;
-            AGNES_LAUNCH((k_sage_gemm<true, false>), grid, dim3(kBlock), 0, st, A,
-                               (const uint16_t*)m.weight[i], m.bias[i], M, dout, 2 * din, z);
-            hin = z;
-        } else {
-            AGNES_LAUNCH((k_sage_gemm<false, true>), grid, dim3(kBlock), 0, st, A,
-                               (const uint16_t*)m.weight[i], m.bias[i], M, dout, 2 * din, (void*)out);
+        int64_t* d_off = offs + ((size_t)i * 4 + 0) * (H + 1);
+        int64_t* in_off = offs + ((size_t)i * 4 + 1) * (H + 1);
+        int64_t* rp = offs + ((size_t)i * 4 + 2) * (H + 1);
+        int64_t* co = offs + ((size_t)i * 4 + 3) * (H + 1);
+        const int64_t* prev_d = i > 0 ? offs + ((size_t)(i - 1) * 4 + 0) * (H + 1) : node_off;
+        int64_t cd = 0, cr = 0, cc = 0;
+        for (int base = 0; base < H; base += kBlock) {
+            const int j = base + threadIdx.x;
+            const int64_t n = j < H ? (int64_t)lsz[(int64_t)j * (L + 1) + l] : 0;
+            const int64_t e = j < H ? ecount[(int64_t)j * L + l] : 0;
+            int64_t t;
+            const int64_t xd = block_exclusive_scan(n, lds, t);
+            if (j < H) d_off[j] = cd + xd;
+            cd += t;
+            const int64_t xr = block_exclusive_scan(j < H ? n + 1 : (int64_t)0, lds, t);
+            if (j < H) rp[j] = cr + xr;
+            cr += t;
+            const int64_t xc = block_exclusive_scan(e, lds, t);
+            if (j < H) co[j] = cc + xc;
+            cc += t;
         }
-        AGNES_CHECK_HIP(hipGetLastError());
+        if (threadIdx.x == 0) {
+            d_off[H] = cd;
+            rp[H] = cr;
+            co[H] = cc;
+        }
+        __syncthreads();
+        for (int j = threadIdx.x; j <= H; j += kBlock) in_off[j] = prev_d[j];
+        __syncthreads();
     }
-    // what the next hyperbatch or forward on this batch waits for
+}
+
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+void sage_forward_noalloc(Batch& b, const agnes_sage_model& m, float* out, hipStream_t st) {
+    check_forward(b, m, out);
+    const int H = b.H, L = b.L;
+    const ForwardSizes z = forward_sizes(b, m);
+    const size_t off_bytes = align256((size_t)L * 4 * (H + 1) * sizeof(int64_t));
+    const size_t a_bytes = align256((size_t)std::max<int64_t>(z.Amax, 1) * 2);
+    const size_t h_bytes = align256((size_t)z.Hmax * 2);
+    const size_t need = off_bytes + a_bytes + 2 * h_bytes;
+    AGNES_REQUIRE(need <= kNoAllocScratchBytes, AGNES_ERR_RANGE,
+                  "the forward needs " + std::to_string(need) + " bytes of scratch; the no-allocation forward has " +
+                      std::to_string(kNoAllocScratchBytes));
+    int dev = 0;
+    AGNES_CHECK_HIP(hipGetDevice(&dev));
+    AGNES_REQUIRE(dev == b.store->device, AGNES_ERR_INVALID, "the current device is not the batch's device");
+    char* base = (char*)scratch_on_device(dev);
+    int64_t* offs = (int64_t*)base;
+    uint16_t* A = (uint16_t*)(base + off_bytes);
+    void* const hidden[2] = {base + off_bytes + a_bytes, base + off_bytes + a_bytes + h_bytes};
+    if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.gathered_at, 0));
+    AGNES_LAUNCH(k_sage_offsets, dim3(1), dim3(kBlock), 0, st, b.d_lsz, b.d_ecount, b.ws.mb_off.as<int64_t>(), H,
+                 L, offs);
+    enqueue_forward(b, m, z, offs, A, hidden, out, st);
+    // what the next hyperbatch on this batch waits for (created with the batch)
     AGNES_CHECK_HIP(hipEventRecord(b.sage_done, st));
     b.sage_pending = true;
 }
