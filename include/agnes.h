@@ -284,6 +284,16 @@ agnes_status agnes_set_device_allocator(agnes_device_alloc_fn alloc, agnes_devic
  *     one such graph and captures again when the shape changes.  Replay
  *     shortens one hyperbatch's latency on small shapes but slows hyperbatches
  *     that sample concurrently on several streams.
+ *   AGNES_OPT_JOIN_PATH: how each hop unites the sampled neighbours with the
+ *     nodes already held and relabels them.  0 (default): a device-wide radix
+ *     sort of the sampled neighbours and a merge-path join with the list;
+ *     1: node-range buckets, each joined in workgroup memory (a dense
+ *     (node, minibatch) table for narrow buckets such as one hub, a sort in
+ *     workgroup memory for the others).
+ *   AGNES_OPT_BUCKET_CAP: old and new entries one sorted node-range bucket may
+ *     hold, in [64, 2048] (default 2048).  A hyperbatch with a bucket above it
+ *     is sampled again with the radix sort (same results); a smaller value
+ *     only makes that happen more often.
  * Options change launch shapes and store kinds only, never results. */
 typedef enum {
     AGNES_OPT_PROFILE = 1,
@@ -291,7 +301,9 @@ typedef enum {
     AGNES_OPT_GATHER_UNROLL = 3,
     AGNES_OPT_GATHER_NONTEMPORAL = 4,
     AGNES_OPT_GATHER_CHUNKS = 5,
-    AGNES_OPT_SAMPLING_GRAPH = 6
+    AGNES_OPT_SAMPLING_GRAPH = 6,
+    AGNES_OPT_JOIN_PATH = 7,
+    AGNES_OPT_BUCKET_CAP = 8
 } agnes_option;
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value);
 

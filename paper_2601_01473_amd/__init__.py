@@ -149,6 +149,15 @@ class Store:
         captured HIP graph, or launch them one by one (the default)."""
         agnes_store_set_option(self.handle, B.AGNES_OPT_SAMPLING_GRAPH, 1 if on else 0)
 
+    def set_join_path(self, buckets: bool = True, bucket_cap: int | None = None) -> None:
+        """Node-range buckets joined in workgroup memory (the default) or the
+        device-wide radix sort and merge-path join; bucket_cap: entries of one
+        sorted bucket before the hyperbatch is sampled again with the radix
+        sort (never changes results)."""
+        agnes_store_set_option(self.handle, B.AGNES_OPT_JOIN_PATH, 1 if buckets else 0)
+        if bucket_cap is not None:
+            agnes_store_set_option(self.handle, B.AGNES_OPT_BUCKET_CAP, int(bucket_cap))
+
     def set_gather_shape(self, groups: int | None = None, unroll: int | None = None,
                          nontemporal: bool | None = None, chunks: int | None = None) -> None:
         """Launch shape and store kind of the row-copy kernel (never change results)."""

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libagnes.so")
-SOURCES = ["prims.hip", "store.hip", "pipeline.hip", "sage.hip", "api.hip"]
+SOURCES = ["prims.hip", "store.hip", "pipeline.hip", "bucket.hip", "sage.hip", "api.hip"]
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.environ.get("HIPCC", os.path.join(ROCM, "bin", "hipcc"))
 ARCH = "gfx950"

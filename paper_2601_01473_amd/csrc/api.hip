@@ -7,6 +7,7 @@
 
 #include <rocprofiler-sdk-roctx/roctx.h>
 
+#include "bucket.hpp"
 #include "runtime.hpp"
 
 namespace agnes {
@@ -319,6 +320,12 @@ agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_
             s->gather_chunks = (int)value;
         } else if (opt == AGNES_OPT_SAMPLING_GRAPH) {
             s->sampling_graph = value ? 1 : 0;
+        } else if (opt == AGNES_OPT_JOIN_PATH) {
+            AGNES_REQUIRE(value == 0 || value == 1, AGNES_ERR_INVALID, "join path must be 0 or 1");
+            s->join_path = (int)value;
+        } else if (opt == AGNES_OPT_BUCKET_CAP) {
+            AGNES_REQUIRE(value >= 64 && value <= kBucketCap, AGNES_ERR_INVALID, "bucket capacity must be in [64, 2048]");
+            s->bucket_cap = (int)value;
         } else {
             throw Error{AGNES_ERR_INVALID, "unknown option"};
         }

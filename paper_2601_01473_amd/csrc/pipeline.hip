@@ -27,6 +27,7 @@
 #include <functional>
 #include <vector>
 
+#include "bucket.hpp"
 #include "device.hpp"
 #include "runtime.hpp"
 
@@ -38,6 +39,10 @@ struct Geometry {
     int64_t cap[AGNES_MAX_LAYERS + 1]; // cap[l] = frontier capacity of hop l (cap[L] = capN)
     int64_t Rmax, Smax, rows_max, sort_max;
     int jbits;
+    // node-range buckets: per hop the most coarse buckets and the count
+    // table's row stride
+    int bcoarse[AGNES_MAX_LAYERS], bstride[AGNES_MAX_LAYERS];
+    int bstride_max;
 };
 
 // Edge numbers, sort positions and positions in the join of one hop are
@@ -63,6 +68,14 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
     int jb = 0;
     while ((1 << jb) < H) jb++;
     g.jbits = jb;
+    g.bstride_max = kBlock;
+    for (int l = 0; l < L; l++) {
+        const int64_t load = (int64_t)H * g.cap[l] * (1 + (int64_t)fanouts[l]);
+        const BucketBounds bb = bucket_bounds(s, load, H);
+        g.bcoarse[l] = bb.coarse;
+        g.bstride[l] = bucket_table_stride(bb);
+        g.bstride_max = std::max(g.bstride_max, g.bstride[l]);
+    }
     return g;
 }
 
@@ -174,10 +187,13 @@ __global__ __launch_bounds__(kBlock) void k_begin(int l, int L, int H, Ctl* ctl,
         __syncthreads();
     }
     int64_t* out = (l < L) ? req_off : node_off;
+    // after a node-range bucket overflowed (err bit 3) the hyperbatch is
+    // sampled again on the radix-sort path: every later hop gets no requests
+    const bool dead = (ctl->err & 8) != 0;
     int64_t carry = 0;
     for (int base = 0; base < H; base += kBlock) {
         int j = base + threadIdx.x;
-        int64_t v = (j < H) ? size[j] : 0;
+        int64_t v = (j < H && !dead) ? size[j] : 0;
         if (j < H) lsz[(int64_t)j * (L + 1) + l] = (int32_t)v;
         int64_t total;
         int64_t ex = block_exclusive_scan(v, lds, total);
@@ -1164,8 +1180,10 @@ static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout&
     w.skey2.reserve((size_t)g.sort_max * 4);
     w.sval2.reserve((size_t)g.sort_max * 4);
     w.split.reserve((size_t)(join_tiles_max(g) + 2) * 8);
-    w.ghist.reserve((size_t)H * join_groups(g.H, join_tiles_max(g)) * 8);
-    w.gemit.reserve((size_t)join_groups(g.H, join_tiles_max(g)) * 8);
+    const int64_t G = std::max<int64_t>(join_groups(g.H, join_tiles_max(g)), g.bstride_max);
+    w.ghist.reserve((size_t)H * G * 8);
+    w.gemit.reserve((size_t)G * 8);
+    w.acoff.reserve((size_t)(kCoarseMax + 1) * 8);
     w.rs_hist.reserve((size_t)radix_hist_entries(g.sort_max) * 4);
     w.rs_dtot.reserve((size_t)radix_dtot_entries() * 4);
     w.scan_part.reserve((size_t)scan_partials_needed() * 8);
@@ -1177,7 +1195,7 @@ static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout&
 
 template <typename OffT>
 static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l, int32_t f, Batch& b,
-                         const SyncLayout& y, int cur, hipStream_t st) {
+                         const SyncLayout& y, int cur, bool legacy, hipStream_t st) {
     const ChainParams* prm = w.params.as<ChainParams>();
     Ctl* ctl = w.sync.as<Ctl>();
     int32_t* lsz = (int32_t*)((char*)w.sync.ptr + y.lsz);
@@ -1217,10 +1235,50 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     else if (f <= 32) AGNES_SAMPLE(32);
     else AGNES_SAMPLE(0);
 #undef AGNES_SAMPLE
+    const int64_t s_max = std::max<int64_t>(1, std::min<int64_t>(g.Smax, (int64_t)g.H * g.cap[l] * f));
+    if (!legacy) {
+        // node-range buckets: the sampled edges grouped by coarse bucket, then
+        // each bucket joined with its part of the list in LDS
+        const int64_t load_max = (int64_t)g.H * g.cap[l] * (1 + (int64_t)f);
+        bucket_partition(w.skey.as<uint32_t>(), w.skey2.as<uint32_t>(), w.sval2.as<uint32_t>(), &ctl->S, &ctl->R,
+                         s_max, load_max, s, g.H, w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), rlk,
+                         w.acoff.as<int64_t>(), st);
+        BucketJoinArgs j{};
+        j.store = &s;
+        j.H = g.H;
+        j.jbits = g.jbits;
+        j.write_nodes = l + 1 < g.L;
+        j.capN = g.capN;
+        j.rows_cap = g.rows_max;
+        j.cap = s.bucket_cap;
+        j.coarse_max = g.bcoarse[l];
+        j.G = g.bstride[l];
+        j.n_dev = &ctl->S;
+        j.old_dev = &ctl->R;
+        j.rk = w.skey2.as<uint32_t>();
+        j.rv = w.sval2.as<uint32_t>();
+        j.dtot = w.rs_dtot.as<uint32_t>();
+        j.acoff = w.acoff.as<int64_t>();
+        j.ak = rlk;
+        j.av = rlv;
+        j.req_off = w.req_off.as<int64_t>();
+        j.e_off = w.e_off.as<int64_t>();
+        j.size = w.size.as<int32_t>();
+        j.ghist = w.ghist.as<int64_t>();
+        j.gemit = w.gemit.as<int64_t>();
+        j.newcnt = w.newcnt.as<int64_t>();
+        j.row_ptr = b.row_ptr[l].as<int32_t>();
+        j.nodes = w.nodes.as<int32_t>();
+        j.ck = w.rl_key[cur ^ 1].as<uint64_t>();
+        j.cv = w.rl_val[cur ^ 1].as<int32_t>();
+        j.col = b.col[l].as<int32_t>();
+        j.ctl = ctl;
+        bucket_join(j, st);
+        return;
+    }
     // sampled neighbours sorted by node id; values = edge numbers (stable: minibatch order kept).
     // This hop's own bound sizes the sort's tiles and grid (hop 0 samples far
     // fewer edges than the last hop).
-    const int64_t s_max = std::max<int64_t>(1, std::min<int64_t>(g.Smax, (int64_t)g.H * g.cap[l] * f));
     int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
                                     w.sval2.as<uint32_t>(), &ctl->S, s_max, s.node_bits,
                                     w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
@@ -1381,7 +1439,7 @@ static std::vector<TierRound> plan_staging(const Store& s, Batch& b, hipStream_t
 // value from the params block, so the sequence depends only on the shape, the
 // store and the buffer addresses (the key of a captured graph).
 static void launch_chain(const Store& s, Batch& b, const Geometry& g, const SyncLayout& y,
-                         const int32_t* fanouts, hipStream_t st) {
+                         const int32_t* fanouts, bool legacy, hipStream_t st) {
     Workspace& w = b.ws;
     const int32_t H = g.H, B = g.B, L = g.L;
     Ctl* ctl = w.sync.as<Ctl>();
@@ -1390,6 +1448,8 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     AGNES_LAUNCH(k_init, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
                        w.params.as<ChainParams>(), H, B, s.num_nodes, g.capN, w.nodes.as<int32_t>(),
                        w.size.as<int32_t>(), w.newcnt.as<int64_t>(), w.skey.as<uint32_t>(), ctl);
+    // the list of hop 0 (Bck of the targets): targets sorted by (node,
+    // minibatch) with the radix sort, on either join path
     int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
                                     w.sval2.as<uint32_t>(), &ctl->targets, (int64_t)H * B, s.node_bits,
                                     w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
@@ -1400,8 +1460,8 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     AGNES_CHECK_HIP(hipGetLastError());
     int cur = 0;
     for (int l = 0; l < L; l++) {
-        if (s.offsets64) launch_layer<int64_t>(s, w, g, l, fanouts[l], b, y, cur, st);
-        else launch_layer<int32_t>(s, w, g, l, fanouts[l], b, y, cur, st);
+        if (s.offsets64) launch_layer<int64_t>(s, w, g, l, fanouts[l], b, y, cur, legacy, st);
+        else launch_layer<int32_t>(s, w, g, l, fanouts[l], b, y, cur, legacy, st);
         cur ^= 1;
     }
     // close the last hop: edge counts, final node counts, output row offsets
@@ -1419,12 +1479,13 @@ static std::vector<uint64_t> chain_key(const Store& s, const Batch& b, const Geo
     auto a = [](const void* p) { return (uint64_t)(uintptr_t)p; };
     std::vector<uint64_t> k = {a(&s), (uint64_t)s.num_nodes, (uint64_t)s.nblk, (uint64_t)s.offsets64,
                                (uint64_t)s.node_bits, (uint64_t)s.e_blk_log2, (uint64_t)s.rpb,
+                               (uint64_t)s.join_path, (uint64_t)s.bucket_cap,
                                a(s.offsets.ptr), a(s.indices.ptr), (uint64_t)g.H, (uint64_t)g.B, (uint64_t)g.L};
     for (int l = 0; l < g.L; l++) k.push_back((uint64_t)fanouts[l]);
     for (const DevBuf* d : {&w.nodes, &w.size, &w.newcnt, &w.req_off, &w.mb_off, &w.sync, &w.cnt, &w.e_off,
                             &w.rl_key[0], &w.rl_key[1], &w.rl_val[0], &w.rl_val[1], &w.skey, &w.sval, &w.skey2,
                             &w.sval2, &w.split, &w.ghist, &w.gemit, &w.rs_hist, &w.rs_dtot, &w.scan_part,
-                            &w.topo_part, &w.params})
+                            &w.topo_part, &w.params, &w.acoff})
         k.push_back(a(d->ptr));
     for (int l = 0; l < g.L; l++) {
         k.push_back(a(b.row_ptr[l].ptr));
@@ -1446,7 +1507,7 @@ static void capture_chain(const Store& s, Batch& b, const Geometry& g, const Syn
     AGNES_CHECK_HIP(hipStreamBeginCapture(b.cap_stream, hipStreamCaptureModeThreadLocal));
     hipGraph_t graph = nullptr;
     try {
-        launch_chain(s, b, g, y, fanouts, b.cap_stream);
+        launch_chain(s, b, g, y, fanouts, s.join_path == 0, b.cap_stream);
     } catch (...) {
         (void)hipStreamEndCapture(b.cap_stream, &graph);
         if (graph) (void)hipGraphDestroy(graph);
@@ -1515,7 +1576,12 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, bool tar
     if (s.sampling_graph && !(b.chain && key == b.chain_key) && key == b.last_key)
         capture_chain(s, b, g, y, fanouts, key);
     if (s.sampling_graph && b.chain && key == b.chain_key) AGNES_CHECK_HIP(hipGraphLaunch(b.chain, st));
-    else launch_chain(s, b, g, y, fanouts, st);
+    else launch_chain(s, b, g, y, fanouts, s.join_path == 0, st);
+    // what finish needs to sample the hyperbatch again on the radix-sort path
+    b.fanouts.assign(fanouts, fanouts + L);
+    b.seed = seed;
+    b.mb_base = mb_base;
+    b.targets_dev = targets;
     b.last_key = std::move(key);
     b.cur = L & 1;                    // the list buffers alternate hop by hop
     // sizes of the outputs travel to pinned host memory; finish reads them
@@ -1536,6 +1602,19 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     b.state = kIdle;   // until the gather is enqueued
     Ctl hc;
     memcpy(&hc, w.sync_host.ptr, sizeof(Ctl));
+    if (hc.err & 8) {
+        // a sorted sub-bucket exceeded its capacity: the hyperbatch's sampling
+        // runs again on the radix-sort path (same results), then as before
+        const Geometry g = plan(s, H, b.B, b.fanouts.data(), L);
+        AGNES_LAUNCH(k_params, dim3(1), dim3(kBlock), 0, b.stream, w.params.as<ChainParams>(), b.targets_dev,
+                     b.seed, b.mb_base, w.sync.as<Ctl>(), (int64_t)H * b.B);
+        launch_chain(s, b, g, y, b.fanouts.data(), true, b.stream);
+        AGNES_CHECK_HIP(hipMemcpyAsync(w.sync_host.ptr, w.sync.ptr, y.bytes, hipMemcpyDeviceToHost, b.stream));
+        AGNES_CHECK_HIP(hipEventRecord(b.sampled_at, b.stream));
+        AGNES_CHECK_HIP(hipEventSynchronize(b.sampled_at));
+        memcpy(&hc, w.sync_host.ptr, sizeof(Ctl));
+        b.fallbacks++;
+    }
     AGNES_REQUIRE(!(hc.err & 1), AGNES_ERR_INVALID, "a target is outside [0, num_nodes)");
     AGNES_REQUIRE(!(hc.err & 2), AGNES_ERR_INVALID, "a target appears twice in one minibatch");
     AGNES_REQUIRE(!(hc.err & 4), AGNES_ERR_INTERNAL, "node capacity exceeded");

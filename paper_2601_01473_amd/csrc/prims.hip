@@ -169,6 +169,7 @@ void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_
 // digit's run contiguously.
 constexpr int64_t kSmallSort = 1 << 21;
 static int sort_items(int64_t n_max) { return n_max <= kSmallSort ? 8 : 16; }
+int radix_items(int64_t n_max) { return sort_items(n_max); }
 constexpr int kMaxRadixBits = 10;
 
 // Tiles rounded up to a multiple of the XCD count (the scatter's grid).

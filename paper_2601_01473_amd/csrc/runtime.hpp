@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <climits>
 #include <deque>
 #include <string>
 #include <utility>
@@ -189,6 +190,7 @@ struct Workspace {
     DevBuf rs_hist, rs_dtot;          // radix-sort histograms
     DevBuf scan_part;                 // scan partial sums
     DevBuf topo_part;                 // per sampler workgroup: Bck rows it opened
+    DevBuf acoff;                     // node-range buckets: old list entries before each coarse bucket
     DevBuf params;                    // per-call values the sampling kernels read (targets, seed, minibatch base)
     DevBuf targets;                   // targets uploaded from host memory by the call
     PinnedBuf targets_host;           // their pinned staging copy
@@ -218,6 +220,15 @@ struct Store {
     int64_t max_degree = 0;
     int node_bits = 0;                // bits of a node id (ceil log2 num_nodes)
     DevBuf offsets, indices, features, first_node, last_node;
+    // Node-range buckets of the join (bucket.hip): nlev nested levels, finest
+    // first; lev_info_host / lev_info: [nlev][2] (offset of the level's
+    // boundaries in bnd, bucket count); bnd: every level's boundaries
+    // (count + 1 ascending node ids from 0 to num_nodes).
+    int nlev = 0;
+    std::vector<int32_t> lev_info_host;
+    DevBuf bnd, lev_info;
+    int join_path = 0;                // 1 = node-range buckets, 0 = radix sort and merge-path join (default)
+    int bucket_cap = 2048;            // entries of a sorted sub-bucket (at most kBucketCap)
     // Staged feature tier (features in pinned host memory, an HBM pool of
     // feature-block slots).  Not used when tiered == 0 (features in HBM).
     // The pool's host-side bookkeeping changes with every planned hyperbatch.
@@ -276,6 +287,13 @@ struct Batch {
     int64_t capN = 0;
     int64_t rows_max = 0;             // node-list capacity of the hyperbatch (sizes the sync block)
     int cur = 0;                      // which list buffer holds the final list
+    // The begun hyperbatch's arguments, for sampling it again on the radix-sort
+    // path when a node-range bucket overflows (fallbacks counts those).
+    std::vector<int32_t> fanouts;
+    uint64_t seed = 0;
+    int64_t mb_base = 0;
+    const int32_t* targets_dev = nullptr;
+    int64_t fallbacks = 0;
     int64_t need_cap = 0;             // staged tier: entries of each array in ws.need
     std::vector<int64_t> node_off;
     std::vector<int32_t> layer_sizes;
@@ -364,6 +382,9 @@ int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint3
                        const int64_t* n_dev, int64_t n_max, int bits, uint32_t* hist,
                        uint32_t* dtot, hipStream_t st, bool vals_iota = false);
 int64_t radix_hist_entries(int64_t n_max);
+// Keys per thread (8 or 16) and tiles of a radix pass over at most n_max keys.
+int radix_items(int64_t n_max);
+int64_t radix_tiles(int64_t n_max);
 int64_t radix_dtot_entries();
 
 // Philox4x64-10 words of n (counter [4], key [2]) pairs, device arrays (prims.hip).

@@ -10,6 +10,7 @@
 #include <cstring>
 #include <memory>
 
+#include "bucket.hpp"
 #include "device.hpp"
 #include "runtime.hpp"
 
@@ -165,6 +166,7 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
                            s->first_node.as<int32_t>(), s->last_node.as<int32_t>());
     AGNES_CHECK_HIP(hipGetLastError());
     AGNES_CHECK_HIP(hipStreamSynchronize(st));
+    build_bucket_levels(*s, csr->indices, n, e);
     return s.release();
 }
 
