@@ -422,6 +422,68 @@ def copy_calibration(torch, nbytes=4 << 30, reps=5):
                       "GBps_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
+class Pipeline:
+    """The schedule the benchmark times.  Step s is the hyperbatch of
+    targets[s] with mb_base s * H; the sampling of steps s+1 .. s+depth runs
+    on `sample_streams` streams (alternating, default priority) while step s
+    gathers on the default stream (or a stream of its own).  Each step's batch
+    lives in one of NSLOT slots and is reused depth + lag steps later; when a
+    step is retired (its outputs complete), on_retire(s, batch, record) is
+    called before its slot is reused.
+    ahead: gather s is queued (behind gather s-1) as soon as step s's sizes
+      are known; only then is step s-2 retired and step s+depth begun in its
+      slot, so the gather stream never drains while the host enqueues sampling.
+    sample-first: step s-1 is retired, step s+depth begun, then gather s queued.
+    gather-first: gather s queued, step s-1 retired, step s+depth begun."""
+
+    def __init__(self, store, cfg, H, targets, depth=3, sample_streams=3, gather_stream="default",
+                 schedule="ahead", on_retire=None):
+        import torch
+        self.store, self.cfg, self.H, self.targets = store, cfg, H, targets
+        self.D = max(1, depth)
+        self.schedule = schedule
+        # "ahead" keeps two finished steps unread, so it holds two more slots
+        # than the hyperbatches in flight
+        self.lag = 2 if schedule == "ahead" else 1
+        self.NSLOT = self.D + self.lag
+        self.slots = [None] * self.NSLOT
+        self.s_streams = [torch.cuda.Stream() for _ in range(max(1, sample_streams))]
+        self.g_stream = torch.cuda.default_stream() if gather_stream == "default" else torch.cuda.Stream()
+        self.on_retire = on_retire or (lambda s, b, record: b.wait())
+
+    def begin(self, s):
+        k = s % self.NSLOT
+        self.slots[k] = self.store.begin(self.targets[s], self.cfg.fanouts, seed=self.cfg.seed, mb_base=s * self.H,
+                                         batch=self.slots[k], stream=self.s_streams[s % len(self.s_streams)])
+
+    def retire(self, s, record):
+        self.on_retire(s, self.slots[s % self.NSLOT], record)
+
+    def run(self, first, n, record):
+        """Steps first .. first+n-1 with the sampling of steps s+1 .. s+depth in
+        flight while step s gathers; every step is retired before returning."""
+        D, lag = self.D, self.lag
+        for s in range(first, first + min(D, n)):
+            self.begin(s)
+        for i in range(n):
+            s = first + i
+            if self.schedule != "sample-first":
+                self.slots[s % self.NSLOT].finish(stream=self.g_stream)   # waits for step s's sizes only
+            if i >= lag:
+                self.retire(s - lag, record)                              # its slot is free for step s+D
+            if i + D < n:
+                self.begin(s + D)
+            if self.schedule == "sample-first":
+                self.slots[s % self.NSLOT].finish(stream=self.g_stream)
+        for s in range(first + max(0, n - lag), first + n):
+            self.retire(s, record)
+
+    def close(self):
+        for b in self.slots:
+            if b is not None:
+                b.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -451,6 +513,10 @@ def main():
                     help="rows in flight per lane group, 4, 8 or 16 (default: 16 for rows of 1-2 KiB, else 4)")
     ap.add_argument("--gather-nt", type=int, default=None, help="1 = non-temporal row stores, 0 = ordinary")
     ap.add_argument("--gather-chunks", type=int, default=None, help="launches the row copy is split into")
+    ap.add_argument("--sampling-groups", type=int, default=None,
+                    help="most workgroups of each sampling-phase kernel that loops over its work")
+    ap.add_argument("--join-path", type=int, choices=[0, 1], default=None,
+                    help="0: radix sort and merge-path join (default); 1: node-range buckets")
     ap.add_argument("--sampling-graph", type=int, choices=[0, 1], default=0,
                     help="1: replay the sampling kernels from a captured HIP graph; 0: launch them one by one")
     ap.add_argument("--ablation", action="store_true",
@@ -522,16 +588,14 @@ def main():
     store.set_gather_shape(args.gather_groups, args.gather_unroll,
                            None if args.gather_nt is None else bool(args.gather_nt), args.gather_chunks)
     store.set_sampling_graph(bool(args.sampling_graph))
+    if args.sampling_groups is not None:
+        store.set_sampling_groups(args.sampling_groups)
+    if args.join_path is not None:
+        store.set_join_path(bool(args.join_path))
     stream = torch.cuda.current_stream()
     ob = 8 if w["offsets"].dtype == np.int64 else 4
     rb = cfg.row_bytes
 
-    # sampling runs on one or more streams, gathers on another (all default priority)
-    s_streams = [torch.cuda.Stream() for _ in range(max(1, args.sample_streams))]
-    # the gather may run on the default stream, leaving the process's other
-    # hardware queues to sampling
-    g_stream = torch.cuda.default_stream() if args.gather_stream == "default" else torch.cuda.Stream()
-    s_stream = s_streams[0]
     acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, distinct=0, block_model=0, sample_ms=0.0, gather_ms=0.0,
                copy_ms=0.0, steps=0)
 
@@ -551,48 +615,14 @@ def main():
         acc["copy_ms"] += st["copy_ms"]
         acc["steps"] += 1
 
-    D = max(1, args.depth)                      # hyperbatches sampled ahead of the one gathering
-    # "ahead" keeps two finished steps unread, so it holds two more slots than
-    # the hyperbatches in flight
-    NSLOT = D + (2 if args.schedule == "ahead" else 1)
-    slots = [None] * NSLOT
-
-    # where step s's targets come from: device tensors (resident in HBM before
-    # timing, the benchmark's value) or host arrays that every begin uploads
-    src = {"targets": dev_targets}
-
-    def begin(s):
-        k = s % NSLOT
-        slots[k] = store.begin(src["targets"][s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[k],
-                               stream=s_streams[s % len(s_streams)])
-
-    def retire(s, record):
-        b = slots[s % NSLOT]
-        account(b) if record else b.wait()
+    pipe = Pipeline(store, cfg, H, dev_targets, depth=args.depth, sample_streams=args.sample_streams,
+                    gather_stream=args.gather_stream, schedule=args.schedule,
+                    on_retire=lambda s, b, record: account(b) if record else b.wait())
+    D, NSLOT, slots = pipe.D, pipe.NSLOT, pipe.slots
+    s_streams = pipe.s_streams
 
     def pipeline(first, n, record):
-        """Steps first .. first+n-1 with the sampling of steps s+1 .. s+D in flight
-        while step s gathers.
-        ahead: gather s is queued (behind gather s-1) as soon as step s's sizes
-          are known; only then is step s-2 retired and step s+D begun in its slot,
-          so the gather stream never drains while the host enqueues sampling.
-        sample-first: step s-1 is retired, step s+D begun, then gather s queued.
-        gather-first: gather s queued, step s-1 retired, step s+D begun."""
-        for s in range(first, first + min(D, n)):
-            begin(s)
-        lag = 2 if args.schedule == "ahead" else 1
-        for i in range(n):
-            s = first + i
-            if args.schedule != "sample-first":
-                slots[s % NSLOT].finish(stream=g_stream)   # waits for step s's sizes only
-            if i >= lag:
-                retire(s - lag, record)                    # its slot is free for step s+D
-            if i + D < n:
-                begin(s + D)
-            if args.schedule == "sample-first":
-                slots[s % NSLOT].finish(stream=g_stream)
-        for s in range(first + max(0, n - lag), first + n):
-            retire(s, record)
+        pipe.run(first, n, record)
 
     # warm-up: every slot allocated at the largest shape seen so far
     pipeline(0, args.warmup, record=False)
@@ -614,7 +644,7 @@ def main():
     saved = dict(acc)
     for key in acc:
         acc[key] = 0 if isinstance(acc[key], int) else 0.0
-    src["targets"] = step_targets
+    pipe.targets = step_targets
     torch.cuda.synchronize()
     t_h = time.perf_counter()
     pipeline(s0, K, record=True)
@@ -622,7 +652,7 @@ def main():
     host_elapsed = time.perf_counter() - t_h
     host_bytes = acc["bytes"]
     acc.update(saved)
-    src["targets"] = dev_targets
+    pipe.targets = dev_targets
 
     # reference: the same work one hyperbatch at a time (synchronous prepare)
     nser = min(K, 5)
@@ -631,7 +661,7 @@ def main():
     for k in range(nser):
         s = s0 + k
         slots[0] = store.prepare(dev_targets[s], cfg.fanouts, seed=cfg.seed, mb_base=s * H, batch=slots[0],
-                                 stream=s_stream)
+                                 stream=s_streams[0])
     torch.cuda.synchronize()
     serial_ms = (time.perf_counter() - t1) / nser * 1e3
 

@@ -294,6 +294,11 @@ agnes_status agnes_set_device_allocator(agnes_device_alloc_fn alloc, agnes_devic
  *     hold, in [64, 2048] (default 2048).  A hyperbatch with a bucket above it
  *     is sampled again with the radix sort (same results); a smaller value
  *     only makes that happen more often.
+ *   AGNES_OPT_SAMPLING_GROUPS: most workgroups of each sampling-phase kernel
+ *     that loops over its work (the sampler, the radix passes, the join), in
+ *     [256, 4096] (default 512; 4096 leaves each kernel at its own limit,
+ *     2048 for most).  Fewer need fewer dispatch slots beside a running row
+ *     copy of another hyperbatch, which holds most of them.
  * Options change launch shapes and store kinds only, never results. */
 typedef enum {
     AGNES_OPT_PROFILE = 1,
@@ -303,7 +308,8 @@ typedef enum {
     AGNES_OPT_GATHER_CHUNKS = 5,
     AGNES_OPT_SAMPLING_GRAPH = 6,
     AGNES_OPT_JOIN_PATH = 7,
-    AGNES_OPT_BUCKET_CAP = 8
+    AGNES_OPT_BUCKET_CAP = 8,
+    AGNES_OPT_SAMPLING_GROUPS = 9
 } agnes_option;
 agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_t value);
 

@@ -158,6 +158,11 @@ class Store:
         if bucket_cap is not None:
             agnes_store_set_option(self.handle, B.AGNES_OPT_BUCKET_CAP, int(bucket_cap))
 
+    def set_sampling_groups(self, groups: int) -> None:
+        """Most workgroups of each sampling-phase kernel that loops over its
+        work (never changes results)."""
+        agnes_store_set_option(self.handle, B.AGNES_OPT_SAMPLING_GROUPS, int(groups))
+
     def set_gather_shape(self, groups: int | None = None, unroll: int | None = None,
                          nontemporal: bool | None = None, chunks: int | None = None) -> None:
         """Launch shape and store kind of the row-copy kernel (never change results)."""

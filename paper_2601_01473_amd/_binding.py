@@ -24,6 +24,7 @@ AGNES_OPT_GATHER_CHUNKS = 5
 AGNES_OPT_SAMPLING_GRAPH = 6
 AGNES_OPT_JOIN_PATH = 7
 AGNES_OPT_BUCKET_CAP = 8
+AGNES_OPT_SAMPLING_GROUPS = 9
 
 EXPORTED = ["agnes_build_blocks", "agnes_build_blocks_staged", "agnes_build_blocks_cached", "agnes_hyperbatch_prepare",
             "agnes_hyperbatch_prepare_device", "agnes_hyperbatch_begin", "agnes_hyperbatch_begin_device", "agnes_batch_finish", "agnes_batch_wait", "agnes_batch_view_get",

@@ -80,7 +80,9 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
 }
 
 // Workgroups of the per-request kernels (k_count, k_sample) of hop l.
-static int hop_grid(const Geometry& g, int l) { return grid_for((int64_t)g.H * g.cap[l], 2048); }
+static int hop_grid(const Store& s, const Geometry& g, int l) {
+    return grid_for((int64_t)g.H * g.cap[l], std::min(2048, s.sample_groups));
+}
 
 // ----------------------------------------------------------------- small kernels
 
@@ -1205,8 +1207,8 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     // this hop's requests are at most H cap[l]: its own bound sizes the grids
     // (beside a long kernel of another stream even an idle workgroup waits for
     // a slot); k_begin sums the previous hop's per-workgroup counts
-    const int gR = hop_grid(g, l);
-    const int gPrev = l > 0 ? hop_grid(g, l - 1) : 0;
+    const int gR = hop_grid(s, g, l);
+    const int gPrev = l > 0 ? hop_grid(s, g, l - 1) : 0;
     int64_t* part = w.scan_part.as<int64_t>();
     const uint64_t* rlk = w.rl_key[cur].as<uint64_t>();
     const int32_t* rlv = w.rl_val[cur].as<int32_t>();
@@ -1281,16 +1283,16 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     // fewer edges than the last hop).
     int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
                                     w.sval2.as<uint32_t>(), &ctl->S, s_max, s.node_bits,
-                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
+                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true, s.sample_groups);
     const uint32_t* su = in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>();
     const uint32_t* se = in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>();
     // join with the list: the next list, new node ids and the hop's columns
     const int64_t tiles_l = ((int64_t)g.H * g.cap[l] * (1 + (int64_t)f)) / kJoinTile + 1;
-    const int gJ = (int)std::min<int64_t>(2048, (tiles_l + 1) * kSplitLanes / kBlock + 1);
+    const int gJ = (int)std::min<int64_t>(std::min(2048, s.sample_groups), (tiles_l + 1) * kSplitLanes / kBlock + 1);
     int64_t* split = w.split.as<int64_t>();
     AGNES_LAUNCH(k_join_split, dim3(gJ), dim3(kBlock), lds_h, st, g.H, w.req_off.as<int64_t>(),
                        w.e_off.as<int64_t>(), rlk, su, se, split, ctl);
-    const int G = join_groups(g.H, tiles_l);
+    const int G = std::min(join_groups(g.H, tiles_l), std::max(kBlock, s.sample_groups / kBlock * kBlock));
     AGNES_LAUNCH(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H), st, g.H,
                        w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se, split, G,
                        w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), b.row_ptr[l].as<int32_t>(), ctl);
@@ -1452,7 +1454,7 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     // minibatch) with the radix sort, on either join path
     int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
                                     w.sval2.as<uint32_t>(), &ctl->targets, (int64_t)H * B, s.node_bits,
-                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true);
+                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true, s.sample_groups);
     AGNES_LAUNCH(k_list0, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
                        in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>(),
                        in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>(), B, w.rl_key[0].as<uint64_t>(),
@@ -1467,7 +1469,7 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     // close the last hop: edge counts, final node counts, output row offsets
     AGNES_LAUNCH(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
-                       w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), hop_grid(g, L - 1));
+                       w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), hop_grid(s, g, L - 1));
     AGNES_LAUNCH(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
                        (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl);
     AGNES_CHECK_HIP(hipGetLastError());
@@ -1479,7 +1481,7 @@ static std::vector<uint64_t> chain_key(const Store& s, const Batch& b, const Geo
     auto a = [](const void* p) { return (uint64_t)(uintptr_t)p; };
     std::vector<uint64_t> k = {a(&s), (uint64_t)s.num_nodes, (uint64_t)s.nblk, (uint64_t)s.offsets64,
                                (uint64_t)s.node_bits, (uint64_t)s.e_blk_log2, (uint64_t)s.rpb,
-                               (uint64_t)s.join_path, (uint64_t)s.bucket_cap,
+                               (uint64_t)s.join_path, (uint64_t)s.bucket_cap, (uint64_t)s.sample_groups,
                                a(s.offsets.ptr), a(s.indices.ptr), (uint64_t)g.H, (uint64_t)g.B, (uint64_t)g.L};
     for (int l = 0; l < g.L; l++) k.push_back((uint64_t)fanouts[l]);
     for (const DevBuf* d : {&w.nodes, &w.size, &w.newcnt, &w.req_off, &w.mb_off, &w.sync, &w.cnt, &w.e_off,

@@ -378,21 +378,24 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
 // no tile, waits for a slot: a capped grid keeps such kernels short.  A
 // multiple of 8 (the scatter splits its workgroups evenly over the XCDs).
 constexpr int kRadixGroups = 2048;
-static int radix_grid(int tiles) { return std::min(kRadixGroups, (tiles + kXcds - 1) / kXcds * kXcds); }
+static int radix_grid(int tiles, int cap) {
+    const int c = std::max(kXcds, std::min(kRadixGroups, cap) / kXcds * kXcds);
+    return std::min(c, (tiles + kXcds - 1) / kXcds * kXcds);
+}
 
 template <int ITEMS, int RB>
 static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                          const int64_t* n_dev, int tiles, int passes, uint32_t* hist, uint32_t* dtot,
-                         hipStream_t st, bool vals_iota) {
+                         hipStream_t st, bool vals_iota, int cap) {
     uint32_t *ka = keys, *kb = keys_tmp;
     uint32_t *va = vals, *vb = vals_tmp;
     for (int p = 0; p < passes; p++) {
         int shift = p * RB;
         const uint32_t* vin = (p == 0 && vals_iota) ? nullptr : va;
-        AGNES_LAUNCH((k_rs_hist<ITEMS, RB>), dim3(radix_grid(tiles)), dim3(kBlock), 0, st, ka, n_dev, shift,
+        AGNES_LAUNCH((k_rs_hist<ITEMS, RB>), dim3(radix_grid(tiles, cap)), dim3(kBlock), 0, st, ka, n_dev, shift,
                            hist);
         AGNES_LAUNCH((k_rs_scan<ITEMS, RB>), dim3(1 << RB), dim3(kBlock), 0, st, hist, n_dev, dtot);
-        AGNES_LAUNCH((k_rs_scatter<ITEMS, RB>), dim3(radix_grid(tiles)), dim3(kBlock), 0, st, ka, vin, kb,
+        AGNES_LAUNCH((k_rs_scatter<ITEMS, RB>), dim3(radix_grid(tiles, cap)), dim3(kBlock), 0, st, ka, vin, kb,
                            vb, n_dev, shift, hist, dtot);
         uint32_t* tk = ka; ka = kb; kb = tk;
         uint32_t* tv = va; va = vb; vb = tv;
@@ -402,18 +405,18 @@ static void radix_passes(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uin
 template <int ITEMS>
 static void radix_passes_rb(int rb, uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                             const int64_t* n_dev, int tiles, int passes, uint32_t* hist, uint32_t* dtot,
-                            hipStream_t st, bool vals_iota) {
+                            hipStream_t st, bool vals_iota, int cap) {
     if (rb == 8)
-        radix_passes<ITEMS, 8>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+        radix_passes<ITEMS, 8>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota, cap);
     else if (rb == 9)
-        radix_passes<ITEMS, 9>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+        radix_passes<ITEMS, 9>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota, cap);
     else
-        radix_passes<ITEMS, 10>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+        radix_passes<ITEMS, 10>(keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota, cap);
 }
 
 int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                        const int64_t* n_dev, int64_t n_max, int bits, uint32_t* hist,
-                       uint32_t* dtot, hipStream_t st, bool vals_iota) {
+                       uint32_t* dtot, hipStream_t st, bool vals_iota, int max_groups) {
     if (bits < 1) bits = 1;
     // the fewest passes with digits of at most 10 bits, then the narrowest
     // digit (at least 8 bits) that covers the key in that many passes
@@ -421,9 +424,11 @@ int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint3
     const int rb = std::max(8, (bits + passes - 1) / passes);
     const int tiles = (int)radix_tiles(n_max);
     if (sort_items(n_max) == 8)
-        radix_passes_rb<8>(rb, keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+        radix_passes_rb<8>(rb, keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota,
+                           max_groups);
     else
-        radix_passes_rb<16>(rb, keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota);
+        radix_passes_rb<16>(rb, keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota,
+                            max_groups);
     AGNES_CHECK_HIP(hipGetLastError());
     return passes & 1;   // 1: the sorted pairs are in keys_tmp / vals_tmp
 }

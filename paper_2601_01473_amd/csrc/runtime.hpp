@@ -229,6 +229,7 @@ struct Store {
     DevBuf bnd, lev_info;
     int join_path = 0;                // 1 = node-range buckets, 0 = radix sort and merge-path join (default)
     int bucket_cap = 2048;            // entries of a sorted sub-bucket (at most kBucketCap)
+    int sample_groups = 512;          // most workgroups of a sampling-phase kernel that loops over its work
     // Staged feature tier (features in pinned host memory, an HBM pool of
     // feature-block slots).  Not used when tiered == 0 (features in HBM).
     // The pool's host-side bookkeeping changes with every planned hyperbatch.
@@ -378,9 +379,11 @@ int64_t scan_partials_needed();
 // buffer).  hist needs radix_hist_entries(n_max) entries, dtot
 // radix_dtot_entries().  Returns 0 when the result is in keys/vals and 1 when it
 // is in keys_tmp/vals_tmp.
+// max_groups caps the workgroups of the histogram and scatter kernels (they
+// loop over the tiles).
 int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint32_t* vals_tmp,
                        const int64_t* n_dev, int64_t n_max, int bits, uint32_t* hist,
-                       uint32_t* dtot, hipStream_t st, bool vals_iota = false);
+                       uint32_t* dtot, hipStream_t st, bool vals_iota = false, int max_groups = 2048);
 int64_t radix_hist_entries(int64_t n_max);
 // Keys per thread (8 or 16) and tiles of a radix pass over at most n_max keys.
 int radix_items(int64_t n_max);
