@@ -484,6 +484,30 @@ class Pipeline:
                 b.close()
 
 
+def gather_calibration(ag, w, cfg, torch, reps=5):
+    """The row-copy kernel on a list whose rows are all distinct: one
+    hyperbatch of 2^21 distinct targets and no sampling (fanout 0), so every
+    launch reads and writes exactly rows x row_bytes (plus 4-byte node ids
+    and 12-byte list entries per row)."""
+    n = min(cfg.num_nodes, 1 << 21)
+    import synth
+    tg = synth.targets(cfg.num_nodes, n, cfg.data_seed + 11).reshape(1, n)
+    store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
+    store.set_profiling(True)
+    b = None
+    ms = []
+    for _ in range(reps):
+        b = store.prepare(tg, [0], seed=cfg.seed, batch=b)
+        st = b.stats()
+        ms.append(st["copy_ms"])
+    assert st["rows"] == n and st["distinct_rows"] == n
+    print(json.dumps({"mode": "row copy over all-distinct rows (fanout 0)", "rows": n, "row_bytes": cfg.row_bytes,
+                      "bytes_read": n * cfg.row_bytes, "bytes_written": n * cfg.row_bytes,
+                      "copy_ms": [round(x, 4) for x in ms]}), flush=True)
+    b.close()
+    store.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -534,6 +558,8 @@ def main():
                     help="with --cache-rows: access count at which a row enters the cache")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
+    ap.add_argument("--gather-calibration", action="store_true",
+                    help="run the row-copy kernel over 2^21 all-distinct rows (reference for its HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -571,6 +597,9 @@ def main():
         print(json.dumps(staged_tier(ag, w, cfg, dev_targets, H, args.staged, args.warmup, args.steps,
                                      8 if w["offsets"].dtype == np.int64 else 4, cfg.row_bytes, torch,
                                      args.cache_rows, args.cache_threshold)), flush=True)
+        return
+    if args.gather_calibration:
+        gather_calibration(ag, w, cfg, torch)
         return
     store = ag.Store(w["offsets"], w["indices"], w["features"], cfg.block_bytes, feat_dtype=cfg.feat_dtype)
     if args.sage is not None:

@@ -114,6 +114,24 @@ __device__ __forceinline__ int64_t wave_partition_point(int64_t lo, int64_t hi, 
     return lo;
 }
 
+// ----------------------------------------------------------------- device-wide scan layout
+
+// A scan over n elements (n read on the device) is split into G ranges of
+// whole tiles, one per workgroup: a reduce pass writes each range's sum, a
+// final pass adds the sums before its range and scans it.
+constexpr int kScanGroups = 1024;   // partial sums per scan
+constexpr int kScanItems = 4;       // consecutive elements per thread per tile
+constexpr int kScanTile = kBlock * kScanItems;
+
+__device__ __forceinline__ void scan_range(int64_t n, int G, int g, int64_t& lo, int64_t& hi) {
+    int64_t chunk = (n + G - 1) / G;
+    chunk = (chunk + kScanTile - 1) / kScanTile * kScanTile;
+    lo = (int64_t)g * chunk;
+    if (lo > n) lo = n;
+    hi = lo + chunk;
+    if (hi > n) hi = n;
+}
+
 // ----------------------------------------------------------------- RNG
 
 // Philox4x64 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC 2011): two 64x64->128

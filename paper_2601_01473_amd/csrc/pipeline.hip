@@ -232,6 +232,32 @@ __global__ __launch_bounds__(kBlock) void k_count(int H, int64_t capN, int32_t f
     }
 }
 
+// k_count fused with the reduce pass of the edge-offset scan: the counts of
+// scan range g (scan_range over the hop's R requests, G ranges) and their sum
+// in partials[g]; the scan's final pass follows.
+template <typename OffT>
+__global__ __launch_bounds__(kBlock) void k_count_reduce(int H, int64_t capN, int32_t f, const OffT* off,
+                                                         const int32_t* nodes, const int64_t* req_off_g,
+                                                         int32_t* cnt, int G, int64_t* partials, const Ctl* ctl) {
+    extern __shared__ int64_t req_off[];
+    __shared__ int64_t lds[kWavesPerBlock];
+    load_offsets(req_off, req_off_g, H);
+    int64_t lo, hi;
+    scan_range(ctl->R, G, blockIdx.x, lo, hi);
+    int64_t sum = 0;
+    for (int64_t q = lo + threadIdx.x; q < hi; q += kBlock) {
+        const int j = upper_segment(req_off, H, q);
+        const int32_t v = nodes[(int64_t)j * capN + (q - req_off[j])];
+        const int64_t deg = (int64_t)off[v + 1] - (int64_t)off[v];
+        const int32_t k = (int32_t)(deg < f ? deg : f);
+        cnt[q] = k;
+        sum += k;
+    }
+    int64_t total;
+    (void)block_exclusive_scan(sum, lds, total);
+    if (threadIdx.x == 0) partials[blockIdx.x] = total;
+}
+
 // Sample every request of the hop, walking the list in (node, minibatch) order:
 // consecutive threads serve the requests of the same topology block from every
 // minibatch, and the requests of one node are neighbours.  Also counts the
@@ -310,7 +336,7 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, cons
 // first on equal keys, so the pair of a run of equal edge keys, if A holds it,
 // sits right before the run.  Merge path cuts the merged sequence into tiles of
 // kJoinTile entries: tile t holds A[a_t, a_{t+1}) and B[t*T - a_t, ...) with
-// a_t from k_join_split.  An edge whose key differs from the previous edge's
+// a_t from k_join_count.  An edge whose key differs from the previous edge's
 // is a run head; a head whose pair A holds is an old node (the pair is in the
 // tile's A part or is A[a_t - 1]), otherwise a new one.  New nodes take local
 // ids |S_{j,l-1}| + (rank among the new nodes of minibatch j in key order), so
@@ -330,28 +356,10 @@ __device__ __forceinline__ uint64_t edge_key(const uint32_t* su, const uint32_t*
     return ((uint64_t)su[p] << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)se[p]);
 }
 
-// a_t for every tile boundary t: the number of A entries among the first
-// t * kJoinTile merged entries.  Groups of kSplitLanes lanes search one boundary
-// each (a few rounds of 16 probes).
+// Merge path: a_t, the number of A entries among the first t * kJoinTile
+// merged entries, is found for every tile boundary t by groups of
+// kSplitLanes lanes (a few rounds of 16 probes) in k_join_count.
 constexpr int kSplitLanes = 16;
-
-__global__ __launch_bounds__(kBlock) void k_join_split(int H, const int64_t* req_off, const int64_t* e_off,
-                                                       const uint64_t* ak, const uint32_t* su, const uint32_t* se,
-                                                       int64_t* split, const Ctl* ctl) {
-    extern __shared__ int64_t mb_e[];
-    load_mb_edges(mb_e, req_off, e_off, H);
-    const int64_t na = ctl->R, nb = ctl->S, n = na + nb;
-    const int64_t tiles = (n + kJoinTile - 1) / kJoinTile;
-    const int64_t ng = (int64_t)gridDim.x * kBlock / kSplitLanes;
-    for (int64_t t = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kSplitLanes; t <= tiles; t += ng) {
-        const int64_t d = std::min<int64_t>(t * kJoinTile, n);
-        const int64_t lo = d > nb ? d - nb : 0, hi = d < na ? d : na;
-        // A[i] goes before B[d-1-i] when A[i] <= B[d-1-i] (A first on equal keys)
-        const int64_t x = group_partition_point<kSplitLanes>(
-            lo, hi, [&](int64_t i) { return ak[i] <= edge_key(su, se, mb_e, H, d - 1 - i); });
-        if (lane_id() % kSplitLanes == 0) split[t] = x;
-    }
-}
 
 struct JoinSpan {
     int64_t a0, b0;
@@ -361,8 +369,8 @@ struct JoinSpan {
 __device__ __forceinline__ JoinSpan join_span(int64_t t, int64_t n, const int64_t* split) {
     JoinSpan s;
     const int64_t d0 = t * kJoinTile, d1 = std::min<int64_t>(d0 + kJoinTile, n);
-    s.a0 = split[t];
-    const int64_t a1 = split[t + 1];
+    s.a0 = split[0];
+    const int64_t a1 = split[1];
     s.b0 = d0 - s.a0;
     s.nA = (int)(a1 - s.a0);
     s.nB = (int)((d1 - a1) - s.b0);
@@ -431,13 +439,15 @@ __device__ __forceinline__ void group_tiles(int64_t n, int g, int G, int64_t& t0
     t1 = std::min<int64_t>(tiles, t0 + per);
 }
 
-// Pass 1: per group, new nodes per minibatch (ghist[j][g]) and merged entries
+// Pass 1: per group, the merge-path boundaries of its tiles (into split, for
+// pass 2 too: a_t of every tile boundary t, searched by groups of kSplitLanes
+// lanes), new nodes per minibatch (ghist[j][g]) and merged entries
 // (gemit[g]).  Also writes the hop's row pointers in request order: row r of
 // minibatch j starts at its edge offset minus the minibatch's first edge.
-// Dynamic LDS: mb_e[H+1], ro[H+1], sk[T], sv[T], count[H].
+// Dynamic LDS: mb_e[H+1], ro[H+1], sk[T], sv[T], count[H], ssplit[per].
 __global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req_off, const int64_t* e_off,
                                                        const uint64_t* ak, const int32_t* av, const uint32_t* su,
-                                                       const uint32_t* se, const int64_t* split, int G,
+                                                       const uint32_t* se, int64_t* split, int G,
                                                        int64_t* ghist, int64_t* gemit, int32_t* row_ptr,
                                                        const Ctl* ctl) {
     extern __shared__ int64_t lds[];
@@ -446,6 +456,7 @@ __global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req
     uint64_t* sk = (uint64_t*)(ro + H + 1);
     int32_t* sv = (int32_t*)(sk + kJoinTile);
     uint32_t* count = (uint32_t*)(sv + kJoinTile);
+    int64_t* ssplit = (int64_t*)(((uintptr_t)(count + H) + 7) & ~(uintptr_t)7);
     __shared__ uint64_t pre[2];
     __shared__ int32_t pre_val;
     __shared__ uint32_t nh_total;
@@ -460,13 +471,27 @@ __global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req
         row_ptr[q + j] = (int32_t)(e_off[q] - mb_e[j]);
         if (q + 1 == ro[j + 1]) row_ptr[q + j + 1] = (int32_t)(e_off[q + 1] - mb_e[j]);
     }
-    const int64_t n = R + ctl->S;
+    const int64_t nb = ctl->S, n = R + nb;
     int64_t t0, t1;
     group_tiles(n, g, G, t0, t1);
+    // boundaries t0 .. t1: A[i] goes before B[d-1-i] when A[i] <= B[d-1-i]
+    // (A first on equal keys); a neighbouring group writes the same value at
+    // a shared boundary
+    for (int64_t t = t0 + tid / kSplitLanes; t <= t1; t += kBlock / kSplitLanes) {
+        const int64_t d = std::min<int64_t>(t * kJoinTile, n);
+        const int64_t lo = d > nb ? d - nb : 0, hi = d < R ? d : R;
+        const int64_t x = group_partition_point<kSplitLanes>(
+            lo, hi, [&](int64_t i) { return ak[i] <= edge_key(su, se, mb_e, H, d - 1 - i); });
+        if (lane_id() % kSplitLanes == 0) {
+            ssplit[t - t0] = x;
+            split[t] = x;
+        }
+    }
+    __syncthreads();
     int64_t a_total = 0;
     uint32_t nh = 0;
     for (int64_t t = t0; t < t1; t++) {
-        const JoinSpan s = join_span(t, n, split);
+        const JoinSpan s = join_span(t, n, ssplit + (t - t0));
         join_stage(s, ak, av, su, se, mb_e, H, sk, sv, pre, &pre_val);
         a_total += s.nA;
         __syncthreads();
@@ -552,7 +577,7 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
     int64_t run = gemit[g];                  // merged entries before the tile
     const uint64_t lane_le = lanemask_lt() | (1ull << lane);
     for (int64_t t = t0; t < t1; t++) {
-        const JoinSpan s = join_span(t, n, split);
+        const JoinSpan s = join_span(t, n, split + t);
         join_stage(s, ak, av, su, se, mb_e, H, sk, sv, pre, &pre_val);
         __syncthreads();
         if (tid == 0) {
@@ -683,7 +708,10 @@ static int join_groups(int H, int64_t tiles) {
     return (int)((G + kBlock - 1) / kBlock * kBlock);
 }
 
-static size_t join_count_lds(int H) { return (size_t)(H + 1) * 16 + (size_t)kJoinTile * 12 + (size_t)H * 4; }
+// per: the most tile boundaries of one group (its tiles + 1)
+static size_t join_count_lds(int H, int64_t per) {
+    return (size_t)(H + 1) * 16 + (size_t)kJoinTile * 12 + (size_t)H * 4 + 8 + (size_t)per * 8;
+}
 static size_t join_write_lds(int H) {
     return (size_t)(H + 1) * 8 + (size_t)kJoinTile * 8 + (size_t)kJoinTile * 4 * 3 + 4 + (size_t)H * 4 +
            (size_t)kWavesPerBlock * H * 2;
@@ -1216,10 +1244,12 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     AGNES_LAUNCH(k_begin, dim3(1), dim3(kBlock), 0, st, l, g.L, g.H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ecount, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
                        (int64_t*)nullptr, w.topo_part.as<uint32_t>(), gPrev);
-    AGNES_LAUNCH(k_count<OffT>, dim3(gR), dim3(kBlock), lds_h, st, g.H, g.capN, f, off,
-                       w.nodes.as<int32_t>(), w.req_off.as<int64_t>(), w.cnt.as<int32_t>(), ctl);
-    scan_counts(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, std::max<int64_t>(1, (int64_t)g.H * g.cap[l]),
-                &ctl->S, part, st);
+    // counts and the edge-offset scan: counts with the reduce pass, then the final pass
+    const int64_t r_max = std::max<int64_t>(1, (int64_t)g.H * g.cap[l]);
+    const int gS = scan_groups(r_max);
+    AGNES_LAUNCH(k_count_reduce<OffT>, dim3(gS), dim3(kBlock), lds_h, st, g.H, g.capN, f, off,
+                 w.nodes.as<int32_t>(), w.req_off.as<int64_t>(), w.cnt.as<int32_t>(), gS, part, ctl);
+    scan_counts_final(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, r_max, &ctl->S, part, st);
     const int32_t* adj = s.indices.as<int32_t>();
     int32_t* cg = w.skey.as<int32_t>();
 #define AGNES_SAMPLE(MK)                                                                               \
@@ -1288,12 +1318,10 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     const uint32_t* se = in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>();
     // join with the list: the next list, new node ids and the hop's columns
     const int64_t tiles_l = ((int64_t)g.H * g.cap[l] * (1 + (int64_t)f)) / kJoinTile + 1;
-    const int gJ = (int)std::min<int64_t>(std::min(2048, s.sample_groups), (tiles_l + 1) * kSplitLanes / kBlock + 1);
     int64_t* split = w.split.as<int64_t>();
-    AGNES_LAUNCH(k_join_split, dim3(gJ), dim3(kBlock), lds_h, st, g.H, w.req_off.as<int64_t>(),
-                       w.e_off.as<int64_t>(), rlk, su, se, split, ctl);
     const int G = std::min(join_groups(g.H, tiles_l), std::max(kBlock, s.sample_groups / kBlock * kBlock));
-    AGNES_LAUNCH(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H), st, g.H,
+    const int64_t per = (tiles_l + G - 1) / G + 2;
+    AGNES_LAUNCH(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H, per), st, g.H,
                        w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se, split, G,
                        w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), b.row_ptr[l].as<int32_t>(), ctl);
     AGNES_LAUNCH(k_join_scan, dim3(g.H + 1), dim3(kBlock), 0, st, g.H, G, w.ghist.as<int64_t>(),

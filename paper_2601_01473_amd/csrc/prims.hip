@@ -41,20 +41,7 @@ void philox_words(const uint64_t* c, const uint64_t* k, int64_t n, uint64_t* out
 
 // ----------------------------------------------------------------- scan
 
-constexpr int kScanGroups = 1024;   // partial sums per scan
-constexpr int kScanItems = 4;       // consecutive elements per thread per tile
-constexpr int kScanTile = kBlock * kScanItems;
-
 int64_t scan_partials_needed() { return kScanGroups + 1; }
-
-__device__ __forceinline__ void scan_range(int64_t n, int G, int g, int64_t& lo, int64_t& hi) {
-    int64_t chunk = (n + G - 1) / G;
-    chunk = (chunk + kScanTile - 1) / kScanTile * kScanTile;
-    lo = (int64_t)g * chunk;
-    if (lo > n) lo = n;
-    hi = lo + chunk;
-    if (hi > n) hi = n;
-}
 
 template <typename T>
 __global__ void k_scan_reduce(const T* in, const int64_t* n_dev, int G, int64_t* partials,
@@ -135,11 +122,21 @@ __global__ void k_scan_final(const T* in, int64_t* out, const int64_t* n_dev, in
     }
 }
 
+int scan_groups(int64_t n_max) {
+    const int64_t g = (n_max + kScanTile - 1) / kScanTile;
+    return (int)(g < 1 ? 1 : (g > kScanGroups ? kScanGroups : g));
+}
+
+void scan_counts_final(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max, int64_t* total_dev,
+                       const int64_t* partials, hipStream_t st) {
+    const int G = scan_groups(n_max);
+    AGNES_LAUNCH(k_scan_final<int32_t>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials, total_dev);
+}
+
 template <typename T>
 static void scan_impl(const T* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
                       int64_t* total_dev, int64_t* partials, int64_t* nonzero, hipStream_t st) {
-    int64_t g = (n_max + kScanTile - 1) / kScanTile;
-    int G = (int)(g < 1 ? 1 : (g > kScanGroups ? kScanGroups : g));
+    const int G = scan_groups(n_max);
     AGNES_LAUNCH(k_scan_reduce<T>, dim3(G), dim3(kBlock), 0, st, in, n_dev, G, partials, nonzero);
     AGNES_LAUNCH(k_scan_final<T>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials, total_dev);
     AGNES_CHECK_HIP(hipGetLastError());
