@@ -83,6 +83,19 @@ def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int) -> tuple:
     return bs, bg, copy
 
 
+def sampling_replayed(mode: int, H: int, B: int, fanouts, num_nodes: int) -> bool:
+    """Whether the library replays the sampling kernels from a HIP graph for
+    this shape: always (1), never (0), or (2) when its hops can sample at most
+    2^20 edges (H x frontier capacity x fanout summed over the hops)."""
+    if mode != 2:
+        return mode == 1
+    cap, edges = B, 0
+    for f in fanouts:
+        edges += H * cap * f
+        cap = min(cap * (1 + f), max(num_nodes, B))
+    return edges <= (1 << 20)
+
+
 def block_model_bytes(st: dict, block_bytes: int) -> int:
     """Bytes the paper's I/O model reads: every non-empty topology block row of
     every hop and every non-empty feature block row, one whole block each."""
@@ -541,8 +554,9 @@ def main():
                     help="most workgroups of each sampling-phase kernel that loops over its work")
     ap.add_argument("--join-path", type=int, choices=[0, 1], default=None,
                     help="0: radix sort and merge-path join (default); 1: node-range buckets")
-    ap.add_argument("--sampling-graph", type=int, choices=[0, 1], default=0,
-                    help="1: replay the sampling kernels from a captured HIP graph; 0: launch them one by one")
+    ap.add_argument("--sampling-graph", type=int, choices=[0, 1, 2], default=2,
+                    help="1: replay the sampling kernels from a captured HIP graph; 0: launch them one by one; "
+                         "2: replay for shapes of at most 2^20 sampled edges (the library's default)")
     ap.add_argument("--ablation", action="store_true",
                     help="instead of the benchmark line, compare the hyperbatch with its minibatches "
                          "prepared one at a time (time, bytes, block reads)")
@@ -616,7 +630,7 @@ def main():
     store.set_profiling(True)
     store.set_gather_shape(args.gather_groups, args.gather_unroll,
                            None if args.gather_nt is None else bool(args.gather_nt), args.gather_chunks)
-    store.set_sampling_graph(bool(args.sampling_graph))
+    store.set_sampling_graph({0: False, 1: True, 2: "auto"}[args.sampling_graph])
     if args.sampling_groups is not None:
         store.set_sampling_groups(args.sampling_groups)
     if args.join_path is not None:
@@ -700,6 +714,8 @@ def main():
     sample_ms, gather_ms, copy_ms = acc["sample_ms"], acc["gather_ms"], acc["copy_ms"]
     value = tot_bytes / elapsed / 1e9
     copy_avg_ms = copy_ms / K
+    replayed = sampling_replayed(args.sampling_graph, H, B, cfg.fanouts, cfg.num_nodes)
+    graph_mode = "replayed from a HIP graph" if replayed else "launched one by one"
     achieved = (tot_copy_bytes / K) / (copy_avg_ms * 1e-3) / 1e9
     result = {
         "metric": "sampled edges/s + gathered feature GB/s per hyperbatch (% of HBM peak)",
@@ -727,7 +743,7 @@ def main():
         "mode": f"pipelined ({args.schedule}): {NSLOT} batch slots; "
                 f"hyperbatches t+1..t+{D} sample while t gathers"
                 f"; {len(s_streams)} sampling stream(s); gather on the {args.gather_stream} stream"
-                f"; sampling kernels {'replayed from a HIP graph' if args.sampling_graph else 'launched one by one'}",
+                f"; sampling kernels {graph_mode}",
         "serial_ms_per_step": round(serial_ms, 4),
         "host_targets": {"ms_per_step": round(host_elapsed / K * 1e3, 4),
                          "GBps": round(host_bytes / host_elapsed / 1e9, 2),

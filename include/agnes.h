@@ -276,13 +276,15 @@ agnes_status agnes_set_device_allocator(agnes_device_alloc_fn alloc, agnes_devic
  *   AGNES_OPT_GATHER_CHUNKS: the row copy runs as this many consecutive
  *     launches over consecutive parts of the bucket, in [1, 64] (default 1);
  *     kernels of other streams are dispatched between them.
- *   AGNES_OPT_SAMPLING_GRAPH: 0 = (default) every hyperbatch launches its
- *     sampling kernels one by one.  1 = a batch that begins two hyperbatches
- *     of the same shape in a row (same H, B, fanouts and store, and the same
- *     scratch buffers) captures the sampling kernels as a HIP graph and from
- *     then on replays it with one graph launch per hyperbatch; a batch holds
- *     one such graph and captures again when the shape changes.  Replay
- *     shortens one hyperbatch's latency on small shapes but slows hyperbatches
+ *   AGNES_OPT_SAMPLING_GRAPH: 0 = every hyperbatch launches its sampling
+ *     kernels one by one.  1 = a batch that begins two hyperbatches of the
+ *     same shape in a row (same H, B, fanouts and store, and the same scratch
+ *     buffers) captures the sampling kernels as a HIP graph and from then on
+ *     replays it with one graph launch per hyperbatch; a batch holds one such
+ *     graph and captures again when the shape changes.  2 (default) = as 1
+ *     for shapes whose hops can sample at most 2^20 edges in all (H x frontier
+ *     capacity x fanout, summed over the hops), as 0 for larger ones.  Replay
+ *     shortens small, launch-bound hyperbatches but slows large hyperbatches
  *     that sample concurrently on several streams.
  *   AGNES_OPT_JOIN_PATH: how each hop unites the sampled neighbours with the
  *     nodes already held and relabels them.  0 (default): a device-wide radix

@@ -18,13 +18,23 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# AGNES_SANITIZE (e.g. "address,undefined") selects a separate build with
+# LLVM's sanitizers, loaded only under their preloaded runtime
+# (tests/sanitized_cpu_suite.py)
+_SAN = os.environ.get("AGNES_SANITIZE", "")
+_LIB = os.path.join(_HERE, "liboracle.san.so" if _SAN else "liboracle.so")
 
 
 def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC])
+        if _SAN:
+            clang = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "llvm", "bin", "clang")
+            cmd = [clang, "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=" + _SAN,
+                   "-fno-sanitize-recover=all", "-std=gnu11", "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC]
+        else:
+            cmd = ["gcc", "-O2", "-std=gnu11", "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC]
+        subprocess.check_call(cmd)
         os.replace(tmp, _LIB)
     return _LIB
 

@@ -144,16 +144,19 @@ class Store:
     def set_profiling(self, on: bool) -> None:
         agnes_store_set_option(self.handle, B.AGNES_OPT_PROFILE, 1 if on else 0)
 
-    def set_sampling_graph(self, on: bool) -> None:
-        """Replay the sampling kernels of a repeated hyperbatch shape from a
-        captured HIP graph, or launch them one by one (the default)."""
-        agnes_store_set_option(self.handle, B.AGNES_OPT_SAMPLING_GRAPH, 1 if on else 0)
+    def set_sampling_graph(self, mode) -> None:
+        """True: replay the sampling kernels of a repeated hyperbatch shape
+        from a captured HIP graph; False: launch them one by one; "auto" (the
+        default): replay for shapes of at most 2^20 sampled edges."""
+        v = 2 if mode == "auto" else (1 if mode else 0)
+        agnes_store_set_option(self.handle, B.AGNES_OPT_SAMPLING_GRAPH, v)
 
     def set_join_path(self, buckets: bool = True, bucket_cap: int | None = None) -> None:
-        """Node-range buckets joined in workgroup memory (the default) or the
-        device-wide radix sort and merge-path join; bucket_cap: entries of one
-        sorted bucket before the hyperbatch is sampled again with the radix
-        sort (never changes results)."""
+        """buckets=True: node-range buckets joined in workgroup memory;
+        False: the device-wide radix sort and merge-path join (the store's
+        default).  bucket_cap: entries of one sorted bucket before the
+        hyperbatch is sampled again with the radix sort (never changes
+        results)."""
         agnes_store_set_option(self.handle, B.AGNES_OPT_JOIN_PATH, 1 if buckets else 0)
         if bucket_cap is not None:
             agnes_store_set_option(self.handle, B.AGNES_OPT_BUCKET_CAP, int(bucket_cap))

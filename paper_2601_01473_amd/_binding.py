@@ -10,7 +10,7 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libagnes.so")
+LIB_PATH = os.path.join(_HERE, "libagnes.san.so" if os.environ.get("AGNES_SANITIZE") else "libagnes.so")
 
 AGNES_OK, AGNES_ERR_INVALID, AGNES_ERR_NOMEM, AGNES_ERR_DEVICE, AGNES_ERR_RANGE, AGNES_ERR_INTERNAL = range(6)
 STATUS_NAMES = {0: "OK", 1: "INVALID", 2: "NOMEM", 3: "DEVICE", 4: "RANGE", 5: "INTERNAL"}

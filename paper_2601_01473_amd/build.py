@@ -13,7 +13,13 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
-LIB = os.path.join(HERE, "libagnes.so")
+# AGNES_SANITIZE (e.g. "address,undefined"): the host code is built with
+# LLVM's sanitizers (device code unchanged) into a separate library, which
+# loads only under the sanitizer runtime (tests/sanitized_cpu_suite.py).
+SANITIZE = os.environ.get("AGNES_SANITIZE", "")
+LIB = os.path.join(HERE, "libagnes.san.so" if SANITIZE else "libagnes.so")
+if SANITIZE:
+    BUILD = os.path.join(HERE, "_build_san")
 SOURCES = ["prims.hip", "store.hip", "pipeline.hip", "bucket.hip", "sage.hip", "api.hip"]
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.environ.get("HIPCC", os.path.join(ROCM, "bin", "hipcc"))
@@ -23,9 +29,20 @@ FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
+def _host_sanitizer_flags() -> list:
+    """Each sanitizer flag for the host pass only; vptr and function checks
+    are left out (they need the C++ parts of the runtime, which a preloaded
+    runtime does not bring)."""
+    flags = ["-g", "-fno-omit-frame-pointer"]
+    for f in ("-fsanitize=" + SANITIZE, "-fno-sanitize=vptr,function", "-fno-sanitize-recover=all"):
+        flags += ["-Xarch_host", f]
+    return flags
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *(_host_sanitizer_flags() if SANITIZE else []), "-c", os.path.join(CSRC, src),
+           "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, r.stdout, r.stderr))

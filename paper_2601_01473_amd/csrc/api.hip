@@ -319,7 +319,8 @@ agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_
             AGNES_REQUIRE(value >= 1 && value <= 64, AGNES_ERR_INVALID, "gather chunks must be in [1, 64]");
             s->gather_chunks = (int)value;
         } else if (opt == AGNES_OPT_SAMPLING_GRAPH) {
-            s->sampling_graph = value ? 1 : 0;
+            AGNES_REQUIRE(value >= 0 && value <= 2, AGNES_ERR_INVALID, "sampling graph must be 0, 1 or 2");
+            s->sampling_graph = (int)value;
         } else if (opt == AGNES_OPT_JOIN_PATH) {
             AGNES_REQUIRE(value == 0 || value == 1, AGNES_ERR_INVALID, "join path must be 0 or 1");
             s->join_path = (int)value;

@@ -1524,6 +1524,20 @@ static std::vector<uint64_t> chain_key(const Store& s, const Batch& b, const Geo
     return k;
 }
 
+// Graph replay pays where the launches, not the work, set a hyperbatch's
+// time: on the automatic setting, for hyperbatches whose hops can sample at
+// most kGraphAutoEdges edges in all (H cap_l f_l summed over the hops).  On
+// larger ones the kernels launched one by one overlap better with those of
+// hyperbatches sampling on other streams.
+constexpr int64_t kGraphAutoEdges = (int64_t)1 << 20;
+
+static bool replay_chain(const Store& s, const Geometry& g, const int32_t* fanouts) {
+    if (s.sampling_graph != 2) return s.sampling_graph == 1;
+    int64_t edges = 0;
+    for (int l = 0; l < g.L; l++) edges += (int64_t)g.H * g.cap[l] * fanouts[l];
+    return edges <= kGraphAutoEdges;
+}
+
 // Captures launch_chain as a HIP graph on the batch's private stream (nothing
 // runs during a capture) and keeps its executable instance.
 static void capture_chain(const Store& s, Batch& b, const Geometry& g, const SyncLayout& y,
@@ -1600,12 +1614,13 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, bool tar
     AGNES_LAUNCH(k_params, dim3(1), dim3(kBlock), 0, st, w.params.as<ChainParams>(), targets, seed, mb_base,
                        w.sync.as<Ctl>(), (int64_t)H * B);
     AGNES_CHECK_HIP(hipGetLastError());
-    // With the graph option, a shape seen twice in a row is captured once and
-    // then replayed: one graph launch instead of about 25 launches per hop.
+    // With graph replay, a shape seen twice in a row is captured once and
+    // then replayed: one graph launch instead of about 20 launches per hop.
     std::vector<uint64_t> key = chain_key(s, b, g, fanouts);
-    if (s.sampling_graph && !(b.chain && key == b.chain_key) && key == b.last_key)
+    const bool replay = replay_chain(s, g, fanouts);
+    if (replay && !(b.chain && key == b.chain_key) && key == b.last_key)
         capture_chain(s, b, g, y, fanouts, key);
-    if (s.sampling_graph && b.chain && key == b.chain_key) AGNES_CHECK_HIP(hipGraphLaunch(b.chain, st));
+    if (replay && b.chain && key == b.chain_key) AGNES_CHECK_HIP(hipGraphLaunch(b.chain, st));
     else launch_chain(s, b, g, y, fanouts, s.join_path == 0, st);
     // what finish needs to sample the hyperbatch again on the radix-sort path
     b.fanouts.assign(fanouts, fanouts + L);

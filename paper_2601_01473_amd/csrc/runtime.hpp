@@ -260,7 +260,8 @@ struct Store {
         if (pool_free) (void)hipEventDestroy(pool_free);
     }
     int profile = 0;
-    int sampling_graph = 0;           // 1 = replay the sampling kernels from a captured HIP graph
+    int sampling_graph = 2;           // 1 = replay the sampling kernels from a captured HIP graph, 0 = never,
+                                      // 2 = for hyperbatches of at most kGraphAutoEdges sampled edges
     int gather_groups = 1 << 22;      // workgroups of the row-copy kernel (upper bound)
     int gather_unroll = 0;            // rows in flight per lane group (4, 8 or 16; 0 = by row width)
     int gather_nt = 1;                // 1 = non-temporal stores of the gathered rows

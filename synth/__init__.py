@@ -24,7 +24,10 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "synth.c")
-_LIB = os.path.join(_HERE, "libsynth.so")
+# AGNES_SANITIZE (e.g. "address,undefined"): a separate build with LLVM's
+# sanitizers, loaded only under their preloaded runtime
+_SAN = os.environ.get("AGNES_SANITIZE", "")
+_LIB = os.path.join(_HERE, "libsynth.san.so" if _SAN else "libsynth.so")
 
 FEATURE_DTYPES = {"float32": (0, 4), "float16": (1, 2), "bfloat16": (2, 2)}
 
@@ -33,8 +36,12 @@ def build(force: bool = True) -> str:
     """Compile libsynth.so with gcc (OpenMP)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O3", "-std=c11", "-fopenmp", "-fPIC", "-shared",
-                               "-o", tmp, _SRC, "-lm"])
+        if _SAN:
+            clang = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "llvm", "bin", "clang")
+            cc = [clang, "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=" + _SAN, "-fno-sanitize-recover=all"]
+        else:
+            cc = ["gcc", "-O3"]
+        subprocess.check_call([*cc, "-std=c11", "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
