@@ -572,6 +572,8 @@ def main():
                     help="with --cache-rows: access count at which a row enters the cache")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time a plain 4 GiB device-to-device copy (reference for the HBM counters)")
+    ap.add_argument("--hbm-ceiling", action="store_true",
+                    help="run the HBM ceiling probe (plain streaming read, write and copy kernels) and exit")
     ap.add_argument("--gather-calibration", action="store_true",
                     help="run the row-copy kernel over 2^21 all-distinct rows (reference for its HBM counters)")
     args = ap.parse_args()
@@ -583,6 +585,13 @@ def main():
 
     root = os.path.dirname(os.path.abspath(__file__))
     sys.path.insert(0, root)
+    if args.hbm_ceiling:
+        # a child process, started before this one touches the GPU
+        import subprocess
+        probe = os.path.join(root, "paper_2601_01473_amd", "hbm_ceiling")
+        if not os.path.exists(probe):
+            sys.exit("the HBM ceiling probe is not built (python -c 'import __graft_entry__ as g; g.build()')")
+        sys.exit(subprocess.call([probe]))
     import torch
     if args.copy_calibration:
         copy_calibration(torch)

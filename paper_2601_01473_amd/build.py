@@ -49,8 +49,25 @@ def _compile(src: str) -> str:
     return obj
 
 
+PROBE = os.path.join(HERE, "hbm_ceiling")
+PROBE_SRC = "hbm_ceiling.hip"
+
+
+def build_probe() -> str:
+    """The HBM ceiling probe (a standalone program that bench.py --hbm-ceiling
+    runs), next to the library."""
+    tmp = PROBE + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, *FLAGS, os.path.join(CSRC, PROBE_SRC), "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (PROBE_SRC, r.stdout, r.stderr))
+    os.replace(tmp, PROBE)
+    return PROBE
+
+
 def build(verbose: bool = False) -> str:
-    """Compile all sources and link libagnes.so; returns its path."""
+    """Compile all sources and link libagnes.so (and the HBM ceiling probe);
+    returns the library's path."""
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(_compile, SOURCES))
@@ -61,6 +78,8 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s\n%s" % (r.stdout, r.stderr))
     os.replace(tmp, LIB)
+    if not SANITIZE:
+        build_probe()
     if verbose:
         print("built", LIB)
     return LIB
