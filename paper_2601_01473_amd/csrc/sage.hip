@@ -372,6 +372,7 @@ static void enqueue_forward(const Batch& b, const agnes_sage_model& m, const For
 }
 
 void sage_forward(Batch& b, const agnes_sage_model& m, float* out, hipStream_t st) {
+    Range range("agnes_sage_forward");
     check_forward(b, m, out);
     const int H = b.H, L = b.L;
     const ForwardSizes z = forward_sizes(b, m);
@@ -481,6 +482,7 @@ __global__ __launch_bounds__(kBlock) void k_sage_offsets(const int32_t* lsz, con
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 void sage_forward_noalloc(Batch& b, const agnes_sage_model& m, float* out, hipStream_t st) {
+    Range range("agnes_sage_forward_noalloc");
     check_forward(b, m, out);
     const int H = b.H, L = b.L;
     const ForwardSizes z = forward_sizes(b, m);

@@ -57,6 +57,7 @@ static int64_t validate_offsets(const OffT* off, int64_t n, int64_t e) {
 
 Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t block_bytes,
                    int64_t pool_blocks, int64_t cache_rows, int64_t cache_threshold, hipStream_t st) {
+    Range range("agnes_build_blocks");
     AGNES_REQUIRE(pool_blocks >= 0, AGNES_ERR_INVALID, "pool_blocks must not be negative");
     AGNES_REQUIRE(cache_rows >= 0, AGNES_ERR_INVALID, "cache_rows must not be negative");
     AGNES_REQUIRE(cache_threshold >= 1, AGNES_ERR_INVALID, "the cache threshold must be >= 1");
