@@ -51,9 +51,10 @@ def gather_fingerprint(root: str) -> str:
     return hashlib.sha256((src[a:b] + "\n".join(shape)).encode()).hexdigest()
 
 
-def measured_traffic(root: str):
+def measured_traffic(root: str, workload: str):
     """(GB per launch, algorithmic GB per launch) of the row-copy kernel from the
-    committed counter summary, or None when the kernel changed since."""
+    committed counter summary, or None when the kernel changed since or the
+    summary was taken on another workload."""
     path = os.path.join(root, GATHER_TRAFFIC_FILE)
     if not os.path.exists(path):
         return None
@@ -63,7 +64,7 @@ def measured_traffic(root: str):
             k, v = ln[2:].split(": ", 1)
             vals[k.strip()] = v.strip().strip("`")
     fp = gather_fingerprint(root)
-    if not fp or vals.get("kernel_fingerprint") != fp:
+    if not fp or vals.get("kernel_fingerprint") != fp or vals.get("workload") != workload:
         return None
     return float(vals["traffic_GB_per_launch"]), float(vals["algorithmic_GB_per_launch"])
 
@@ -94,6 +95,14 @@ def sampling_replayed(mode: int, H: int, B: int, fanouts, num_nodes: int) -> boo
         edges += H * cap * f
         cap = min(cap * (1 + f), max(num_nodes, B))
     return edges <= (1 << 20)
+
+
+def copy_kernel_name(row_bytes: int) -> str:
+    """The library's row copy: one wave per row for rows of 1 KiB and more
+    (whole 16-byte units), lane groups per row below."""
+    if row_bytes % 16 == 0 and row_bytes >= 1024:
+        return "k_gather_rows (row copy)"
+    return "k_gather (row copy, rows under 1 KiB)"
 
 
 def block_model_bytes(st: dict, block_bytes: int) -> int:
@@ -717,7 +726,7 @@ def main():
     torch.cuda.synchronize()
     serial_ms = (time.perf_counter() - t1) / nser * 1e3
 
-    traffic = measured_traffic(root)
+    traffic = measured_traffic(root, f"{cfg.describe()}|H={H}")
     tot_bytes, tot_sample, tot_gather = acc["bytes"], acc["sample"], acc["gather"]
     tot_copy_bytes, edges, rows = acc["copy_bytes"], acc["edges"], acc["rows"]
     sample_ms, gather_ms, copy_ms = acc["sample_ms"], acc["gather_ms"], acc["copy_ms"]
@@ -762,7 +771,7 @@ def main():
                      "gather_bytes": tot_gather // K, "rows": rows // K,
                      "distinct_rows": acc["distinct"] // K, "sampled_edges": edges // K,
                      "block_model_bytes": acc["block_model"] // K},
-        "roofline": {"kernel": "k_gather_rows (row copy)", "bound": "hbm", "achieved": round(achieved, 1),
+        "roofline": {"kernel": copy_kernel_name(cfg.row_bytes), "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic[0] if traffic else None,
                      "traffic_unit": "GB per launch, HBM (FETCH_SIZE x2.0 + WRITE_SIZE x1.0, copy-calibrated)",

@@ -7,8 +7,10 @@
 // objects are laid out in ascending node order and a long list continues into
 // the following blocks.  Feature block c holds rows [c * rpb, (c + 1) * rpb),
 // rpb = floor(block_bytes / row_bytes).  Both arrays are padded to whole blocks.
+#include <cstdlib>
 #include <cstring>
 #include <memory>
+#include <vector>
 
 #include "bucket.hpp"
 #include "device.hpp"
@@ -94,7 +96,14 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
     AGNES_CHECK_HIP(hipDeviceGetAttribute(&s->max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, s->device));
     s->num_nodes = n;
     s->num_edges = e;
-    s->offsets64 = o64 ? 1 : 0;
+    // int64 offsets of a graph with fewer than 2^31 edges are kept on the
+    // device as int32: the same values in half the bytes, so more of them
+    // share a cache line in the samplers' random reads.  AGNES_WIDE_OFFSETS=1
+    // keeps them as given (so that the int64 kernels can be tested on small
+    // graphs).
+    const char* wide = std::getenv("AGNES_WIDE_OFFSETS");
+    const bool narrow = o64 && e < 0x7FFFFFFFll && !(wide && wide[0] == '1');
+    s->offsets64 = (o64 && !narrow) ? 1 : 0;
     s->block_bytes = (int64_t)block_bytes;
     s->e_blk = (int64_t)block_bytes / 4;
     s->e_blk_log2 = 0;
@@ -108,7 +117,7 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
     s->node_bits = 1;
     while (((int64_t)1 << s->node_bits) < n) s->node_bits++;
 
-    const size_t obytes = (size_t)(n + 1) * (o64 ? 8 : 4);
+    const size_t obytes = (size_t)(n + 1) * (s->offsets64 ? 8 : 4);
     const size_t ibytes = (size_t)(s->nblk * s->e_blk) * 4;
     const size_t fbytes = (size_t)(s->nfblk * s->rpb) * (size_t)row_bytes;
     const size_t fdata = (size_t)n * (size_t)row_bytes;
@@ -116,7 +125,16 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
     s->indices.reserve(ibytes);
     s->first_node.reserve((size_t)s->nblk * 4);
     s->last_node.reserve((size_t)s->nblk * 4);
-    AGNES_CHECK_HIP(hipMemcpyAsync(s->offsets.ptr, csr->offsets, obytes, hipMemcpyHostToDevice, st));
+    if (narrow) {
+        // a synchronous copy from pageable memory: o32 outlives it
+        const int64_t* src = (const int64_t*)csr->offsets;
+        std::vector<int32_t> o32((size_t)n + 1);
+        for (int64_t i = 0; i <= n; i++) o32[i] = (int32_t)src[i];
+        AGNES_CHECK_HIP(hipStreamSynchronize(st));
+        AGNES_CHECK_HIP(hipMemcpy(s->offsets.ptr, o32.data(), obytes, hipMemcpyHostToDevice));
+    } else {
+        AGNES_CHECK_HIP(hipMemcpyAsync(s->offsets.ptr, csr->offsets, obytes, hipMemcpyHostToDevice, st));
+    }
     if (e > 0)
         AGNES_CHECK_HIP(hipMemcpyAsync(s->indices.ptr, csr->indices, (size_t)e * 4, hipMemcpyHostToDevice, st));
     if (ibytes > (size_t)e * 4)
@@ -157,7 +175,7 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
     }
     fill_u32(s->first_node.ptr, 0xFFFFFFFFu, s->nblk, st);
     fill_u32(s->last_node.ptr, 0xFFFFFFFFu, s->nblk, st);
-    if (o64)
+    if (s->offsets64)
         AGNES_LAUNCH(k_object_table<int64_t>, dim3(grid_for(n, 4096)), dim3(kBlock), 0, st,
                            s->offsets.as<int64_t>(), n, s->e_blk_log2, s->nblk,
                            s->first_node.as<int32_t>(), s->last_node.as<int32_t>());

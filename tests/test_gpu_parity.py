@@ -95,6 +95,20 @@ def test_random_graphs_int64(agnes, seed):
              tag=("rand64", seed))
 
 
+@pytest.mark.parametrize("seed", range(2))
+def test_random_graphs_int64_kept_wide_on_device(agnes, seed, monkeypatch):
+    """int64 offsets of a graph below 2^31 edges are narrowed to int32 on the
+    device; AGNES_WIDE_OFFSETS=1 keeps them 64-bit, so the int64 sampling
+    kernels run here too, with the same results."""
+    monkeypatch.setenv("AGNES_WIDE_OFFSETS", "1")
+    off, idx = random_graph(3000, 14, seed + 20, hubs=4, hub_deg=900)
+    tg = distinct_targets(3000, 5, 37, seed + 30)
+    feat = features(3000, 20, seed)
+    log("random int64 kept wide", seed)
+    run_case(agnes, off, idx, feat, tg, [7, 3, 2], seed=seed, mb_base=3 * seed, block_bytes=256,
+             tag=("wide64", seed))
+
+
 def test_random_graph_int32_offsets_fp16(agnes):
     off, idx = random_graph(2000, 9, 7, hubs=3, hub_deg=700)
     tg = distinct_targets(2000, 3, 64, 1)
