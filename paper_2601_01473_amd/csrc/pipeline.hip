@@ -377,24 +377,67 @@ __device__ __forceinline__ JoinSpan join_span(int64_t t, int64_t n, const int64_
     return s;
 }
 
-// The tile in LDS: sk[0, nA) = A keys, sk[nA, nA + nB) = edge keys; sv = A local
-// ids, then edge numbers.  pre = {key of the edge before the tile, key of the A
-// entry before the tile} (kNoKey if none), pre_val = that A entry's local id.
-__device__ __forceinline__ void join_stage(const JoinSpan& s, const uint64_t* ak, const int32_t* av,
-                                           const uint32_t* su, const uint32_t* se, const int64_t* mb_e, int H,
-                                           uint64_t* sk, int32_t* sv, uint64_t* pre, int32_t* pre_val) {
-    for (int i = threadIdx.x; i < s.nA; i += kBlock) {
-        sk[i] = ak[s.a0 + i];
-        sv[i] = av[s.a0 + i];
-    }
-    for (int i = threadIdx.x; i < s.nB; i += kBlock) {
-        sk[s.nA + i] = edge_key(su, se, mb_e, H, s.b0 + i);
-        sv[s.nA + i] = (int32_t)se[s.b0 + i];
+// A tile's entries, one thread's share in registers: merged slot
+// m = tid + k kBlock (k < kJoinSlots) is A[a0 + m] for m < nA (key, local id)
+// and edge b0 + m - nA for nA <= m < nA + nB (node, edge number).  Thread 0
+// also holds the entries just before the tile.  The loads for tile t + 1 are
+// issued before tile t is processed, so their latency hides behind that work
+// (a workgroup barrier waits for LDS operations only).
+constexpr int kJoinSlots = kJoinTile / kBlock;
+static_assert(kJoinTile % kBlock == 0, "whole slots per thread");
+
+struct JoinRegs {
+    uint64_t k[kJoinSlots];
+    int32_t v[kJoinSlots];
+    uint64_t pk;         // thread 0: A[a0 - 1] (kNoKey if none)
+    int32_t pv;          // its local id
+    uint32_t pu, pe;     // thread 0: node and edge number of edge b0 - 1 (if b0 > 0)
+};
+
+__device__ __forceinline__ void join_load(const JoinSpan& s, const uint64_t* ak, const int32_t* av,
+                                          const uint32_t* su, const uint32_t* se, JoinRegs& r) {
+#pragma unroll
+    for (int k = 0; k < kJoinSlots; k++) {
+        const int m = threadIdx.x + k * kBlock;
+        if (m < s.nA) {
+            r.k[k] = ak[s.a0 + m];
+            r.v[k] = av[s.a0 + m];
+        } else if (m < s.nA + s.nB) {
+            const int64_t p = s.b0 + (m - s.nA);
+            r.k[k] = su[p];
+            r.v[k] = (int32_t)se[p];
+        }
     }
     if (threadIdx.x == 0) {
-        pre[0] = s.b0 > 0 ? edge_key(su, se, mb_e, H, s.b0 - 1) : kNoKey;
-        pre[1] = s.a0 > 0 ? ak[s.a0 - 1] : kNoKey;
-        *pre_val = s.a0 > 0 ? av[s.a0 - 1] : 0;
+        r.pk = s.a0 > 0 ? ak[s.a0 - 1] : kNoKey;
+        r.pv = s.a0 > 0 ? av[s.a0 - 1] : 0;
+        r.pu = s.b0 > 0 ? su[s.b0 - 1] : 0u;
+        r.pe = s.b0 > 0 ? se[s.b0 - 1] : 0u;
+    }
+}
+
+// The tile in LDS: sk[0, nA) = A keys, sk[nA, nA + nB) = edge keys (node,
+// minibatch); sv = A local ids, then edge numbers.  pre = {key of the edge
+// before the tile, key of the A entry before the tile} (kNoKey if none),
+// pre_val = that A entry's local id.
+__device__ __forceinline__ void join_store(const JoinSpan& s, const JoinRegs& r, const int64_t* mb_e, int H,
+                                           uint64_t* sk, int32_t* sv, uint64_t* pre, int32_t* pre_val) {
+#pragma unroll
+    for (int k = 0; k < kJoinSlots; k++) {
+        const int m = threadIdx.x + k * kBlock;
+        if (m < s.nA) {
+            sk[m] = r.k[k];
+            sv[m] = r.v[k];
+        } else if (m < s.nA + s.nB) {
+            const uint32_t e = (uint32_t)r.v[k];
+            sk[m] = (r.k[k] << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)e);
+            sv[m] = r.v[k];
+        }
+    }
+    if (threadIdx.x == 0) {
+        pre[0] = s.b0 > 0 ? (((uint64_t)r.pu << 32) | (uint32_t)upper_segment(mb_e, H, (int64_t)r.pe)) : kNoKey;
+        pre[1] = r.pk;
+        *pre_val = r.pv;
     }
 }
 
@@ -490,9 +533,12 @@ __global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req
     __syncthreads();
     int64_t a_total = 0;
     uint32_t nh = 0;
+    JoinRegs regs;
+    if (t0 < t1) join_load(join_span(t0, n, ssplit), ak, av, su, se, regs);
     for (int64_t t = t0; t < t1; t++) {
         const JoinSpan s = join_span(t, n, ssplit + (t - t0));
-        join_stage(s, ak, av, su, se, mb_e, H, sk, sv, pre, &pre_val);
+        join_store(s, regs, mb_e, H, sk, sv, pre, &pre_val);
+        if (t + 1 < t1) join_load(join_span(t + 1, n, ssplit + (t + 1 - t0)), ak, av, su, se, regs);
         a_total += s.nA;
         __syncthreads();
         for (int i = tid; i < s.nB; i += kBlock) {
@@ -545,7 +591,8 @@ __global__ __launch_bounds__(kBlock) void k_join_scan(int H, int G, int64_t* ghi
 // nodes (the per-minibatch lists that the next hop's requests read) is
 // written only when another hop follows (write_nodes); the gather writes the
 // final lists itself.
-// Dynamic LDS: mb_e[H+1], sk[T], sv[T], loc[T], nhx[T+1], cursor[H], wcnt[4][H] (16-bit).
+// Dynamic LDS: mb_e[H+1], sk[T], sv[T], loc[T], nhx[T+1], cursor[H], wcnt[4][H] (16-bit),
+// ssplit[per] (the group's tile boundaries).
 __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t capN, int64_t rows_cap,
                                                        int write_nodes,
                                                        const int64_t* req_off, const int64_t* e_off,
@@ -562,6 +609,7 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
     int32_t* nhx = loc + kJoinTile;
     int32_t* cursor = nhx + kJoinTile + 1;
     uint16_t* wcnt = (uint16_t*)(cursor + H);
+    int64_t* ssplit = (int64_t*)(((uintptr_t)(wcnt + kWavesPerBlock * H) + 7) & ~(uintptr_t)7);
     __shared__ uint64_t pre[2];
     __shared__ int32_t pre_val, cont_local;
     __shared__ int32_t wnh[kWavesPerBlock], wanc[kWavesPerBlock];
@@ -570,15 +618,19 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
         cursor[j] = size[j] + (int32_t)ghist[(int64_t)j * G + g];
         for (int x = 0; x < kWavesPerBlock; x++) wcnt[x * H + j] = 0;
     }
-    load_mb_edges(mb_e, req_off, e_off, H);
     const int64_t n = ctl->R + ctl->S;
     int64_t t0, t1;
     group_tiles(n, g, G, t0, t1);
+    for (int64_t t = t0 + tid; t <= t1; t += kBlock) ssplit[t - t0] = split[t];
+    load_mb_edges(mb_e, req_off, e_off, H);  // ends with a barrier
     int64_t run = gemit[g];                  // merged entries before the tile
     const uint64_t lane_le = lanemask_lt() | (1ull << lane);
+    JoinRegs regs;
+    if (t0 < t1) join_load(join_span(t0, n, ssplit), ak, av, su, se, regs);
     for (int64_t t = t0; t < t1; t++) {
-        const JoinSpan s = join_span(t, n, split + t);
-        join_stage(s, ak, av, su, se, mb_e, H, sk, sv, pre, &pre_val);
+        const JoinSpan s = join_span(t, n, ssplit + (t - t0));
+        join_store(s, regs, mb_e, H, sk, sv, pre, &pre_val);
+        if (t + 1 < t1) join_load(join_span(t + 1, n, ssplit + (t + 1 - t0)), ak, av, su, se, regs);
         __syncthreads();
         if (tid == 0) {
             // edges at the start of the tile that continue a run begun before it
@@ -700,21 +752,34 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
 // Tiles of the join at any hop: the list and the edges together fit the maxima.
 static int64_t join_tiles_max(const Geometry& g) { return (g.Rmax + g.Smax) / kJoinTile + 1; }
 
+// A group of the join passes keeps the merge-path boundaries of its tiles in
+// LDS, so it takes at most this many tiles.
+constexpr int64_t kJoinGroupTilesMax = 2048;
+
+// Fewest groups that keep every group within kJoinGroupTilesMax tiles.
+static int64_t join_groups_min(int64_t tiles) {
+    const int64_t G = (tiles + kJoinGroupTilesMax - 1) / kJoinGroupTilesMax;
+    return (G + kBlock - 1) / kBlock * kBlock;
+}
+
 // Workgroups of the join passes: one tile each up to 4096 groups, while the
-// per-minibatch count table (H x G) stays near 4M entries.
+// per-minibatch count table (H x G) stays near 4M entries; never fewer than
+// join_groups_min.  A multiple of kBlock.
 static int join_groups(int H, int64_t tiles) {
     int64_t G = std::min<int64_t>(4096, std::max<int64_t>(256, (int64_t)(4 << 20) / H));
     G = std::min<int64_t>(G, std::max<int64_t>(256, tiles));
-    return (int)((G + kBlock - 1) / kBlock * kBlock);
+    G = (G + kBlock - 1) / kBlock * kBlock;
+    return (int)std::max<int64_t>(G, join_groups_min(tiles));
 }
 
-// per: the most tile boundaries of one group (its tiles + 1)
+// per: the most tile boundaries of one group (its tiles + 1), at most
+// kJoinGroupTilesMax + 2
 static size_t join_count_lds(int H, int64_t per) {
     return (size_t)(H + 1) * 16 + (size_t)kJoinTile * 12 + (size_t)H * 4 + 8 + (size_t)per * 8;
 }
-static size_t join_write_lds(int H) {
+static size_t join_write_lds(int H, int64_t per) {
     return (size_t)(H + 1) * 8 + (size_t)kJoinTile * 8 + (size_t)kJoinTile * 4 * 3 + 4 + (size_t)H * 4 +
-           (size_t)kWavesPerBlock * H * 2;
+           (size_t)kWavesPerBlock * H * 2 + 8 + (size_t)per * 8;
 }
 
 // Statistics of the final list (the feature bucket): distinct rows (runs of one
@@ -1319,14 +1384,16 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     // join with the list: the next list, new node ids and the hop's columns
     const int64_t tiles_l = ((int64_t)g.H * g.cap[l] * (1 + (int64_t)f)) / kJoinTile + 1;
     int64_t* split = w.split.as<int64_t>();
-    const int G = std::min(join_groups(g.H, tiles_l), std::max(kBlock, s.sample_groups / kBlock * kBlock));
+    const int G = (int)std::max<int64_t>(
+        std::min(join_groups(g.H, tiles_l), std::max(kBlock, s.sample_groups / kBlock * kBlock)),
+        join_groups_min(tiles_l));
     const int64_t per = (tiles_l + G - 1) / G + 2;
     AGNES_LAUNCH(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H, per), st, g.H,
                        w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se, split, G,
                        w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), b.row_ptr[l].as<int32_t>(), ctl);
     AGNES_LAUNCH(k_join_scan, dim3(g.H + 1), dim3(kBlock), 0, st, g.H, G, w.ghist.as<int64_t>(),
                        w.gemit.as<int64_t>(), w.newcnt.as<int64_t>(), ctl);
-    AGNES_LAUNCH(k_join_write, dim3(G), dim3(kBlock), join_write_lds(g.H), st, g.H, g.jbits,
+    AGNES_LAUNCH(k_join_write, dim3(G), dim3(kBlock), join_write_lds(g.H, per), st, g.H, g.jbits,
                        g.capN, g.rows_max, (int)(l + 1 < g.L), w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se,
                        split, G, w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), w.size.as<int32_t>(),
                        w.nodes.as<int32_t>(), w.rl_key[cur ^ 1].as<uint64_t>(), w.rl_val[cur ^ 1].as<int32_t>(),
@@ -1578,7 +1645,8 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, bool tar
     // a forward still reading the batch's CSR and rows: this hyperbatch's
     // kernels overwrite them, so they queue behind it
     if (b.sage_pending) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.sage_done, 0));
-    AGNES_REQUIRE(join_write_lds(H) <= (size_t)s.max_lds && (size_t)(H + 1) * 16 <= (size_t)s.max_lds,
+    AGNES_REQUIRE(join_write_lds(H, kJoinGroupTilesMax + 2) <= (size_t)s.max_lds &&
+                      join_count_lds(H, kJoinGroupTilesMax + 2) <= (size_t)s.max_lds,
                   AGNES_ERR_RANGE, "H is too large for the device's workgroup memory");
     SyncLayout y = sync_layout(H, L, g.rows_max);
     Workspace& w = b.ws;
