@@ -275,15 +275,31 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, cons
     if (threadIdx.x == 0) opened = 0;
     load_offsets(req_off, req_off_g, H);
     const int64_t R = ctl->R;
-    for (int64_t base = (int64_t)blockIdx.x * kBlock; base < R; base += (int64_t)gridDim.x * kBlock) {
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    // the next request's list entry is loaded while this one is sampled
+    uint64_t next_key = 0;
+    int32_t next_val = 0;
+    {
+        const int64_t p0 = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+        if (p0 < R) {
+            next_key = rl_key[p0];
+            next_val = rl_val[p0];
+        }
+    }
+    for (int64_t base = (int64_t)blockIdx.x * kBlock; base < R; base += stride) {
         int64_t p = base + threadIdx.x;
         bool active = p < R;
         int64_t blk = -1;
+        const uint64_t key = next_key;
+        const int32_t val = next_val;
+        if (p + stride < R) {
+            next_key = rl_key[p + stride];
+            next_val = rl_val[p + stride];
+        }
         if (active) {
-            uint64_t key = rl_key[p];
             int32_t v = (int32_t)(key >> 32);
             int j = (int)(uint32_t)key;
-            int64_t r = rl_val[p];
+            int64_t r = val;
             int64_t q = req_off[j] + r;
             int64_t o0 = (int64_t)off[v];
             int64_t deg = (int64_t)off[v + 1] - o0;

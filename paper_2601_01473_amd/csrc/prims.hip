@@ -191,20 +191,26 @@ __global__ __launch_bounds__(kBlock) void k_rs_hist(const uint32_t* keys, const 
     __shared__ uint32_t h[BINS];
     const int64_t n = *n_dev;
     const int64_t tiles = (n + kBlock * ITEMS - 1) / (kBlock * ITEMS);
-    for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    // a tile's keys are loaded while the previous tile is counted and written
+    uint32_t k[ITEMS];
+    auto load = [&](int64_t tile) {
         const int64_t t0 = tile * (kBlock * ITEMS);
-        __syncthreads();                        // the previous tile's counts are written out
-        for (int d = threadIdx.x; d < BINS; d += kBlock) h[d] = 0;
-        uint32_t k[ITEMS];
 #pragma unroll
         for (int q = 0; q < ITEMS; q++) {
             const int64_t i = t0 + q * kBlock + threadIdx.x;
             k[q] = i < n ? keys[i] : 0u;
         }
+    };
+    if (blockIdx.x < tiles) load(blockIdx.x);
+    for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+        const int64_t t0 = tile * (kBlock * ITEMS);
+        __syncthreads();                        // the previous tile's counts are written out
+        for (int d = threadIdx.x; d < BINS; d += kBlock) h[d] = 0;
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < ITEMS; q++)
             if (t0 + q * kBlock + threadIdx.x < n) atomicAdd(&h[(k[q] >> shift) & (BINS - 1)], 1u);
+        if (tile + gridDim.x < tiles) load(tile + gridDim.x);
         __syncthreads();
         for (int d = threadIdx.x; d < BINS; d += kBlock) hist[tile * BINS + d] = h[d];
     }
@@ -272,6 +278,21 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
     const int64_t per = (tiles + kXcds - 1) / kXcds;
     const int64_t wx = gridDim.x / kXcds;          // workgroups of one XCD
     const int t = threadIdx.x, w = wave_id(), lane = lane_id();
+    // a tile's keys and values are loaded while the previous tile is written
+    uint32_t key[ITEMS], val[ITEMS], rnk[ITEMS];
+    auto load = [&](int64_t tile) {
+        const int64_t t0 = tile * (kBlock * ITEMS);
+#pragma unroll
+        for (int r = 0; r < ITEMS; r++) {
+            int64_t i = t0 + w * (ITEMS * kWave) + r * kWave + lane;
+            key[r] = i < n ? kin[i] : 0u;
+            val[r] = i < n ? (vin ? vin[i] : (uint32_t)i) : 0u;
+        }
+    };
+    {
+        const int64_t first = (int64_t)(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+        if (blockIdx.x / kXcds < per && first < tiles) load(first);
+    }
     for (int64_t local = blockIdx.x / kXcds; local < per; local += wx) {
     const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per + local;
     if (tile >= tiles) break;
@@ -295,13 +316,6 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
         }
     }
     __syncthreads();
-    uint32_t key[ITEMS], val[ITEMS], rnk[ITEMS];
-#pragma unroll
-    for (int r = 0; r < ITEMS; r++) {
-        int64_t i = t0 + w * (ITEMS * kWave) + r * kWave + lane;
-        key[r] = i < n ? kin[i] : 0u;
-        val[r] = i < n ? (vin ? vin[i] : (uint32_t)i) : 0u;
-    }
 #pragma unroll
     for (int r = 0; r < ITEMS; r++) {
         int64_t i = t0 + w * (ITEMS * kWave) + r * kWave + lane;
@@ -355,6 +369,10 @@ __global__ __launch_bounds__(kBlock) void k_rs_scatter(const uint32_t* kin, cons
             sk[pos] = key[r];
             sv[pos] = val[r];
         }
+    }
+    {
+        const int64_t next = (int64_t)(blockIdx.x % kXcds) * per + local + wx;
+        if (local + wx < per && next < tiles) load(next);
     }
     __syncthreads();
     const int cnt = (int)((n - t0) < (kBlock * ITEMS) ? (n - t0) : (kBlock * ITEMS));
