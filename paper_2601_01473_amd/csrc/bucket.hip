@@ -397,7 +397,7 @@ struct BucketArgs {
     const uint64_t* ak;             // old list keys (node << 32 | minibatch), sorted
     const int32_t* av;              // old list local ids
     const int64_t* req_off;         // [H+1] requests before minibatch j
-    const int64_t* e_off;           // edge offset of every request
+    const uint32_t* e_off;          // edge offset of every request
     const int32_t* size;            // nodes of minibatch j before the hop
     int G;                          // row stride of ghist (>= sub-buckets, multiple of kBlock)
     int64_t* ghist;                 // [H][G] new nodes per minibatch and sub-bucket (scanned by k_bkt_scan)
@@ -859,7 +859,7 @@ __global__ __launch_bounds__(kBlock) void k_bkt(BucketArgs a) {
     const BucketLevels lv = pick_levels(a.info, a.nlev, n + na, H, a.ccap, a.G);
     const int nbc = a.info[lv.tc * 2 + 1], offc = a.info[lv.tc * 2];
     const int nbs = a.info[lv.ts * 2 + 1], offs = a.info[lv.ts * 2];
-    for (int i = t; i <= H; i += kBlock) L.mb_e[i] = a.e_off[a.req_off[i]];
+    for (int i = t; i <= H; i += kBlock) L.mb_e[i] = (int64_t)a.e_off[a.req_off[i]];
     if (!WRITE) {
         // row pointers in request order: row r of minibatch j starts at its
         // edge offset minus the minibatch's first edge
@@ -867,8 +867,8 @@ __global__ __launch_bounds__(kBlock) void k_bkt(BucketArgs a) {
         __syncthreads();
         for (int64_t q = (int64_t)blockIdx.x * kBlock + t; q < R; q += (int64_t)gridDim.x * kBlock) {
             const int j = upper_segment(a.req_off, H, q);
-            a.row_ptr[q + j] = (int32_t)(a.e_off[q] - L.mb_e[j]);
-            if (q + 1 == a.req_off[j + 1]) a.row_ptr[q + j + 1] = (int32_t)(a.e_off[q + 1] - L.mb_e[j]);
+            a.row_ptr[q + j] = (int32_t)((int64_t)a.e_off[q] - L.mb_e[j]);
+            if (q + 1 == a.req_off[j + 1]) a.row_ptr[q + j + 1] = (int32_t)((int64_t)a.e_off[q + 1] - L.mb_e[j]);
         }
     }
     for (int j = t; j < H; j += kBlock) L.cnt[j] = 0;

@@ -87,7 +87,8 @@ struct BucketJoinArgs {
     const int64_t* acoff;
     const uint64_t* ak;
     const int32_t* av;
-    const int64_t *req_off, *e_off;
+    const int64_t* req_off;
+    const uint32_t* e_off;
     const int32_t* size;
     int64_t *ghist, *gemit, *newcnt;
     int32_t* row_ptr;

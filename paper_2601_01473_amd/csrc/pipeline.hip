@@ -92,8 +92,8 @@ __device__ __forceinline__ void load_offsets(int64_t* dst, const int64_t* src, i
 }
 
 // Minibatch of edge e given the request offsets: mb_e[j] = e_off[req_off[j]].
-__device__ __forceinline__ void load_mb_edges(int64_t* mb_e, const int64_t* req_off, const int64_t* e_off, int H) {
-    for (int i = threadIdx.x; i <= H; i += kBlock) mb_e[i] = e_off[req_off[i]];
+__device__ __forceinline__ void load_mb_edges(int64_t* mb_e, const int64_t* req_off, const uint32_t* e_off, int H) {
+    for (int i = threadIdx.x; i <= H; i += kBlock) mb_e[i] = (int64_t)e_off[req_off[i]];
     __syncthreads();
 }
 
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(kBlock) void k_list0(const uint32_t* sk, const uint
 // the output row offsets.
 __global__ __launch_bounds__(kBlock) void k_begin(int l, int L, int H, Ctl* ctl, int32_t* size,
                                                   int64_t* newcnt, int32_t* lsz, int64_t* ecount,
-                                                  int64_t* req_off, const int64_t* e_off, int64_t* node_off,
+                                                  int64_t* req_off, const uint32_t* e_off, int64_t* node_off,
                                                   const uint32_t* topo_part, int n_part) {
     __shared__ int64_t lds[kWavesPerBlock];
     if (l > 0) {
@@ -178,7 +178,7 @@ __global__ __launch_bounds__(kBlock) void k_begin(int l, int L, int H, Ctl* ctl,
         (void)block_exclusive_scan(t, lds, tot);
         if (threadIdx.x == 0) ctl->topo_blocks[l - 1] = tot;
         for (int j = threadIdx.x; j < H; j += kBlock) {
-            ecount[(int64_t)j * L + (l - 1)] = e_off[req_off[j + 1]] - e_off[req_off[j]];
+            ecount[(int64_t)j * L + (l - 1)] = (int64_t)e_off[req_off[j + 1]] - (int64_t)e_off[req_off[j]];
             size[j] += (int32_t)newcnt[j];
             newcnt[j] = 0;
         }
@@ -266,7 +266,7 @@ template <typename OffT, int MAXK>
 __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, const ChainParams* prm,
                                                    const OffT* off, const int32_t* adj, int e_blk_log2,
                                                    int64_t nblk, const uint64_t* rl_key, const int32_t* rl_val,
-                                                   const int64_t* req_off_g, const int64_t* e_off,
+                                                   const int64_t* req_off_g, const uint32_t* e_off,
                                                    int32_t* cg, uint32_t* topo_part, const Ctl* ctl) {
     extern __shared__ int64_t req_off[];      // [H+1] request offsets
     __shared__ uint32_t opened;
@@ -306,7 +306,7 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, cons
             blk = o0 >> e_blk_log2;
             if (blk >= nblk) blk = nblk - 1;
             int k = (int)(deg < f ? deg : f);
-            int64_t eo = e_off[q];
+            int64_t eo = (int64_t)e_off[q];
             int32_t* out = cg + eo;
             const int32_t* a = adj + o0;
             if (MAXK > 0) {
@@ -504,7 +504,7 @@ __device__ __forceinline__ void group_tiles(int64_t n, int g, int G, int64_t& t0
 // (gemit[g]).  Also writes the hop's row pointers in request order: row r of
 // minibatch j starts at its edge offset minus the minibatch's first edge.
 // Dynamic LDS: mb_e[H+1], ro[H+1], sk[T], sv[T], count[H], ssplit[per].
-__global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req_off, const int64_t* e_off,
+__global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req_off, const uint32_t* e_off,
                                                        const uint64_t* ak, const int32_t* av, const uint32_t* su,
                                                        const uint32_t* se, int64_t* split, int G,
                                                        int64_t* ghist, int64_t* gemit, int32_t* row_ptr,
@@ -527,8 +527,8 @@ __global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req
     const int64_t R = ctl->R;
     for (int64_t q = (int64_t)g * kBlock + tid; q < R; q += (int64_t)G * kBlock) {
         const int j = upper_segment(ro, H, q);
-        row_ptr[q + j] = (int32_t)(e_off[q] - mb_e[j]);
-        if (q + 1 == ro[j + 1]) row_ptr[q + j + 1] = (int32_t)(e_off[q + 1] - mb_e[j]);
+        row_ptr[q + j] = (int32_t)((int64_t)e_off[q] - mb_e[j]);
+        if (q + 1 == ro[j + 1]) row_ptr[q + j + 1] = (int32_t)((int64_t)e_off[q + 1] - mb_e[j]);
     }
     const int64_t nb = ctl->S, n = R + nb;
     int64_t t0, t1;
@@ -611,7 +611,7 @@ __global__ __launch_bounds__(kBlock) void k_join_scan(int H, int G, int64_t* ghi
 // ssplit[per] (the group's tile boundaries).
 __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t capN, int64_t rows_cap,
                                                        int write_nodes,
-                                                       const int64_t* req_off, const int64_t* e_off,
+                                                       const int64_t* req_off, const uint32_t* e_off,
                                                        const uint64_t* ak, const int32_t* av, const uint32_t* su,
                                                        const uint32_t* se, const int64_t* split, int G,
                                                        const int64_t* ghist, const int64_t* gemit,
@@ -1281,7 +1281,7 @@ static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout&
     w.sync.reserve(y.bytes);
     w.sync_host.reserve(y.bytes);
     w.cnt.reserve((size_t)g.Rmax * 4);
-    w.e_off.reserve((size_t)(g.Rmax + 1) * 8);
+    w.e_off.reserve((size_t)(g.Rmax + 1) * 4);     // edge numbers are below 2^32 (plan)
     for (int i = 0; i < 2; i++) {
         w.rl_key[i].reserve((size_t)g.rows_max * 8);
         w.rl_val[i].reserve((size_t)g.rows_max * 4);
@@ -1323,20 +1323,20 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     const int32_t* rlv = w.rl_val[cur].as<int32_t>();
 
     AGNES_LAUNCH(k_begin, dim3(1), dim3(kBlock), 0, st, l, g.L, g.H, ctl, w.size.as<int32_t>(),
-                       w.newcnt.as<int64_t>(), lsz, ecount, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
+                       w.newcnt.as<int64_t>(), lsz, ecount, w.req_off.as<int64_t>(), w.e_off.as<uint32_t>(),
                        (int64_t*)nullptr, w.topo_part.as<uint32_t>(), gPrev);
     // counts and the edge-offset scan: counts with the reduce pass, then the final pass
     const int64_t r_max = std::max<int64_t>(1, (int64_t)g.H * g.cap[l]);
     const int gS = scan_groups(r_max);
     AGNES_LAUNCH(k_count_reduce<OffT>, dim3(gS), dim3(kBlock), lds_h, st, g.H, g.capN, f, off,
                  w.nodes.as<int32_t>(), w.req_off.as<int64_t>(), w.cnt.as<int32_t>(), gS, part, ctl);
-    scan_counts_final(w.cnt.as<int32_t>(), w.e_off.as<int64_t>(), &ctl->R, r_max, &ctl->S, part, st);
+    scan_counts_final(w.cnt.as<int32_t>(), w.e_off.as<uint32_t>(), &ctl->R, r_max, &ctl->S, part, st);
     const int32_t* adj = s.indices.as<int32_t>();
     int32_t* cg = w.skey.as<int32_t>();
 #define AGNES_SAMPLE(MK)                                                                               \
     AGNES_LAUNCH((k_sample<OffT, MK>), dim3(gR), dim3(kBlock), lds_h, st, l, g.H, f, prm,      \
                        off, adj, s.e_blk_log2, s.nblk, rlk, rlv, w.req_off.as<int64_t>(),      \
-                       w.e_off.as<int64_t>(), cg, w.topo_part.as<uint32_t>(), ctl)
+                       w.e_off.as<uint32_t>(), cg, w.topo_part.as<uint32_t>(), ctl)
     // the register sampler's work grows with MAXK^2 (ranks) and MAXK/4 (Philox
     // calls), so common fanouts get a bound of their own
     if (f <= 4) AGNES_SAMPLE(4);
@@ -1375,7 +1375,7 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
         j.ak = rlk;
         j.av = rlv;
         j.req_off = w.req_off.as<int64_t>();
-        j.e_off = w.e_off.as<int64_t>();
+        j.e_off = w.e_off.as<uint32_t>();
         j.size = w.size.as<int32_t>();
         j.ghist = w.ghist.as<int64_t>();
         j.gemit = w.gemit.as<int64_t>();
@@ -1405,12 +1405,12 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
         join_groups_min(tiles_l));
     const int64_t per = (tiles_l + G - 1) / G + 2;
     AGNES_LAUNCH(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H, per), st, g.H,
-                       w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se, split, G,
+                       w.req_off.as<int64_t>(), w.e_off.as<uint32_t>(), rlk, rlv, su, se, split, G,
                        w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), b.row_ptr[l].as<int32_t>(), ctl);
     AGNES_LAUNCH(k_join_scan, dim3(g.H + 1), dim3(kBlock), 0, st, g.H, G, w.ghist.as<int64_t>(),
                        w.gemit.as<int64_t>(), w.newcnt.as<int64_t>(), ctl);
     AGNES_LAUNCH(k_join_write, dim3(G), dim3(kBlock), join_write_lds(g.H, per), st, g.H, g.jbits,
-                       g.capN, g.rows_max, (int)(l + 1 < g.L), w.req_off.as<int64_t>(), w.e_off.as<int64_t>(), rlk, rlv, su, se,
+                       g.capN, g.rows_max, (int)(l + 1 < g.L), w.req_off.as<int64_t>(), w.e_off.as<uint32_t>(), rlk, rlv, su, se,
                        split, G, w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), w.size.as<int32_t>(),
                        w.nodes.as<int32_t>(), w.rl_key[cur ^ 1].as<uint64_t>(), w.rl_val[cur ^ 1].as<int32_t>(),
                        b.col[l].as<int32_t>(), ctl);
@@ -1579,7 +1579,7 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     }
     // close the last hop: edge counts, final node counts, output row offsets
     AGNES_LAUNCH(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
-                       w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<int64_t>(),
+                       w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<uint32_t>(),
                        w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), hop_grid(s, g, L - 1));
     AGNES_LAUNCH(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
                        (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl);

@@ -78,8 +78,8 @@ __global__ void k_scan_reduce(const T* in, const int64_t* n_dev, int G, int64_t*
 // kScanGroups = 4 * kBlock: four per thread), so no separate launch scans
 // them; block 0 also writes the total after the last element and to
 // total_dev.
-template <typename T>
-__global__ void k_scan_final(const T* in, int64_t* out, const int64_t* n_dev, int G,
+template <typename T, typename OutT>
+__global__ void k_scan_final(const T* in, OutT* out, const int64_t* n_dev, int G,
                              const int64_t* partials, int64_t* total_dev) {
     __shared__ int64_t lds[kWavesPerBlock];
     const int64_t n = *n_dev;
@@ -97,7 +97,7 @@ __global__ void k_scan_final(const T* in, int64_t* out, const int64_t* n_dev, in
     __syncthreads();                                  // lds is reused
     (void)block_exclusive_scan(all, lds, total);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
-        out[n] = total;
+        out[n] = (OutT)total;
         if (total_dev) *total_dev = total;
     }
     for (int64_t base = lo; base < hi; base += kScanTile) {
@@ -115,7 +115,7 @@ __global__ void k_scan_final(const T* in, int64_t* out, const int64_t* n_dev, in
 #pragma unroll
         for (int k = 0; k < kScanItems; k++) {
             int64_t i = base + (int64_t)threadIdx.x * kScanItems + k;
-            if (i < hi) out[i] = ex;
+            if (i < hi) out[i] = (OutT)ex;
             ex += v[k];
         }
         carry += total;
@@ -127,10 +127,11 @@ int scan_groups(int64_t n_max) {
     return (int)(g < 1 ? 1 : (g > kScanGroups ? kScanGroups : g));
 }
 
-void scan_counts_final(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max, int64_t* total_dev,
+void scan_counts_final(const int32_t* in, uint32_t* out, const int64_t* n_dev, int64_t n_max, int64_t* total_dev,
                        const int64_t* partials, hipStream_t st) {
     const int G = scan_groups(n_max);
-    AGNES_LAUNCH(k_scan_final<int32_t>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials, total_dev);
+    AGNES_LAUNCH((k_scan_final<int32_t, uint32_t>), dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials,
+                 total_dev);
 }
 
 template <typename T>
@@ -138,7 +139,7 @@ static void scan_impl(const T* in, int64_t* out, const int64_t* n_dev, int64_t n
                       int64_t* total_dev, int64_t* partials, int64_t* nonzero, hipStream_t st) {
     const int G = scan_groups(n_max);
     AGNES_LAUNCH(k_scan_reduce<T>, dim3(G), dim3(kBlock), 0, st, in, n_dev, G, partials, nonzero);
-    AGNES_LAUNCH(k_scan_final<T>, dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials, total_dev);
+    AGNES_LAUNCH((k_scan_final<T, int64_t>), dim3(G), dim3(kBlock), 0, st, in, out, n_dev, G, partials, total_dev);
     AGNES_CHECK_HIP(hipGetLastError());
 }
 

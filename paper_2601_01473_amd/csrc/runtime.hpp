@@ -376,7 +376,7 @@ int64_t scan_partials_needed();
 // pass alone, for a reduce pass fused into the kernel that produces the counts
 // (it must write partials[g] = the sum of range g, as scan_range splits them).
 int scan_groups(int64_t n_max);
-void scan_counts_final(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max, int64_t* total_dev,
+void scan_counts_final(const int32_t* in, uint32_t* out, const int64_t* n_dev, int64_t n_max, int64_t* total_dev,
                        const int64_t* partials, hipStream_t st);
 
 // Stable LSD radix sort of 32-bit keys with 32-bit values on key bits
