@@ -3,18 +3,29 @@
 // the library).  Four kernels over 4 GiB, 16 bytes per lane, grid-stride
 // loops: read only, write only, copy, and copy with one read written to three
 // places (the 1:3 read:write mix of the row copy at the default workload).
-// Stores are non-temporal, as in the row copy.  Prints one JSON line per
-// kernel: best and mean rate over 10 timed launches.
+// Then row gathers out[dst[i]] = table[src[i]] over 2 GiB of 256-B and 1-KiB
+// rows of an 8 GiB table: random sources with sequential destinations, with
+// random destinations (a permutation), and with random destinations plus a
+// lone 4-B id store per row at its destination index, the access pattern of
+// the row copy, which writes each row where its minibatch needs it.  Stores
+// are non-temporal, as in the row copy.  Prints one JSON line per kernel:
+// best and mean rate over 10 timed launches (row gathers: row bytes read and
+// written only).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
+#include <numeric>
+#include <random>
+#include <vector>
 
 namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 256;
+constexpr int kWave = 64;
 constexpr int kGrid = 8192;
 constexpr int kUnroll = 8;
 constexpr int kReps = 10;
@@ -78,6 +89,37 @@ __global__ __launch_bounds__(kBlock) void k_copy(const u32x4* __restrict__ a, u3
     }
 }
 
+// One row of RU 16-byte units per group of RU lanes, U rows in flight per
+// group; entries [0, n) of src / dst.
+template <int RU, int U, bool IDS>
+__global__ __launch_bounds__(kBlock) void k_rows(const u32x4* __restrict__ table, u32x4* __restrict__ out,
+                                                 const int* __restrict__ src, const int* __restrict__ dst,
+                                                 int* __restrict__ ids, long n) {
+    constexpr int GPW = kWave / RU;                 // row groups per wave
+    const int lane = threadIdx.x % kWave, g = lane / RU, li = lane % RU;
+    const long wave = (long)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+    const long nw = (long)gridDim.x * (kBlock / kWave);
+    for (long r0 = (wave * GPW + g) * U; r0 < n; r0 += nw * GPW * U) {
+        int s[U], d[U];
+        u32x4 x[U];
+#pragma unroll
+        for (int k = 0; k < U; k++) {
+            s[k] = r0 + k < n ? src[r0 + k] : 0;
+            d[k] = r0 + k < n ? dst[r0 + k] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < U; k++)
+            if (r0 + k < n) x[k] = table[(long)s[k] * RU + li];
+#pragma unroll
+        for (int k = 0; k < U; k++) {
+            if (r0 + k < n) {
+                __builtin_nontemporal_store(x[k], out + (long)d[k] * RU + li);
+                if (IDS && li == 0) ids[d[k]] = s[k];
+            }
+        }
+    }
+}
+
 }  // namespace
 
 int main() {
@@ -92,7 +134,7 @@ int main() {
     hipEvent_t e0, e1;
     CHECK(hipEventCreate(&e0));
     CHECK(hipEventCreate(&e1));
-    auto timed = [&](const char* name, double moved, auto launch) {
+    auto timed = [&](const char* name, double moved, int grid, auto launch) {
         launch();
         CHECK(hipGetLastError());
         CHECK(hipDeviceSynchronize());
@@ -109,14 +151,70 @@ int main() {
         }
         std::printf("{\"kernel\": \"%s\", \"bytes\": %.0f, \"best_ms\": %.4f, \"best_GBps\": %.1f, "
                     "\"mean_GBps\": %.1f, \"grid\": %d, \"launches\": %d}\n",
-                    name, moved, best, moved / best / 1e6, moved / (total / kReps) / 1e6, kGrid, kReps);
+                    name, moved, best, moved / best / 1e6, moved / (total / kReps) / 1e6, grid, kReps);
         std::fflush(stdout);
     };
     const double B = (double)bytes;
-    timed("read", B, [&] { hipLaunchKernelGGL(k_read, dim3(kGrid), dim3(kBlock), 0, 0, a, n, sink); });
-    timed("write", B, [&] { hipLaunchKernelGGL(k_write, dim3(kGrid), dim3(kBlock), 0, 0, o, n); });
-    timed("copy", 2 * B, [&] { hipLaunchKernelGGL(k_copy, dim3(kGrid), dim3(kBlock), 0, 0, a, o, n, 1); });
-    timed("copy 1:3", 4 * B, [&] { hipLaunchKernelGGL(k_copy, dim3(kGrid), dim3(kBlock), 0, 0, a, o, n, 3); });
+    timed("read", B, kGrid, [&] { hipLaunchKernelGGL(k_read, dim3(kGrid), dim3(kBlock), 0, 0, a, n, sink); });
+    timed("write", B, kGrid, [&] { hipLaunchKernelGGL(k_write, dim3(kGrid), dim3(kBlock), 0, 0, o, n); });
+    timed("copy", 2 * B, kGrid, [&] { hipLaunchKernelGGL(k_copy, dim3(kGrid), dim3(kBlock), 0, 0, a, o, n, 1); });
+    timed("copy 1:3", 4 * B, kGrid, [&] { hipLaunchKernelGGL(k_copy, dim3(kGrid), dim3(kBlock), 0, 0, a, o, n, 3); });
+    // row gathers: rows of an 8 GiB table of their own, 2 GiB of them written
+    // into the first 2 GiB of o
+    {
+        const size_t tbytes = (size_t)8 << 30, obytes = (size_t)2 << 30;
+        u32x4* table = nullptr;
+        CHECK(hipMalloc(&table, tbytes));
+        CHECK(hipMemset(table, 3, tbytes));
+        u32x4* rows_out = o;                            // 12 GiB buffer: rows use the first 2 GiB
+        int *src = nullptr, *seq = nullptr, *perm = nullptr, *ids = nullptr;
+        const long nmax = (long)(obytes / 256);
+        CHECK(hipMalloc(&src, nmax * sizeof(int)));
+        CHECK(hipMalloc(&seq, nmax * sizeof(int)));
+        CHECK(hipMalloc(&perm, nmax * sizeof(int)));
+        CHECK(hipMalloc(&ids, nmax * sizeof(int)));
+        std::vector<int> h((size_t)nmax);
+        for (int rb : {256, 1024}) {
+            const long n = (long)(obytes / rb), nt = (long)(tbytes / rb);
+            std::mt19937_64 rng(rb);
+            for (long i = 0; i < n; i++) h[i] = (int)(rng() % (unsigned long long)nt);
+            CHECK(hipMemcpy(src, h.data(), n * sizeof(int), hipMemcpyHostToDevice));
+            std::iota(h.begin(), h.begin() + n, 0);
+            CHECK(hipMemcpy(seq, h.data(), n * sizeof(int), hipMemcpyHostToDevice));
+            std::shuffle(h.begin(), h.begin() + n, rng);
+            CHECK(hipMemcpy(perm, h.data(), n * sizeof(int), hipMemcpyHostToDevice));
+            const double moved = 2.0 * (double)obytes;
+            char name[96];
+            auto launch = [&](const int* dst, bool with_ids) {
+                if (rb == 256) {
+                    if (with_ids)
+                        hipLaunchKernelGGL((k_rows<16, 4, true>), dim3(kGrid * 8), dim3(kBlock), 0, 0, table,
+                                           rows_out, src, dst, ids, n);
+                    else
+                        hipLaunchKernelGGL((k_rows<16, 4, false>), dim3(kGrid * 8), dim3(kBlock), 0, 0, table,
+                                           rows_out, src, dst, ids, n);
+                } else {
+                    if (with_ids)
+                        hipLaunchKernelGGL((k_rows<64, 4, true>), dim3(kGrid * 8), dim3(kBlock), 0, 0, table,
+                                           rows_out, src, dst, ids, n);
+                    else
+                        hipLaunchKernelGGL((k_rows<64, 4, false>), dim3(kGrid * 8), dim3(kBlock), 0, 0, table,
+                                           rows_out, src, dst, ids, n);
+                }
+            };
+            std::snprintf(name, sizeof(name), "rows %d B: random sources, sequential destinations", rb);
+            timed(name, moved, kGrid * 8, [&] { launch(seq, false); });
+            std::snprintf(name, sizeof(name), "rows %d B: random sources, random destinations", rb);
+            timed(name, moved, kGrid * 8, [&] { launch(perm, false); });
+            std::snprintf(name, sizeof(name), "rows %d B: random sources and destinations, 4-B id per row", rb);
+            timed(name, moved, kGrid * 8, [&] { launch(perm, true); });
+        }
+        CHECK(hipFree(table));
+        CHECK(hipFree(src));
+        CHECK(hipFree(seq));
+        CHECK(hipFree(perm));
+        CHECK(hipFree(ids));
+    }
     CHECK(hipFree(a));
     CHECK(hipFree(o));
     CHECK(hipFree(sink));
