@@ -7,7 +7,8 @@
 // minibatch.  Objects are stored in ascending node order, so a block's row of
 // Bck is a contiguous run of this list, and a node needed by several
 // minibatches is a run inside it.  Each hop (Alg. 1, sampling loop):
-//   k_count     k = min(deg, f_l) per request, in (minibatch, row) order
+//   counts      k = min(deg, f_l) per request, in (minibatch, row) order, with
+//               the reduce pass of the edge-offset scan (k_count_reduce)
 //   scan        edge offset of every request (the hop's row pointers)
 //   k_sample    walks the list in block order: Floyd subsets from Philox words,
 //               neighbours written at the request's edge offset
@@ -16,7 +17,7 @@
 //               equal (node, minibatch) keys is an old node when the list holds
 //               the pair, else a new node; new nodes get local ids in id order
 //               per minibatch, every edge gets its column, and the new pairs
-//               are merged into the list (split, count, scan, write)
+//               are merged into the list (count, scan, write)
 // Gather (Alg. 1, gathering loop): the final list is the feature bucket in block
 // order; k_gather copies each row to every minibatch that needs it.
 //
@@ -79,7 +80,7 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
     return g;
 }
 
-// Workgroups of the per-request kernels (k_count, k_sample) of hop l.
+// Workgroups of the sampler (k_sample) of hop l.
 static int hop_grid(const Store& s, const Geometry& g, int l) {
     return grid_for((int64_t)g.H * g.cap[l], std::min(2048, s.sample_groups));
 }
@@ -217,22 +218,7 @@ __global__ __launch_bounds__(kBlock) void k_begin(int l, int L, int H, Ctl* ctl,
 
 // ----------------------------------------------------------------- sampling
 
-template <typename OffT>
-__global__ __launch_bounds__(kBlock) void k_count(int H, int64_t capN, int32_t f, const OffT* off,
-                                                  const int32_t* nodes, const int64_t* req_off_g,
-                                                  int32_t* cnt, const Ctl* ctl) {
-    extern __shared__ int64_t req_off[];
-    load_offsets(req_off, req_off_g, H);
-    const int64_t R = ctl->R;
-    for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < R; q += (int64_t)gridDim.x * kBlock) {
-        int j = upper_segment(req_off, H, q);
-        int32_t v = nodes[(int64_t)j * capN + (q - req_off[j])];
-        int64_t deg = (int64_t)off[v + 1] - (int64_t)off[v];
-        cnt[q] = (int32_t)(deg < f ? deg : f);
-    }
-}
-
-// k_count fused with the reduce pass of the edge-offset scan: the counts of
+// Per-request counts fused with the reduce pass of the edge-offset scan: the counts of
 // scan range g (scan_range over the hop's R requests, G ranges) and their sum
 // in partials[g]; the scan's final pass follows.
 template <typename OffT>

@@ -148,11 +148,6 @@ void scan_counts(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t 
     scan_impl<int32_t>(in, out, n_dev, n_max, total_dev, partials, nonzero, st);
 }
 
-void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
-                   int64_t* total_dev, int64_t* partials, hipStream_t st, int64_t* nonzero) {
-    scan_impl<int64_t>(in, out, n_dev, n_max, total_dev, partials, nonzero, st);
-}
-
 // ----------------------------------------------------------------- radix sort
 
 // LSD radix sort of 32-bit keys with 32-bit values, tiles of 256 x ITEMS keys

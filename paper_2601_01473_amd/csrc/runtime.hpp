@@ -368,9 +368,7 @@ Store* build_store(const agnes_csr* csr, const agnes_features* feat, uint64_t bl
 // `nonzero` is not null, the number of nonzero inputs is added to *nonzero.
 void scan_counts(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
                  int64_t* total_dev, int64_t* partials, hipStream_t st, int64_t* nonzero = nullptr);
-// Same for int64 counts.
-void scan_counts64(const int64_t* in, int64_t* out, const int64_t* n_dev, int64_t n_max,
-                   int64_t* total_dev, int64_t* partials, hipStream_t st, int64_t* nonzero = nullptr);
+// Partial sums a scan needs (the size of `partials`).
 int64_t scan_partials_needed();
 // Workgroups (ranges) of a scan over at most n_max elements, and its final
 // pass alone, for a reduce pass fused into the kernel that produces the counts
