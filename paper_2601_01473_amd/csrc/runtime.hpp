@@ -373,6 +373,8 @@ int64_t scan_partials_needed();
 // Workgroups (ranges) of a scan over at most n_max elements, and its final
 // pass alone, for a reduce pass fused into the kernel that produces the counts
 // (it must write partials[g] = the sum of range g, as scan_range splits them).
+// The final pass writes 32-bit offsets: the caller guarantees a total below
+// 2^32 (a hop's edge numbers, by the plan's bound); *total_dev is 64-bit.
 int scan_groups(int64_t n_max);
 void scan_counts_final(const int32_t* in, uint32_t* out, const int64_t* n_dev, int64_t n_max, int64_t* total_dev,
                        const int64_t* partials, hipStream_t st);
