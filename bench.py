@@ -69,6 +69,16 @@ def measured_traffic(root: str, workload: str):
     return float(vals["traffic_GB_per_launch"]), float(vals["algorithmic_GB_per_launch"])
 
 
+def offset_bytes(w: dict) -> int:
+    """Width of the CSR offsets the method needs: 4 bytes for any graph below
+    2^31 edges (the library keeps int64 offsets of such graphs as int32 on the
+    device), 8 above or when AGNES_WIDE_OFFSETS=1 keeps them 64-bit."""
+    if w["offsets"].dtype != np.int64:
+        return 4
+    wide = os.environ.get("AGNES_WIDE_OFFSETS") == "1"
+    return 8 if (wide or len(w["indices"]) >= (1 << 31) - 1) else 4
+
+
 def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int) -> tuple:
     """Bytes the method must move (exact counts from the batch statistics).
 
@@ -371,7 +381,7 @@ def cpu_baseline(w, cfg, steps_targets, budget_s=20.0):
     import oracle
     o = oracle.Oracle(w["offsets64"], w["indices"])
     fb = np.ascontiguousarray(w["features"]).view(np.uint8).reshape(w["num_nodes"], -1)
-    ob = 8 if w["offsets"].dtype == np.int64 else 4
+    ob = offset_bytes(w)
     rb = cfg.row_bytes
     L = len(cfg.fanouts)
     H = w["H"]
@@ -640,7 +650,7 @@ def main():
         return
     if args.ablation:
         tg = torch.from_numpy(np.ascontiguousarray(step_targets[0])).cuda()
-        ob_ = 8 if w["offsets"].dtype == np.int64 else 4
+        ob_ = offset_bytes(w)
         print(json.dumps(ablation(store, cfg, tg, H, max(1, min(args.steps, 5)), ob_, cfg.row_bytes, torch)),
               flush=True)
         store.close()
@@ -654,7 +664,7 @@ def main():
     if args.join_path is not None:
         store.set_join_path(bool(args.join_path))
     stream = torch.cuda.current_stream()
-    ob = 8 if w["offsets"].dtype == np.int64 else 4
+    ob = offset_bytes(w)
     rb = cfg.row_bytes
 
     acc = dict(bytes=0, sample=0, gather=0, copy_bytes=0, edges=0, rows=0, distinct=0, block_model=0, sample_ms=0.0, gather_ms=0.0,

@@ -42,3 +42,14 @@ def test_graph_replay_rule():
     # exactly at the bound: 2^20 edges
     assert bench.sampling_replayed(2, 1, 1 << 20, (1,), 1 << 22)
     assert not bench.sampling_replayed(2, 1, (1 << 20) + 1, (1,), 1 << 22)
+
+
+def test_offset_width_counted_as_the_device_keeps_it(monkeypatch):
+    import numpy as np
+    small64 = {"offsets": np.zeros(4, np.int64), "indices": np.zeros(10, np.int32)}
+    small32 = {"offsets": np.zeros(4, np.int32), "indices": np.zeros(10, np.int32)}
+    assert bench.offset_bytes(small64) == 4
+    assert bench.offset_bytes(small32) == 4
+    monkeypatch.setenv("AGNES_WIDE_OFFSETS", "1")
+    assert bench.offset_bytes(small64) == 8
+    assert bench.offset_bytes(small32) == 4
