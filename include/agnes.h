@@ -298,9 +298,12 @@ agnes_status agnes_set_device_allocator(agnes_device_alloc_fn alloc, agnes_devic
  *     only makes that happen more often.
  *   AGNES_OPT_SAMPLING_GROUPS: most workgroups of each sampling-phase kernel
  *     that loops over its work (the sampler, the radix passes, the join), in
- *     [256, 4096] (default 512; 4096 leaves each kernel at its own limit,
- *     2048 for most).  Fewer need fewer dispatch slots beside a running row
- *     copy of another hyperbatch, which holds most of them.
+ *     [256, 4096]; 0 (default) chooses per hop: the power of two at or below
+ *     its bound of sampled edges (H x frontier capacity x fanout) / 32768,
+ *     within [512, 2048].  4096
+ *     leaves each kernel at its own limit, 2048 for most.  Fewer need fewer
+ *     dispatch slots beside a running row copy of another hyperbatch, which
+ *     holds most of them; a large hop needs more to hide its latency.
  * Options change launch shapes and store kinds only, never results. */
 typedef enum {
     AGNES_OPT_PROFILE = 1,

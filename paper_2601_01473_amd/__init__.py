@@ -163,7 +163,8 @@ class Store:
 
     def set_sampling_groups(self, groups: int) -> None:
         """Most workgroups of each sampling-phase kernel that loops over its
-        work (never changes results)."""
+        work, in [256, 4096], or 0 (the default) to choose per hop by its
+        size (never changes results)."""
         agnes_store_set_option(self.handle, B.AGNES_OPT_SAMPLING_GROUPS, int(groups))
 
     def set_gather_shape(self, groups: int | None = None, unroll: int | None = None,

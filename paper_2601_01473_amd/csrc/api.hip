@@ -325,7 +325,8 @@ agnes_status agnes_store_set_option(agnes_store* store, agnes_option opt, int64_
             AGNES_REQUIRE(value == 0 || value == 1, AGNES_ERR_INVALID, "join path must be 0 or 1");
             s->join_path = (int)value;
         } else if (opt == AGNES_OPT_SAMPLING_GROUPS) {
-            AGNES_REQUIRE(value >= 256 && value <= 4096, AGNES_ERR_INVALID, "sampling groups must be in [256, 4096]");
+            AGNES_REQUIRE(value == 0 || (value >= 256 && value <= 4096), AGNES_ERR_INVALID,
+                          "sampling groups must be 0 or in [256, 4096]");
             s->sample_groups = (int)value;
         } else if (opt == AGNES_OPT_BUCKET_CAP) {
             AGNES_REQUIRE(value >= 64 && value <= kBucketCap, AGNES_ERR_INVALID, "bucket capacity must be in [64, 2048]");

@@ -39,6 +39,7 @@ struct Geometry {
     int64_t capN;                      // node capacity of one minibatch
     int64_t cap[AGNES_MAX_LAYERS + 1]; // cap[l] = frontier capacity of hop l (cap[L] = capN)
     int64_t Rmax, Smax, rows_max, sort_max;
+    int64_t ebound[AGNES_MAX_LAYERS];  // sampled edges of hop l at most: H cap[l] f_l
     int jbits;
     // node-range buckets: per hop the most coarse buckets and the count
     // table's row stride
@@ -61,6 +62,7 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
                       "a hop's requests and sampled edges can reach 2^32 (H * frontier capacity * (1 + fanout))");
         g.Rmax = std::max<int64_t>(g.Rmax, (int64_t)H * g.cap[l]);
         g.Smax = std::max<int64_t>(g.Smax, (int64_t)H * g.cap[l] * fanouts[l]);
+        g.ebound[l] = (int64_t)H * g.cap[l] * fanouts[l];
         g.cap[l + 1] = std::min<int64_t>(g.cap[l] * (1 + (int64_t)fanouts[l]), nmax);
     }
     g.capN = g.cap[L];
@@ -80,9 +82,23 @@ static Geometry plan(const Store& s, int32_t H, int32_t B, const int32_t* fanout
     return g;
 }
 
+// Most workgroups of each looping sampling kernel (the sampler, the radix
+// passes, the join) of a hop of at most `bound` sampled edges: the store's
+// setting, or by default the power of two at or below bound / 32768, within
+// [512, 2048].  Beside a running row copy fewer workgroups start sooner, while
+// a large hop needs more to hide its latency; measured: 512 suits hops of
+// about 2M edges (the 2^23-node workload), 2048 those of 15M (the 2^26-node
+// workload's last hop).
+static int hop_cap(const Store& s, int64_t bound) {
+    if (s.sample_groups > 0) return s.sample_groups;
+    int cap = 512;
+    while (cap < 2048 && (int64_t)cap * 2 <= bound / 32768) cap *= 2;
+    return cap;
+}
+
 // Workgroups of the sampler (k_sample) of hop l.
 static int hop_grid(const Store& s, const Geometry& g, int l) {
-    return grid_for((int64_t)g.H * g.cap[l], std::min(2048, s.sample_groups));
+    return grid_for((int64_t)g.H * g.cap[l], std::min(2048, hop_cap(s, g.ebound[l])));
 }
 
 // ----------------------------------------------------------------- small kernels
@@ -1380,14 +1396,15 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     // fewer edges than the last hop).
     int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
                                     w.sval2.as<uint32_t>(), &ctl->S, s_max, s.node_bits,
-                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true, s.sample_groups);
+                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true,
+                                    hop_cap(s, g.ebound[l]));
     const uint32_t* su = in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>();
     const uint32_t* se = in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>();
     // join with the list: the next list, new node ids and the hop's columns
     const int64_t tiles_l = ((int64_t)g.H * g.cap[l] * (1 + (int64_t)f)) / kJoinTile + 1;
     int64_t* split = w.split.as<int64_t>();
     const int G = (int)std::max<int64_t>(
-        std::min(join_groups(g.H, tiles_l), std::max(kBlock, s.sample_groups / kBlock * kBlock)),
+        std::min(join_groups(g.H, tiles_l), std::max(kBlock, hop_cap(s, g.ebound[l]) / kBlock * kBlock)),
         join_groups_min(tiles_l));
     const int64_t per = (tiles_l + G - 1) / G + 2;
     AGNES_LAUNCH(k_join_count, dim3(G), dim3(kBlock), join_count_lds(g.H, per), st, g.H,
@@ -1551,7 +1568,8 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     // minibatch) with the radix sort, on either join path
     int in_tmp = radix_sort_pairs32(w.skey.as<uint32_t>(), w.sval.as<uint32_t>(), w.skey2.as<uint32_t>(),
                                     w.sval2.as<uint32_t>(), &ctl->targets, (int64_t)H * B, s.node_bits,
-                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true, s.sample_groups);
+                                    w.rs_hist.as<uint32_t>(), w.rs_dtot.as<uint32_t>(), st, true,
+                                    hop_cap(s, (int64_t)H * B));
     AGNES_LAUNCH(k_list0, dim3(grid_for((int64_t)H * B, 1024)), dim3(kBlock), 0, st,
                        in_tmp ? w.skey2.as<uint32_t>() : w.skey.as<uint32_t>(),
                        in_tmp ? w.sval2.as<uint32_t>() : w.sval.as<uint32_t>(), B, w.rl_key[0].as<uint64_t>(),

@@ -229,7 +229,8 @@ struct Store {
     DevBuf bnd, lev_info;
     int join_path = 0;                // 1 = node-range buckets, 0 = radix sort and merge-path join (default)
     int bucket_cap = 2048;            // entries of a sorted sub-bucket (at most kBucketCap)
-    int sample_groups = 512;          // most workgroups of a sampling-phase kernel that loops over its work
+    int sample_groups = 0;            // most workgroups of a sampling-phase kernel that loops over its
+                                      // work; 0 = chosen per hop by its size
     // Staged feature tier (features in pinned host memory, an HBM pool of
     // feature-block slots).  Not used when tiered == 0 (features in HBM).
     // The pool's host-side bookkeeping changes with every planned hyperbatch.
