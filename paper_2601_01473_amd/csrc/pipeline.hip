@@ -459,14 +459,6 @@ __device__ __forceinline__ void join_store(const JoinSpan& s, const JoinRegs& r,
     }
 }
 
-__device__ __forceinline__ int lds_lower_bound(const uint64_t* sk, int lo, int hi, uint64_t key) {
-    while (lo < hi) {
-        int mid = (lo + hi) >> 1;
-        if (sk[mid] < key) lo = mid + 1; else hi = mid;
-    }
-    return lo;
-}
-
 // Edge i of the tile (key K): head?  For a head, idx = lower bound of K in the
 // tile's A part, and found / floc = whether A holds K and its local id.
 struct EdgeFlags {
@@ -475,22 +467,54 @@ struct EdgeFlags {
     int32_t floc;
 };
 
-__device__ __forceinline__ EdgeFlags edge_flags(const uint64_t* sk, const int32_t* sv, int nA, int i, uint64_t K,
-                                                const uint64_t* pre, int32_t pre_val) {
-    EdgeFlags f{false, false, 0, 0};
-    const uint64_t prevK = i > 0 ? sk[nA + i - 1] : pre[0];
-    f.head = K != prevK;
-    if (f.head) {
-        f.idx = lds_lower_bound(sk, 0, nA, K);
-        if (f.idx < nA && sk[f.idx] == K) {
-            f.found = true;
-            f.floc = sv[f.idx];
-        } else if (pre[1] == K) {
-            f.found = true;
-            f.floc = pre_val;
+// Lower bounds of Q keys in the sorted sk[lo, hi), searched in lockstep: a
+// fixed sequence of halving steps, the same for every key and lane, so the Q
+// searches' LDS reads overlap.  The answer stays in [base, base + n].
+template <int Q>
+__device__ __forceinline__ void lds_lower_bounds(const uint64_t* sk, int lo, int hi, const uint64_t (&key)[Q],
+                                                 int (&out)[Q]) {
+    int base[Q];
+#pragma unroll
+    for (int q = 0; q < Q; q++) base[q] = lo;
+    int n = hi - lo;
+    while (n > 1) {
+        const int half = n >> 1;
+#pragma unroll
+        for (int q = 0; q < Q; q++) base[q] = sk[base[q] + half] < key[q] ? base[q] + half : base[q];
+        n -= half;
+    }
+#pragma unroll
+    for (int q = 0; q < Q; q++) out[q] = (n == 1 && sk[base[q]] < key[q]) ? base[q] + 1 : base[q];
+}
+
+// Edges i[q] of the tile (valid[q]: i[q] < nB): their keys, whether each is a
+// head and, for a head, idx = lower bound of its key in the tile's A part and
+// found / floc = whether A holds the key and its local id.  The Q searches run
+// together (lds_lower_bounds).
+template <int Q>
+__device__ __forceinline__ void edge_flags(const uint64_t* sk, const int32_t* sv, int nA, const int (&i)[Q],
+                                           const bool (&valid)[Q], uint64_t (&K)[Q], const uint64_t* pre,
+                                           int32_t pre_val, EdgeFlags (&f)[Q]) {
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+        K[q] = valid[q] ? sk[nA + i[q]] : 0;
+        const uint64_t prevK = (valid[q] && i[q] > 0) ? sk[nA + i[q] - 1] : pre[0];
+        f[q] = EdgeFlags{valid[q] && K[q] != prevK, false, 0, 0};
+    }
+    int lb[Q];
+    lds_lower_bounds<Q>(sk, 0, nA, K, lb);
+#pragma unroll
+    for (int q = 0; q < Q; q++) {
+        if (!f[q].head) continue;
+        f[q].idx = lb[q];
+        if (lb[q] < nA && sk[lb[q]] == K[q]) {
+            f[q].found = true;
+            f[q].floc = sv[lb[q]];
+        } else if (pre[1] == K[q]) {
+            f[q].found = true;
+            f[q].floc = pre_val;
         }
     }
-    return f;
 }
 
 __device__ __forceinline__ void group_tiles(int64_t n, int g, int G, int64_t& t0, int64_t& t1) {
@@ -559,12 +583,23 @@ __global__ __launch_bounds__(kBlock) void k_join_count(int H, const int64_t* req
         if (t + 1 < t1) join_load(join_span(t + 1, n, ssplit + (t + 1 - t0)), ak, av, su, se, regs);
         a_total += s.nA;
         __syncthreads();
-        for (int i = tid; i < s.nB; i += kBlock) {
-            const uint64_t K = sk[s.nA + i];
-            const EdgeFlags f = edge_flags(sk, sv, s.nA, i, K, pre, pre_val);
-            if (f.head && !f.found) {
-                atomicAdd(&count[(uint32_t)K], 1u);
-                nh++;
+        {
+            int ii[kJoinSlots];
+            bool vv[kJoinSlots];
+            uint64_t K[kJoinSlots];
+            EdgeFlags f[kJoinSlots];
+#pragma unroll
+            for (int k = 0; k < kJoinSlots; k++) {
+                ii[k] = tid + k * kBlock;
+                vv[k] = ii[k] < s.nB;
+            }
+            edge_flags<kJoinSlots>(sk, sv, s.nA, ii, vv, K, pre, pre_val, f);
+#pragma unroll
+            for (int k = 0; k < kJoinSlots; k++) {
+                if (f[k].head && !f[k].found) {
+                    atomicAdd(&count[(uint32_t)K[k]], 1u);
+                    nh++;
+                }
             }
         }
         __syncthreads();
@@ -660,13 +695,19 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
         int32_t nhw[kJoinRounds], jrk[kJoinRounds], anc[kJoinRounds], idx[kJoinRounds], floc[kJoinRounds];
         uint32_t kind = 0;                   // per round: bit 2r = head, bit 2r+1 = new
         int nh_run = 0, anc_run = -1;
+        int items[kJoinRounds];
+        bool inb[kJoinRounds];
+        EdgeFlags fl[kJoinRounds];
 #pragma unroll
         for (int r = 0; r < kJoinRounds; r++) {
-            const int i = w * kJoinWaveItems + r * kWave + lane;
-            const bool valid = i < s.nB;
-            const uint64_t K = valid ? sk[s.nA + i] : 0;
-            EdgeFlags f{false, false, 0, 0};
-            if (valid) f = edge_flags(sk, sv, s.nA, i, K, pre, pre_val);
+            items[r] = w * kJoinWaveItems + r * kWave + lane;
+            inb[r] = items[r] < s.nB;
+        }
+        edge_flags<kJoinRounds>(sk, sv, s.nA, items, inb, key, pre, pre_val, fl);
+#pragma unroll
+        for (int r = 0; r < kJoinRounds; r++) {
+            const uint64_t K = key[r];
+            const EdgeFlags f = fl[r];
             const bool nh = f.head && !f.found;
             const uint64_t nhm = __ballot(nh);
             nhw[r] = nh_run + __popcll(nhm & lanemask_lt());
@@ -693,7 +734,6 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
             const int base = w * kJoinWaveItems + r * kWave;
             anc[r] = le ? base + 63 - __clzll(le) : anc_run;
             if (hm) anc_run = base + 63 - __clzll(hm);
-            key[r] = K;
             idx[r] = f.idx;
             floc[r] = f.floc;
             kind |= ((f.head ? 1u : 0u) | (nh ? 2u : 0u)) << (2 * r);
@@ -745,13 +785,24 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
             const int i = w * kJoinWaveItems + r * kWave + lane;
             if (i < s.nB) col[sv[s.nA + i]] = anc[r] >= 0 ? loc[anc[r]] : cont_local;
         }
-        for (int ia = tid; ia < s.nA; ia += kBlock) {
-            const uint64_t K = sk[ia];
-            const int lb = lds_lower_bound(sk, s.nA, s.nA + s.nB, K) - s.nA;
-            const int64_t pos = run + ia + nhx[lb];
-            if (pos < rows_cap) {
-                ck[pos] = K;
-                cv[pos] = sv[ia];
+        {
+            uint64_t AK[kJoinSlots];
+            int lb[kJoinSlots];
+#pragma unroll
+            for (int k = 0; k < kJoinSlots; k++) {
+                const int ia = tid + k * kBlock;
+                AK[k] = ia < s.nA ? sk[ia] : 0;
+            }
+            lds_lower_bounds<kJoinSlots>(sk, s.nA, s.nA + s.nB, AK, lb);
+#pragma unroll
+            for (int k = 0; k < kJoinSlots; k++) {
+                const int ia = tid + k * kBlock;
+                if (ia >= s.nA) continue;
+                const int64_t pos = run + ia + nhx[lb[k] - s.nA];
+                if (pos < rows_cap) {
+                    ck[pos] = AK[k];
+                    cv[pos] = sv[ia];
+                }
             }
         }
         for (int j = tid; j < H; j += kBlock) {
