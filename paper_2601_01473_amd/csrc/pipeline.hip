@@ -96,9 +96,10 @@ static int hop_cap(const Store& s, int64_t bound) {
     return cap;
 }
 
-// Workgroups of the sampler (k_sample) of hop l.
+// Workgroups of the sampler (k_sample) of hop l: a multiple of the XCD count.
 static int hop_grid(const Store& s, const Geometry& g, int l) {
-    return grid_for((int64_t)g.H * g.cap[l], std::min(2048, hop_cap(s, g.ebound[l])));
+    const int G = grid_for((int64_t)g.H * g.cap[l], std::min(2048, hop_cap(s, g.ebound[l])));
+    return (G + kXcds - 1) / kXcds * kXcds;
 }
 
 // ----------------------------------------------------------------- small kernels
@@ -277,24 +278,32 @@ __global__ __launch_bounds__(kBlock) void k_sample(int l, int H, int32_t f, cons
     if (threadIdx.x == 0) opened = 0;
     load_offsets(req_off, req_off_g, H);
     const int64_t R = ctl->R;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    // XCD x (workgroups dealt to the 8 XCDs in turn; the grid is a multiple of
+    // 8) walks the x-th eighth of the list, so the lines that neighbouring
+    // requests share (offsets, edge offsets of a minibatch's consecutive rows)
+    // are fetched into one L2 rather than eight
+    const int xcd = (int)(blockIdx.x % kXcds);
+    const int64_t part = ((R + kXcds - 1) / kXcds + kBlock - 1) / kBlock * kBlock;
+    const int64_t lo = std::min<int64_t>(R, (int64_t)xcd * part), hi = std::min<int64_t>(R, lo + part);
+    const int64_t stride = (int64_t)(gridDim.x / kXcds) * kBlock;
+    const int64_t first = lo + (int64_t)(blockIdx.x / kXcds) * kBlock;
     // the next request's list entry is loaded while this one is sampled
     uint64_t next_key = 0;
     int32_t next_val = 0;
     {
-        const int64_t p0 = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-        if (p0 < R) {
+        const int64_t p0 = first + threadIdx.x;
+        if (p0 < hi) {
             next_key = rl_key[p0];
             next_val = rl_val[p0];
         }
     }
-    for (int64_t base = (int64_t)blockIdx.x * kBlock; base < R; base += stride) {
+    for (int64_t base = first; base < hi; base += stride) {
         int64_t p = base + threadIdx.x;
-        bool active = p < R;
+        bool active = p < hi;
         int64_t blk = -1;
         const uint64_t key = next_key;
         const int32_t val = next_val;
-        if (p + stride < R) {
+        if (p + stride < hi) {
             next_key = rl_key[p + stride];
             next_val = rl_val[p + stride];
         }
@@ -1351,7 +1360,7 @@ static void reserve_workspace(Workspace& w, const Geometry& g, const SyncLayout&
     w.rs_hist.reserve((size_t)radix_hist_entries(g.sort_max) * 4);
     w.rs_dtot.reserve((size_t)radix_dtot_entries() * 4);
     w.scan_part.reserve((size_t)scan_partials_needed() * 8);
-    w.topo_part.reserve((size_t)grid_for(g.Rmax, 2048) * 4);
+    w.topo_part.reserve((size_t)((grid_for(g.Rmax, 2048) + kXcds - 1) / kXcds * kXcds) * 4);
     w.params.reserve(sizeof(ChainParams));
     if (!w.ev[0])
         for (auto& e : w.ev) AGNES_CHECK_HIP(hipEventCreate(&e));
