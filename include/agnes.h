@@ -15,6 +15,14 @@
  *     memory of the current device.
  *   - hip_stream is a hipStream_t passed as void* (NULL = the null stream).
  *   - All node ids are int32 in [0, num_nodes); num_nodes < 2^31.
+ *
+ * Environment variables read by the library (none changes any result):
+ *   - AGNES_DEBUG_SYNC=1: every kernel launch synchronises its stream and
+ *     checks for an error right after it (outside graph capture), so a fault
+ *     is reported at the launch that caused it.  Read once per process.
+ *   - AGNES_WIDE_OFFSETS=1: agnes_build_blocks* keep int64 CSR offsets 64-bit
+ *     on the device; by default the offsets of a graph with fewer than 2^31
+ *     edges are stored as int32.  Read at every build.
  */
 #ifndef AGNES_H
 #define AGNES_H
