@@ -5,6 +5,8 @@ offsets (int64 also kept 64-bit on the device), row widths and dtypes, block
 sizes, the sampling kernels' workgroup cap and graph replay.  Every case runs
 twice on one batch with new targets, seed and minibatch base (the second call
 replays the sampling kernels from a graph when the shape is small enough)."""
+import os
+
 import numpy as np
 import pytest
 
@@ -14,7 +16,8 @@ from tests.parity import compare_minibatch, feature_bytes, log
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 64
+# AGNES_FUZZ_CASES widens the sweep (the default suite runs 64)
+N_CASES = int(os.environ.get("AGNES_FUZZ_CASES", "64"))
 
 
 @pytest.fixture(scope="module")
