@@ -81,3 +81,49 @@ def test_random_shape_matches_oracle(agnes, seed, monkeypatch):
             assert st[k] == v, ("fuzz", seed, rep, k, st[k], v)
     b.close()
     store.close()
+
+
+N_LARGE = int(os.environ.get("AGNES_FUZZ_LARGE_CASES", "6"))
+
+
+def _large_case(seed):
+    rng = np.random.default_rng(5000 + seed)
+    scale = int(rng.integers(12, 18))
+    ef = int(rng.integers(4, 24))
+    abc = [(0.57, 0.19, 0.19), (0.65, 0.15, 0.15), (0.45, 0.25, 0.15)][int(rng.integers(0, 3))]
+    n = 1 << scale
+    H = int(rng.choice([16, 64, 128, 256]))
+    bmax = max(1, min(n // H, 1024))                 # H * B <= n: distinct targets
+    B = int(rng.integers(min(64, bmax), bmax + 1))
+    L = int(rng.integers(1, 4))
+    fan = [int(x) for x in rng.choice([2, 5, 10, 15, 25], size=L)]
+    groups = int(rng.choice([0, 256, 512, 2048]))
+    return dict(scale=scale, ef=ef, abc=abc, n=n, H=H, B=B, fan=fan, groups=groups)
+
+
+@pytest.mark.parametrize("seed", range(N_LARGE))
+def test_random_rmat_shape_matches_oracle(agnes, seed):
+    """Larger R-MAT graphs (2^12 to 2^17 nodes, three skews) with hyperbatches
+    of up to 256 x 1024 targets: join groups take several tiles each and the
+    sampling kernels loop; every minibatch is compared with the oracle."""
+    import synth
+    c = _large_case(seed)
+    log("fuzz large", seed, c)
+    off, idx = synth.rmat_csr(c["scale"], c["ef"], c["abc"], 6000 + seed)
+    feat = features(c["n"], 16, 7000 + seed)
+    store = agnes.Store(off, idx, feat, 1024)
+    if c["groups"]:
+        store.set_sampling_groups(c["groups"])
+    tg = synth.targets(c["n"], c["H"] * c["B"], 8000 + seed).reshape(c["H"], c["B"])
+    b = store.prepare(tg, c["fan"], seed=seed, mb_base=11 * seed)
+    got = b.to_host()
+    ref = oracle.Oracle(off, idx).hyperbatch(tg, c["fan"], seed, 11 * seed)
+    fb = feature_bytes(feat)
+    for j in range(c["H"]):
+        compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes), tag=("fuzz large", seed, j))
+    st = b.stats()
+    want = oracle.hyperbatch_stats(off, 1024, fb.shape[1], ref, len(c["fan"]))
+    for k, v in want.items():
+        assert st[k] == v, ("fuzz large", seed, k, st[k], v)
+    b.close()
+    store.close()
