@@ -90,7 +90,9 @@ def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int) -> tuple:
     for R, S, U in zip(st["requests"], st["sampled"], st["new_nodes"]):
         bs += R * (4 + 2 * offset_bytes + 4) + 8 * S + 4 * U
     bg = st["rows"] * (4 + row_bytes) + st["distinct_rows"] * row_bytes
-    copy = st["rows"] * row_bytes + st["distinct_rows"] * row_bytes
+    # the row-copy kernel moves all of the gather's bytes (it also writes the
+    # node ids)
+    copy = bg
     return bs, bg, copy
 
 
