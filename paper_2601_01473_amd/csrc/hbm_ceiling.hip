@@ -10,7 +10,12 @@
 // the row copy, which writes each row where its minibatch needs it.  Stores
 // are non-temporal, as in the row copy.  Prints one JSON line per kernel:
 // best and mean rate over 10 timed launches (row gathers: row bytes read and
-// written only).
+// written only).  Last, lone 4-byte stores: 3.2 M of them into a 12.8 MB
+// array (the column stores of the join at the default workload), consecutive,
+// at a random permutation of the places, random inside one eighth of the array
+// per XCD (workgroup w takes eighth w mod 8: workgroups are dealt to the XCDs
+// in turn), and in runs of 10 consecutive places per lane (the sampler's
+// pattern): best of 10 launches.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -120,6 +125,28 @@ __global__ __launch_bounds__(kBlock) void k_rows(const u32x4* __restrict__ table
     }
 }
 
+// Lone 4-byte stores.  mode 0: out[i]; 1: out[perm[i]]; 2: workgroup w
+// stores the permutation of eighth c = w mod 8 (perm8 holds, at [c m, (c+1) m),
+// a permutation of those places); 3: runs of R consecutive places per lane
+// (start[q] for q < n / R).
+template <int MODE, int R>
+__global__ __launch_bounds__(kBlock) void k_stores(int* __restrict__ out, const int* __restrict__ perm, long n) {
+    if (MODE == 2) {
+        const long m = n / 8, parts = gridDim.x / 8, part = blockIdx.x / 8;
+        const long c = blockIdx.x % 8;
+        for (long i = part * kBlock + threadIdx.x; i < m; i += parts * kBlock) out[perm[c * m + i]] = (int)i;
+    } else if (MODE == 3) {
+        for (long q = (long)blockIdx.x * kBlock + threadIdx.x; q < n / R; q += (long)gridDim.x * kBlock) {
+            const int s0 = perm[q];
+#pragma unroll
+            for (int r = 0; r < R; r++) out[s0 + r] = r;
+        }
+    } else {
+        for (long i = (long)blockIdx.x * kBlock + threadIdx.x; i < n; i += (long)gridDim.x * kBlock)
+            out[MODE == 1 ? perm[i] : i] = (int)i;
+    }
+}
+
 }  // namespace
 
 int main() {
@@ -214,6 +241,40 @@ int main() {
         CHECK(hipFree(seq));
         CHECK(hipFree(perm));
         CHECK(hipFree(ids));
+    }
+    // lone 4-byte stores
+    {
+        const long n = 3200000, m = n / 8;      // n is a multiple of 80
+        int *out = nullptr, *perm = nullptr, *perm8 = nullptr, *starts = nullptr;
+        CHECK(hipMalloc(&out, n * sizeof(int)));
+        CHECK(hipMalloc(&perm, n * sizeof(int)));
+        CHECK(hipMalloc(&perm8, n * sizeof(int)));
+        CHECK(hipMalloc(&starts, n / 10 * sizeof(int)));
+        std::vector<int> h((size_t)n);
+        std::mt19937_64 rng(7);
+        std::iota(h.begin(), h.end(), 0);
+        std::shuffle(h.begin(), h.end(), rng);
+        CHECK(hipMemcpy(perm, h.data(), n * sizeof(int), hipMemcpyHostToDevice));
+        std::iota(h.begin(), h.end(), 0);
+        for (int c = 0; c < 8; c++) std::shuffle(h.begin() + c * m, h.begin() + (c + 1) * m, rng);
+        CHECK(hipMemcpy(perm8, h.data(), n * sizeof(int), hipMemcpyHostToDevice));
+        for (long q = 0; q < n / 10; q++) h[q] = (int)(q * 10);
+        std::shuffle(h.begin(), h.begin() + n / 10, rng);
+        CHECK(hipMemcpy(starts, h.data(), n / 10 * sizeof(int), hipMemcpyHostToDevice));
+        const double moved = 4.0 * (double)n;
+        const int g = 2048;
+        timed("4-B stores: consecutive", moved, g,
+              [&] { hipLaunchKernelGGL((k_stores<0, 1>), dim3(g), dim3(kBlock), 0, 0, out, perm, n); });
+        timed("4-B stores: random permutation", moved, g,
+              [&] { hipLaunchKernelGGL((k_stores<1, 1>), dim3(g), dim3(kBlock), 0, 0, out, perm, n); });
+        timed("4-B stores: random inside one eighth per XCD", moved, g,
+              [&] { hipLaunchKernelGGL((k_stores<2, 1>), dim3(g), dim3(kBlock), 0, 0, out, perm8, n); });
+        timed("4-B stores: runs of 10 per lane", moved, g,
+              [&] { hipLaunchKernelGGL((k_stores<3, 10>), dim3(g), dim3(kBlock), 0, 0, out, starts, n); });
+        CHECK(hipFree(out));
+        CHECK(hipFree(perm));
+        CHECK(hipFree(perm8));
+        CHECK(hipFree(starts));
     }
     CHECK(hipFree(a));
     CHECK(hipFree(o));
