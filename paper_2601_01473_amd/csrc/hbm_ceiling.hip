@@ -15,7 +15,9 @@
 // at a random permutation of the places, random inside one eighth of the array
 // per XCD (workgroup w takes eighth w mod 8: workgroups are dealt to the XCDs
 // in turn), and in runs of 10 consecutive places per lane (the sampler's
-// pattern): best of 10 launches.
+// pattern); and 4 M lone 4-byte loads at random places of a 1 GiB table (the
+// sampler's neighbour reads), 8 independent loads per lane: best of 10
+// launches.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -147,6 +149,22 @@ __global__ __launch_bounds__(kBlock) void k_stores(int* __restrict__ out, const 
     }
 }
 
+// Lone 4-byte loads: 8 per lane, all issued before any is used; the xor of
+// everything goes to sink[0] only if it matches an arbitrary pattern.
+__global__ __launch_bounds__(kBlock) void k_loads(const int* __restrict__ tab, const unsigned* __restrict__ idx,
+                                                  long n, int* sink) {
+    constexpr int R = 8;
+    for (long i = ((long)blockIdx.x * kBlock + threadIdx.x) * R; i < n; i += (long)gridDim.x * kBlock * R) {
+        int v[R];
+#pragma unroll
+        for (int r = 0; r < R; r++) v[r] = tab[idx[i + r]];
+        int acc = 0;
+#pragma unroll
+        for (int r = 0; r < R; r++) acc ^= v[r];
+        if (acc == 0x2545f491) sink[0] = acc;
+    }
+}
+
 }  // namespace
 
 int main() {
@@ -275,6 +293,24 @@ int main() {
         CHECK(hipFree(perm));
         CHECK(hipFree(perm8));
         CHECK(hipFree(starts));
+    }
+    // lone 4-byte loads
+    {
+        const long tn = 1L << 28, n = 1L << 22;   // a 1 GiB table; n is a multiple of 8
+        int* tab = nullptr;
+        unsigned* idx = nullptr;
+        CHECK(hipMalloc(&tab, tn * sizeof(int)));
+        CHECK(hipMalloc(&idx, n * sizeof(unsigned)));
+        CHECK(hipMemset(tab, 1, tn * sizeof(int)));
+        std::vector<unsigned> h((size_t)n);
+        std::mt19937_64 rng(11);
+        for (long i = 0; i < n; i++) h[i] = (unsigned)(rng() % (unsigned long long)tn);
+        CHECK(hipMemcpy(idx, h.data(), n * sizeof(unsigned), hipMemcpyHostToDevice));
+        const int g = 4096;
+        timed("4-B loads: random places of a 1 GiB table", 4.0 * (double)n, g,
+              [&] { hipLaunchKernelGGL(k_loads, dim3(g), dim3(kBlock), 0, 0, tab, idx, n, (int*)sink); });
+        CHECK(hipFree(tab));
+        CHECK(hipFree(idx));
     }
     CHECK(hipFree(a));
     CHECK(hipFree(o));
