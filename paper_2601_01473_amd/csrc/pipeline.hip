@@ -998,12 +998,13 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
 // row.  A wave takes U consecutive entries of the list; lane k < U reads entry
 // k and resolves its source row (the node) and destination row (node_off[j] +
 // local id), and the wave then broadcasts them with readlane, so each row's
-// addresses live in scalar registers and a lane holds only the data: U rows x
-// UPR units in flight per lane.  Chunks of 64 * UPR units cover longer rows.
-// An entry whose node repeats the previous entry's (within the wave's U) reuses
-// the row already in registers.  Waves take blocks of U entries in grid-stride
-// order (wave w of the grid, then w + all waves, ...).
-template <int U, int UPR, bool NT, bool TIER>
+// addresses live in scalar registers and a lane holds only the data: the U
+// entries are copied in rounds of V, V rows x UPR units in flight per lane.
+// Chunks of 64 * UPR units cover longer rows.  An entry whose node repeats the
+// previous entry's (within the wave's U) reuses the row already in registers.
+// Waves take blocks of U entries in grid-stride order (wave w of the grid,
+// then w + all waves, ...).
+template <int U, int V, int UPR, bool NT, bool TIER>
 __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict__ feat, u32x4* __restrict__ out,
                                                         int32_t* __restrict__ nodes_out,
                                                         const uint64_t* __restrict__ rl_key,
@@ -1013,6 +1014,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict_
                                                         const int32_t* __restrict__ tbuf, uint32_t rpb,
                                                         const int32_t* __restrict__ tch, uint32_t pool_rows) {
     static_assert(U <= kWave, "one lane per entry");
+    static_assert(U % V == 0, "whole rounds");
     extern __shared__ int64_t node_off[];
     load_offsets(node_off, node_off_g, H);
     const int lane = lane_id();
@@ -1039,30 +1041,41 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict_
             dst[k] = (uint32_t)__builtin_amdgcn_readlane((int)d, k);
         }
         for (int64_t c0 = 0; c0 < row_units; c0 += (int64_t)kWave * UPR) {
-            u32x4 x[U][UPR];
+            u32x4 prev[UPR];                 // the previous round's last row
 #pragma unroll
-            for (int k = 0; k < U; k++) {
-                if ((fresh >> k) & 1) {
-                    const u32x4* p = feat + (int64_t)src[k] * row_units + c0 + lane;
+            for (int h = 0; h < U / V; h++) {
+                u32x4 x[V][UPR];
 #pragma unroll
-                    for (int q = 0; q < UPR; q++)
-                        if (c0 + lane + q * kWave < row_units) x[k][q] = p[q * kWave];
-                } else if (k > 0) {
+                for (int k = 0; k < V; k++) {
+                    const int kk = h * V + k;
+                    if ((fresh >> kk) & 1) {
+                        const u32x4* p = feat + (int64_t)src[kk] * row_units + c0 + lane;
 #pragma unroll
-                    for (int q = 0; q < UPR; q++) x[k][q] = x[k - 1][q];
-                }
-            }
+                        for (int q = 0; q < UPR; q++)
+                            if (c0 + lane + q * kWave < row_units) x[k][q] = p[q * kWave];
+                    } else if (k > 0) {
 #pragma unroll
-            for (int k = 0; k < U; k++) {
-                if (!((okm >> k) & 1)) continue;
-                u32x4* o = out + (int64_t)dst[k] * row_units + c0 + lane;
+                        for (int q = 0; q < UPR; q++) x[k][q] = x[k - 1][q];
+                    } else if (kk > 0) {
 #pragma unroll
-                for (int q = 0; q < UPR; q++) {
-                    if (c0 + lane + q * kWave < row_units) {
-                        if (NT) __builtin_nontemporal_store(x[k][q], o + q * kWave);
-                        else o[q * kWave] = x[k][q];
+                        for (int q = 0; q < UPR; q++) x[k][q] = prev[q];
                     }
                 }
+#pragma unroll
+                for (int k = 0; k < V; k++) {
+                    const int kk = h * V + k;
+                    if (!((okm >> kk) & 1)) continue;
+                    u32x4* o = out + (int64_t)dst[kk] * row_units + c0 + lane;
+#pragma unroll
+                    for (int q = 0; q < UPR; q++) {
+                        if (c0 + lane + q * kWave < row_units) {
+                            if (NT) __builtin_nontemporal_store(x[k][q], o + q * kWave);
+                            else o[q * kWave] = x[k][q];
+                        }
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < UPR; q++) prev[q] = x[V - 1][q];
             }
         }
     }
@@ -1119,17 +1132,22 @@ static void launch_gather_lpr(const GatherArgs& a, int G, int unroll, bool nt, h
     }
 }
 
+// Rows in flight per round: 16 entries per wave are copied 8 at a time.
+// Beside the sampling of later hyperbatches, half the bytes in flight per wave
+// leave the sampling's dependent loads shorter queues (its chains finish in
+// 1.9 instead of 2.9 ms), while the copy keeps its pace.
 template <int U, int UPR, bool NT>
 static void launch_gather_rows_k(const GatherArgs& a, int groups, hipStream_t st) {
+    constexpr int V = U >= 16 ? 8 : U;
     const size_t lds = (size_t)(a.H + 1) * sizeof(int64_t);
     constexpr int64_t per_wg = (int64_t)kWavesPerBlock * U;
     const int G = (int)std::max<int64_t>(1, std::min<int64_t>(groups, (a.rows + per_wg - 1) / per_wg));
     if (a.tbuf)
-        AGNES_LAUNCH((k_gather_rows<U, UPR, NT, true>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
+        AGNES_LAUNCH((k_gather_rows<U, V, UPR, NT, true>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
                            (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
                            a.row_units, a.tbuf, a.rpb, a.tch, a.pool_rows);
     else
-        AGNES_LAUNCH((k_gather_rows<U, UPR, NT, false>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
+        AGNES_LAUNCH((k_gather_rows<U, V, UPR, NT, false>), dim3(G), dim3(kBlock), lds, st, (const u32x4*)a.feat,
                            (u32x4*)a.out, a.nodes_out, a.rl_key, a.rl_val, a.node_off, a.H, a.base, a.rows,
                            a.row_units, a.tbuf, a.rpb, a.tch, a.pool_rows);
 }

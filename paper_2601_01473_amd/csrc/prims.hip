@@ -152,7 +152,8 @@ void scan_counts(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t 
 
 // LSD radix sort of 32-bit keys with 32-bit values, tiles of 256 x ITEMS keys
 // (2048 for sorts of at most 2M keys, where more and shorter workgroups hide
-// latency better; 4096 above, for longer runs per digit).  Digits are RB = 8,
+// latency better; 4096 above, and 8192 above 8M keys with 8-bit digits, for
+// longer runs per digit).  Digits are RB = 8,
 // 9 or 10 bits, the fewest passes that cover the key bits with digits of at
 // most 10 bits: 20-bit keys take two passes of 10, 26-bit keys three of 9,
 // 23-bit keys three of 8.  Per pass: (1) digit histogram of every tile, stored
@@ -163,6 +164,13 @@ void scan_counts(const int32_t* in, int64_t* out, const int64_t* n_dev, int64_t 
 constexpr int64_t kSmallSort = 1 << 21;
 static int sort_items(int64_t n_max) { return n_max <= kSmallSort ? 8 : 16; }
 int radix_items(int64_t n_max) { return sort_items(n_max); }
+// Sorts of more than kLargeSort keys with 8-bit digits take tiles of 8192
+// keys: a digit's run is then 32 keys on average, a whole 128-byte line of
+// keys, where 4096-key tiles leave half lines behind.  (With 9- or 10-bit
+// digits the runs stay shorter than a line, and the larger tiles only cost
+// occupancy: 2 workgroups per CU.)  Tile counts, and so the histogram, stay
+// below the 4096-key sizing above.
+constexpr int64_t kLargeSort = (int64_t)1 << 23;
 constexpr int kMaxRadixBits = 10;
 
 // Tiles rounded up to a multiple of the XCD count (the scatter's grid).
@@ -437,6 +445,9 @@ int radix_sort_pairs32(uint32_t* keys, uint32_t* vals, uint32_t* keys_tmp, uint3
     if (sort_items(n_max) == 8)
         radix_passes_rb<8>(rb, keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota,
                            max_groups);
+    else if (n_max > kLargeSort && rb == 8)
+        radix_passes<32, 8>(keys, vals, keys_tmp, vals_tmp, n_dev, (int)((n_max + 8191) / 8192 + 1), passes, hist,
+                            dtot, st, vals_iota, max_groups);
     else
         radix_passes_rb<16>(rb, keys, vals, keys_tmp, vals_tmp, n_dev, tiles, passes, hist, dtot, st, vals_iota,
                             max_groups);

@@ -106,3 +106,10 @@ def test_config_c4(agnes):
 @pytest.mark.parametrize("H", [1, 8, 64, 256])
 def test_config_c5_hyperbatch_sweep(agnes, H):
     run_config(agnes, "c5", H=H)
+
+
+def test_config_c2_with_64_minibatches(agnes):
+    """C2's graph (20-bit node ids: two radix passes of 10-bit digits) with 64
+    minibatches: the last hop's bound (64 x 16384 x 10 edges) is above 8M keys,
+    where 8-bit digits would take 8192-key tiles; 10-bit digits keep 4096."""
+    run_config(agnes, "c2", H=64)
