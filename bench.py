@@ -79,7 +79,7 @@ def offset_bytes(w: dict) -> int:
     return 8 if (wide or len(w["indices"]) >= (1 << 31) - 1) else 4
 
 
-def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int) -> tuple:
+def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int, ids_in_copy: bool = False) -> tuple:
     """Bytes the method must move (exact counts from the batch statistics).
 
     sampling, per hop: per request the node id, two offsets and the row-pointer
@@ -90,9 +90,10 @@ def algorithmic_bytes(st: dict, offset_bytes: int, row_bytes: int) -> tuple:
     for R, S, U in zip(st["requests"], st["sampled"], st["new_nodes"]):
         bs += R * (4 + 2 * offset_bytes + 4) + 8 * S + 4 * U
     bg = st["rows"] * (4 + row_bytes) + st["distinct_rows"] * row_bytes
-    # the row-copy kernel moves all of the gather's bytes (it also writes the
-    # node ids)
-    copy = bg
+    # the row-copy kernel moves the rows; the sampling phase packs the output
+    # node ids (k_list_stats), except on the node-range bucket path, where the
+    # row copy writes them
+    copy = bg if ids_in_copy else bg - st["rows"] * 4
     return bs, bg, copy
 
 
@@ -521,8 +522,9 @@ class Pipeline:
 def gather_calibration(ag, w, cfg, torch, reps=5):
     """The row-copy kernel on a list whose rows are all distinct: one
     hyperbatch of 2^21 distinct targets and no sampling (fanout 0), so every
-    launch reads and writes exactly rows x row_bytes (plus 4-byte node ids
-    and 12-byte list entries per row)."""
+    launch reads and writes exactly rows x row_bytes (plus a 12-byte list
+    entry read per row; the output node ids are packed by the sampling
+    phase)."""
     n = min(cfg.num_nodes, 1 << 21)
     import synth
     tg = synth.targets(cfg.num_nodes, n, cfg.data_seed + 11).reshape(1, n)
@@ -674,7 +676,7 @@ def main():
 
     def account(batch):
         st = batch.stats()                      # waits for the batch
-        bs, bg, bc = algorithmic_bytes(st, ob, rb)
+        bs, bg, bc = algorithmic_bytes(st, ob, rb, ids_in_copy=args.join_path == 1)
         acc["sample"] += bs
         acc["gather"] += bg
         acc["copy_bytes"] += bc

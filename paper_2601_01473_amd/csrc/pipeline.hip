@@ -650,13 +650,11 @@ __global__ __launch_bounds__(kBlock) void k_join_scan(int H, int G, int64_t* ghi
 // counts wcnt[w][j]); after a barrier the waves' totals are stacked.  An edge
 // takes the local id of the last head at or before it (a head before the tile:
 // the old pair A[a_t - 1], or the newest new node of its minibatch so far).
-// nodes (the per-minibatch lists that the next hop's requests read) is
-// written only when another hop follows (write_nodes); the gather writes the
-// final lists itself.
+// New nodes go to nodes (the per-minibatch lists: the next hop's requests, and
+// after the last hop the output lists that k_list_stats packs).
 // Dynamic LDS: mb_e[H+1], sk[T], sv[T], loc[T], nhx[T+1], cursor[H], wcnt[4][H] (16-bit),
 // ssplit[per] (the group's tile boundaries).
 __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t capN, int64_t rows_cap,
-                                                       int write_nodes,
                                                        const int64_t* req_off, const uint32_t* e_off,
                                                        const uint64_t* ak, const int32_t* av, const uint32_t* su,
                                                        const uint32_t* se, const int64_t* split, int G,
@@ -778,7 +776,7 @@ __global__ __launch_bounds__(kBlock) void k_join_write(int H, int jbits, int64_t
                     if (lc >= capN || pos >= rows_cap) {
                         atomicOr((unsigned long long*)&ctl->err, 4ull);
                     } else {
-                        if (write_nodes) nodes[(int64_t)j * capN + lc] = (int32_t)(key[r] >> 32);
+                        nodes[(int64_t)j * capN + lc] = (int32_t)(key[r] >> 32);
                         ck[pos] = key[r];
                         cv[pos] = lc;
                     }
@@ -862,16 +860,30 @@ static size_t join_write_lds(int H, int64_t per) {
 
 // Statistics of the final list (the feature bucket): distinct rows (runs of one
 // node) and non-empty feature-block rows (runs of one feature block), one
-// partial pair per workgroup for the host to add up.  Runs on the sampling
-// stream so that the row copy does nothing but copy.
+// partial pair per workgroup for the host to add up.  With nodes_out, also the
+// output node lists: minibatch j's list (nodes_ws[j capN ..], local-id order)
+// is packed to nodes_out[node_off[j] ..], read and written in consecutive
+// order (the row copy, which meets the entries in node order, would store each
+// id alone at a scattered place).  Runs on the sampling stream so that the row
+// copy does nothing but copy.
 constexpr int kStatItems = 8;   // entries per thread per round (independent loads in flight)
 
 __global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, uint32_t rpb, uint64_t* part,
-                                                       const Ctl* ctl) {
+                                                       const Ctl* ctl, const int32_t* nodes_ws, int64_t capN,
+                                                       const int64_t* node_off_g, int H, int32_t* nodes_out) {
+    extern __shared__ int64_t node_off[];      // [H+1] when nodes_out is given
     __shared__ unsigned long long cnt[2];
     if (threadIdx.x < 2) cnt[threadIdx.x] = 0;
     __syncthreads();
     const int64_t n = ctl->rows;
+    // (not after a node-capacity error: the sizes may then exceed capN)
+    if (nodes_out && !(ctl->err & 4)) {
+        load_offsets(node_off, node_off_g, H);
+        for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) {
+            const int j = upper_segment(node_off, H, i);
+            nodes_out[i] = nodes_ws[(int64_t)j * capN + (i - node_off[j])];
+        }
+    }
     unsigned long long nd = 0, nf = 0;
     const int64_t step = (int64_t)gridDim.x * kBlock * kStatItems;
     for (int64_t b = (int64_t)blockIdx.x * kBlock * kStatItems + threadIdx.x; b < n; b += step) {
@@ -972,7 +984,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(const Unit* __restrict__ feat
             fresh[k] = ok[k] && (k == 0 || u != pu);
             src[k] = (TIER && ok[k]) ? source_row(tbuf, rpb, tch, pool_rows, u) : u;
             dst[k] = d;
-            if (ok[k] && li == 0) nodes_out[d] = (int32_t)u;
+            if (nodes_out && ok[k] && li == 0) nodes_out[d] = (int32_t)u;
         }
         const int64_t c_end = ONE ? std::min<int64_t>(row_units, li + 1) : row_units;
         for (int64_t c = li; c < c_end; c += LPR) {
@@ -1029,7 +1041,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict_
             u = (uint32_t)(key >> 32);
             d = (uint32_t)(node_off[(uint32_t)key] + rl_val[e]);
             row = TIER ? source_row(tbuf, rpb, tch, pool_rows, u) : u;
-            nodes_out[d] = (int32_t)u;
+            if (nodes_out) nodes_out[d] = (int32_t)u;
         }
         const uint32_t pu = (uint32_t)__shfl_up((int)u, 1, kWave);
         const uint64_t okm = __ballot(mine);
@@ -1084,7 +1096,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(const u32x4* __restrict_
 struct GatherArgs {
     const void* feat;
     void* out;
-    int32_t* nodes_out;
+    int32_t* nodes_out;              // output node ids, or null when the sampling phase wrote them
     const uint64_t* rl_key;
     const int32_t* rl_val;
     const int64_t* node_off;
@@ -1491,7 +1503,7 @@ static void launch_layer(const Store& s, Workspace& w, const Geometry& g, int l,
     AGNES_LAUNCH(k_join_scan, dim3(g.H + 1), dim3(kBlock), 0, st, g.H, G, w.ghist.as<int64_t>(),
                        w.gemit.as<int64_t>(), w.newcnt.as<int64_t>(), ctl);
     AGNES_LAUNCH(k_join_write, dim3(G), dim3(kBlock), join_write_lds(g.H, per), st, g.H, g.jbits,
-                       g.capN, g.rows_max, (int)(l + 1 < g.L), w.req_off.as<int64_t>(), w.e_off.as<uint32_t>(), rlk, rlv, su, se,
+                       g.capN, g.rows_max, w.req_off.as<int64_t>(), w.e_off.as<uint32_t>(), rlk, rlv, su, se,
                        split, G, w.ghist.as<int64_t>(), w.gemit.as<int64_t>(), w.size.as<int32_t>(),
                        w.nodes.as<int32_t>(), w.rl_key[cur ^ 1].as<uint64_t>(), w.rl_val[cur ^ 1].as<int32_t>(),
                        b.col[l].as<int32_t>(), ctl);
@@ -1663,8 +1675,14 @@ static void launch_chain(const Store& s, Batch& b, const Geometry& g, const Sync
     AGNES_LAUNCH(k_begin, dim3(1), dim3(kBlock), 0, st, L, L, H, ctl, w.size.as<int32_t>(),
                        w.newcnt.as<int64_t>(), lsz, ec, w.req_off.as<int64_t>(), w.e_off.as<uint32_t>(),
                        w.mb_off.as<int64_t>(), w.topo_part.as<uint32_t>(), hop_grid(s, g, L - 1));
-    AGNES_LAUNCH(k_list_stats, dim3(y.n_lstat), dim3(kBlock), 0, st, w.rl_key[cur].as<uint64_t>(),
-                       (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl);
+    // the radix-sort path keeps every minibatch's node list in nodes (capN
+    // apart), and the statistics kernel packs them into the output; on the
+    // bucket path the row copy writes the output ids
+    int32_t* packed = legacy ? b.nodes.as<int32_t>() : nullptr;
+    AGNES_LAUNCH(k_list_stats, dim3(y.n_lstat), dim3(kBlock), packed ? (size_t)(H + 1) * sizeof(int64_t) : 0, st,
+                 w.rl_key[cur].as<uint64_t>(), (uint32_t)s.rpb, (uint64_t*)((char*)w.sync.ptr + y.lstat), ctl,
+                 w.nodes.as<int32_t>(), g.capN, w.mb_off.as<int64_t>(), H, packed);
+    b.ids_in_chain = legacy;
     AGNES_CHECK_HIP(hipGetLastError());
 }
 
@@ -1686,6 +1704,7 @@ static std::vector<uint64_t> chain_key(const Store& s, const Batch& b, const Geo
         k.push_back(a(b.row_ptr[l].ptr));
         k.push_back(a(b.col[l].ptr));
     }
+    k.push_back(a(b.nodes.ptr));
     return k;
 }
 
@@ -1763,6 +1782,8 @@ void begin_hyperbatch(const Store& s, Batch& b, const int32_t* targets, bool tar
         b.row_ptr[l].reserve((size_t)(H * g.cap[l] + H) * 4);
         b.col[l].reserve((size_t)std::max<int64_t>(1, H * g.cap[l] * fanouts[l]) * 4);
     }
+    // the output node ids are written by the sampling phase (at most rows_max)
+    b.nodes.reserve((size_t)g.rows_max * 4);
 
     b.prof = s.profile;
     if (b.prof) AGNES_CHECK_HIP(hipEventRecord(w.ev[0], st));
@@ -1876,7 +1897,8 @@ void finish_hyperbatch(Batch& b, hipStream_t st) {
     if (st != b.stream) AGNES_CHECK_HIP(hipStreamWaitEvent(st, b.sampled_at, 0));
     const uint64_t* rlk = w.rl_key[b.cur].as<uint64_t>();
     const int32_t* rlv = w.rl_val[b.cur].as<int32_t>();
-    GatherArgs ga{s.features.ptr, b.features.ptr, b.nodes.as<int32_t>(), rlk, rlv, w.mb_off.as<int64_t>(),
+    int32_t* ids = b.ids_in_chain ? nullptr : b.nodes.as<int32_t>();   // else written by the sampling phase
+    GatherArgs ga{s.features.ptr, b.features.ptr, ids, rlk, rlv, w.mb_off.as<int64_t>(),
                   H, 0, rows, 0, nullptr, (uint32_t)s.rpb};
     const bool wide = s.row_bytes % 16 == 0;
     ga.row_units = wide ? s.row_bytes / 16 : s.row_bytes / 4;

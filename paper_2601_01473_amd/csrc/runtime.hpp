@@ -290,6 +290,9 @@ struct Batch {
     int64_t capN = 0;
     int64_t rows_max = 0;             // node-list capacity of the hyperbatch (sizes the sync block)
     int cur = 0;                      // which list buffer holds the final list
+    // The sampling phase wrote the output node ids (nodes) itself (radix-sort
+    // path); otherwise the row copy writes them.
+    bool ids_in_chain = false;
     // The begun hyperbatch's arguments, for sampling it again on the radix-sort
     // path when a node-range bucket overflows (fallbacks counts those).
     std::vector<int32_t> fanouts;
