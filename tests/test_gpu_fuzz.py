@@ -127,3 +127,32 @@ def test_random_rmat_shape_matches_oracle(agnes, seed):
         assert st[k] == v, ("fuzz large", seed, k, st[k], v)
     b.close()
     store.close()
+
+
+@pytest.mark.parametrize("scale,abc", [(21, (0.57, 0.19, 0.19)), (22, (0.45, 0.25, 0.15))])
+def test_rmat_large_sort_tiles_match_oracle(agnes, scale, abc):
+    """2^21 and 2^22 nodes (three radix passes of 8-bit digits) with 64 x 1024
+    targets and fanouts [25, 10]: the last hop's bound (about 17 M edges) is
+    above 8 M keys, so its sort takes the 8192-key tiles; every minibatch is
+    compared with the oracle, and every gathered row through the oracle's
+    gather on four of them."""
+    import synth
+    off, idx = synth.rmat_csr(scale, 16, abc, 9000 + scale)
+    n = 1 << scale
+    feat = features(n, 16, 9100 + scale)
+    store = agnes.Store(off, idx, feat, 1024)
+    H, B, fan = 64, 1024, [25, 10]
+    tg = synth.targets(n, H * B, 9200 + scale).reshape(H, B)
+    b = store.prepare(tg, fan, seed=scale, mb_base=5)
+    got = b.to_host()
+    ref = oracle.Oracle(off, idx).hyperbatch(tg, fan, scale, 5)
+    fb = feature_bytes(feat)
+    for j in range(H):
+        compare_minibatch(got[j], ref[j], oracle.gather(fb, ref[j].nodes) if j % 16 == 0 else None,
+                          tag=("large sort", scale, j))
+    st = b.stats()
+    want = oracle.hyperbatch_stats(off, 1024, fb.shape[1], ref, len(fan))
+    for k, v in want.items():
+        assert st[k] == v, ("large sort", scale, k, st[k], v)
+    b.close()
+    store.close()
