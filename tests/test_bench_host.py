@@ -53,3 +53,16 @@ def test_offset_width_counted_as_the_device_keeps_it(monkeypatch):
     monkeypatch.setenv("AGNES_WIDE_OFFSETS", "1")
     assert bench.offset_bytes(small64) == 8
     assert bench.offset_bytes(small32) == 4
+
+
+def test_algorithmic_bytes_split_between_sampling_and_copy():
+    # one hop: 10 requests, 30 sampled edges, 20 new nodes; 100 output rows
+    # of 1 KiB, 40 of them distinct; 4-byte offsets
+    st = {"requests": [10], "sampled": [30], "new_nodes": [20], "rows": 100, "distinct_rows": 40}
+    bs, bg, copy = bench.algorithmic_bytes(st, 4, 1024)
+    assert bs == 10 * (4 + 2 * 4 + 4) + 8 * 30 + 4 * 20
+    assert bg == 100 * (4 + 1024) + 40 * 1024
+    # the sampling phase packs the output node ids, so the row copy moves rows only
+    assert copy == 100 * 1024 + 40 * 1024
+    # on the node-range bucket path the row copy also stores the ids
+    assert bench.algorithmic_bytes(st, 4, 1024, ids_in_copy=True)[2] == bg
