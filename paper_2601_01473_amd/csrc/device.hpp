@@ -68,6 +68,22 @@ __device__ __forceinline__ int upper_segment(const T* off, int n, T x) {
     return lo;
 }
 
+// upper_segment for Q values at once: the halving steps depend on n only, so
+// the Q searches advance together and their LDS reads overlap.  Every x[q] <
+// off[n].
+template <int Q, typename T>
+__device__ __forceinline__ void upper_segments(const T* off, int n, const T (&x)[Q], int (&out)[Q]) {
+#pragma unroll
+    for (int q = 0; q < Q; q++) out[q] = 0;
+    int len = n;   // invariant: off[out] <= x < off[out + len]
+    while (len > 1) {
+        const int half = len >> 1;
+#pragma unroll
+        for (int q = 0; q < Q; q++) out[q] = off[out[q] + half] <= x[q] ? out[q] + half : out[q];
+        len -= half;
+    }
+}
+
 // The same search by a group of P lanes (P divides 64; lanes [g*P, (g+1)*P)
 // form group g and the groups of a wave search independently): log_P(n) rounds
 // of P probes.  All lanes of a group must call it together.

@@ -877,11 +877,22 @@ __global__ __launch_bounds__(kBlock) void k_list_stats(const uint64_t* rl_key, u
     __syncthreads();
     const int64_t n = ctl->rows;
     // (not after a node-capacity error: the sizes may then exceed capN)
+    // kStatItems entries per thread per round, all loaded before any is stored
     if (nodes_out && !(ctl->err & 4)) {
         load_offsets(node_off, node_off_g, H);
-        for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) {
-            const int j = upper_segment(node_off, H, i);
-            nodes_out[i] = nodes_ws[(int64_t)j * capN + (i - node_off[j])];
+        const int64_t stride = (int64_t)gridDim.x * kBlock;
+        for (int64_t b = (int64_t)blockIdx.x * kBlock + threadIdx.x; b < n; b += stride * kStatItems) {
+            int64_t x[kStatItems];
+            int j[kStatItems];
+            int32_t v[kStatItems];
+#pragma unroll
+            for (int k = 0; k < kStatItems; k++) x[k] = std::min<int64_t>(b + k * stride, n - 1);
+            upper_segments<kStatItems>(node_off, H, x, j);
+#pragma unroll
+            for (int k = 0; k < kStatItems; k++) v[k] = nodes_ws[(int64_t)j[k] * capN + (x[k] - node_off[j[k]])];
+#pragma unroll
+            for (int k = 0; k < kStatItems; k++)
+                if (b + k * stride < n) nodes_out[b + k * stride] = v[k];
         }
     }
     unsigned long long nd = 0, nf = 0;
